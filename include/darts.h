@@ -1,0 +1,269 @@
+/*
+ * darts.h -- C ABI of the MI355X (gfx950) rollout hot path of DARTS
+ * (Distribution-Aware Active Rollout Trajectory Shaping).
+ *
+ * What the library computes (paper Sec. 4.1, Sec. 4.3.1, Alg. 2):
+ *   For a batch of N prompts it decodes M'_i = m redundant trajectories per
+ *   prompt (intra-prompt redundant rollout), scores every generated token
+ *   (log-probability of the taken token and entropy of the next-token
+ *   distribution), and per prompt selects the training group of M = k
+ *   trajectories: shortest-only selection with proactive early stopping when
+ *   m >= m_up (aborting the remaining candidates and reclaiming their KV
+ *   pages), or dual-end selection (top-K shortest + top-L longest valid) when
+ *   m < m_up.  The notation follows the paper's Tab. 1: q_i prompt, M group
+ *   size, M'_i redundant rollout size, N prompts per batch.
+ *
+ * Conventions for every call
+ *   - Return value: 0 (DARTS_OK) or a positive darts_status.  No C++
+ *     exception ever crosses this boundary.
+ *   - "d_" pointers are device pointers (HIP global memory on the context's
+ *     device), "h_" pointers are host pointers.  All are caller-owned unless
+ *     stated otherwise; the library never frees them.
+ *   - Work is enqueued on the HIP stream given at init (run->stream, NULL is
+ *     the legacy default stream).  Calls that return host values synchronise
+ *     that stream first.
+ *   - Calls on one context must not run concurrently.  Different contexts are
+ *     independent.
+ *   - After DARTS_EHIP the context is poisoned: every call except
+ *     darts_destroy returns DARTS_EHIP again; darts_last_error has the text.
+ *
+ * Trajectory ids: trajectory j of prompt i has global id g = i*m + j.
+ * Random numbers: Philox4x32-10 (Salmon et al., SC'11), key = 64-bit seed,
+ * so every trajectory's tokens depend only on (seed, g, step), never on batch
+ * composition, row order or physical page ids.
+ */
+#ifndef DARTS_H
+#define DARTS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DARTS_OK = 0,
+  DARTS_EINVAL = 1,   /* bad argument or inconsistent shapes */
+  DARTS_ENOMEM = 2,   /* device allocation failed or KV page pool exhausted */
+  DARTS_ESTATE = 3,   /* call out of order (e.g. decode before prefill) */
+  DARTS_EHIP = 4      /* HIP runtime error; context poisoned */
+} darts_status;
+
+typedef enum { DARTS_F32 = 0, DARTS_BF16 = 1 } darts_dtype;
+
+/* Flags for darts_run_cfg.flags */
+#define DARTS_FLAG_NO_ABORT      0x1u  /* counterfactual: no proactive early stop; every
+                                          trajectory runs to its own end before its group
+                                          is selected (kept sets are unchanged) */
+#define DARTS_FLAG_PERMUTE_PAGES 0x2u  /* initial free list in a seeded random order
+                                          (physical page ids must not change any output) */
+#define DARTS_FLAG_TIMING        0x4u  /* record HIP events around attention launches
+                                          (darts_get_stats reports them) */
+
+/* Decoder shape.  Weights are generated on the device from weight_seed
+ * (Philox uniform, variance 1/fan_in, rounded to bf16 for DARTS_BF16).
+ * Dense SwiGLU when n_experts == 0, else top_k-of-n_experts MoE.            */
+typedef struct {
+  int32_t n_layers;
+  int32_t d_model;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;    /* n_q_heads % n_kv_heads == 0 (GQA) */
+  int32_t head_dim;      /* 32, 64 or 128 */
+  int32_t ffn_dim;       /* dense FFN hidden size */
+  int32_t vocab;         /* multiple of 4; the end-of-sequence id is vocab-1 */
+  int32_t n_experts;     /* 0 for dense */
+  int32_t top_k;
+  int32_t expert_ffn;
+  float rope_theta;
+  float rms_eps;
+  int32_t dtype;         /* darts_dtype: F32 (all fp32) or BF16 (bf16 operands,
+                            fp32 accumulation and residual stream) */
+  uint64_t weight_seed;
+} darts_model_cfg;
+
+/* One rollout batch.  m and k are passed to darts_init separately.          */
+typedef struct {
+  int32_t n_prompts;     /* N */
+  int32_t prompt_len;    /* Lp, multiple of page_size */
+  int32_t cap;           /* system length limit: max generated tokens, < 2^20 */
+  int32_t L;             /* dual-end long side size, 1 <= L < k when used (paper: 1) */
+  int32_t m_up;          /* shortest-only threshold M_up; 0 means 2k (paper default) */
+  int32_t page_size;     /* must be 16 */
+  uint64_t kv_pool_bytes;/* KV pool budget in bytes; 0 sizes it for the worst case
+                            (every trajectory reaching cap) */
+  uint64_t sample_seed;
+  float temperature;     /* > 0 */
+  uint32_t flags;        /* DARTS_FLAG_* */
+  uint64_t page_perm_seed; /* used with DARTS_FLAG_PERMUTE_PAGES */
+  void* stream;          /* hipStream_t */
+} darts_run_cfg;
+
+/* Per-step outputs, one row per trajectory decoded in the step (live-list
+ * order, ascending trajectory id).  Every pointer is a caller-owned device
+ * buffer of capacity n_prompts*m; `sampled` may be NULL.  n_rows is written
+ * on the host by the call.                                                  */
+typedef struct {
+  int32_t* traj_id;      /* global trajectory id g of the row */
+  int32_t* token;        /* taken token: end-of-sequence at the forced length,
+                            else the teacher-forced token if given, else the sample */
+  int32_t* sampled;      /* Gumbel-max sample before any forcing (may be NULL) */
+  float* logprob;        /* log p(taken token) under softmax(logits / T) */
+  float* entropy;        /* entropy of softmax(logits / T) */
+  uint8_t* finished;     /* 0 live, 1 end-of-sequence (valid), 2 truncated at cap */
+  int32_t n_rows;
+} darts_step_out;
+
+typedef struct {
+  int64_t steps;             /* sampling steps done (prefill counts as step 1) */
+  int64_t tokens_decoded;    /* all generated tokens, including later-aborted ones */
+  int64_t n_pages;           /* KV pool size in pages */
+  int64_t pages_used;        /* pages in use now */
+  int64_t pages_hwm;         /* high-water mark of pages in use */
+  int32_t n_live;
+  int32_t n_done;            /* prompts whose kept set is complete */
+  double attn_ms;            /* with DARTS_FLAG_TIMING: summed attention kernel time */
+  double attn_bytes;         /* algorithmic bytes of those launches */
+  int64_t attn_launches;
+} darts_stats;
+
+typedef struct darts_ctx darts_ctx;
+
+/* ---------------------------------------------------------------- stateful */
+
+/* Allocate a context: generated weights, paged KV pool (page = 16 tokens,
+ * one pool per layer, prompt pages shared by the prompt's m trajectories),
+ * page tables, per-trajectory state and scratch, all owned by the context.
+ * m = M'_i (uniform), k = M (paper Tab. 1).  Errors: DARTS_EINVAL if k < 1,
+ * k > m, m > 64, L < 1 or L >= k, prompt_len % 16 != 0, cap out of range,
+ * unsupported head_dim, or GEMM dimensions that are not multiples of 64/128
+ * for BF16; DARTS_ENOMEM if device memory is short.  *out is written only
+ * on success.                                                              */
+int darts_init(const darts_model_cfg* model, int32_t m, int32_t k,
+               const darts_run_cfg* run, darts_ctx** out);
+
+/* Prefill every prompt and sample generated token 0 of every trajectory
+ * (paper Alg. 2: rollout of the candidate pool T_i).
+ *   d_prompts      [n_prompts * prompt_len] int32 token ids in [0, vocab)
+ *   d_forced_len   [n_prompts * m] int32 >= 1: trajectory g emits the
+ *                  end-of-sequence id as its d-th generated token when
+ *                  d <= cap; d > cap means it is truncated at cap
+ *   d_force_tokens NULL or [n_prompts * m] int32 teacher-forced token 0 per
+ *                  trajectory (-1: no force)
+ * Writes `out` (n_rows = n_prompts*m).  DARTS_ESTATE if called twice.      */
+int darts_prefill(darts_ctx* ctx, const int32_t* d_prompts, const int32_t* d_forced_len,
+                  const int32_t* d_force_tokens, darts_step_out* out);
+
+/* One decode step over the live trajectories: consume each one's last token,
+ * append its key/value to the paged pool (taking a fresh page when a page
+ * fills), run the decoder, and sample + score the next token.
+ *   d_force_tokens NULL or [n_prompts * m] int32 indexed by trajectory id
+ *                  (-1: no force): the token to take at this step.
+ * DARTS_ENOMEM when the pool lacks the pages this step needs (checked before
+ * any write; state unchanged).  DARTS_ESTATE before prefill or when no
+ * trajectory is live.                                                      */
+int darts_decode_step(darts_ctx* ctx, const int32_t* d_force_tokens, darts_step_out* out);
+
+/* Apply the selection of Alg. 2 to every prompt whose group can complete
+ * after the latest step: shortest-only with early stop (m >= m_up) keeps the
+ * first k valid finished trajectories in shortest-first order and aborts the
+ * live rest; dual-end (m < m_up) waits for all members, then keeps the K
+ * shortest followed by the L longest valid of the rest.  Frees the private
+ * pages of every trajectory that finished or was aborted, and a prompt's
+ * shared pages when its last member is done; compacts the live list.
+ *   d_kept      [n_prompts * k] int32, row i = prompt i's kept ids (short
+ *               side first); rows of incomplete prompts are left untouched
+ *   d_done_step [n_prompts] int32: the step at which prompt i completed
+ *               (untouched while incomplete)
+ *   h_n_live, h_n_done: host outputs (may be NULL).
+ * Idempotent when nothing changed.                                          */
+int darts_select_and_prune(darts_ctx* ctx, int32_t* d_kept, int32_t* d_done_step,
+                           int32_t* h_n_live, int32_t* h_n_done);
+
+int darts_get_stats(const darts_ctx* ctx, darts_stats* out);
+
+/* Final per-trajectory scores (device buffers of n_prompts*m, each may be
+ * NULL): generated length, float32 sum of log-probs in step order, mean
+ * = sum / length, status (0 live, 1 eos, 2 truncated, 3 aborted).          */
+int darts_get_traj_scores(darts_ctx* ctx, int32_t* d_len, float* d_sum_lp, float* d_mean_lp,
+                          uint8_t* d_status);
+
+/* Copy the last step's float32 logits [n_rows * vocab] (rows in the order of
+ * the last darts_step_out) into d_dst.  For verification.                  */
+int darts_debug_logits(darts_ctx* ctx, float* d_dst, int32_t* h_n_rows);
+
+int darts_destroy(darts_ctx* ctx);
+const char* darts_strerror(int status);
+const char* darts_last_error(const darts_ctx* ctx);
+
+/* ----------------------------------------------------- stateless kernels  */
+/* These run one kernel of the path on caller-provided device buffers, for
+ * kernel sweeps and parity checks "given the same inputs".                 */
+
+/* Fill d_dst[0..n) with element idx = bf16(((w>>8)|1)*2^-23 - 1),
+ * w = Philox(key=seed, counter=(idx>>2, tensor, 0, 3)) word idx&3, stored as
+ * bf16 or (dtype DARTS_F32) as the same value in float32.                  */
+int darts_fill_uniform(void* d_dst, uint64_t n, int32_t tensor, uint64_t seed, int32_t dtype,
+                       void* stream);
+
+/* Fill the paged K and V pools of the attention sweep with the values above
+ * (tensor 1 for K, 2 for V) at logical index ((page*Hkv + h)*16 + slot)*hd + d,
+ * written in the library's physical pool layouts (n_pages pages, dtype as
+ * for darts_fill_uniform).  Each pool holds n_pages*Hkv*16*hd elements.    */
+int darts_fill_kv_pool(void* d_k_pool, void* d_v_pool, int64_t n_pages, int32_t n_kv_heads,
+                       int32_t head_dim, uint64_t seed, int32_t dtype, void* stream);
+
+/* Bytes of workspace darts_attn_decode needs for these sizes.              */
+size_t darts_attn_workspace_bytes(int32_t n_rows, int32_t n_q_heads, int32_t n_kv_heads,
+                                  int32_t head_dim, int32_t max_ctx);
+
+/* Paged GQA decode attention (the scaled dot-product attention of the
+ * decoder): for each row r and q head h,
+ *   out[r][h] = sum_j softmax_j(q[r][h] . k_j / sqrt(hd)) v_j,  j < ctx_len[r],
+ * key j of row r lives in page page_table[r*pt_stride + j/16], slot j%16, kv
+ * head h / (n_q_heads/n_kv_heads).
+ *   d_q, d_out    [n_rows][n_q_heads][head_dim] (bf16, or f32 with DARTS_F32)
+ *   d_k_pool/v    pools of n_pages pages in the library layout (as filled by
+ *                 darts_fill_kv_pool); page ids are clamped into [0, n_pages)
+ *   d_page_table  [n_rows][pt_stride] int32, pt_stride >= ceil(max_ctx/16)
+ *   d_ctx_len     [n_rows] int32 in [1, max_ctx] (larger values are clamped,
+ *                 rows with ctx <= 0 are left unwritten)
+ *   d_workspace   darts_attn_workspace_bytes(...) bytes, 256-byte aligned
+ */
+int darts_attn_decode(const void* d_q, const void* d_k_pool, const void* d_v_pool,
+                      int64_t n_pages, const int32_t* d_page_table, int32_t pt_stride,
+                      const int32_t* d_ctx_len, int32_t n_rows, int32_t n_q_heads,
+                      int32_t n_kv_heads, int32_t head_dim, int32_t max_ctx, int32_t dtype,
+                      void* d_out, void* d_workspace, size_t workspace_bytes, void* stream);
+
+/* Fused sampler: for each row, Gumbel-max token with counter (traj, step),
+ * log-prob of the taken token (d_force[r] if d_force != NULL and >= 0, else
+ * the sample) and entropy of softmax(logits / T).
+ *   d_logits [n_rows][vocab] (bf16 or f32), d_traj/d_step [n_rows] int32.   */
+int darts_sample(const void* d_logits, int32_t n_rows, int32_t vocab, int32_t dtype,
+                 uint64_t seed, const int32_t* d_traj, const int32_t* d_step, float temperature,
+                 const int32_t* d_force, int32_t* d_token, float* d_logprob, float* d_entropy,
+                 void* stream);
+
+/* Stateless selection over groups of m consecutive trajectories (Alg. 2).
+ *   d_status   [n_traj] uint8 in/out: 0 live, 1 eos, 2 truncated, 3 aborted
+ *              (aborted is written for pruned live members)
+ *   d_len      [n_traj] int32 generated lengths (< 2^20)
+ *   d_mean_lp  [n_traj] float32 mean log-probs (tie-break only)
+ *   d_kept     [n_groups * k] int32 out (rows of incomplete groups untouched)
+ *   d_complete [n_groups] uint8 out: 1 if the group completed now
+ *   m_up: shortest-only when m >= m_up; early_stop: 0 or 1.                 */
+int darts_select_groups(uint8_t* d_status, const int32_t* d_len, const float* d_mean_lp,
+                        int32_t n_traj, int32_t m, int32_t k, int32_t L, int32_t m_up,
+                        int32_t early_stop, int32_t* d_kept, uint8_t* d_complete, void* stream);
+
+/* Gumbel noise map used by darts_sample: d_g[i] = -ln(-ln(d_u[i])) with the
+ * library's float32 logarithm (a fixed sequence of correctly rounded float32
+ * operations: atanh series on the reduced mantissa).  d_u in (0, 1).  For
+ * bit-exact verification of the sampler's noise.                           */
+int darts_debug_gumbel(const float* d_u, float* d_g, int64_t n, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DARTS_H */

@@ -1,0 +1,280 @@
+"""ctypes binding of include/darts.h.  Argument marshalling only: every step of
+the rollout runs in the HIP library (libdarts.so, built for gfx950).  PyTorch
+provides device memory and the stream; there is no CPU fallback -- a missing
+library raises."""
+import ctypes as C
+import os
+
+import numpy as np
+
+DARTS_OK, DARTS_EINVAL, DARTS_ENOMEM, DARTS_ESTATE, DARTS_EHIP = 0, 1, 2, 3, 4
+DARTS_F32, DARTS_BF16 = 0, 1
+FLAG_NO_ABORT, FLAG_PERMUTE_PAGES, FLAG_TIMING = 0x1, 0x2, 0x4
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+lib_path = os.path.join(_HERE, "libdarts.so")
+
+
+class DartsError(RuntimeError):
+    def __init__(self, status, msg=""):
+        super().__init__(f"darts status {status}: {msg}")
+        self.status = status
+
+
+class ModelCfg(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_q_heads", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("ffn_dim", C.c_int32),
+                ("vocab", C.c_int32), ("n_experts", C.c_int32), ("top_k", C.c_int32),
+                ("expert_ffn", C.c_int32), ("rope_theta", C.c_float), ("rms_eps", C.c_float),
+                ("dtype", C.c_int32), ("weight_seed", C.c_uint64)]
+
+
+class RunCfg(C.Structure):
+    _fields_ = [("n_prompts", C.c_int32), ("prompt_len", C.c_int32), ("cap", C.c_int32),
+                ("L", C.c_int32), ("m_up", C.c_int32), ("page_size", C.c_int32),
+                ("kv_pool_bytes", C.c_uint64), ("sample_seed", C.c_uint64),
+                ("temperature", C.c_float), ("flags", C.c_uint32),
+                ("page_perm_seed", C.c_uint64), ("stream", C.c_void_p)]
+
+
+class StepOut(C.Structure):
+    _fields_ = [("traj_id", C.c_void_p), ("token", C.c_void_p), ("sampled", C.c_void_p),
+                ("logprob", C.c_void_p), ("entropy", C.c_void_p), ("finished", C.c_void_p),
+                ("n_rows", C.c_int32)]
+
+
+class Stats(C.Structure):
+    _fields_ = [("steps", C.c_int64), ("tokens_decoded", C.c_int64), ("n_pages", C.c_int64),
+                ("pages_used", C.c_int64), ("pages_hwm", C.c_int64), ("n_live", C.c_int32),
+                ("n_done", C.c_int32), ("attn_ms", C.c_double), ("attn_bytes", C.c_double),
+                ("attn_launches", C.c_int64)]
+
+
+_P = C.c_void_p
+_SIGS = {
+    "darts_init": (C.c_int, [C.POINTER(ModelCfg), C.c_int32, C.c_int32, C.POINTER(RunCfg), C.POINTER(_P)]),
+    "darts_prefill": (C.c_int, [_P, _P, _P, _P, C.POINTER(StepOut)]),
+    "darts_decode_step": (C.c_int, [_P, _P, C.POINTER(StepOut)]),
+    "darts_select_and_prune": (C.c_int, [_P, _P, _P, C.POINTER(C.c_int32), C.POINTER(C.c_int32)]),
+    "darts_get_stats": (C.c_int, [_P, C.POINTER(Stats)]),
+    "darts_get_traj_scores": (C.c_int, [_P, _P, _P, _P, _P]),
+    "darts_debug_logits": (C.c_int, [_P, _P, C.POINTER(C.c_int32)]),
+    "darts_destroy": (C.c_int, [_P]),
+    "darts_strerror": (C.c_char_p, [C.c_int]),
+    "darts_last_error": (C.c_char_p, [_P]),
+    "darts_fill_uniform": (C.c_int, [_P, C.c_uint64, C.c_int32, C.c_uint64, C.c_int32, _P]),
+    "darts_fill_kv_pool": (C.c_int, [_P, _P, C.c_int64, C.c_int32, C.c_int32, C.c_uint64, C.c_int32, _P]),
+    "darts_attn_workspace_bytes": (C.c_size_t, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32]),
+    "darts_attn_decode": (C.c_int, [_P, _P, _P, C.c_int64, _P, C.c_int32, _P, C.c_int32, C.c_int32,
+                                    C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P, _P, C.c_size_t, _P]),
+    "darts_sample": (C.c_int, [_P, C.c_int32, C.c_int32, C.c_int32, C.c_uint64, _P, _P, C.c_float,
+                               _P, _P, _P, _P, _P]),
+    "darts_debug_gumbel": (C.c_int, [_P, _P, C.c_int64, _P]),
+    "darts_select_groups": (C.c_int, [_P, _P, _P, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                      C.c_int32, C.c_int32, _P, _P, _P]),
+}
+
+_lib = None
+
+
+def load_library(path=None):
+    """Load libdarts.so (raises if it is missing: there is no fallback path)."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or lib_path
+    if not os.path.exists(p):
+        raise DartsError(DARTS_EHIP, f"HIP library not built: {p} (run __graft_entry__.build())")
+    lib = C.CDLL(p)
+    for name, (res, args) in _SIGS.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def _ptr(t):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    return C.c_void_p(stream.cuda_stream)
+
+
+def _check(status, ctx=None):
+    if status != DARTS_OK:
+        lib = load_library()
+        msg = lib.darts_strerror(status).decode()
+        if ctx:
+            extra = lib.darts_last_error(ctx).decode()
+            if extra:
+                msg += " | " + extra
+        raise DartsError(status, msg)
+
+
+# ---------------------------------------------------------------- stateless
+def darts_fill_uniform(dst, tensor_id, seed, dtype, stream=None):
+    _check(load_library().darts_fill_uniform(_ptr(dst), dst.numel(), tensor_id, seed, dtype,
+                                             _stream(stream)))
+
+
+def darts_fill_kv_pool(k_pool, v_pool, n_pages, n_kv_heads, head_dim, seed, dtype, stream=None):
+    _check(load_library().darts_fill_kv_pool(_ptr(k_pool), _ptr(v_pool), n_pages, n_kv_heads,
+                                             head_dim, seed, dtype, _stream(stream)))
+
+
+def darts_attn_workspace_bytes(n_rows, n_q_heads, n_kv_heads, head_dim, max_ctx):
+    return int(load_library().darts_attn_workspace_bytes(n_rows, n_q_heads, n_kv_heads, head_dim,
+                                                         max_ctx))
+
+
+def darts_attn_decode(q, k_pool, v_pool, n_pages, page_table, ctx_len, n_q_heads, n_kv_heads,
+                      head_dim, max_ctx, dtype, out, workspace, stream=None):
+    n_rows = ctx_len.numel()
+    _check(load_library().darts_attn_decode(
+        _ptr(q), _ptr(k_pool), _ptr(v_pool), n_pages, _ptr(page_table), page_table.shape[1],
+        _ptr(ctx_len), n_rows, n_q_heads, n_kv_heads, head_dim, max_ctx, dtype, _ptr(out),
+        _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def darts_sample(logits, dtype, seed, traj, step, temperature, force, token, logprob, entropy,
+                 stream=None):
+    n_rows, vocab = logits.shape
+    _check(load_library().darts_sample(_ptr(logits), n_rows, vocab, dtype, seed, _ptr(traj),
+                                       _ptr(step), float(temperature), _ptr(force), _ptr(token),
+                                       _ptr(logprob), _ptr(entropy), _stream(stream)))
+
+
+def darts_select_groups(status, length, mean_lp, m, k, L, m_up, early_stop, kept, complete,
+                        stream=None):
+    _check(load_library().darts_select_groups(_ptr(status), _ptr(length), _ptr(mean_lp),
+                                              status.numel(), m, k, L, m_up, int(early_stop),
+                                              _ptr(kept), _ptr(complete), _stream(stream)))
+
+
+def darts_debug_gumbel(u, g, stream=None):
+    _check(load_library().darts_debug_gumbel(_ptr(u), _ptr(g), u.numel(), _stream(stream)))
+
+
+# ---------------------------------------------------------------- stateful
+def model_cfg_struct(model):
+    return ModelCfg(model.n_layers, model.d_model, model.n_q_heads, model.n_kv_heads,
+                    model.head_dim, model.ffn_dim, model.vocab, model.n_experts, model.top_k,
+                    model.expert_ffn, model.rope_theta, model.rms_eps,
+                    DARTS_BF16 if model.dtype == "bf16" else DARTS_F32, model.weight_seed)
+
+
+def run_cfg_struct(run, stream, flags=0, page_perm_seed=0, kv_pool_bytes=None):
+    pool = int(run.kv_pool_gb * (1 << 30)) if kv_pool_bytes is None else int(kv_pool_bytes)
+    return RunCfg(run.n_prompts, run.prompt_len, run.cap, run.L, run.m_up or 0, 16, pool,
+                  run.sample_seed, run.temperature, flags, page_perm_seed, stream)
+
+
+class Rollout:
+    """One rollout batch on the GPU through the C ABI (darts_init / darts_prefill /
+    darts_decode_step / darts_select_and_prune).  Output buffers are torch
+    tensors on the current device; PyTorch only allocates them."""
+
+    def __init__(self, model, run, flags=0, page_perm_seed=0, kv_pool_bytes=None, stream=None):
+        import torch
+        self.torch = torch
+        self.lib = load_library()
+        self.model, self.run = model, run
+        self.m, self.k = run.m, run.k
+        self.n_traj = run.n_prompts * run.m
+        self.stream = stream or torch.cuda.current_stream()
+        self._mc = model_cfg_struct(model)
+        self._rc = run_cfg_struct(run, self.stream.cuda_stream, flags, page_perm_seed, kv_pool_bytes)
+        ctx = C.c_void_p()
+        _check(self.lib.darts_init(C.byref(self._mc), run.m, run.k, C.byref(self._rc), C.byref(ctx)))
+        self.ctx = ctx
+        dev = torch.device("cuda", torch.cuda.current_device())
+        n = self.n_traj
+        self.o_traj = torch.zeros(n, dtype=torch.int32, device=dev)
+        self.o_tok = torch.zeros(n, dtype=torch.int32, device=dev)
+        self.o_samp = torch.zeros(n, dtype=torch.int32, device=dev)
+        self.o_lp = torch.zeros(n, dtype=torch.float32, device=dev)
+        self.o_ent = torch.zeros(n, dtype=torch.float32, device=dev)
+        self.o_fin = torch.zeros(n, dtype=torch.uint8, device=dev)
+        self.kept = torch.full((run.n_prompts, run.k), -1, dtype=torch.int32, device=dev)
+        self.done_step = torch.full((run.n_prompts,), -1, dtype=torch.int32, device=dev)
+        self._out = StepOut(self.o_traj.data_ptr(), self.o_tok.data_ptr(), self.o_samp.data_ptr(),
+                            self.o_lp.data_ptr(), self.o_ent.data_ptr(), self.o_fin.data_ptr(), 0)
+        self.n_live = n
+        self.n_done = 0
+
+    def close(self):
+        if self.ctx:
+            self.lib.darts_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _rows(self):
+        n = self._out.n_rows
+        return dict(traj=self.o_traj[:n], token=self.o_tok[:n], sampled=self.o_samp[:n],
+                    logprob=self.o_lp[:n], entropy=self.o_ent[:n], finished=self.o_fin[:n])
+
+    def darts_prefill(self, prompts, forced_len, force_tokens=None):
+        _check(self.lib.darts_prefill(self.ctx, _ptr(prompts), _ptr(forced_len), _ptr(force_tokens),
+                                      C.byref(self._out)), self.ctx)
+        return self._rows()
+
+    def darts_decode_step(self, force_tokens=None):
+        _check(self.lib.darts_decode_step(self.ctx, _ptr(force_tokens), C.byref(self._out)), self.ctx)
+        return self._rows()
+
+    def darts_select_and_prune(self):
+        nl, nd = C.c_int32(), C.c_int32()
+        _check(self.lib.darts_select_and_prune(self.ctx, _ptr(self.kept), _ptr(self.done_step),
+                                               C.byref(nl), C.byref(nd)), self.ctx)
+        self.n_live, self.n_done = nl.value, nd.value
+        return self.n_live, self.n_done
+
+    def stats(self):
+        s = Stats()
+        _check(self.lib.darts_get_stats(self.ctx, C.byref(s)), self.ctx)
+        return {f: getattr(s, f) for f, _ in Stats._fields_}
+
+    def traj_scores(self):
+        t = self.torch
+        dev = self.o_tok.device
+        ln = t.zeros(self.n_traj, dtype=t.int32, device=dev)
+        slp = t.zeros(self.n_traj, dtype=t.float32, device=dev)
+        mlp = t.zeros(self.n_traj, dtype=t.float32, device=dev)
+        st = t.zeros(self.n_traj, dtype=t.uint8, device=dev)
+        _check(self.lib.darts_get_traj_scores(self.ctx, _ptr(ln), _ptr(slp), _ptr(mlp), _ptr(st)), self.ctx)
+        return ln, slp, mlp, st
+
+    def debug_logits(self, rows):
+        t = self.torch
+        buf = t.empty((rows, self.model.vocab), dtype=t.float32, device=self.o_tok.device)
+        n = C.c_int32()
+        _check(self.lib.darts_debug_logits(self.ctx, _ptr(buf), C.byref(n)), self.ctx)
+        return buf[:n.value]
+
+    def run_to_completion(self, prompts, forced_len, on_step=None, force_fn=None):
+        """prefill, then decode + select until every prompt's kept set is complete.
+        on_step(step_index, rows) is called after every sampling step;
+        force_fn(step_index) may return a [n_traj] int32 device tensor."""
+        rows = self.darts_prefill(prompts, forced_len, force_fn(0) if force_fn else None)
+        if on_step:
+            on_step(0, rows)
+        self.darts_select_and_prune()
+        s = 0
+        while self.n_done < self.run.n_prompts:
+            s += 1
+            rows = self.darts_decode_step(force_fn(s) if force_fn else None)
+            if on_step:
+                on_step(s, rows)
+            self.darts_select_and_prune()
+        return self.stats()

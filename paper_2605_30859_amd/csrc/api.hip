@@ -1,0 +1,677 @@
+// C ABI of the rollout library: context, memory plan, per-step launch
+// sequence, selection/pruning, statistics, and the stateless kernel entries.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/darts.h"
+#include "common.h"
+#include "kernels.h"
+
+using namespace darts;
+
+enum : uint32_t { T_EMBED = 0, T_WQ, T_WK, T_WV, T_WO, T_WGATE, T_WUP, T_WDOWN, T_LM,
+                  T_ROUTER, T_EGATE, T_EUP, T_EDOWN };
+
+namespace {
+
+struct LayerW {
+  void* wqkv = nullptr;   // [(hq + 2 hkv) hd][d]
+  void* wo = nullptr;     // [d][hq hd]
+  void* wgu = nullptr;    // [2F][d], gate/up interleaved in groups of 16 rows
+  void* wdown = nullptr;  // [d][F]
+};
+
+struct TimedLaunch {
+  hipEvent_t a, b;
+  double bytes;
+};
+
+}  // namespace
+
+struct darts_ctx {
+  darts_model_cfg mc{};
+  darts_run_cfg rc{};
+  int m = 0, k = 0, L = 1, m_up = 0;
+  hipStream_t st = nullptr;
+  bool bf16 = false;
+  size_t esz = 4;
+  int P = 0, Lp = 0, cap = 0, pp = 0, max_pages = 0, n_traj = 0;
+  int64_t n_pages = 0;
+  int d = 0, hq = 0, hkv = 0, hd = 0, F = 0, V = 0, nl = 0, qkv_w = 0;
+  // device memory
+  std::vector<void*> allocs;
+  void* embed = nullptr;
+  void* lm_head = nullptr;
+  std::vector<LayerW> layers;
+  void* kpool = nullptr;
+  void* vpool = nullptr;
+  int64_t pool_layer_elems = 0;
+  float2* rope = nullptr;
+  int32_t* page_table = nullptr;
+  int32_t* free_stack = nullptr;
+  int32_t* dcnt = nullptr;        // [0] free_top, [4..7] info
+  int32_t* gen = nullptr;
+  float* sum_lp = nullptr;
+  uint8_t* status = nullptr;
+  uint8_t* freed = nullptr;
+  int32_t* last_tok = nullptr;
+  int32_t* forced_len = nullptr;
+  int32_t* refcnt = nullptr;
+  uint8_t* group_done = nullptr;
+  int32_t* done_step = nullptr;
+  int32_t* kept = nullptr;
+  int32_t* live[2] = {nullptr, nullptr};
+  int32_t* grp_cnt = nullptr;
+  int32_t* grp_rel = nullptr;
+  int32_t* trj_cnt = nullptr;
+  int32_t* prefill_pt = nullptr;   // [P*Lp] page-table row of each prompt position
+  int32_t* last_rows = nullptr;    // [P] index of each prompt's last position
+  float* x = nullptr;
+  void* xn = nullptr;
+  float* qkv = nullptr;
+  void* q = nullptr;
+  void* attn = nullptr;
+  void* hbuf = nullptr;
+  float* xlast = nullptr;
+  float* logits = nullptr;
+  void* gemm_ws = nullptr;
+  size_t gemm_ws_bytes = 0;
+  void* attn_ws = nullptr;
+  size_t attn_ws_bytes = 0;
+  int32_t* h_info = nullptr;       // pinned host
+  // host state
+  int phase = 0;                   // 0 init, 1 decoding, 2 done
+  int cur = 0;
+  int n_live = 0;
+  int n_done = 0;
+  int free_top = 0;
+  int64_t step = 0;
+  int64_t tokens = 0;
+  int64_t hwm = 0;
+  int last_rows_out = 0;
+  bool poisoned = false;
+  std::string err;
+  std::vector<TimedLaunch> pending;
+  double attn_ms = 0.0, attn_bytes = 0.0;
+  int64_t attn_launches = 0;
+};
+
+#define HIPCHK(ctx, expr)                                                      \
+  do {                                                                         \
+    hipError_t _e = (expr);                                                    \
+    if (_e != hipSuccess) return fail_hip((ctx), _e, #expr);                   \
+  } while (0)
+
+static int fail_hip(darts_ctx* c, hipError_t e, const char* what) {
+  if (c) {
+    c->poisoned = true;
+    c->err = std::string(what) + ": " + hipGetErrorString(e);
+  }
+  return DARTS_EHIP;
+}
+
+template <typename T>
+static hipError_t dalloc(darts_ctx* c, T** p, size_t bytes) {
+  void* v = nullptr;
+  hipError_t e = hipMalloc(&v, bytes ? bytes : 256);
+  if (e == hipSuccess) {
+    c->allocs.push_back(v);
+    *p = (T*)v;
+  }
+  return e;
+}
+
+static void free_all(darts_ctx* c) {
+  for (void* p : c->allocs) (void)hipFree(p);
+  c->allocs.clear();
+  if (c->h_info) (void)hipHostFree(c->h_info);
+  c->h_info = nullptr;
+  for (auto& t : c->pending) {
+    (void)hipEventDestroy(t.a);
+    (void)hipEventDestroy(t.b);
+  }
+  c->pending.clear();
+}
+
+static int init_weights(darts_ctx* c) {
+  const int d = c->d, hq = c->hq, hkv = c->hkv, hd = c->hd, F = c->F, V = c->V;
+  const bool b = c->bf16;
+  const uint64_t seed = c->mc.weight_seed;
+  HIPCHK(c, launch_init_weights(c->embed, b, V, d, 1, T_EMBED, 0, seed, rowmap_plain(V, 0), c->st));
+  HIPCHK(c, launch_init_weights(c->lm_head, b, V, d, d, T_LM, 0, seed, rowmap_plain(V, 0), c->st));
+  for (int l = 0; l < c->nl; ++l) {
+    LayerW& w = c->layers[l];
+    HIPCHK(c, launch_init_weights(w.wqkv, b, (int64_t)hq * hd, d, d, T_WQ, l, seed,
+                                  rowmap_plain(hq * hd, 0), c->st));
+    HIPCHK(c, launch_init_weights(w.wqkv, b, (int64_t)hkv * hd, d, d, T_WK, l, seed,
+                                  rowmap_plain(hkv * hd, hq * hd), c->st));
+    HIPCHK(c, launch_init_weights(w.wqkv, b, (int64_t)hkv * hd, d, d, T_WV, l, seed,
+                                  rowmap_plain(hkv * hd, (hq + hkv) * hd), c->st));
+    HIPCHK(c, launch_init_weights(w.wo, b, d, (int64_t)hq * hd, (int64_t)hq * hd, T_WO, l, seed,
+                                  rowmap_plain(d, 0), c->st));
+    RowMap gate{F, 0, 16, 32, 0}, up{F, 0, 16, 32, 16};
+    HIPCHK(c, launch_init_weights(w.wgu, b, F, d, d, T_WGATE, l, seed, gate, c->st));
+    HIPCHK(c, launch_init_weights(w.wgu, b, F, d, d, T_WUP, l, seed, up, c->st));
+    HIPCHK(c, launch_init_weights(w.wdown, b, d, F, F, T_WDOWN, l, seed, rowmap_plain(d, 0), c->st));
+  }
+  return DARTS_OK;
+}
+
+static size_t gemm_ws_need(const darts_ctx* c) {
+  size_t need = 0;
+  std::vector<int> ms;
+  for (int mm = 16; mm < c->n_traj; mm *= 2) ms.push_back(mm);
+  ms.push_back(c->n_traj);
+  ms.push_back(c->P);
+  for (int M : ms) {
+    need = std::max(need, gemm_workspace_bytes(M, c->qkv_w, c->d));
+    need = std::max(need, gemm_workspace_bytes(M, c->d, c->hq * c->hd));
+    need = std::max(need, gemm_workspace_bytes(M, 2 * c->F, c->d));
+    need = std::max(need, gemm_workspace_bytes(M, c->d, c->F));
+    need = std::max(need, gemm_workspace_bytes(M, c->V, c->d));
+  }
+  return need;
+}
+
+extern "C" {
+
+const char* darts_strerror(int s) {
+  switch (s) {
+    case DARTS_OK: return "ok";
+    case DARTS_EINVAL: return "invalid argument";
+    case DARTS_ENOMEM: return "out of memory (device memory or KV page pool)";
+    case DARTS_ESTATE: return "call out of order";
+    case DARTS_EHIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* darts_last_error(const darts_ctx* c) { return c ? c->err.c_str() : ""; }
+
+int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_run_cfg* run,
+               darts_ctx** out) {
+  if (!model || !run || !out) return DARTS_EINVAL;
+  const darts_model_cfg& mc = *model;
+  const darts_run_cfg& rc = *run;
+  const int L = rc.L > 0 ? rc.L : 1;
+  const int m_up = rc.m_up > 0 ? rc.m_up : 2 * k;
+  if (k < 1 || k > m || m > 64 || L >= k) return DARTS_EINVAL;
+  if (rc.page_size != 16 || rc.prompt_len < 16 || rc.prompt_len % 16 != 0) return DARTS_EINVAL;
+  if (rc.n_prompts < 1 || rc.cap < 1 || rc.cap >= (1 << 20) || !(rc.temperature > 0.f))
+    return DARTS_EINVAL;
+  if (mc.n_layers < 1 || mc.d_model < 1 || mc.n_q_heads < 1 || mc.n_kv_heads < 1 ||
+      mc.n_q_heads % mc.n_kv_heads != 0 || mc.n_q_heads / mc.n_kv_heads > 16)
+    return DARTS_EINVAL;
+  if (!(mc.head_dim == 32 || mc.head_dim == 64 || mc.head_dim == 128)) return DARTS_EINVAL;
+  if (mc.vocab < 8 || mc.vocab % 4 != 0) return DARTS_EINVAL;
+  if (mc.dtype != DARTS_F32 && mc.dtype != DARTS_BF16) return DARTS_EINVAL;
+  if (mc.n_experts != 0) return DARTS_EINVAL;   // MoE decoder: not in this build yet
+  if (mc.ffn_dim < 16 || mc.ffn_dim % 16 != 0) return DARTS_EINVAL;
+  const int qkv_w = (mc.n_q_heads + 2 * mc.n_kv_heads) * mc.head_dim;
+  if (mc.dtype == DARTS_BF16) {
+    const int K1 = mc.d_model, K2 = mc.n_q_heads * mc.head_dim, K3 = mc.ffn_dim;
+    if (K1 % 64 || K2 % 64 || K3 % 64) return DARTS_EINVAL;
+    if (qkv_w % 128 || mc.d_model % 128 || (2 * mc.ffn_dim) % 128 || mc.vocab % 128)
+      return DARTS_EINVAL;
+  }
+  const int64_t n_traj64 = (int64_t)rc.n_prompts * m;
+  if (n_traj64 > 65536 || (int64_t)rc.n_prompts * rc.prompt_len > (1 << 22)) return DARTS_EINVAL;
+
+  darts_ctx* c = new (std::nothrow) darts_ctx();
+  if (!c) return DARTS_ENOMEM;
+  c->mc = mc; c->rc = rc; c->m = m; c->k = k; c->L = L; c->m_up = m_up;
+  c->st = (hipStream_t)rc.stream;
+  c->bf16 = mc.dtype == DARTS_BF16;
+  c->esz = c->bf16 ? 2 : 4;
+  c->P = rc.n_prompts; c->Lp = rc.prompt_len; c->cap = rc.cap;
+  c->pp = c->Lp / kPage;
+  c->max_pages = c->pp + (c->cap + kPage - 1) / kPage;
+  c->n_traj = (int)n_traj64;
+  c->d = mc.d_model; c->hq = mc.n_q_heads; c->hkv = mc.n_kv_heads; c->hd = mc.head_dim;
+  c->F = mc.ffn_dim; c->V = mc.vocab; c->nl = mc.n_layers; c->qkv_w = qkv_w;
+
+  const int64_t page_bytes_all = (int64_t)c->nl * c->hkv * kPage * c->hd * 2 * c->esz;
+  const int64_t worst = (int64_t)c->P * c->pp + (int64_t)c->n_traj * ((c->cap + kPage - 1) / kPage);
+  int64_t n_pages = worst;
+  if (rc.kv_pool_bytes > 0) n_pages = std::min<int64_t>(worst, (int64_t)(rc.kv_pool_bytes / page_bytes_all));
+  if (n_pages < (int64_t)c->P * c->pp || n_pages >= (1ll << 31)) { delete c; return DARTS_ENOMEM; }
+  c->n_pages = n_pages;
+  c->pool_layer_elems = n_pages * c->hkv * kPage * c->hd;
+
+  size_t free_b = 0, total_b = 0;
+  if (hipMemGetInfo(&free_b, &total_b) != hipSuccess) { delete c; return DARTS_EHIP; }
+  const int rows_pf = c->P * c->Lp;
+  const int rows_max = std::max(rows_pf, c->n_traj);
+  const size_t wbytes = ((size_t)c->V * c->d * 2 +
+                         (size_t)c->nl * ((size_t)qkv_w * c->d + (size_t)c->d * c->hq * c->hd +
+                                          (size_t)3 * c->F * c->d)) * c->esz;
+  const size_t poolb = (size_t)n_pages * page_bytes_all;
+  if (wbytes + poolb + (size_t)rows_max * c->V * 0 > free_b) { delete c; return DARTS_ENOMEM; }
+
+  hipError_t e = hipSuccess;
+  auto A = [&](auto** p, size_t bytes) { if (e == hipSuccess) e = dalloc(c, p, bytes); };
+  A(&c->embed, (size_t)c->V * c->d * c->esz);
+  A(&c->lm_head, (size_t)c->V * c->d * c->esz);
+  c->layers.resize(c->nl);
+  for (auto& w : c->layers) {
+    A(&w.wqkv, (size_t)qkv_w * c->d * c->esz);
+    A(&w.wo, (size_t)c->d * c->hq * c->hd * c->esz);
+    A(&w.wgu, (size_t)2 * c->F * c->d * c->esz);
+    A(&w.wdown, (size_t)c->d * c->F * c->esz);
+  }
+  A(&c->kpool, (size_t)c->nl * c->pool_layer_elems * c->esz);
+  A(&c->vpool, (size_t)c->nl * c->pool_layer_elems * c->esz);
+  const int max_pos = c->Lp + c->cap + 1;
+  A(&c->rope, (size_t)max_pos * (c->hd / 2) * sizeof(float2));
+  A(&c->page_table, (size_t)c->n_traj * c->max_pages * 4);
+  A(&c->free_stack, (size_t)n_pages * 4);
+  A(&c->dcnt, 64);
+  A(&c->gen, (size_t)c->n_traj * 4);
+  A(&c->sum_lp, (size_t)c->n_traj * 4);
+  A(&c->status, (size_t)c->n_traj);
+  A(&c->freed, (size_t)c->n_traj);
+  A(&c->last_tok, (size_t)c->n_traj * 4);
+  A(&c->forced_len, (size_t)c->n_traj * 4);
+  A(&c->refcnt, (size_t)c->P * 4);
+  A(&c->group_done, (size_t)c->P);
+  A(&c->done_step, (size_t)c->P * 4);
+  A(&c->kept, (size_t)c->P * k * 4);
+  A(&c->live[0], (size_t)c->n_traj * 4);
+  A(&c->live[1], (size_t)c->n_traj * 4);
+  A(&c->grp_cnt, (size_t)c->P * 4);
+  A(&c->grp_rel, (size_t)c->P * 4);
+  A(&c->trj_cnt, (size_t)c->n_traj * 4);
+  A(&c->prefill_pt, (size_t)rows_pf * 4);
+  A(&c->last_rows, (size_t)c->P * 4);
+  A(&c->x, (size_t)rows_max * c->d * 4);
+  A(&c->xn, (size_t)rows_max * c->d * c->esz);
+  A(&c->qkv, (size_t)rows_max * qkv_w * 4);
+  A(&c->q, (size_t)rows_max * c->hq * c->hd * c->esz);
+  A(&c->attn, (size_t)rows_max * c->hq * c->hd * c->esz);
+  A(&c->hbuf, (size_t)rows_max * c->F * c->esz);
+  A(&c->xlast, (size_t)c->P * c->d * 4);
+  A(&c->logits, (size_t)c->n_traj * c->V * 4);
+  c->gemm_ws_bytes = gemm_ws_need(c);
+  A(&c->gemm_ws, c->gemm_ws_bytes);
+  c->attn_ws_bytes = std::max(attn_workspace_bytes(c->n_traj, c->hq, c->hkv, c->hd, c->Lp + c->cap),
+                              attn_workspace_bytes(rows_pf, c->hq, c->hkv, c->hd, c->Lp));
+  A(&c->attn_ws, c->attn_ws_bytes);
+  if (e == hipSuccess) e = hipHostMalloc((void**)&c->h_info, 64, hipHostMallocDefault);
+  if (e != hipSuccess) {
+    free_all(c);
+    delete c;
+    (void)hipGetLastError();
+    return e == hipErrorOutOfMemory ? DARTS_ENOMEM : DARTS_EHIP;
+  }
+  // host-computed index tables (uploaded once)
+  {
+    std::vector<int32_t> pf(rows_pf), lr(c->P), iota(c->n_traj);
+    for (int r = 0; r < rows_pf; ++r) pf[r] = (r / c->Lp) * c->m;
+    for (int i = 0; i < c->P; ++i) lr[i] = i * c->Lp + c->Lp - 1;
+    for (int g = 0; g < c->n_traj; ++g) iota[g] = g;
+    e = hipMemcpyAsync(c->prefill_pt, pf.data(), pf.size() * 4, hipMemcpyHostToDevice, c->st);
+    if (e == hipSuccess) e = hipMemcpyAsync(c->last_rows, lr.data(), lr.size() * 4, hipMemcpyHostToDevice, c->st);
+    if (e == hipSuccess) e = hipMemcpyAsync(c->live[0], iota.data(), iota.size() * 4, hipMemcpyHostToDevice, c->st);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->st);
+  }
+  int rcode = DARTS_OK;
+  if (e != hipSuccess) rcode = fail_hip(c, e, "upload index tables");
+  if (rcode == DARTS_OK) rcode = init_weights(c);
+  if (rcode == DARTS_OK) {
+    e = launch_rope_table(c->rope, max_pos, c->hd, (double)mc.rope_theta, c->st);
+    if (e == hipSuccess)
+      e = launch_iota_perm(c->free_stack, n_pages, rc.page_perm_seed,
+                           (rc.flags & DARTS_FLAG_PERMUTE_PAGES) != 0, c->st);
+    const int32_t top = (int32_t)n_pages;
+    if (e == hipSuccess) e = hipMemcpyAsync(c->dcnt, &top, 4, hipMemcpyHostToDevice, c->st);
+    if (e == hipSuccess) e = hipMemsetAsync(c->gen, 0, (size_t)c->n_traj * 4, c->st);
+    if (e == hipSuccess) e = hipMemsetAsync(c->sum_lp, 0, (size_t)c->n_traj * 4, c->st);
+    if (e == hipSuccess) e = hipMemsetAsync(c->status, 0, (size_t)c->n_traj, c->st);
+    if (e == hipSuccess) e = hipMemsetAsync(c->freed, 0, (size_t)c->n_traj, c->st);
+    if (e == hipSuccess) e = hipMemsetAsync(c->group_done, 0, (size_t)c->P, c->st);
+    if (e == hipSuccess) e = hipMemsetAsync(c->page_table, 0xff, (size_t)c->n_traj * c->max_pages * 4, c->st);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->st);
+    if (e != hipSuccess) rcode = fail_hip(c, e, "init");
+  }
+  if (rcode != DARTS_OK) {
+    free_all(c);
+    delete c;
+    return rcode;
+  }
+  c->free_top = (int)n_pages;
+  *out = c;
+  return DARTS_OK;
+}
+
+int darts_destroy(darts_ctx* c) {
+  if (!c) return DARTS_EINVAL;
+  (void)hipStreamSynchronize(c->st);
+  free_all(c);
+  delete c;
+  return DARTS_OK;
+}
+
+}  // extern "C"
+
+// Attention with optional event timing.
+static int run_attention(darts_ctx* c, int layer, int n_rows, const int32_t* row_pt, int ctx_mod,
+                         int ctx_base, int max_ctx) {
+  void* kp = (char*)c->kpool + (size_t)layer * c->pool_layer_elems * c->esz;
+  void* vp = (char*)c->vpool + (size_t)layer * c->pool_layer_elems * c->esz;
+  const bool timing = (c->rc.flags & DARTS_FLAG_TIMING) != 0 && ctx_mod == 0;
+  TimedLaunch tl{};
+  if (timing) {
+    HIPCHK(c, hipEventCreate(&tl.a));
+    HIPCHK(c, hipEventCreate(&tl.b));
+    HIPCHK(c, hipEventRecord(tl.a, c->st));
+  }
+  HIPCHK(c, launch_attention(c->q, kp, vp, c->n_pages, c->page_table, c->max_pages, row_pt, nullptr,
+                             ctx_mod, ctx_base, n_rows, c->hq, c->hkv, c->hd, max_ctx, c->bf16,
+                             c->attn, c->attn_ws, c->attn_ws_bytes, c->st));
+  if (timing) {
+    HIPCHK(c, hipEventRecord(tl.b, c->st));
+    const double ctx = ctx_base;
+    tl.bytes = (double)n_rows * (ctx * c->hkv * c->hd * 2.0 * c->esz + 2.0 * c->hq * c->hd * c->esz +
+                                 std::ceil(ctx / kPage) * 4.0);
+    c->pending.push_back(tl);
+  }
+  return DARTS_OK;
+}
+
+// Decoder layers over n rows whose residual stream is in c->x.
+static int run_layers(darts_ctx* c, int n, const int32_t* row_pt, int pos_mod, int pos_base,
+                      int ctx_mod, int ctx_base, int max_ctx) {
+  const bool b = c->bf16;
+  const int d = c->d, hqd = c->hq * c->hd;
+  for (int l = 0; l < c->nl; ++l) {
+    LayerW& w = c->layers[l];
+    void* kp = (char*)c->kpool + (size_t)l * c->pool_layer_elems * c->esz;
+    void* vp = (char*)c->vpool + (size_t)l * c->pool_layer_elems * c->esz;
+    HIPCHK(c, launch_rmsnorm(c->x, n, d, c->mc.rms_eps, c->xn, b, c->st));
+    HIPCHK(c, launch_gemm(b, c->xn, d, w.wqkv, d, c->qkv, c->qkv_w, n, c->qkv_w, d, EPI_F32,
+                          c->gemm_ws, c->gemm_ws_bytes, c->st));
+    HIPCHK(c, launch_rope_append2(c->qkv, n, c->hq, c->hkv, c->hd, row_pt, pos_mod, pos_base,
+                                  c->page_table, c->max_pages, c->n_pages, c->rope, c->q, kp, vp, b,
+                                  c->st));
+    int r = run_attention(c, l, n, row_pt, ctx_mod, ctx_base, max_ctx);
+    if (r != DARTS_OK) return r;
+    HIPCHK(c, launch_gemm(b, c->attn, hqd, w.wo, hqd, c->x, d, n, d, hqd, EPI_ADD_F32, c->gemm_ws,
+                          c->gemm_ws_bytes, c->st));
+    HIPCHK(c, launch_rmsnorm(c->x, n, d, c->mc.rms_eps, c->xn, b, c->st));
+    HIPCHK(c, launch_gemm(b, c->xn, d, w.wgu, d, c->hbuf, c->F, n, 2 * c->F, d, EPI_SWIGLU,
+                          c->gemm_ws, c->gemm_ws_bytes, c->st));
+    HIPCHK(c, launch_gemm(b, c->hbuf, c->F, w.wdown, c->F, c->x, d, n, d, c->F, EPI_ADD_F32,
+                          c->gemm_ws, c->gemm_ws_bytes, c->st));
+  }
+  return DARTS_OK;
+}
+
+static int write_out_rows(darts_ctx* c, darts_step_out* out, int n) {
+  if (out) out->n_rows = n;
+  c->last_rows_out = n;
+  return DARTS_OK;
+}
+
+extern "C" {
+
+int darts_prefill(darts_ctx* c, const int32_t* d_prompts, const int32_t* d_forced_len,
+                  const int32_t* d_force_tokens, darts_step_out* out) {
+  if (!c || !d_prompts || !d_forced_len || !out) return DARTS_EINVAL;
+  if (c->poisoned) return DARTS_EHIP;
+  if (c->phase != 0) return DARTS_ESTATE;
+  if (!out->traj_id || !out->token || !out->logprob || !out->entropy || !out->finished)
+    return DARTS_EINVAL;
+  const bool b = c->bf16;
+  const int rows = c->P * c->Lp;
+  HIPCHK(c, hipMemcpyAsync(c->forced_len, d_forced_len, (size_t)c->n_traj * 4,
+                           hipMemcpyDeviceToDevice, c->st));
+  HIPCHK(c, launch_prefill_pages(c->P, c->m, c->pp, c->page_table, c->max_pages, c->free_stack,
+                                 c->dcnt, c->refcnt, c->st));
+  HIPCHK(c, launch_embed_v(c->embed, b, d_prompts, nullptr, rows, c->d, c->V, c->x, c->st));
+  int r = run_layers(c, rows, c->prefill_pt, c->Lp, 0, c->Lp, 1, c->Lp);
+  if (r != DARTS_OK) return r;
+  HIPCHK(c, launch_gather_rows(c->x, c->last_rows, c->P, c->d, c->xlast, c->st));
+  HIPCHK(c, launch_rmsnorm(c->xlast, c->P, c->d, c->mc.rms_eps, c->xn, b, c->st));
+  HIPCHK(c, launch_gemm(b, c->xn, c->d, c->lm_head, c->d, c->logits, c->V, c->P, c->V, c->d,
+                        EPI_F32, c->gemm_ws, c->gemm_ws_bytes, c->st));
+  SampleArgs a{};
+  a.logits = c->logits; a.n_rows = c->n_traj; a.vocab = c->V; a.bf16 = false;
+  a.seed = c->rc.sample_seed; a.temperature = c->rc.temperature;
+  a.row_logit = nullptr; a.logit_div = c->m;
+  a.traj = c->live[c->cur]; a.step = nullptr; a.force = d_force_tokens;
+  a.token_out = out->token; a.sampled_out = out->sampled; a.logprob_out = out->logprob;
+  a.entropy_out = out->entropy; a.gen = c->gen; a.sum_lp = c->sum_lp; a.status = c->status;
+  a.last_tok = c->last_tok; a.forced_len = c->forced_len; a.finished_out = out->finished;
+  a.traj_out = out->traj_id; a.cap = c->cap; a.eos = c->V - 1;
+  HIPCHK(c, launch_sample(a, c->st));
+  c->free_top -= c->P * c->pp;
+  c->hwm = std::max<int64_t>(c->hwm, c->n_pages - c->free_top);
+  c->phase = 1;
+  c->step = 1;
+  c->n_live = c->n_traj;
+  c->tokens += c->n_traj;
+  HIPCHK(c, hipStreamSynchronize(c->st));
+  return write_out_rows(c, out, c->n_traj);
+}
+
+int darts_decode_step(darts_ctx* c, const int32_t* d_force_tokens, darts_step_out* out) {
+  if (!c || !out) return DARTS_EINVAL;
+  if (c->poisoned) return DARTS_EHIP;
+  if (c->phase != 1 || c->n_live <= 0) return DARTS_ESTATE;
+  if (!out->traj_id || !out->token || !out->logprob || !out->entropy || !out->finished)
+    return DARTS_EINVAL;
+  const bool b = c->bf16;
+  const int n = c->n_live;
+  const int64_t s_before = c->step;               // tokens generated so far by every live row
+  const int pos = c->Lp + (int)s_before - 1;      // position of the token consumed now
+  if (pos + 1 > c->Lp + c->cap) return DARTS_ESTATE;
+  const bool need_pages = ((s_before - 1) % kPage) == 0;
+  if (need_pages && n > c->free_top) return DARTS_ENOMEM;
+  int32_t* live = c->live[c->cur];
+  if (need_pages) {
+    HIPCHK(c, launch_alloc_pages(live, n, c->gen, c->pp, c->page_table, c->max_pages, c->free_stack,
+                                 c->dcnt, c->dcnt + 4, c->st));
+    c->free_top -= n;
+    c->hwm = std::max<int64_t>(c->hwm, c->n_pages - c->free_top);
+  }
+  HIPCHK(c, launch_embed_v(c->embed, b, c->last_tok, live, n, c->d, c->V, c->x, c->st));
+  int r = run_layers(c, n, live, 0, pos, 0, pos + 1, pos + 1);
+  if (r != DARTS_OK) return r;
+  HIPCHK(c, launch_rmsnorm(c->x, n, c->d, c->mc.rms_eps, c->xn, b, c->st));
+  HIPCHK(c, launch_gemm(b, c->xn, c->d, c->lm_head, c->d, c->logits, c->V, n, c->V, c->d, EPI_F32,
+                        c->gemm_ws, c->gemm_ws_bytes, c->st));
+  SampleArgs a{};
+  a.logits = c->logits; a.n_rows = n; a.vocab = c->V; a.bf16 = false;
+  a.seed = c->rc.sample_seed; a.temperature = c->rc.temperature;
+  a.row_logit = nullptr; a.logit_div = 0;
+  a.traj = live; a.step = nullptr; a.force = d_force_tokens;
+  a.token_out = out->token; a.sampled_out = out->sampled; a.logprob_out = out->logprob;
+  a.entropy_out = out->entropy; a.gen = c->gen; a.sum_lp = c->sum_lp; a.status = c->status;
+  a.last_tok = c->last_tok; a.forced_len = c->forced_len; a.finished_out = out->finished;
+  a.traj_out = out->traj_id; a.cap = c->cap; a.eos = c->V - 1;
+  HIPCHK(c, launch_sample(a, c->st));
+  c->step += 1;
+  c->tokens += n;
+  return write_out_rows(c, out, n);
+}
+
+int darts_select_and_prune(darts_ctx* c, int32_t* d_kept, int32_t* d_done_step, int32_t* h_n_live,
+                           int32_t* h_n_done) {
+  if (!c) return DARTS_EINVAL;
+  if (c->poisoned) return DARTS_EHIP;
+  if (c->phase == 0) return DARTS_ESTATE;
+  PruneArgs a{};
+  a.status = c->status; a.gen = c->gen; a.sum_lp = c->sum_lp; a.freed = c->freed;
+  a.refcnt = c->refcnt; a.group_done = c->group_done; a.done_step = c->done_step; a.kept = c->kept;
+  a.n_groups = c->P; a.m = c->m; a.k = c->k; a.L = c->L; a.m_up = c->m_up;
+  a.early_stop = (c->rc.flags & DARTS_FLAG_NO_ABORT) ? 0 : 1;
+  a.step = (int)c->step;
+  a.page_table = c->page_table; a.pt_stride = c->max_pages; a.prompt_pages = c->pp;
+  a.free_stack = c->free_stack; a.free_top = c->dcnt; a.n_pages = (int)c->n_pages;
+  a.grp_cnt = c->grp_cnt; a.grp_rel = c->grp_rel; a.trj_cnt = c->trj_cnt;
+  a.live_in = c->live[c->cur]; a.n_live_in = c->n_live; a.live_out = c->live[c->cur ^ 1];
+  a.info = c->dcnt + 4;
+  HIPCHK(c, launch_prune(a, c->st));
+  if (d_kept)
+    HIPCHK(c, hipMemcpyAsync(d_kept, c->kept, (size_t)c->P * c->k * 4, hipMemcpyDeviceToDevice, c->st));
+  if (d_done_step)
+    HIPCHK(c, hipMemcpyAsync(d_done_step, c->done_step, (size_t)c->P * 4, hipMemcpyDeviceToDevice, c->st));
+  HIPCHK(c, hipMemcpyAsync(c->h_info, c->dcnt + 4, 16, hipMemcpyDeviceToHost, c->st));
+  HIPCHK(c, hipStreamSynchronize(c->st));
+  c->cur ^= 1;
+  c->n_live = c->h_info[0];
+  c->n_done = c->h_info[1];
+  c->free_top = c->h_info[2];
+  if (c->n_done == c->P) c->phase = 2;
+  for (auto& t : c->pending) {
+    float ms = 0.f;
+    HIPCHK(c, hipEventElapsedTime(&ms, t.a, t.b));
+    c->attn_ms += ms;
+    c->attn_bytes += t.bytes;
+    c->attn_launches += 1;
+    (void)hipEventDestroy(t.a);
+    (void)hipEventDestroy(t.b);
+  }
+  c->pending.clear();
+  if (h_n_live) *h_n_live = c->n_live;
+  if (h_n_done) *h_n_done = c->n_done;
+  return DARTS_OK;
+}
+
+int darts_get_stats(const darts_ctx* c, darts_stats* s) {
+  if (!c || !s) return DARTS_EINVAL;
+  s->steps = c->step;
+  s->tokens_decoded = c->tokens;
+  s->n_pages = c->n_pages;
+  s->pages_used = c->n_pages - c->free_top;
+  s->pages_hwm = c->hwm;
+  s->n_live = c->n_live;
+  s->n_done = c->n_done;
+  s->attn_ms = c->attn_ms;
+  s->attn_bytes = c->attn_bytes;
+  s->attn_launches = c->attn_launches;
+  return DARTS_OK;
+}
+
+int darts_get_traj_scores(darts_ctx* c, int32_t* d_len, float* d_sum_lp, float* d_mean_lp,
+                          uint8_t* d_status) {
+  if (!c) return DARTS_EINVAL;
+  if (c->poisoned) return DARTS_EHIP;
+  if (d_len) HIPCHK(c, hipMemcpyAsync(d_len, c->gen, (size_t)c->n_traj * 4, hipMemcpyDeviceToDevice, c->st));
+  if (d_sum_lp)
+    HIPCHK(c, hipMemcpyAsync(d_sum_lp, c->sum_lp, (size_t)c->n_traj * 4, hipMemcpyDeviceToDevice, c->st));
+  if (d_status)
+    HIPCHK(c, hipMemcpyAsync(d_status, c->status, (size_t)c->n_traj, hipMemcpyDeviceToDevice, c->st));
+  if (d_mean_lp) {
+    // mean = fl32(sum / len), computed on the host copy to keep the device path small
+    std::vector<float> s(c->n_traj), mlp(c->n_traj);
+    std::vector<int32_t> ln(c->n_traj);
+    HIPCHK(c, hipMemcpyAsync(s.data(), c->sum_lp, (size_t)c->n_traj * 4, hipMemcpyDeviceToHost, c->st));
+    HIPCHK(c, hipMemcpyAsync(ln.data(), c->gen, (size_t)c->n_traj * 4, hipMemcpyDeviceToHost, c->st));
+    HIPCHK(c, hipStreamSynchronize(c->st));
+    for (int g = 0; g < c->n_traj; ++g) mlp[g] = ln[g] > 0 ? s[g] / (float)ln[g] : 0.f;
+    HIPCHK(c, hipMemcpyAsync(d_mean_lp, mlp.data(), (size_t)c->n_traj * 4, hipMemcpyHostToDevice, c->st));
+  }
+  HIPCHK(c, hipStreamSynchronize(c->st));
+  return DARTS_OK;
+}
+
+int darts_debug_logits(darts_ctx* c, float* d_dst, int32_t* h_n_rows) {
+  if (!c || !d_dst) return DARTS_EINVAL;
+  if (c->poisoned) return DARTS_EHIP;
+  const int rows = c->phase == 1 && c->step == 1 ? c->P : c->last_rows_out;
+  HIPCHK(c, hipMemcpyAsync(d_dst, c->logits, (size_t)rows * c->V * 4, hipMemcpyDeviceToDevice, c->st));
+  HIPCHK(c, hipStreamSynchronize(c->st));
+  if (h_n_rows) *h_n_rows = rows;
+  return DARTS_OK;
+}
+
+// ------------------------------------------------------------- stateless
+
+int darts_fill_uniform(void* d_dst, uint64_t n, int32_t tensor, uint64_t seed, int32_t dtype,
+                       void* stream) {
+  if ((!d_dst && n) || (dtype != DARTS_F32 && dtype != DARTS_BF16)) return DARTS_EINVAL;
+  hipError_t e = launch_fill_uniform(d_dst, n, (uint32_t)tensor, seed, dtype == DARTS_BF16,
+                                     (hipStream_t)stream);
+  return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
+}
+
+int darts_fill_kv_pool(void* d_k_pool, void* d_v_pool, int64_t n_pages, int32_t n_kv_heads,
+                       int32_t head_dim, uint64_t seed, int32_t dtype, void* stream) {
+  if (!d_k_pool || !d_v_pool || n_pages < 1 || n_kv_heads < 1 || head_dim % 8) return DARTS_EINVAL;
+  if (dtype != DARTS_F32 && dtype != DARTS_BF16) return DARTS_EINVAL;
+  hipError_t e = launch_fill_kv_pool(d_k_pool, d_v_pool, n_pages, n_kv_heads, head_dim, seed,
+                                     dtype == DARTS_BF16, (hipStream_t)stream);
+  return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
+}
+
+size_t darts_attn_workspace_bytes(int32_t n_rows, int32_t n_q_heads, int32_t n_kv_heads,
+                                  int32_t head_dim, int32_t max_ctx) {
+  if (n_rows < 1 || n_q_heads < 1 || n_kv_heads < 1 || max_ctx < 1) return 0;
+  return attn_workspace_bytes(n_rows, n_q_heads, n_kv_heads, head_dim, max_ctx);
+}
+
+int darts_attn_decode(const void* d_q, const void* d_k_pool, const void* d_v_pool,
+                           int64_t n_pages, const int32_t* d_page_table, int32_t pt_stride,
+                           const int32_t* d_ctx_len, int32_t n_rows, int32_t n_q_heads,
+                           int32_t n_kv_heads, int32_t head_dim, int32_t max_ctx, int32_t dtype,
+                           void* d_out, void* d_workspace, size_t workspace_bytes, void* stream) {
+  if (!d_q || !d_k_pool || !d_v_pool || !d_page_table || !d_ctx_len || !d_out) return DARTS_EINVAL;
+  if (n_rows < 0 || n_q_heads < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads ||
+      n_q_heads / n_kv_heads > 16 || max_ctx < 1 || n_pages < 1)
+    return DARTS_EINVAL;
+  if (!(head_dim == 32 || head_dim == 64 || head_dim == 128)) return DARTS_EINVAL;
+  if (dtype != DARTS_F32 && dtype != DARTS_BF16) return DARTS_EINVAL;
+  if (pt_stride < (max_ctx + kPage - 1) / kPage) return DARTS_EINVAL;
+  if (workspace_bytes < attn_workspace_bytes(n_rows, n_q_heads, n_kv_heads, head_dim, max_ctx))
+    return DARTS_EINVAL;
+  hipError_t e = launch_attention(d_q, d_k_pool, d_v_pool, n_pages, d_page_table, pt_stride, nullptr,
+                                  d_ctx_len, 0, 0, n_rows, n_q_heads, n_kv_heads, head_dim, max_ctx,
+                                  dtype == DARTS_BF16, d_out, d_workspace, workspace_bytes,
+                                  (hipStream_t)stream);
+  return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
+}
+
+int darts_sample(const void* d_logits, int32_t n_rows, int32_t vocab, int32_t dtype, uint64_t seed,
+                 const int32_t* d_traj, const int32_t* d_step, float temperature,
+                 const int32_t* d_force, int32_t* d_token, float* d_logprob, float* d_entropy,
+                 void* stream) {
+  if (!d_logits || !d_traj || !d_step || n_rows < 0 || vocab < 4 || vocab % 4 || !(temperature > 0.f))
+    return DARTS_EINVAL;
+  if (dtype != DARTS_F32 && dtype != DARTS_BF16) return DARTS_EINVAL;
+  SampleArgs a{};
+  a.logits = d_logits; a.n_rows = n_rows; a.vocab = vocab; a.bf16 = dtype == DARTS_BF16;
+  a.seed = seed; a.temperature = temperature; a.traj = d_traj; a.step = d_step; a.force = d_force;
+  a.token_out = d_token; a.logprob_out = d_logprob; a.entropy_out = d_entropy;
+  hipError_t e = launch_sample(a, (hipStream_t)stream);
+  return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
+}
+
+int darts_debug_gumbel(const float* d_u, float* d_g, int64_t n, void* stream) {
+  if ((!d_u || !d_g) && n > 0) return DARTS_EINVAL;
+  hipError_t e = launch_gumbel_map(d_u, d_g, n, (hipStream_t)stream);
+  return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
+}
+
+int darts_select_groups(uint8_t* d_status, const int32_t* d_len, const float* d_mean_lp,
+                        int32_t n_traj, int32_t m, int32_t k, int32_t L, int32_t m_up,
+                        int32_t early_stop, int32_t* d_kept, uint8_t* d_complete, void* stream) {
+  if (!d_status || !d_len || !d_mean_lp || !d_kept || !d_complete) return DARTS_EINVAL;
+  if (m < 1 || m > 64 || k < 1 || k > m || n_traj < 0 || n_traj % m) return DARTS_EINVAL;
+  if (m < m_up && (L < 1 || L >= k)) return DARTS_EINVAL;
+  GroupArgs a{};
+  a.status = d_status; a.len = d_len; a.mean_lp = d_mean_lp; a.n_groups = n_traj / m;
+  a.m = m; a.k = k; a.L = L; a.m_up = m_up; a.early_stop = early_stop ? 1 : 0;
+  a.kept = d_kept; a.complete = d_complete;
+  hipError_t e = launch_select(a, (hipStream_t)stream);
+  return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,404 @@
+// Paged GQA decode attention on gfx950.
+//
+// out[r][h] = sum_j softmax_j(q[r][h] . k_j / sqrt(hd)) v_j over the row's ctx
+// keys; key j sits in page page_table[pt_row][j/16], slot j%16, kv head
+// h / G (G = Hq/Hkv).
+//
+// Work unit = (row, kv head, chunk of C pages), one wavefront each, taken
+// from a device-built work list with a grid-stride loop (no host round trip,
+// no idle blocks for ragged contexts).  Per pair of pages (32 keys):
+//   S[16 x 32]  = Q[16 x hd] . K^T      MFMA 16x16x32 bf16 (the G query heads
+//                                       sharing the kv head fill rows 0..G-1)
+//   online softmax per head row (16-lane shuffles)
+//   O[16 x hd] += P[16 x 32] . V[32 x hd]   MFMA 16x16x32 bf16, P via LDS
+// K is read token-major straight into the MFMA B operand (16 B per lane);
+// V pages store 8 consecutive tokens of one dim contiguously, so the P.V
+// B operand is also one 16 B load per lane.  A row whose context spans
+// several chunks writes unnormalised partials (o, max, sum) and a combine
+// kernel merges them.
+#include <math.h>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace darts {
+
+struct CtxSpec {
+  const int32_t* ctx_len;  // per-row context, or NULL
+  int mod, base;           // ctx(r) = ctx_len ? ctx_len[r] : (mod ? r % mod : 0) + base
+  const int32_t* row_pt;   // page-table row of row r, or NULL (identity)
+  int max_ctx;             // contexts are clamped to max_ctx (memory safety)
+  int64_t n_pages;         // page ids are clamped into [0, n_pages)
+};
+__device__ __forceinline__ int ctx_of(const CtxSpec& c, int r) {
+  const int v = c.ctx_len ? c.ctx_len[r] : (c.mod ? r % c.mod : 0) + c.base;
+  return min(v, c.max_ctx);
+}
+__device__ __forceinline__ int clamp_page(const CtxSpec& c, int p) {
+  return (int)min((int64_t)max(p, 0), c.n_pages - 1);
+}
+
+// Single block: per-row chunk counts -> exclusive offsets and the work list.
+__global__ void attn_plan_kernel(CtxSpec cs, int n_rows, int chunk_tokens, int32_t* chunk_off,
+                                 int2* work, int32_t* info) {
+  __shared__ int32_t sums[1024];
+  __shared__ int32_t running;
+  const int tid = threadIdx.x;
+  if (tid == 0) running = 0;
+  __syncthreads();
+  for (int base = 0; base < n_rows; base += 1024) {
+    const int r = base + tid;
+    const int c = r < n_rows ? (ctx_of(cs, r) + chunk_tokens - 1) / chunk_tokens : 0;
+    sums[tid] = c;
+    __syncthreads();
+    for (int o = 1; o < 1024; o <<= 1) {     // inclusive Hillis-Steele scan
+      const int v = tid >= o ? sums[tid - o] : 0;
+      __syncthreads();
+      sums[tid] += v;
+      __syncthreads();
+    }
+    const int excl = running + sums[tid] - c;
+    if (r < n_rows) {
+      chunk_off[r] = excl;
+      for (int j = 0; j < c; ++j) work[excl + j] = make_int2(r, j);
+    }
+    __syncthreads();
+    if (tid == 1023) running += sums[1023];
+    __syncthreads();
+  }
+  if (tid == 0) info[0] = running;
+}
+
+template <int HD>
+__global__ void __launch_bounds__(256) attn_bf16_kernel(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ kpool, const bf16_t* __restrict__ vpool,
+    const int32_t* __restrict__ page_table, int pt_stride, CtxSpec cs, int hq, int hkv,
+    int chunk_pages, const int2* __restrict__ work, const int32_t* __restrict__ chunk_off,
+    const int32_t* __restrict__ info, float* __restrict__ ws_o, float2* __restrict__ ws_ml,
+    bf16_t* __restrict__ out) {
+  constexpr int NKK = HD / 32, NNB = HD / 16, PST = 40;   // P row stride (bf16), 80 B
+  __shared__ __attribute__((aligned(16))) bf16_t plds[4][16 * PST];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int G = hq / hkv;
+  const int quad = lane >> 4, col = lane & 15;
+  const float scale = 1.0f / sqrtf((float)HD);
+  const int total = info[0] * hkv;
+  bf16_t* P = plds[w];
+  for (int item = blockIdx.x * 4 + w; item < total; item += gridDim.x * 4) {
+    const int wi = item / hkv, kvh = item - wi * hkv;
+    const int2 rc = work[wi];
+    const int row = rc.x, chunk = rc.y;
+    const int ctx = ctx_of(cs, row);
+    const int ptr = cs.row_pt ? cs.row_pt[row] : row;
+    const int32_t* pt = page_table + (int64_t)ptr * pt_stride;
+    const int npg = (ctx + kPage - 1) / kPage;
+    const int pbeg = chunk * chunk_pages;
+    const int pend = min(pbeg + chunk_pages, npg);
+
+    bf16x8_t qa[NKK];
+    {
+      const bool valid = col < G;
+      const bf16_t* qrow = q + ((int64_t)row * hq + kvh * G + (valid ? col : 0)) * HD + quad * 8;
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk) {
+        u32x4_t v = valid ? *(const u32x4_t*)(qrow + 32 * kk) : (u32x4_t){0u, 0u, 0u, 0u};
+        qa[kk] = __builtin_bit_cast(bf16x8_t, v);
+      }
+    }
+    float mrun[4], lpart[4];
+    f32x4_t O[NNB];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) { mrun[i] = -INFINITY; lpart[i] = 0.f; }
+#pragma unroll
+    for (int nb = 0; nb < NNB; ++nb) O[nb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+
+    for (int p = pbeg; p < pend; p += 2) {
+      const int pa = clamp_page(cs, pt[p]);
+      const bool hasb = (p + 1) < pend;
+      const int pb = hasb ? clamp_page(cs, pt[p + 1]) : pa;
+      bf16x8_t ka[NKK], kb[NKK], vv[NNB];
+      const bf16_t* kpa = kpool + k_off(pa, kvh, col, quad * 8, hkv, HD);
+      const bf16_t* kpb = kpool + k_off(pb, kvh, col, quad * 8, hkv, HD);
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk) {
+        ka[kk] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(kpa + 32 * kk));
+        kb[kk] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(kpb + 32 * kk));
+      }
+      {
+        const int vpage = quad < 2 ? pa : pb;
+        const int slot0 = (quad & 1) * 8;
+        const bf16_t* vb = vpool + v_off(vpage, kvh, slot0, col, hkv, HD);
+#pragma unroll
+        for (int nb = 0; nb < NNB; ++nb)
+          vv[nb] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(vb + nb * 16 * 8));
+      }
+      f32x4_t sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk) {
+        sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kk], ka[kk], sa, 0, 0, 0);
+        sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kk], kb[kk], sb, 0, 0, 0);
+      }
+      // lane holds S[head 4*quad+i][token p*16+col] (sa) and [(p+1)*16+col] (sb)
+      const bool va = p * kPage + col < ctx;
+      const bool vb2 = hasb && ((p + 1) * kPage + col < ctx);
+      float pva[4], pvb[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float s1 = va ? sa[i] * scale : -INFINITY;
+        const float s2 = vb2 ? sb[i] * scale : -INFINITY;
+        float mx = fmaxf(s1, s2);
+        mx = fmaxf(mx, __shfl_xor(mx, 1, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 2, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 4, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 8, 64));
+        const float mnew = fmaxf(mrun[i], mx);
+        const float alpha = __expf(mrun[i] - mnew);
+        // the denominator sums the same bf16-rounded weights that multiply V
+        pva[i] = bf16_to_f32(f32_to_bf16(__expf(s1 - mnew)));
+        pvb[i] = bf16_to_f32(f32_to_bf16(__expf(s2 - mnew)));
+        lpart[i] = lpart[i] * alpha + pva[i] + pvb[i];
+        mrun[i] = mnew;
+#pragma unroll
+        for (int nb = 0; nb < NNB; ++nb) O[nb][i] *= alpha;
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        P[(4 * quad + i) * PST + col] = f32_to_bf16(pva[i]);
+        P[(4 * quad + i) * PST + 16 + col] = f32_to_bf16(pvb[i]);
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      const bf16x8_t pa8 = *(const bf16x8_t*)(&P[col * PST + quad * 8]);
+#pragma unroll
+      for (int nb = 0; nb < NNB; ++nb) O[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa8, vv[nb], O[nb], 0, 0, 0);
+      __builtin_amdgcn_wave_barrier();   // P is rewritten next iteration
+    }
+    // finish: per head row, total softmax denominator over the 16 lanes
+    const int nch = (npg + chunk_pages - 1) / chunk_pages;
+    const int cid = chunk_off[row] + chunk;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float l = lpart[i];
+      l += __shfl_xor(l, 1, 64);
+      l += __shfl_xor(l, 2, 64);
+      l += __shfl_xor(l, 4, 64);
+      l += __shfl_xor(l, 8, 64);
+      const int h = 4 * quad + i;
+      if (h >= G) continue;
+      const int qh = kvh * G + h;
+      if (nch == 1) {
+        const float inv = 1.0f / l;
+        bf16_t* orow = out + ((int64_t)row * hq + qh) * HD + col;
+#pragma unroll
+        for (int nb = 0; nb < NNB; ++nb) orow[nb * 16] = f32_to_bf16(O[nb][i] * inv);
+      } else {
+        float* po = ws_o + ((int64_t)cid * hq + qh) * HD + col;
+#pragma unroll
+        for (int nb = 0; nb < NNB; ++nb) po[nb * 16] = O[nb][i];
+        if (col == 0) ws_ml[(int64_t)cid * hq + qh] = make_float2(mrun[i], l);
+      }
+    }
+  }
+}
+
+// fp32 attention (fp32 models): one wavefront per (row, q head, chunk).
+template <int HD>
+__global__ void __launch_bounds__(256) attn_f32_kernel(
+    const float* __restrict__ q, const float* __restrict__ kpool, const float* __restrict__ vpool,
+    const int32_t* __restrict__ page_table, int pt_stride, CtxSpec cs, int hq, int hkv,
+    int chunk_pages, const int2* __restrict__ work, const int32_t* __restrict__ chunk_off,
+    const int32_t* __restrict__ info, float* __restrict__ ws_o, float2* __restrict__ ws_ml,
+    float* __restrict__ out) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int G = hq / hkv;
+  const float scale = 1.0f / sqrtf((float)HD);
+  const int total = info[0] * hq;
+  for (int item = blockIdx.x * 4 + w; item < total; item += gridDim.x * 4) {
+    const int wi = item / hq, qh = item - wi * hq, kvh = qh / G;
+    const int2 rc = work[wi];
+    const int row = rc.x, chunk = rc.y;
+    const int ctx = ctx_of(cs, row);
+    const int ptr = cs.row_pt ? cs.row_pt[row] : row;
+    const int32_t* pt = page_table + (int64_t)ptr * pt_stride;
+    const int tbeg = chunk * chunk_pages * kPage;
+    const int tend = min(tbeg + chunk_pages * kPage, ctx);
+    const float* qv = q + ((int64_t)row * hq + qh) * HD;
+    float qreg[HD];
+#pragma unroll
+    for (int d = 0; d < HD; ++d) qreg[d] = qv[d];
+    float m = -INFINITY, l = 0.f, o[HD];
+#pragma unroll
+    for (int d = 0; d < HD; ++d) o[d] = 0.f;
+    for (int j = tbeg + lane; j < tend; j += 64) {
+      const int page = clamp_page(cs, pt[j / kPage]), slot = j % kPage;
+      const float* kp = kpool + k_off(page, kvh, slot, 0, hkv, HD);
+      float s = 0.f;
+#pragma unroll
+      for (int d = 0; d < HD; ++d) s = fmaf(qreg[d], kp[d], s);
+      s *= scale;
+      const float mn = fmaxf(m, s);
+      const float a = __expf(m - mn), pj = __expf(s - mn);
+      l = l * a + pj;
+#pragma unroll
+      for (int d = 0; d < HD; ++d) o[d] = o[d] * a + pj * vpool[v_off(page, kvh, slot, d, hkv, HD)];
+      m = mn;
+    }
+    const float mw = wave_max(m);
+    const float a = (m == -INFINITY) ? 0.f : __expf(m - mw);
+    const float lw = wave_sum(l * a);
+    const int nch = ((ctx + kPage - 1) / kPage + chunk_pages - 1) / chunk_pages;
+    const int cid = chunk_off[row] + chunk;
+#pragma unroll
+    for (int d = 0; d < HD; ++d) {
+      const float v = wave_sum(o[d] * a);
+      if ((d & 63) == lane) {
+        if (nch == 1) out[((int64_t)row * hq + qh) * HD + d] = v / lw;
+        else ws_o[((int64_t)cid * hq + qh) * HD + d] = v;
+      }
+    }
+    if (nch > 1 && lane == 0) ws_ml[(int64_t)cid * hq + qh] = make_float2(mw, lw);
+  }
+}
+
+// Merge chunk partials: one wavefront per (row, q head); rows with a single
+// chunk were written directly by the attention kernel.
+template <typename OUT>
+__global__ void attn_combine_kernel(CtxSpec cs, int n_rows, int hq, int hd, int chunk_tokens,
+                                    const int32_t* __restrict__ chunk_off,
+                                    const float* __restrict__ ws_o, const float2* __restrict__ ws_ml,
+                                    OUT* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (item >= n_rows * hq) return;
+  const int row = item / hq, qh = item % hq;
+  const int ctx = ctx_of(cs, row);
+  const int nch = (ctx + chunk_tokens - 1) / chunk_tokens;
+  if (nch <= 1) return;
+  const int c0 = chunk_off[row];
+  float M = -INFINITY;
+  for (int c = 0; c < nch; ++c) M = fmaxf(M, ws_ml[(int64_t)(c0 + c) * hq + qh].x);
+  float L = 0.f;
+  for (int c = 0; c < nch; ++c) {
+    const float2 ml = ws_ml[(int64_t)(c0 + c) * hq + qh];
+    L += ml.y * __expf(ml.x - M);
+  }
+  const float invL = 1.0f / L;
+  for (int d = lane; d < hd; d += 64) {
+    float acc = 0.f;
+    for (int c = 0; c < nch; ++c) {
+      const float2 ml = ws_ml[(int64_t)(c0 + c) * hq + qh];
+      acc += ws_o[((int64_t)(c0 + c) * hq + qh) * hd + d] * __expf(ml.x - M);
+    }
+    const float v = acc * invL;
+    if constexpr (sizeof(OUT) == 2) out[((int64_t)row * hq + qh) * hd + d] = f32_to_bf16(v);
+    else out[((int64_t)row * hq + qh) * hd + d] = v;
+  }
+}
+
+static int choose_chunk_pages(int n_rows, int hkv, int max_ctx) {
+  const int64_t pages = (int64_t)n_rows * ((max_ctx + kPage - 1) / kPage) * hkv;
+  int c = 2;
+  while (c < 64 && pages / c > 8192) c *= 2;
+  return c;
+}
+
+struct AttnWs {
+  int32_t* chunk_off; int2* work; int32_t* info; float* ws_o; float2* ws_ml;
+};
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+static size_t ws_layout(int n_rows, int hq, int hkv, int hd, int max_ctx, char* base, AttnWs* w) {
+  const int cp = choose_chunk_pages(n_rows, hkv, max_ctx);
+  const int64_t maxch = (int64_t)n_rows * ((max_ctx + cp * kPage - 1) / (cp * kPage));
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = align256(off + bytes); return base ? base + o : nullptr; };
+  char* a = take((size_t)n_rows * 4);
+  char* b = take((size_t)maxch * sizeof(int2));
+  char* c = take(64);
+  char* d = take((size_t)maxch * hq * hd * sizeof(float));
+  char* e = take((size_t)maxch * hq * sizeof(float2));
+  if (w) {
+    w->chunk_off = (int32_t*)a; w->work = (int2*)b; w->info = (int32_t*)c;
+    w->ws_o = (float*)d; w->ws_ml = (float2*)e;
+  }
+  return off;
+}
+
+size_t attn_workspace_bytes(int n_rows, int hq, int hkv, int hd, int max_ctx) {
+  return ws_layout(n_rows, hq, hkv, hd, max_ctx, nullptr, nullptr);
+}
+
+template <int HD>
+static void attn_bf16_go(dim3 grid, hipStream_t st, const void* q, const void* k, const void* v,
+                         const int32_t* pt, int pts, CtxSpec cs, int hq, int hkv, int cp, AttnWs w,
+                         void* out) {
+  hipLaunchKernelGGL(attn_bf16_kernel<HD>, grid, dim3(256), 0, st, (const bf16_t*)q,
+                     (const bf16_t*)k, (const bf16_t*)v, pt, pts, cs, hq, hkv, cp, w.work,
+                     w.chunk_off, w.info, w.ws_o, w.ws_ml, (bf16_t*)out);
+}
+template <int HD>
+static void attn_f32_go(dim3 grid, hipStream_t st, const void* q, const void* k, const void* v,
+                        const int32_t* pt, int pts, CtxSpec cs, int hq, int hkv, int cp, AttnWs w,
+                        void* out) {
+  hipLaunchKernelGGL(attn_f32_kernel<HD>, grid, dim3(256), 0, st, (const float*)q,
+                     (const float*)k, (const float*)v, pt, pts, cs, hq, hkv, cp, w.work,
+                     w.chunk_off, w.info, w.ws_o, w.ws_ml, (float*)out);
+}
+
+hipError_t launch_attention_spec(const void* q, const void* k_pool, const void* v_pool,
+                                 const int32_t* page_table, int pt_stride, CtxSpec cs, int n_rows,
+                                 int hq, int hkv, int hd, int max_ctx, bool bf16, void* out,
+                                 void* ws, size_t ws_bytes, hipStream_t st) {
+  if (n_rows <= 0) return hipSuccess;
+  cs.max_ctx = max_ctx;
+  AttnWs w;
+  const size_t need = ws_layout(n_rows, hq, hkv, hd, max_ctx, (char*)ws, &w);
+  if (ws == nullptr || ws_bytes < need) return hipErrorInvalidValue;
+  const int cp = choose_chunk_pages(n_rows, hkv, max_ctx);
+  hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(1024), 0, st, cs, n_rows, cp * kPage,
+                     w.chunk_off, w.work, w.info);
+  const int64_t maxch = (int64_t)n_rows * ((max_ctx + cp * kPage - 1) / (cp * kPage));
+  const int64_t items = maxch * (bf16 ? hkv : hq);
+  int64_t blocks = (items + 3) / 4;
+  if (blocks > 2048) blocks = 2048;
+  if (blocks < 1) blocks = 1;
+  const dim3 grid((unsigned)blocks);
+  if (bf16) {
+    if (hd == 128) attn_bf16_go<128>(grid, st, q, k_pool, v_pool, page_table, pt_stride, cs, hq, hkv, cp, w, out);
+    else if (hd == 64) attn_bf16_go<64>(grid, st, q, k_pool, v_pool, page_table, pt_stride, cs, hq, hkv, cp, w, out);
+    else if (hd == 32) attn_bf16_go<32>(grid, st, q, k_pool, v_pool, page_table, pt_stride, cs, hq, hkv, cp, w, out);
+    else return hipErrorInvalidValue;
+  } else {
+    if (hd == 128) attn_f32_go<128>(grid, st, q, k_pool, v_pool, page_table, pt_stride, cs, hq, hkv, cp, w, out);
+    else if (hd == 64) attn_f32_go<64>(grid, st, q, k_pool, v_pool, page_table, pt_stride, cs, hq, hkv, cp, w, out);
+    else if (hd == 32) attn_f32_go<32>(grid, st, q, k_pool, v_pool, page_table, pt_stride, cs, hq, hkv, cp, w, out);
+    else return hipErrorInvalidValue;
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if ((max_ctx + cp * kPage - 1) / (cp * kPage) > 1) {
+    const int64_t nb = ((int64_t)n_rows * hq + 3) / 4;
+    if (bf16)
+      hipLaunchKernelGGL(attn_combine_kernel<bf16_t>, dim3((unsigned)nb), dim3(256), 0, st, cs,
+                         n_rows, hq, hd, cp * kPage, w.chunk_off, w.ws_o, w.ws_ml, (bf16_t*)out);
+    else
+      hipLaunchKernelGGL(attn_combine_kernel<float>, dim3((unsigned)nb), dim3(256), 0, st, cs,
+                         n_rows, hq, hd, cp * kPage, w.chunk_off, w.ws_o, w.ws_ml, (float*)out);
+    e = hipGetLastError();
+  }
+  return e;
+}
+
+hipError_t launch_attention(const void* q, const void* k_pool, const void* v_pool,
+                            int64_t n_pages, const int32_t* page_table, int pt_stride,
+                            const int32_t* row_pt, const int32_t* ctx_len, int ctx_mod,
+                            int ctx_base, int n_rows, int hq, int hkv, int hd, int max_ctx,
+                            bool bf16, void* out, void* ws, size_t ws_bytes, hipStream_t st) {
+  CtxSpec cs;
+  cs.ctx_len = ctx_len; cs.mod = ctx_mod; cs.base = ctx_base; cs.row_pt = row_pt;
+  cs.max_ctx = max_ctx; cs.n_pages = n_pages;
+  return launch_attention_spec(q, k_pool, v_pool, page_table, pt_stride, cs, n_rows, hq, hkv, hd,
+                               max_ctx, bf16, out, ws, ws_bytes, st);
+}
+
+}  // namespace darts

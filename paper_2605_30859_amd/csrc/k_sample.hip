@@ -1,0 +1,175 @@
+// Fused sampler: one pass over a logits row computes
+//   * the Gumbel-max token  argmax_i fl32(z_i + g_i),  z = logits / T,
+//     g_i = -ln(-ln u_i), u_i from Philox(counter=(i>>2, traj, step, TAG_SAMPLE),
+//     key=seed), ties to the smallest index;
+//   * log-sum-exp and entropy with an online (max, sum e^(z-m), sum e^(z-m)(z-m))
+//     state merged across lanes and wavefronts;
+// then the log-prob of the taken token.  In the stateful form the same block
+// applies the exogenous termination rule (forced end-of-sequence length,
+// truncation at cap) and accumulates the trajectory's score.
+#include <math.h>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace darts {
+
+struct SoftState {
+  float m, s, t;   // max, sum e^(z-m), sum e^(z-m)(z-m)
+};
+__device__ __forceinline__ SoftState soft_merge(SoftState a, SoftState b) {
+  if (a.m == -INFINITY) return b;
+  if (b.m == -INFINITY) return a;
+  const float m = fmaxf(a.m, b.m);
+  const float ea = __expf(a.m - m), eb = __expf(b.m - m);
+  SoftState r;
+  r.m = m;
+  r.s = a.s * ea + b.s * eb;
+  r.t = ea * (a.t + a.s * (a.m - m)) + eb * (b.t + b.s * (b.m - m));
+  return r;
+}
+struct Best {
+  float v;
+  int i;
+};
+__device__ __forceinline__ Best best_merge(Best a, Best b) {
+  if (b.v > a.v || (b.v == a.v && b.i < a.i)) return b;
+  return a;
+}
+
+template <bool BF16>
+__device__ __forceinline__ void load4(const void* row, int j, float z[4]) {
+  if (BF16) {
+    const uint2 v = ((const uint2*)row)[j];
+    z[0] = __uint_as_float(v.x << 16);
+    z[1] = __uint_as_float(v.x & 0xffff0000u);
+    z[2] = __uint_as_float(v.y << 16);
+    z[3] = __uint_as_float(v.y & 0xffff0000u);
+  } else {
+    const float4 v = ((const float4*)row)[j];
+    z[0] = v.x; z[1] = v.y; z[2] = v.z; z[3] = v.w;
+  }
+}
+
+template <bool BF16, bool STATEFUL>
+__global__ void __launch_bounds__(256) sample_kernel(SampleArgs a) {
+  __shared__ SoftState ss[4];
+  __shared__ Best sb[4];
+  const int r = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int lrow = a.row_logit ? a.row_logit[r] : (a.logit_div > 0 ? r / a.logit_div : r);
+  const void* row = BF16 ? (const void*)((const bf16_t*)a.logits + (int64_t)lrow * a.vocab)
+                         : (const void*)((const float*)a.logits + (int64_t)lrow * a.vocab);
+  const int g = a.traj[r];
+  const int step = STATEFUL ? a.gen[g] : a.step[r];
+  const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
+  const bool tscale = a.temperature != 1.0f;
+  SoftState st = {-INFINITY, 0.f, 0.f};
+  Best best = {-INFINITY, 0x7fffffff};
+  const int n4 = a.vocab >> 2;
+  for (int j = tid; j < n4; j += 256) {
+    float z[4];
+    load4<BF16>(row, j, z);
+    if (tscale) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) z[e] = __fdiv_rn(z[e], a.temperature);
+    }
+    const Philox4 p = philox4x32_10((uint32_t)j, (uint32_t)g, (uint32_t)step, kTagSample, k0, k1);
+    float lm = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
+    if (lm > st.m) {
+      if (st.s > 0.f) {   // rescale the running sums to the new maximum
+        const float sc = __expf(st.m - lm);
+        st.t = sc * (st.t + st.s * (st.m - lm));
+        st.s = st.s * sc;
+      }
+      st.m = lm;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float d = z[e] - st.m;
+      const float ez = __expf(d);
+      st.s += ez;
+      st.t = fmaf(ez, d, st.t);
+      const float sc = z[e] + gumbel_of(open_unit(p.x[e]));
+      if (sc > best.v) { best.v = sc; best.i = 4 * j + e; }
+    }
+  }
+  // wavefront merge
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    SoftState other = {__shfl_xor(st.m, o, 64), __shfl_xor(st.s, o, 64), __shfl_xor(st.t, o, 64)};
+    st = soft_merge(st, other);
+    Best ob = {__shfl_xor(best.v, o, 64), __shfl_xor(best.i, o, 64)};
+    best = best_merge(best, ob);
+  }
+  if ((tid & 63) == 0) { ss[tid >> 6] = st; sb[tid >> 6] = best; }
+  __syncthreads();
+  if (tid != 0) return;
+  st = soft_merge(soft_merge(ss[0], ss[1]), soft_merge(ss[2], ss[3]));
+  best = best_merge(best_merge(sb[0], sb[1]), best_merge(sb[2], sb[3]));
+  const float lse = st.m + logf(st.s);
+  const float ent = logf(st.s) - st.t / st.s;
+  const int sampled = best.i;
+  int taken = sampled;
+  uint8_t fin = 0;
+  if (STATEFUL) {
+    const int s_new = step + 1;
+    const int d = a.forced_len[g];
+    if (d <= a.cap && s_new == d) { taken = a.eos; fin = 1; }
+    else {
+      if (a.force && a.force[g] >= 0) taken = a.force[g];
+      if (s_new >= a.cap) fin = 2;
+    }
+  } else if (a.force && a.force[r] >= 0) {
+    taken = a.force[r];
+  }
+  if (taken < 0 || taken >= a.vocab) taken = sampled;
+  float zt;
+  if (BF16) zt = bf16_to_f32(((const bf16_t*)row)[taken]);
+  else zt = ((const float*)row)[taken];
+  if (tscale) zt = __fdiv_rn(zt, a.temperature);
+  const float lp = zt - lse;
+  if (a.token_out) a.token_out[r] = taken;
+  if (a.sampled_out) a.sampled_out[r] = sampled;
+  if (a.logprob_out) a.logprob_out[r] = lp;
+  if (a.entropy_out) a.entropy_out[r] = ent;
+  if (STATEFUL) {
+    a.gen[g] = step + 1;
+    a.sum_lp[g] = a.sum_lp[g] + lp;
+    a.last_tok[g] = taken;
+    if (fin) a.status[g] = fin;
+    if (a.finished_out) a.finished_out[r] = fin;
+    if (a.traj_out) a.traj_out[r] = g;
+  }
+}
+
+hipError_t launch_sample(const SampleArgs& a, hipStream_t st) {
+  if (a.n_rows <= 0) return hipSuccess;
+  const bool stateful = a.gen != nullptr;
+  const dim3 grid(a.n_rows), blk(256);
+  if (a.bf16) {
+    if (stateful) hipLaunchKernelGGL((sample_kernel<true, true>), grid, blk, 0, st, a);
+    else hipLaunchKernelGGL((sample_kernel<true, false>), grid, blk, 0, st, a);
+  } else {
+    if (stateful) hipLaunchKernelGGL((sample_kernel<false, true>), grid, blk, 0, st, a);
+    else hipLaunchKernelGGL((sample_kernel<false, false>), grid, blk, 0, st, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace darts
+
+namespace darts {
+__global__ void gumbel_map_kernel(const float* __restrict__ u, float* __restrict__ g, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    g[i] = gumbel_of(u[i]);
+}
+hipError_t launch_gumbel_map(const float* u, float* g, int64_t n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 16384) blocks = 16384;
+  hipLaunchKernelGGL(gumbel_map_kernel, dim3((unsigned)blocks), dim3(256), 0, st, u, g, n);
+  return hipGetLastError();
+}
+}  // namespace darts

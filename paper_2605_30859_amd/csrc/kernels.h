@@ -1,0 +1,101 @@
+// Host launchers of the gfx950 kernels (one translation unit per family).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+namespace darts {
+
+// ---- init (k_init.hip)
+// Row mapping of a logical [n_out][n_in] tensor into its physical matrix:
+// phys_row = (r / grp_outer) * stride_outer + ((r % grp_outer) / grp_inner) * stride_inner
+//            + (r % grp_outer) % grp_inner + row_off
+struct RowMap {
+  int64_t grp_outer, stride_outer, grp_inner, stride_inner, row_off;
+};
+RowMap rowmap_plain(int64_t n_out, int64_t row_off);
+hipError_t launch_init_weights(void* dst, bool bf16, int64_t n_out, int64_t n_in, int64_t fan_in,
+                               uint32_t tensor_id, uint32_t layer, uint64_t seed, RowMap map,
+                               hipStream_t st);
+hipError_t launch_rope_table(float2* table, int max_pos, int hd, double theta, hipStream_t st);
+hipError_t launch_fill_uniform(void* dst, uint64_t n, uint32_t tensor, uint64_t seed, bool bf16,
+                               hipStream_t st);
+hipError_t launch_fill_kv_pool(void* k, void* v, int64_t n_pages, int hkv, int hd, uint64_t seed,
+                               bool bf16, hipStream_t st);
+hipError_t launch_iota_perm(int32_t* stack, int64_t n, uint64_t perm_seed, bool permute,
+                            hipStream_t st);
+
+// ---- GEMM (k_gemm.hip): C[M,N] (op)= A[M,K] * W[N,K]^T
+enum Epi { EPI_F32 = 0, EPI_BF16 = 1, EPI_ADD_F32 = 2, EPI_SWIGLU = 3 };
+size_t gemm_workspace_bytes(int M, int N, int K);
+hipError_t launch_gemm(bool bf16, const void* A, int lda, const void* W, int ldw, void* C, int ldc,
+                       int M, int N, int K, int epi, void* ws, size_t ws_bytes, hipStream_t st);
+
+// ---- elementwise (k_elem.hip)
+hipError_t launch_embed_v(const void* table, bool bf16, const int32_t* tokens,
+                          const int32_t* rows_traj, int n_rows, int d, int vocab, float* x,
+                          hipStream_t st);
+hipError_t launch_rmsnorm(const float* x, int n_rows, int d, float eps, void* out, bool bf16,
+                          hipStream_t st);
+// pos(r) = pos_mod ? r % pos_mod + pos_base : pos_base
+hipError_t launch_rope_append2(const float* qkv, int n_rows, int hq, int hkv, int hd,
+                               const int32_t* row_pt, int pos_mod, int pos_base,
+                               const int32_t* page_table, int pt_stride, int64_t n_pages,
+                               const float2* rope, void* q_out, void* k_pool, void* v_pool,
+                               bool bf16, hipStream_t st);
+hipError_t launch_gather_rows(const float* src, const int32_t* rows, int n, int d, float* dst,
+                              hipStream_t st);
+
+// ---- attention (k_attn.hip)
+size_t attn_workspace_bytes(int n_rows, int hq, int hkv, int hd, int max_ctx);
+// ctx(r) = ctx_len ? ctx_len[r] : (ctx_mod ? r % ctx_mod : 0) + ctx_base
+hipError_t launch_attention(const void* q, const void* k_pool, const void* v_pool,
+                            int64_t n_pages, const int32_t* page_table, int pt_stride,
+                            const int32_t* row_pt, const int32_t* ctx_len, int ctx_mod,
+                            int ctx_base, int n_rows, int hq, int hkv, int hd, int max_ctx,
+                            bool bf16, void* out, void* ws, size_t ws_bytes, hipStream_t st);
+
+// ---- sampler (k_sample.hip)
+struct SampleArgs {
+  const void* logits; int n_rows; int vocab; bool bf16; uint64_t seed; float temperature;
+  const int32_t* row_logit;   // row r reads logits row row_logit[r], else r / logit_div, else r
+  int logit_div;
+  const int32_t* traj;        // [n_rows] trajectory id (counter word 1)
+  const int32_t* step;        // NULL: use per-trajectory gen count (stateful)
+  const int32_t* force;       // NULL or indexed by row (stateless) / by traj (stateful)
+  int32_t* token_out; int32_t* sampled_out; float* logprob_out; float* entropy_out;
+  // stateful termination (all NULL for the stateless sampler)
+  int32_t* gen; float* sum_lp; uint8_t* status; int32_t* last_tok; const int32_t* forced_len;
+  uint8_t* finished_out; int32_t* traj_out; int cap; int eos;
+  int64_t* tokens_counter;
+};
+hipError_t launch_sample(const SampleArgs& a, hipStream_t st);
+hipError_t launch_gumbel_map(const float* u, float* g, int64_t n, hipStream_t st);
+
+// ---- selection / pages (k_select.hip)
+struct GroupArgs {
+  uint8_t* status; const int32_t* len; const float* sum_lp; const float* mean_lp;
+  int n_groups; int m; int k; int L; int m_up; int early_stop; int step;
+  int32_t* kept; uint8_t* complete;
+};
+hipError_t launch_select(const GroupArgs& a, hipStream_t st);
+struct PruneArgs {
+  uint8_t* status; const int32_t* gen; const float* sum_lp; uint8_t* freed; int32_t* refcnt;
+  uint8_t* group_done; int32_t* done_step; int32_t* kept;
+  int n_groups, m, k, L, m_up, early_stop, step;
+  const int32_t* page_table; int pt_stride; int prompt_pages;
+  int32_t* free_stack; int32_t* free_top;     // free_top: device counter
+  int n_pages;                                // stack capacity
+  int32_t* grp_cnt; int32_t* grp_rel; int32_t* trj_cnt;   // scratch [n_groups] x2, [n_groups*m]
+  const int32_t* live_in; int n_live_in; int32_t* live_out;
+  int32_t* info;    // out: [0] n_live, [1] n_done, [2] free_top
+};
+hipError_t launch_prune(const PruneArgs& a, hipStream_t st);
+hipError_t launch_alloc_pages(const int32_t* live, int n_live, const int32_t* gen, int prompt_pages,
+                              int32_t* page_table, int pt_stride, int32_t* free_stack,
+                              int32_t* free_top, int32_t* info, hipStream_t st);
+hipError_t launch_prefill_pages(int n_prompts, int m, int prompt_pages, int32_t* page_table,
+                                int pt_stride, int32_t* free_stack, int32_t* free_top,
+                                int32_t* refcnt, hipStream_t st);
+
+}  // namespace darts

@@ -1,0 +1,231 @@
+"""Kernel parity on the GPU through the C ABI: Gumbel map (bit-exact over all
+2^23 inputs), fused sampler (tokens bit-exact, log-prob/entropy within
+tolerance), paged decode attention, selection (bit-exact kept sets).  Every
+expected value comes from oracle/ on the same seeded inputs."""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle.fp32math import gumbel_f32
+from oracle.sampler import sample_row
+from oracle.selection import group_decision, LIVE, EOS, TRUNC, ABORTED
+from oracle import sweep as OS
+from workload import sweep_attention_inputs, sweep_sampler_logits, sweep_selection_inputs
+from workload.gen import sweep_page_table, f32_from_bf16_bits
+from workload.configs import SWEEP
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _b():
+    from paper_2605_30859_amd import binding
+    binding.load_library()
+    return binding
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def test_gumbel_map_bit_exact_all_u():
+    B = _b()
+    say("gumbel map: 2^23 inputs")
+    k = np.arange(1 << 23, dtype=np.uint64) * 2 + 1
+    u = (k.astype(np.float32) * np.float32(2.0 ** -24)).astype(np.float32)
+    ref = gumbel_f32(u)
+    ud = torch.from_numpy(u).to(DEV)
+    gd = torch.empty_like(ud)
+    B.darts_debug_gumbel(ud, gd)
+    torch.cuda.synchronize()
+    got = gd.cpu().numpy()
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+
+
+def _bf16_tensor(bits):
+    return torch.from_numpy(bits.view(np.int16)).to(DEV).view(torch.bfloat16)
+
+
+@pytest.mark.parametrize("dtype,rows,vocab,temp", [("bf16", 64, 4096, 1.0), ("f32", 48, 512, 1.0),
+                                                  ("f32", 33, 1000, 0.7), ("bf16", 7, 32000, 1.3)])
+def test_sampler_small(dtype, rows, vocab, temp):
+    B = _b()
+    say(f"sampler {dtype} rows={rows} V={vocab} T={temp}")
+    bits = sweep_sampler_logits(rows=rows, vocab=vocab, seed=5)
+    l32 = f32_from_bf16_bits(bits)
+    if dtype == "bf16":
+        logits = _bf16_tensor(bits)
+        dt = B.DARTS_BF16
+    else:
+        rng = np.random.default_rng(11)
+        l32 = (l32 + rng.normal(0, 1e-3, l32.shape)).astype(np.float32)   # not bf16-exact
+        logits = torch.from_numpy(l32).to(DEV)
+        dt = B.DARTS_F32
+    traj = torch.arange(rows, dtype=torch.int32, device=DEV) * 7 + 3
+    step = torch.arange(rows, dtype=torch.int32, device=DEV) % 5
+    force = torch.full((rows,), -1, dtype=torch.int32, device=DEV)
+    force[::3] = torch.arange(0, rows, 3, dtype=torch.int32, device=DEV) % vocab
+    tok = torch.empty(rows, dtype=torch.int32, device=DEV)
+    lp = torch.empty(rows, dtype=torch.float32, device=DEV)
+    ent = torch.empty(rows, dtype=torch.float32, device=DEV)
+    seed = 1234567
+    B.darts_sample(logits, dt, seed, traj, step, temp, force, tok, lp, ent)
+    torch.cuda.synchronize()
+    tok, lp, ent = tok.cpu().numpy(), lp.cpu().numpy(), ent.cpu().numpy()
+    tr, sp, fo = traj.cpu().numpy(), step.cpu().numpy(), force.cpu().numpy()
+    for r in range(rows):
+        stok, slp, sent = sample_row(l32[r], temp, int(tr[r]), int(sp[r]), seed, int(fo[r]))
+        taken = stok if fo[r] < 0 else int(fo[r])
+        assert tok[r] == taken, (r, tok[r], taken)
+        assert abs(lp[r] - slp) < 1e-4, (r, lp[r], slp)
+        assert abs(ent[r] - sent) < 1e-4, (r, ent[r], sent)
+
+
+def test_sampler_full_sweep_size():
+    """1024 x 151936 bf16 logits ~ N(0, 3) (the sweep's shape); every row's
+    token checked bit-exact on a sample of rows."""
+    B = _b()
+    rows, vocab = SWEEP["samp_rows"], SWEEP["samp_vocab"]
+    say(f"sampler sweep {rows}x{vocab}")
+    bits = sweep_sampler_logits()
+    logits = _bf16_tensor(bits)
+    traj = torch.arange(rows, dtype=torch.int32, device=DEV)
+    step = torch.zeros(rows, dtype=torch.int32, device=DEV)
+    tok = torch.empty(rows, dtype=torch.int32, device=DEV)
+    lp = torch.empty(rows, dtype=torch.float32, device=DEV)
+    ent = torch.empty(rows, dtype=torch.float32, device=DEV)
+    seed = SWEEP["seed"]
+    B.darts_sample(logits, B.DARTS_BF16, seed, traj, step, 1.0, None, tok, lp, ent)
+    torch.cuda.synchronize()
+    tok, lp, ent = tok.cpu().numpy(), lp.cpu().numpy(), ent.cpu().numpy()
+    l32 = None
+    for r in list(range(0, rows, 97)) + [rows - 1]:
+        row = f32_from_bf16_bits(bits[r])
+        stok, slp, sent = sample_row(row, 1.0, r, 0, seed)
+        assert tok[r] == stok
+        assert abs(lp[r] - slp) < 1e-3 and abs(ent[r] - sent) < 1e-3
+    # properties at any size: entropy within [0, ln V], log-prob <= 0
+    assert (ent >= 0).all() and (ent <= math.log(vocab) + 1e-3).all()
+    assert (lp <= 1e-6).all()
+
+
+def _attn_case(rows, hq, hkv, hd, ctx, dtype, seed, spare=3):
+    B = _b()
+    rng = np.random.default_rng(seed)
+    pt, n_pages = sweep_page_table(ctx, 16, rng, spare=spare)
+    max_ctx = int(ctx.max())
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    dt = B.DARTS_BF16 if dtype == "bf16" else B.DARTS_F32
+    q = torch.empty(rows * hq * hd, dtype=tdt, device=DEV)
+    kp = torch.empty(n_pages * hkv * 16 * hd, dtype=tdt, device=DEV)
+    vp = torch.empty_like(kp)
+    B.darts_fill_uniform(q, OS.T_Q, seed, dt)
+    B.darts_fill_kv_pool(kp, vp, n_pages, hkv, hd, seed, dt)
+    ptd = torch.from_numpy(pt).to(DEV)
+    ctxd = torch.from_numpy(ctx.astype(np.int32)).to(DEV)
+    out = torch.zeros(rows * hq * hd, dtype=tdt, device=DEV)
+    ws = torch.empty(B.darts_attn_workspace_bytes(rows, hq, hkv, hd, max_ctx), dtype=torch.uint8,
+                     device=DEV)
+    B.darts_attn_decode(q, kp, vp, n_pages, ptd, ctxd, hq, hkv, hd, max_ctx, dt, out, ws)
+    torch.cuda.synchronize()
+    return out.float().cpu().numpy().reshape(rows, hq, hd), pt
+
+
+@pytest.mark.parametrize("dtype,hq,hkv,hd", [("bf16", 32, 8, 128), ("bf16", 16, 4, 64),
+                                            ("bf16", 8, 8, 128), ("bf16", 32, 4, 128),
+                                            ("f32", 4, 4, 32), ("f32", 8, 2, 64)])
+def test_attention_small_ragged(dtype, hq, hkv, hd):
+    """Ragged contexts (1 .. several chunks, partial last pages) in a shuffled pool."""
+    say(f"attention {dtype} hq={hq} hkv={hkv} hd={hd}")
+    ctx = np.array([1, 15, 16, 17, 31, 33, 100, 257, 513, 1024, 1500, 2049, 3000, 40, 5, 700],
+                   dtype=np.int64)
+    rows = len(ctx)
+    seed = 77
+    got, pt = _attn_case(rows, hq, hkv, hd, ctx, dtype, seed)
+    tol = 2e-2 if dtype == "bf16" else 1e-5
+    for r in range(rows):
+        ref = OS.attention_row(r, int(ctx[r]), pt[r], seed, hq, hkv, hd)
+        err = np.max(np.abs(got[r] - ref))
+        assert err <= tol * max(1.0, np.max(np.abs(ref))), (r, ctx[r], err)
+
+
+def test_attention_full_sweep_sampled_rows():
+    """The sweep's shape: 1024 trajectories, 32/8 heads, hd 128, lognormal
+    contexts in [16, 32768] over a shuffled pool; sampled rows vs the oracle."""
+    say("attention sweep full size")
+    ctx, rng = sweep_attention_inputs()
+    seed = SWEEP["seed"]
+    got, pt = _attn_case(len(ctx), 32, 8, 128, ctx.astype(np.int64), "bf16", seed)
+    order = np.argsort(ctx)
+    sample = list(order[:3]) + list(order[-3:]) + list(range(0, len(ctx), 151))
+    for r in sample:
+        ref = OS.attention_row(int(r), int(ctx[r]), pt[r], seed, 32, 8, 128)
+        err = np.max(np.abs(got[r] - ref))
+        assert err <= 2e-2 * max(1.0, np.max(np.abs(ref))), (r, ctx[r], err)
+    assert np.isfinite(got).all()
+
+
+def _oracle_select(status, length, mlp, m, k, L, m_up, early_stop):
+    n = len(status)
+    kept = {}
+    new_status = status.copy()
+    for grp in range(n // m):
+        mem = []
+        for j in range(m):
+            g = grp * m + j
+            mem.append(dict(g=g, status=int(status[g]), length=int(length[g]),
+                            trunc=int(status[g]) == TRUNC, mean_lp=float(mlp[g])))
+        c, kp, ab = group_decision(mem, k, L, m_up, early_stop)
+        if c:
+            kept[grp] = kp
+            for g in ab:
+                new_status[g] = ABORTED
+    return kept, new_status
+
+
+@pytest.mark.parametrize("mode", ["short_final", "short_mid", "dual_final", "dual_mid", "no_abort_mid"])
+def test_selection_sweep(mode):
+    """65536 trajectories in groups of m=16, k=8 (L=1), lengths lognormal,
+    mean log-probs on a 2^-10 grid (exact ties): kept sets bit-exact."""
+    B = _b()
+    say(f"selection sweep {mode}")
+    raw, mlp = sweep_selection_inputs()
+    cap = SWEEP["sel_cap"]
+    m, k, L = SWEEP["sel_m"], SWEEP["sel_k"], 1
+    m_up = 16 if mode.startswith("short") or mode.startswith("no_abort") else 17
+    early = 0 if mode.startswith("no_abort") else 1
+    length = np.minimum(raw, cap).astype(np.int32)
+    trunc = raw > cap
+    if mode.endswith("final"):
+        s = cap
+    elif m_up <= m and early:
+        s = int(np.median(length))
+    else:
+        # modes that wait for every member: a step at which about half the groups are done
+        s = int(np.median(length.reshape(-1, m).max(axis=1)))
+    status = np.where(length <= s, np.where(trunc, TRUNC, EOS), LIVE).astype(np.uint8)
+    cur_len = np.minimum(length, s).astype(np.int32)
+    kept_ref, st_ref = _oracle_select(status, cur_len, mlp, m, k, L, m_up, early)
+    n = len(status)
+    st_d = torch.from_numpy(status).to(DEV)
+    len_d = torch.from_numpy(cur_len).to(DEV)
+    mlp_d = torch.from_numpy(mlp).to(DEV)
+    kept_d = torch.full((n // m, k), -1, dtype=torch.int32, device=DEV)
+    comp_d = torch.zeros(n // m, dtype=torch.uint8, device=DEV)
+    B.darts_select_groups(st_d, len_d, mlp_d, m, k, L, m_up, early, kept_d, comp_d)
+    torch.cuda.synchronize()
+    kept, comp, st = kept_d.cpu().numpy(), comp_d.cpu().numpy(), st_d.cpu().numpy()
+    assert np.array_equal(st, st_ref)
+    for grp in range(n // m):
+        if grp in kept_ref:
+            assert comp[grp] == 1
+            assert list(kept[grp]) == kept_ref[grp], grp
+        else:
+            assert comp[grp] == 0 and (kept[grp] == -1).all()
+    assert len(kept_ref) > 0
