@@ -58,7 +58,8 @@ typedef enum { DARTS_F32 = 0, DARTS_BF16 = 1 } darts_dtype;
                                           is selected (kept sets are unchanged) */
 #define DARTS_FLAG_PERMUTE_PAGES 0x2u  /* initial free list in a seeded random order
                                           (physical page ids must not change any output) */
-#define DARTS_FLAG_TIMING        0x4u  /* record HIP events around attention launches
+#define DARTS_FLAG_TIMING        0x4u  /* record HIP events around decode-attention and
+                                          GEMM launches on the context's stream
                                           (darts_get_stats reports them) */
 
 /* Decoder shape.  Weights are generated on the device from weight_seed
@@ -122,9 +123,14 @@ typedef struct {
   int64_t pages_hwm;         /* high-water mark of pages in use */
   int32_t n_live;
   int32_t n_done;            /* prompts whose kept set is complete */
-  double attn_ms;            /* with DARTS_FLAG_TIMING: summed attention kernel time */
+  double attn_ms;            /* with DARTS_FLAG_TIMING: summed decode-attention time */
   double attn_bytes;         /* algorithmic bytes of those launches */
   int64_t attn_launches;
+  double gemm_ms;            /* with DARTS_FLAG_TIMING: summed GEMM time (decode and prefill) */
+  double gemm_flop;          /* 2*M*N*K summed over those launches */
+  int64_t gemm_launches;
+  double gemm_cls_ms[5];     /* per GEMM class: QKV, O, gate-up, down, LM head */
+  double gemm_cls_flop[5];
 } darts_stats;
 
 typedef struct darts_ctx darts_ctx;
@@ -172,15 +178,21 @@ int darts_decode_step(darts_ctx* ctx, const int32_t* d_force_tokens, darts_step_
  * pages of every trajectory that finished or was aborted, and a prompt's
  * shared pages when its last member is done; compacts the live list.
  *   d_kept      [n_prompts * k] int32, row i = prompt i's kept ids (short
- *               side first); rows of incomplete prompts are left untouched
+ *               side first); -1 in rows of prompts not complete yet
  *   d_done_step [n_prompts] int32: the step at which prompt i completed
- *               (untouched while incomplete)
+ *               (the prefill is step 1), -1 while incomplete
  *   h_n_live, h_n_done: host outputs (may be NULL).
  * Idempotent when nothing changed.                                          */
 int darts_select_and_prune(darts_ctx* ctx, int32_t* d_kept, int32_t* d_done_step,
                            int32_t* h_n_live, int32_t* h_n_done);
 
 int darts_get_stats(const darts_ctx* ctx, darts_stats* out);
+
+/* Start a new batch on the same context: weights, pool and buffers are
+ * kept; the free list, page tables, per-trajectory and per-prompt state and
+ * the statistics are reset.  Synchronises the stream.  The next call must be
+ * darts_prefill.                                                           */
+int darts_reset(darts_ctx* ctx);
 
 /* Final per-trajectory scores (device buffers of n_prompts*m, each may be
  * NULL): generated length, float32 sum of log-probs in step order, mean

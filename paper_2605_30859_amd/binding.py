@@ -47,7 +47,9 @@ class Stats(C.Structure):
     _fields_ = [("steps", C.c_int64), ("tokens_decoded", C.c_int64), ("n_pages", C.c_int64),
                 ("pages_used", C.c_int64), ("pages_hwm", C.c_int64), ("n_live", C.c_int32),
                 ("n_done", C.c_int32), ("attn_ms", C.c_double), ("attn_bytes", C.c_double),
-                ("attn_launches", C.c_int64)]
+                ("attn_launches", C.c_int64), ("gemm_ms", C.c_double), ("gemm_flop", C.c_double),
+                ("gemm_launches", C.c_int64), ("gemm_cls_ms", C.c_double * 5),
+                ("gemm_cls_flop", C.c_double * 5)]
 
 
 _P = C.c_void_p
@@ -60,6 +62,7 @@ _SIGS = {
     "darts_get_traj_scores": (C.c_int, [_P, _P, _P, _P, _P]),
     "darts_debug_logits": (C.c_int, [_P, _P, C.POINTER(C.c_int32)]),
     "darts_destroy": (C.c_int, [_P]),
+    "darts_reset": (C.c_int, [_P]),
     "darts_strerror": (C.c_char_p, [C.c_int]),
     "darts_last_error": (C.c_char_p, [_P]),
     "darts_fill_uniform": (C.c_int, [_P, C.c_uint64, C.c_int32, C.c_uint64, C.c_int32, _P]),
@@ -240,10 +243,20 @@ class Rollout:
         self.n_live, self.n_done = nl.value, nd.value
         return self.n_live, self.n_done
 
+    def darts_reset(self):
+        _check(self.lib.darts_reset(self.ctx), self.ctx)
+        self.n_live, self.n_done = self.n_traj, 0
+        self.kept.fill_(-1)
+        self.done_step.fill_(-1)
+
     def stats(self):
         s = Stats()
         _check(self.lib.darts_get_stats(self.ctx, C.byref(s)), self.ctx)
-        return {f: getattr(s, f) for f, _ in Stats._fields_}
+        out = {}
+        for f, _ in Stats._fields_:
+            v = getattr(s, f)
+            out[f] = list(v) if f.startswith("gemm_cls") else v
+        return out
 
     def traj_scores(self):
         t = self.torch

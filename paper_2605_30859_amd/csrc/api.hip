@@ -29,8 +29,8 @@ struct LayerW {
 };
 
 struct TimedLaunch {
-  hipEvent_t a, b;
-  double bytes;
+  int kind;        // 0 attention (decode), 1.. GEMM class + 1 (QKV, O, gate-up, down, LM head)
+  double units;    // algorithmic bytes (attention) or FLOP (GEMM)
 };
 
 }  // namespace
@@ -99,8 +99,12 @@ struct darts_ctx {
   bool poisoned = false;
   std::string err;
   std::vector<TimedLaunch> pending;
+  std::vector<hipEvent_t> events;  // pool, two per pending launch
   double attn_ms = 0.0, attn_bytes = 0.0;
   int64_t attn_launches = 0;
+  double gemm_ms = 0.0, gemm_flop = 0.0;
+  int64_t gemm_launches = 0;
+  double cls_ms[5] = {0, 0, 0, 0, 0}, cls_flop[5] = {0, 0, 0, 0, 0};
 };
 
 #define HIPCHK(ctx, expr)                                                      \
@@ -133,11 +137,28 @@ static void free_all(darts_ctx* c) {
   c->allocs.clear();
   if (c->h_info) (void)hipHostFree(c->h_info);
   c->h_info = nullptr;
-  for (auto& t : c->pending) {
-    (void)hipEventDestroy(t.a);
-    (void)hipEventDestroy(t.b);
-  }
+  for (hipEvent_t e : c->events) (void)hipEventDestroy(e);
+  c->events.clear();
   c->pending.clear();
+}
+
+static bool timing_on(const darts_ctx* c) { return (c->rc.flags & DARTS_FLAG_TIMING) != 0; }
+
+// Record the start event of a timed launch; returns its index or -1.
+static int tbegin(darts_ctx* c, int kind, double units) {
+  if (!timing_on(c)) return -1;
+  const size_t i = c->pending.size();
+  while (c->events.size() < 2 * (i + 1)) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return -1;
+    c->events.push_back(e);
+  }
+  if (hipEventRecord(c->events[2 * i], c->st) != hipSuccess) return -1;
+  c->pending.push_back(TimedLaunch{kind, units});
+  return (int)i;
+}
+static void tend(darts_ctx* c, int i) {
+  if (i >= 0) (void)hipEventRecord(c->events[2 * i + 1], c->st);
 }
 
 static int init_weights(darts_ctx* c) {
@@ -336,6 +357,8 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
     if (e == hipSuccess) e = hipMemsetAsync(c->status, 0, (size_t)c->n_traj, c->st);
     if (e == hipSuccess) e = hipMemsetAsync(c->freed, 0, (size_t)c->n_traj, c->st);
     if (e == hipSuccess) e = hipMemsetAsync(c->group_done, 0, (size_t)c->P, c->st);
+    if (e == hipSuccess) e = hipMemsetAsync(c->kept, 0xff, (size_t)c->P * c->k * 4, c->st);
+    if (e == hipSuccess) e = hipMemsetAsync(c->done_step, 0xff, (size_t)c->P * 4, c->st);
     if (e == hipSuccess) e = hipMemsetAsync(c->page_table, 0xff, (size_t)c->n_traj * c->max_pages * 4, c->st);
     if (e == hipSuccess) e = hipStreamSynchronize(c->st);
     if (e != hipSuccess) rcode = fail_hip(c, e, "init");
@@ -347,6 +370,37 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
   }
   c->free_top = (int)n_pages;
   *out = c;
+  return DARTS_OK;
+}
+
+int darts_reset(darts_ctx* c) {
+  if (!c) return DARTS_EINVAL;
+  if (c->poisoned) return DARTS_EHIP;
+  hipError_t e = hipStreamSynchronize(c->st);
+  std::vector<int32_t> iota(c->n_traj);
+  for (int g = 0; g < c->n_traj; ++g) iota[g] = g;
+  const int32_t top = (int32_t)c->n_pages;
+  if (e == hipSuccess)
+    e = launch_iota_perm(c->free_stack, c->n_pages, c->rc.page_perm_seed,
+                         (c->rc.flags & DARTS_FLAG_PERMUTE_PAGES) != 0, c->st);
+  if (e == hipSuccess) e = hipMemcpyAsync(c->dcnt, &top, 4, hipMemcpyHostToDevice, c->st);
+  if (e == hipSuccess) e = hipMemcpyAsync(c->live[0], iota.data(), iota.size() * 4, hipMemcpyHostToDevice, c->st);
+  if (e == hipSuccess) e = hipMemsetAsync(c->gen, 0, (size_t)c->n_traj * 4, c->st);
+  if (e == hipSuccess) e = hipMemsetAsync(c->sum_lp, 0, (size_t)c->n_traj * 4, c->st);
+  if (e == hipSuccess) e = hipMemsetAsync(c->status, 0, (size_t)c->n_traj, c->st);
+  if (e == hipSuccess) e = hipMemsetAsync(c->freed, 0, (size_t)c->n_traj, c->st);
+  if (e == hipSuccess) e = hipMemsetAsync(c->group_done, 0, (size_t)c->P, c->st);
+  if (e == hipSuccess) e = hipMemsetAsync(c->kept, 0xff, (size_t)c->P * c->k * 4, c->st);
+  if (e == hipSuccess) e = hipMemsetAsync(c->done_step, 0xff, (size_t)c->P * 4, c->st);
+  if (e == hipSuccess) e = hipMemsetAsync(c->page_table, 0xff, (size_t)c->n_traj * c->max_pages * 4, c->st);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->st);
+  if (e != hipSuccess) return fail_hip(c, e, "reset");
+  c->phase = 0; c->cur = 0; c->n_live = 0; c->n_done = 0; c->free_top = (int)c->n_pages;
+  c->step = 0; c->tokens = 0; c->hwm = 0; c->last_rows_out = 0;
+  c->pending.clear();
+  c->attn_ms = c->attn_bytes = 0.0; c->attn_launches = 0;
+  c->gemm_ms = c->gemm_flop = 0.0; c->gemm_launches = 0;
+  for (int i = 0; i < 5; ++i) c->cls_ms[i] = c->cls_flop[i] = 0.0;
   return DARTS_OK;
 }
 
@@ -365,24 +419,27 @@ static int run_attention(darts_ctx* c, int layer, int n_rows, const int32_t* row
                          int ctx_base, int max_ctx) {
   void* kp = (char*)c->kpool + (size_t)layer * c->pool_layer_elems * c->esz;
   void* vp = (char*)c->vpool + (size_t)layer * c->pool_layer_elems * c->esz;
-  const bool timing = (c->rc.flags & DARTS_FLAG_TIMING) != 0 && ctx_mod == 0;
-  TimedLaunch tl{};
-  if (timing) {
-    HIPCHK(c, hipEventCreate(&tl.a));
-    HIPCHK(c, hipEventCreate(&tl.b));
-    HIPCHK(c, hipEventRecord(tl.a, c->st));
-  }
+  // algorithmic bytes: every key and value of the context once per kv head,
+  // q and out once, one page id per 16 keys
+  const double ctx = ctx_base;
+  const double bytes = (double)n_rows * (ctx * c->hkv * c->hd * 2.0 * c->esz +
+                                         2.0 * c->hq * c->hd * c->esz + std::ceil(ctx / kPage) * 4.0);
+  const int ti = ctx_mod == 0 ? tbegin(c, 0, bytes) : -1;
   HIPCHK(c, launch_attention(c->q, kp, vp, c->n_pages, c->page_table, c->max_pages, row_pt, nullptr,
                              ctx_mod, ctx_base, n_rows, c->hq, c->hkv, c->hd, max_ctx, c->bf16,
                              c->attn, c->attn_ws, c->attn_ws_bytes, c->st));
-  if (timing) {
-    HIPCHK(c, hipEventRecord(tl.b, c->st));
-    const double ctx = ctx_base;
-    tl.bytes = (double)n_rows * (ctx * c->hkv * c->hd * 2.0 * c->esz + 2.0 * c->hq * c->hd * c->esz +
-                                 std::ceil(ctx / kPage) * 4.0);
-    c->pending.push_back(tl);
-  }
+  tend(c, ti);
   return DARTS_OK;
+}
+
+enum { G_QKV = 0, G_O, G_GU, G_DOWN, G_LM };
+static hipError_t gemm_t(darts_ctx* c, int cls, const void* A, int lda, const void* W, int ldw,
+                         void* C, int ldc, int M, int N, int K, int epi) {
+  const int ti = tbegin(c, 1 + cls, 2.0 * M * N * K);
+  hipError_t e = launch_gemm(c->bf16, A, lda, W, ldw, C, ldc, M, N, K, epi, c->gemm_ws,
+                             c->gemm_ws_bytes, c->st);
+  tend(c, ti);
+  return e;
 }
 
 // Decoder layers over n rows whose residual stream is in c->x.
@@ -395,20 +452,16 @@ static int run_layers(darts_ctx* c, int n, const int32_t* row_pt, int pos_mod, i
     void* kp = (char*)c->kpool + (size_t)l * c->pool_layer_elems * c->esz;
     void* vp = (char*)c->vpool + (size_t)l * c->pool_layer_elems * c->esz;
     HIPCHK(c, launch_rmsnorm(c->x, n, d, c->mc.rms_eps, c->xn, b, c->st));
-    HIPCHK(c, launch_gemm(b, c->xn, d, w.wqkv, d, c->qkv, c->qkv_w, n, c->qkv_w, d, EPI_F32,
-                          c->gemm_ws, c->gemm_ws_bytes, c->st));
+    HIPCHK(c, gemm_t(c, G_QKV, c->xn, d, w.wqkv, d, c->qkv, c->qkv_w, n, c->qkv_w, d, EPI_F32));
     HIPCHK(c, launch_rope_append2(c->qkv, n, c->hq, c->hkv, c->hd, row_pt, pos_mod, pos_base,
                                   c->page_table, c->max_pages, c->n_pages, c->rope, c->q, kp, vp, b,
                                   c->st));
     int r = run_attention(c, l, n, row_pt, ctx_mod, ctx_base, max_ctx);
     if (r != DARTS_OK) return r;
-    HIPCHK(c, launch_gemm(b, c->attn, hqd, w.wo, hqd, c->x, d, n, d, hqd, EPI_ADD_F32, c->gemm_ws,
-                          c->gemm_ws_bytes, c->st));
+    HIPCHK(c, gemm_t(c, G_O, c->attn, hqd, w.wo, hqd, c->x, d, n, d, hqd, EPI_ADD_F32));
     HIPCHK(c, launch_rmsnorm(c->x, n, d, c->mc.rms_eps, c->xn, b, c->st));
-    HIPCHK(c, launch_gemm(b, c->xn, d, w.wgu, d, c->hbuf, c->F, n, 2 * c->F, d, EPI_SWIGLU,
-                          c->gemm_ws, c->gemm_ws_bytes, c->st));
-    HIPCHK(c, launch_gemm(b, c->hbuf, c->F, w.wdown, c->F, c->x, d, n, d, c->F, EPI_ADD_F32,
-                          c->gemm_ws, c->gemm_ws_bytes, c->st));
+    HIPCHK(c, gemm_t(c, G_GU, c->xn, d, w.wgu, d, c->hbuf, c->F, n, 2 * c->F, d, EPI_SWIGLU));
+    HIPCHK(c, gemm_t(c, G_DOWN, c->hbuf, c->F, w.wdown, c->F, c->x, d, n, d, c->F, EPI_ADD_F32));
   }
   return DARTS_OK;
 }
@@ -485,8 +538,7 @@ int darts_decode_step(darts_ctx* c, const int32_t* d_force_tokens, darts_step_ou
   int r = run_layers(c, n, live, 0, pos, 0, pos + 1, pos + 1);
   if (r != DARTS_OK) return r;
   HIPCHK(c, launch_rmsnorm(c->x, n, c->d, c->mc.rms_eps, c->xn, b, c->st));
-  HIPCHK(c, launch_gemm(b, c->xn, c->d, c->lm_head, c->d, c->logits, c->V, n, c->V, c->d, EPI_F32,
-                        c->gemm_ws, c->gemm_ws_bytes, c->st));
+  HIPCHK(c, gemm_t(c, G_LM, c->xn, c->d, c->lm_head, c->d, c->logits, c->V, n, c->V, c->d, EPI_F32));
   SampleArgs a{};
   a.logits = c->logits; a.n_rows = n; a.vocab = c->V; a.bf16 = false;
   a.seed = c->rc.sample_seed; a.temperature = c->rc.temperature;
@@ -530,14 +582,15 @@ int darts_select_and_prune(darts_ctx* c, int32_t* d_kept, int32_t* d_done_step, 
   c->n_done = c->h_info[1];
   c->free_top = c->h_info[2];
   if (c->n_done == c->P) c->phase = 2;
-  for (auto& t : c->pending) {
+  for (size_t i = 0; i < c->pending.size(); ++i) {
     float ms = 0.f;
-    HIPCHK(c, hipEventElapsedTime(&ms, t.a, t.b));
-    c->attn_ms += ms;
-    c->attn_bytes += t.bytes;
-    c->attn_launches += 1;
-    (void)hipEventDestroy(t.a);
-    (void)hipEventDestroy(t.b);
+    HIPCHK(c, hipEventElapsedTime(&ms, c->events[2 * i], c->events[2 * i + 1]));
+    const TimedLaunch& t = c->pending[i];
+    if (t.kind == 0) { c->attn_ms += ms; c->attn_bytes += t.units; c->attn_launches += 1; }
+    else {
+      c->gemm_ms += ms; c->gemm_flop += t.units; c->gemm_launches += 1;
+      c->cls_ms[t.kind - 1] += ms; c->cls_flop[t.kind - 1] += t.units;
+    }
   }
   c->pending.clear();
   if (h_n_live) *h_n_live = c->n_live;
@@ -557,6 +610,10 @@ int darts_get_stats(const darts_ctx* c, darts_stats* s) {
   s->attn_ms = c->attn_ms;
   s->attn_bytes = c->attn_bytes;
   s->attn_launches = c->attn_launches;
+  s->gemm_ms = c->gemm_ms;
+  s->gemm_flop = c->gemm_flop;
+  s->gemm_launches = c->gemm_launches;
+  for (int i = 0; i < 5; ++i) { s->gemm_cls_ms[i] = c->cls_ms[i]; s->gemm_cls_flop[i] = c->cls_flop[i]; }
   return DARTS_OK;
 }
 
