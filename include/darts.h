@@ -269,6 +269,22 @@ int darts_select_groups(uint8_t* d_status, const int32_t* d_len, const float* d_
                         int32_t n_traj, int32_t m, int32_t k, int32_t L, int32_t m_up,
                         int32_t early_stop, int32_t* d_kept, uint8_t* d_complete, void* stream);
 
+/* The decoder's dense projection (a plain GEMM with the decoder's fused
+ * epilogues): C = A[M,K] . W[N,K]^T with fp32 accumulation.
+ *   d_a  [M][K], d_w [N][K]: bf16 (DARTS_BF16) or f32 (DARTS_F32), row-major
+ *   epilogue 0: d_c [M][N] f32 = result
+ *            1: d_c [M][N] in the operand dtype = result (rounded)
+ *            2: d_c [M][N] f32 += result (residual add)
+ *            3: SwiGLU: W rows are interleaved in groups of 16 (16 gate rows,
+ *               then the 16 up rows of the same features); d_c [M][N/2] in
+ *               the operand dtype = silu(gate) * up
+ *   bf16 requires N % 128 == 0 and K % 256 == 0.  d_workspace must hold
+ *   darts_gemm_workspace_bytes(M, N, K) bytes (split-K partial sums).      */
+size_t darts_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K);
+int darts_gemm(const void* d_a, const void* d_w, void* d_c, int32_t M, int32_t N, int32_t K,
+               int32_t dtype, int32_t epilogue, void* d_workspace, size_t workspace_bytes,
+               void* stream);
+
 /* Gumbel noise map used by darts_sample: d_g[i] = -ln(-ln(d_u[i])) with the
  * library's float32 logarithm (a fixed sequence of correctly rounded float32
  * operations: atanh series on the reduced mantissa).  d_u in (0, 1).  For

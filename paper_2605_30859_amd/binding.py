@@ -73,6 +73,9 @@ _SIGS = {
     "darts_sample": (C.c_int, [_P, C.c_int32, C.c_int32, C.c_int32, C.c_uint64, _P, _P, C.c_float,
                                _P, _P, _P, _P, _P]),
     "darts_debug_gumbel": (C.c_int, [_P, _P, C.c_int64, _P]),
+    "darts_gemm_workspace_bytes": (C.c_size_t, [C.c_int32, C.c_int32, C.c_int32]),
+    "darts_gemm": (C.c_int, [_P, _P, _P, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                             _P, C.c_size_t, _P]),
     "darts_select_groups": (C.c_int, [_P, _P, _P, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                                       C.c_int32, C.c_int32, _P, _P, _P]),
 }
@@ -158,6 +161,16 @@ def darts_select_groups(status, length, mean_lp, m, k, L, m_up, early_stop, kept
     _check(load_library().darts_select_groups(_ptr(status), _ptr(length), _ptr(mean_lp),
                                               status.numel(), m, k, L, m_up, int(early_stop),
                                               _ptr(kept), _ptr(complete), _stream(stream)))
+
+
+def darts_gemm_workspace_bytes(M, N, K):
+    return int(load_library().darts_gemm_workspace_bytes(M, N, K))
+
+
+def darts_gemm(a, w, c, M, N, K, dtype, epilogue, workspace=None, stream=None):
+    wb = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(load_library().darts_gemm(_ptr(a), _ptr(w), _ptr(c), M, N, K, dtype, epilogue,
+                                     _ptr(workspace), wb, _stream(stream)))
 
 
 def darts_debug_gumbel(u, g, stream=None):

@@ -186,11 +186,13 @@ static int init_weights(darts_ctx* c) {
 }
 
 static size_t gemm_ws_need(const darts_ctx* c) {
+  // every row count a launch can see: decode batches 1..n_traj, the prefill
+  // (P*Lp rows) and the prefill's LM head (P rows)
   size_t need = 0;
   std::vector<int> ms;
-  for (int mm = 16; mm < c->n_traj; mm *= 2) ms.push_back(mm);
-  ms.push_back(c->n_traj);
+  for (int M = 1; M <= c->n_traj; ++M) ms.push_back(M);
   ms.push_back(c->P);
+  ms.push_back(c->P * c->Lp);
   for (int M : ms) {
     need = std::max(need, gemm_workspace_bytes(M, c->qkv_w, c->d));
     need = std::max(need, gemm_workspace_bytes(M, c->d, c->hq * c->hd));
@@ -708,6 +710,27 @@ int darts_sample(const void* d_logits, int32_t n_rows, int32_t vocab, int32_t dt
   a.seed = seed; a.temperature = temperature; a.traj = d_traj; a.step = d_step; a.force = d_force;
   a.token_out = d_token; a.logprob_out = d_logprob; a.entropy_out = d_entropy;
   hipError_t e = launch_sample(a, (hipStream_t)stream);
+  return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
+}
+
+size_t darts_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K) {
+  if (M < 1 || N < 1 || K < 1) return 0;
+  return gemm_workspace_bytes(M, N, K);
+}
+
+int darts_gemm(const void* d_a, const void* d_w, void* d_c, int32_t M, int32_t N, int32_t K,
+               int32_t dtype, int32_t epilogue, void* d_workspace, size_t workspace_bytes,
+               void* stream) {
+  if (!d_a || !d_w || !d_c || M < 0 || N < 1 || K < 1) return DARTS_EINVAL;
+  if (dtype != DARTS_F32 && dtype != DARTS_BF16) return DARTS_EINVAL;
+  if (epilogue < 0 || epilogue > 3) return DARTS_EINVAL;
+  if (epilogue == 3 && N % 32) return DARTS_EINVAL;
+  if (dtype == DARTS_BF16 && (N % 128 || K % 256)) return DARTS_EINVAL;
+  const int ldc = epilogue == 3 ? N / 2 : N;
+  const size_t need = dtype == DARTS_BF16 ? gemm_workspace_bytes(M, N, K) : 0;
+  if (need > workspace_bytes || (need && !d_workspace)) return DARTS_EINVAL;
+  hipError_t e = launch_gemm(dtype == DARTS_BF16, d_a, K, d_w, K, d_c, ldc, M, N, K, epilogue,
+                             d_workspace, workspace_bytes, (hipStream_t)stream);
   return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
 }
 

@@ -2,15 +2,25 @@
 // bf16 operands on gfx950 MFMA (v_mfma_f32_16x16x32_bf16), fp32 accumulate.
 // Epilogues: store fp32, store bf16, add into an fp32 residual, SwiGLU
 // (W rows interleaved in groups of 16: 16 gate rows then the 16 matching up
-// rows, output silu(gate) * up as bf16).  Small-M launches split K across
-// blocks; partial sums go to a workspace and a second kernel reduces them in
-// a fixed order (bitwise deterministic).
+// rows; output silu(gate) * up as bf16).
+//
+// Two kernel families, chosen per launch from (M, N, K):
+//  * tiled: BM x BN block tile staged through LDS (register-staged double
+//    buffer, BK = 64), 4 wavefronts each owning a WM x WN register tile;
+//    blocks are renumbered so that the blocks an XCD runs are neighbours in
+//    (m, n) and share operand tiles in that XCD's L2.
+//  * skinny (M <= 64, weight-bandwidth bound): no LDS for operands; each
+//    wavefront loads W and A fragments straight into MFMA operand registers,
+//    8 wavefronts of a block split K and are reduced through LDS.
+// Either family may split K across blocks; partial sums then go to a
+// workspace and a reduce kernel adds them in a fixed order (bitwise
+// deterministic).
 #include "common.h"
 #include "kernels.h"
 
 namespace darts {
 
-constexpr int BM = 64, BN = 128, BK = 64, LDSK = BK + 8;  // +8 bf16 pad: conflict-free b128 reads
+constexpr int BK = 64, LDSK = BK + 8;  // +8 bf16 row pad: conflict-free 16-byte fragment reads
 
 __device__ __forceinline__ float silu_f(float g) { return g / (1.0f + __expf(-g)); }
 
@@ -22,69 +32,101 @@ __device__ __forceinline__ void epi_store(void* C, int ldc, int M, int m, int n,
   else if (EPI == EPI_ADD_F32) ((float*)C)[(int64_t)m * ldc + n] += v;
 }
 
-// SPLIT: write raw fp32 partials to ws[z][M][N] instead of the epilogue.
-template <int EPI, bool SPLIT>
-__global__ void __launch_bounds__(256) gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda,
-                                                        const bf16_t* __restrict__ W, int ldw,
-                                                        void* __restrict__ C, int ldc, int M, int N,
-                                                        int K, int k_chunk, float* __restrict__ ws) {
+// Write a 16x16 MFMA output tile pair / single tile.  acc layout: lane holds
+// rows r0 + 4*(lane/16) + i, column c0 + lane%16.
+template <int EPI>
+__device__ __forceinline__ void store_tile(void* C, int ldc, int M, int r0, int c0, int lane,
+                                           const f32x4_t& v) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) epi_store<EPI>(C, ldc, M, r0 + 4 * (lane >> 4) + i, c0 + (lane & 15), v[i]);
+}
+// gate tile (physical cols 32g..32g+15) and up tile (32g+16..32g+31) -> H cols 16g..16g+15
+__device__ __forceinline__ void store_swiglu(bf16_t* H, int ldc, int M, int r0, int pc0, int lane,
+                                             const f32x4_t& g, const f32x4_t& u) {
+  const int col = (pc0 >> 5) * 16 + (lane & 15);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = r0 + 4 * (lane >> 4) + i;
+    if (m < M) H[(int64_t)m * ldc + col] = f32_to_bf16(silu_f(g[i]) * u[i]);
+  }
+}
+__device__ __forceinline__ void store_partial(float* P, int M, int N, int r0, int c0, int lane,
+                                              const f32x4_t& v) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = r0 + 4 * (lane >> 4) + i;
+    if (m < M) P[(int64_t)m * N + c0 + (lane & 15)] = v[i];
+  }
+}
+
+// ------------------------------------------------------------------ tiled
+template <int BM, int BN, int WGM, int WGN, int EPI, bool SPLIT>
+__global__ void __launch_bounds__(256) gemm_tiled_kernel(const bf16_t* __restrict__ A, int lda,
+                                                         const bf16_t* __restrict__ W, int ldw,
+                                                         void* __restrict__ C, int ldc, int M,
+                                                         int N, int K, int k_chunk, int mt, int nt,
+                                                         float* __restrict__ ws) {
+  constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 16, TN = WN / 16;
+  constexpr int ALD = BM / 32, WLD = BN / 32;   // 16-byte chunks per thread per k-tile
   __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * LDSK];
   __shared__ __attribute__((aligned(16))) bf16_t Ws[2][BN * LDSK];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
-  const int kbeg = blockIdx.z * k_chunk;
+  const int wm = wave / WGN, wn = wave % WGN;
+  // XCD-aware renumbering: hardware block b runs on XCD b % 8; give each XCD a
+  // contiguous range of logical tiles (m fastest, then n, then the K split).
+  const int nb = gridDim.x;
+  int b = blockIdx.x;
+  const int full = (nb / 8) * 8;
+  if (b < full) b = (b % 8) * (full / 8) + b / 8;
+  const int mi = b % mt, ni = (b / mt) % nt, z = b / (mt * nt);
+  const int m0 = mi * BM, n0 = ni * BN;
+  const int kbeg = z * k_chunk;
   const int nk = k_chunk / BK;
 
-  // global -> register staging: A 2 x 16B, W 4 x 16B per thread
   const int lr = tid >> 3, lc = (tid & 7) * 8;
-  uint4 ra[2], rw[4];
+  u32x4_t ra[ALD], rw[WLD];
   auto gload = [&](int kt) {
     const int kk = kbeg + kt * BK + lc;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < ALD; ++i) {
       const int r = m0 + lr + 32 * i;
-      if (r < M) ra[i] = *(const uint4*)(A + (int64_t)r * lda + kk);
-      else ra[i] = make_uint4(0, 0, 0, 0);
+      ra[i] = r < M ? *(const u32x4_t*)(A + (int64_t)r * lda + kk) : (u32x4_t){0u, 0u, 0u, 0u};
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = n0 + lr + 32 * i;
-      rw[i] = *(const uint4*)(W + (int64_t)r * ldw + kk);
-    }
+    for (int i = 0; i < WLD; ++i) rw[i] = *(const u32x4_t*)(W + (int64_t)(n0 + lr + 32 * i) * ldw + kk);
   };
   auto sstore = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) *(uint4*)(&As[buf][(lr + 32 * i) * LDSK + lc]) = ra[i];
+    for (int i = 0; i < ALD; ++i) *(u32x4_t*)(&As[buf][(lr + 32 * i) * LDSK + lc]) = ra[i];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) *(uint4*)(&Ws[buf][(lr + 32 * i) * LDSK + lc]) = rw[i];
+    for (int i = 0; i < WLD; ++i) *(u32x4_t*)(&Ws[buf][(lr + 32 * i) * LDSK + lc]) = rw[i];
   };
 
-  f32x4_t acc[2][4];
+  f32x4_t acc[TM][TN];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < TN; ++j) acc[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 
   gload(0);
   sstore(0);
   __syncthreads();
-  const int arow = wm * 32 + (lane & 15), brow = wn * 64 + (lane & 15), kq = (lane >> 4) * 8;
+  const int arow = wm * WM + (lane & 15), brow = wn * WN + (lane & 15), kq = (lane >> 4) * 8;
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
     if (kt + 1 < nk) gload(kt + 1);
 #pragma unroll
     for (int ks = 0; ks < BK; ks += 32) {
-      bf16x8_t a[2], b[4];
+      bf16x8_t a[TM], bb[TN];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) a[i] = *(const bf16x8_t*)(&As[buf][(arow + 16 * i) * LDSK + ks + kq]);
+      for (int i = 0; i < TM; ++i) a[i] = *(const bf16x8_t*)(&As[buf][(arow + 16 * i) * LDSK + ks + kq]);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = *(const bf16x8_t*)(&Ws[buf][(brow + 16 * j) * LDSK + ks + kq]);
+      for (int j = 0; j < TN; ++j) bb[j] = *(const bf16x8_t*)(&Ws[buf][(brow + 16 * j) * LDSK + ks + kq]);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bb[j], acc[i][j], 0, 0, 0);
     }
     if (kt + 1 < nk) {
       sstore(buf ^ 1);
@@ -92,48 +134,102 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const bf16_t* __restrict
     }
   }
 
-  // lane holds C[row = base + 4*(lane/16) + r][col = base + lane%16]
-  const int rbase = m0 + wm * 32 + 4 * (lane >> 4);
-  const int cbase = n0 + wn * 64 + (lane & 15);
-  if (SPLIT) {
-    float* P = ws + (int64_t)blockIdx.z * M * N;
+  const int rb = m0 + wm * WM, cb = n0 + wn * WN;
+  if constexpr (SPLIT) {
+    float* P = ws + (int64_t)z * M * N;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < TN; ++j) store_partial(P, M, N, rb + 16 * i, cb + 16 * j, lane, acc[i][j]);
+  } else if constexpr (EPI == EPI_SWIGLU) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = rbase + 16 * i + r;
-          if (m < M) P[(int64_t)m * N + cbase + 16 * j] = acc[i][j][r];
-        }
-    return;
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; j += 2)
+        store_swiglu((bf16_t*)C, ldc, M, rb + 16 * i, cb + 16 * j, lane, acc[i][j], acc[i][j + 1]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) store_tile<EPI>(C, ldc, M, rb + 16 * i, cb + 16 * j, lane, acc[i][j]);
   }
-  if (EPI == EPI_SWIGLU) {
-    // tiles j=0,1 are (gate, up) of one 16-feature group, tiles 2,3 the next
-    bf16_t* H = (bf16_t*)C;
+}
+
+// ----------------------------------------------------------------- skinny
+// Block: 8 wavefronts, NS*16 output columns, all M <= 16*MT rows.  Wavefront
+// w handles K range [kbeg + w*kw, kbeg + (w+1)*kw).
+template <int MT, int NS, int EPI, bool SPLIT>
+__global__ void __launch_bounds__(512) gemm_skinny_kernel(const bf16_t* __restrict__ A, int lda,
+                                                          const bf16_t* __restrict__ W, int ldw,
+                                                          void* __restrict__ C, int ldc, int M,
+                                                          int N, int K, int k_chunk, int nt,
+                                                          float* __restrict__ ws) {
+  __shared__ f32x4_t red[8][MT * NS][64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int ni = blockIdx.x % nt, z = blockIdx.x / nt;
+  const int n0 = ni * NS * 16;
+  const int kw = k_chunk / 8;
+  const int kbeg = z * k_chunk + wave * kw;
+  const int kq = (lane >> 4) * 8, r = lane & 15;
+  f32x4_t acc[MT][NS];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int jp = 0; jp < 2; ++jp) {
-        const int grp = (n0 + wn * 64 + 32 * jp) >> 5;
-        const int col = grp * 16 + (lane & 15);
+    for (int j = 0; j < NS; ++j) acc[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+  const bf16_t* wp[NS];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = rbase + 16 * i + r;
-          if (m < M) {
-            const float g = acc[i][2 * jp][r], u = acc[i][2 * jp + 1][r];
-            H[(int64_t)m * ldc + col] = f32_to_bf16(silu_f(g) * u);
-          }
-        }
-      }
-    return;
+  for (int j = 0; j < NS; ++j) wp[j] = W + (int64_t)(n0 + 16 * j + r) * ldw + kbeg + kq;
+  const bf16_t* ap[MT];
+  bool av[MT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    av[i] = (16 * i + r) < M;
+    ap[i] = A + (int64_t)(av[i] ? 16 * i + r : 0) * lda + kbeg + kq;
+  }
+#pragma unroll 4
+  for (int k = 0; k < kw; k += 32) {
+    bf16x8_t a[MT], b[NS];
+#pragma unroll
+    for (int j = 0; j < NS; ++j) b[j] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(wp[j] + k));
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      u32x4_t v = *(const u32x4_t*)(ap[i] + k);
+      if (!av[i]) v = (u32x4_t){0u, 0u, 0u, 0u};
+      a[i] = __builtin_bit_cast(bf16x8_t, v);
+    }
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < NS; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
   }
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MT; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < NS; ++j) red[wave][i * NS + j][lane] = acc[i][j];
+  __syncthreads();
+  // wave t sums tile t (in wave order 0..7) and stores it
+  for (int t = wave; t < MT * NS; t += 8) {
+    f32x4_t s = red[0][t][lane];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) epi_store<EPI>(C, ldc, M, rbase + 16 * i + r, cbase + 16 * j, acc[i][j][r]);
+    for (int w = 1; w < 8; ++w) s += red[w][t][lane];
+    red[0][t][lane] = s;
+  }
+  __syncthreads();
+  if constexpr (SPLIT) {
+    float* P = ws + (int64_t)z * M * N;
+    for (int t = wave; t < MT * NS; t += 8)
+      store_partial(P, M, N, 16 * (t / NS), n0 + 16 * (t % NS), lane, red[0][t][lane]);
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    for (int t = wave; t < MT * NS / 2; t += 8) {
+      const int i = t / (NS / 2), jp = t % (NS / 2);
+      store_swiglu((bf16_t*)C, ldc, M, 16 * i, n0 + 32 * jp, lane, red[0][i * NS + 2 * jp][lane],
+                   red[0][i * NS + 2 * jp + 1][lane]);
+    }
+  } else {
+    for (int t = wave; t < MT * NS; t += 8)
+      store_tile<EPI>(C, ldc, M, 16 * (t / NS), n0 + 16 * (t % NS), lane, red[0][t][lane]);
+  }
 }
 
 // Sum split-K partials in order z = 0..S-1 and apply the epilogue.
@@ -143,7 +239,7 @@ __global__ void splitk_reduce_kernel(const float* __restrict__ ws, int S, int M,
   const int64_t nout = (EPI == EPI_SWIGLU) ? (int64_t)M * (N / 2) : (int64_t)M * N;
   for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < nout;
        t += (int64_t)gridDim.x * blockDim.x) {
-    if (EPI == EPI_SWIGLU) {
+    if constexpr (EPI == EPI_SWIGLU) {
       const int F = N / 2;
       const int m = (int)(t / F), c = (int)(t % F);
       const int pg = (c >> 4) * 32 + (c & 15), pu = pg + 16;
@@ -162,7 +258,7 @@ __global__ void splitk_reduce_kernel(const float* __restrict__ ws, int S, int M,
   }
 }
 
-// fp32 GEMM (used by fp32 models): 16x16 output tile per block, K in steps of 16.
+// fp32 GEMM (fp32 models): 16x16 output tile per block, K in steps of 16.
 template <int EPI>
 __global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__ A, int lda,
                                                        const float* __restrict__ W, int ldw, void* C,
@@ -182,7 +278,6 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__
   }
   if (m >= M || n >= N) return;
   if (EPI == EPI_F32) ((float*)C)[(int64_t)m * ldc + n] = acc;
-  else if (EPI == EPI_BF16) ((bf16_t*)C)[(int64_t)m * ldc + n] = f32_to_bf16(acc);
   else if (EPI == EPI_ADD_F32) ((float*)C)[(int64_t)m * ldc + n] += acc;
 }
 
@@ -206,39 +301,133 @@ __global__ void gemm_f32_swiglu_kernel(const float* __restrict__ A, int lda, con
   }
 }
 
-static int choose_splits(int M, int N, int K) {
-  const int blocks = ((M + BM - 1) / BM) * (N / BN);
-  int s = 1;
-  while (blocks * s < 512 && s < 8 && (K / (BK * 2 * s)) >= 2 && (K % (BK * 2 * s)) == 0) s *= 2;
-  return s;
+// ------------------------------------------------------------ dispatch
+struct Plan {
+  int kind;        // 0 skinny, 1..4 tiled configs
+  int mt, nt, S;   // tiles and K splits
+  int MT, NS;      // skinny shape
+};
+
+static int cu_count() { return 256; }
+
+// Tiled configs: (BM, BN)
+static const int kTiles[4][2] = {{64, 128}, {128, 128}, {128, 256}, {256, 128}};
+
+static Plan plan_gemm(int M, int N, int K) {
+  Plan p{};
+  const int cus = cu_count();
+  if (M <= 64) {
+    p.kind = 0;
+    p.MT = (M + 15) / 16;
+    p.NS = (M <= 16) ? 2 : 4;
+    if (N % (p.NS * 16) != 0) p.NS = 2;
+    p.nt = N / (p.NS * 16);
+    p.mt = 1;
+    // split K across blocks until there are ~2 blocks per CU (each wave keeps >= 256 of K)
+    p.S = 1;
+    while (p.nt * p.S < 2 * cus && K % (p.S * 2 * 8 * 32) == 0 && K / (p.S * 2) >= 8 * 256) p.S *= 2;
+    return p;
+  }
+  // tiled: pick the config with the best estimated time = rounds * tile work,
+  // tile work ~ BM*BN*(K/S) / efficiency(config)
+  double best = 1e30;
+  for (int c = 0; c < 4; ++c) {
+    const int BMc = kTiles[c][0], BNc = kTiles[c][1];
+    if (N % BNc) continue;
+    if (BMc > 128 && M <= 128) continue;
+    const int mt = (M + BMc - 1) / BMc, nt = N / BNc;
+    const double eff = (c == 0) ? 0.55 : (c == 1 ? 0.8 : 1.0);   // larger register tiles feed MFMA better
+    for (int S = 1; S <= 8; S *= 2) {
+      if (K % (S * BK) || K / S < 4 * BK) break;
+      const int tiles = mt * nt * S;
+      const int rounds = (tiles + cus - 1) / cus;
+      double t = (double)rounds * BMc * BNc * (double)(K / S) / eff;
+      if (S > 1) t += 4.0 * S * (double)M * N / 64.0;   // partial-sum traffic penalty
+      if (t < best * 0.98) {
+        best = t;
+        p.kind = 1 + c; p.mt = mt; p.nt = nt; p.S = S;
+      }
+    }
+  }
+  if (p.kind == 0) { p.kind = 1; p.mt = (M + 63) / 64; p.nt = N / 128; p.S = 1; }
+  return p;
 }
 
 size_t gemm_workspace_bytes(int M, int N, int K) {
-  const int s = choose_splits(M, N, K);
-  return s > 1 ? (size_t)s * M * N * sizeof(float) : 0;
+  const Plan p = plan_gemm(M, N, K);
+  return p.S > 1 ? (size_t)p.S * M * N * sizeof(float) : 0;
 }
 
 template <int EPI>
-static hipError_t gemm_bf16_launch(const void* A, int lda, const void* W, int ldw, void* C, int ldc,
-                                   int M, int N, int K, void* ws, size_t ws_bytes, hipStream_t st) {
-  int S = choose_splits(M, N, K);
-  if (S > 1 && (ws == nullptr || ws_bytes < (size_t)S * M * N * sizeof(float))) S = 1;
-  dim3 grid(N / BN, (M + BM - 1) / BM, S);
-  if (S == 1) {
-    hipLaunchKernelGGL((gemm_bf16_kernel<EPI, false>), grid, dim3(256), 0, st, (const bf16_t*)A,
-                       lda, (const bf16_t*)W, ldw, C, ldc, M, N, K, K, (float*)nullptr);
-    return hipGetLastError();
-  }
-  hipLaunchKernelGGL((gemm_bf16_kernel<EPI, true>), grid, dim3(256), 0, st, (const bf16_t*)A, lda,
-                     (const bf16_t*)W, ldw, C, ldc, M, N, K, K / S, (float*)ws);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+static hipError_t reduce_launch(const void* ws, int S, int M, int N, void* C, int ldc,
+                                hipStream_t st) {
   const int64_t nout = (EPI == EPI_SWIGLU) ? (int64_t)M * (N / 2) : (int64_t)M * N;
   int64_t blocks = (nout + 255) / 256;
   if (blocks > 16384) blocks = 16384;
   hipLaunchKernelGGL(splitk_reduce_kernel<EPI>, dim3((unsigned)blocks), dim3(256), 0, st,
                      (const float*)ws, S, M, N, C, ldc);
   return hipGetLastError();
+}
+
+template <int EPI, int MT, int NS>
+static void skinny_go(const Plan& p, const void* A, int lda, const void* W, int ldw, void* C,
+                      int ldc, int M, int N, int K, void* ws, hipStream_t st) {
+  const dim3 grid(p.nt * p.S), blk(512);
+  if (p.S == 1)
+    hipLaunchKernelGGL((gemm_skinny_kernel<MT, NS, EPI, false>), grid, blk, 0, st, (const bf16_t*)A,
+                       lda, (const bf16_t*)W, ldw, C, ldc, M, N, K, K, p.nt, (float*)nullptr);
+  else
+    hipLaunchKernelGGL((gemm_skinny_kernel<MT, NS, EPI, true>), grid, blk, 0, st, (const bf16_t*)A,
+                       lda, (const bf16_t*)W, ldw, C, ldc, M, N, K, K / p.S, p.nt, (float*)ws);
+}
+
+template <int EPI, int BM_, int BN_, int WGM, int WGN>
+static void tiled_go(const Plan& p, const void* A, int lda, const void* W, int ldw, void* C,
+                     int ldc, int M, int N, int K, void* ws, hipStream_t st) {
+  const dim3 grid(p.mt * p.nt * p.S), blk(256);
+  if (p.S == 1)
+    hipLaunchKernelGGL((gemm_tiled_kernel<BM_, BN_, WGM, WGN, EPI, false>), grid, blk, 0, st,
+                       (const bf16_t*)A, lda, (const bf16_t*)W, ldw, C, ldc, M, N, K, K, p.mt, p.nt,
+                       (float*)nullptr);
+  else
+    hipLaunchKernelGGL((gemm_tiled_kernel<BM_, BN_, WGM, WGN, EPI, true>), grid, blk, 0, st,
+                       (const bf16_t*)A, lda, (const bf16_t*)W, ldw, C, ldc, M, N, K, K / p.S, p.mt,
+                       p.nt, (float*)ws);
+}
+
+template <int EPI>
+static hipError_t gemm_bf16_launch(const void* A, int lda, const void* W, int ldw, void* C, int ldc,
+                                   int M, int N, int K, void* ws, size_t ws_bytes, hipStream_t st) {
+  Plan p = plan_gemm(M, N, K);
+  if (p.S > 1 && (ws == nullptr || ws_bytes < (size_t)p.S * M * N * sizeof(float)))
+    return hipErrorInvalidValue;
+  if (p.kind == 0) {
+    if (p.NS == 2) {
+      switch (p.MT) {
+        case 1: skinny_go<EPI, 1, 2>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+        case 2: skinny_go<EPI, 2, 2>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+        case 3: skinny_go<EPI, 3, 2>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+        default: skinny_go<EPI, 4, 2>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+      }
+    } else {
+      switch (p.MT) {
+        case 1: skinny_go<EPI, 1, 4>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+        case 2: skinny_go<EPI, 2, 4>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+        case 3: skinny_go<EPI, 3, 4>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+        default: skinny_go<EPI, 4, 4>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+      }
+    }
+  } else {
+    switch (p.kind) {
+      case 1: tiled_go<EPI, 64, 128, 1, 4>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+      case 2: tiled_go<EPI, 128, 128, 2, 2>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+      case 3: tiled_go<EPI, 128, 256, 2, 2>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+      default: tiled_go<EPI, 256, 128, 2, 2>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+    }
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.S == 1) return e;
+  return reduce_launch<EPI>(ws, p.S, M, N, C, ldc, st);
 }
 
 template <int EPI>
@@ -271,7 +460,7 @@ hipError_t launch_gemm(bool bf16, const void* A, int lda, const void* W, int ldw
     }
     return hipErrorInvalidValue;
   }
-  if (N % BN != 0 || K % BK != 0) return hipErrorInvalidValue;
+  if (N % 128 != 0 || K % 256 != 0) return hipErrorInvalidValue;
   switch (epi) {
     case EPI_F32: return gemm_bf16_launch<EPI_F32>(A, lda, W, ldw, C, ldc, M, N, K, ws, ws_bytes, st);
     case EPI_BF16: return gemm_bf16_launch<EPI_BF16>(A, lda, W, ldw, C, ldc, M, N, K, ws, ws_bytes, st);
