@@ -5,10 +5,11 @@
 // rows; output silu(gate) * up as bf16).
 //
 // Two kernel families, chosen per launch from (M, N, K):
-//  * tiled: BM x BN block tile staged through LDS (register-staged double
-//    buffer, BK = 64), 4 wavefronts each owning a WM x WN register tile;
-//    blocks are renumbered so that the blocks an XCD runs are neighbours in
-//    (m, n) and share operand tiles in that XCD's L2.
+//  * tiled: BM x BN block tile staged through LDS, 4 wavefronts each owning
+//    a WM x WN register tile; blocks are renumbered so that the blocks an XCD
+//    runs are neighbours in (m, n) and share operand tiles in that XCD's L2.
+//    The 64x128 tile uses a register-staged double buffer; the larger tiles
+//    use direct global->LDS loads through a 3-4 deep ring of LDS stages.
 //  * skinny (M <= 64, weight-bandwidth bound): no LDS for operands; each
 //    wavefront loads W and A fragments straight into MFMA operand registers,
 //    8 wavefronts of a block split K and are reduced through LDS.
@@ -132,6 +133,140 @@ __global__ void __launch_bounds__(256) gemm_tiled_kernel(const bf16_t* __restric
       sstore(buf ^ 1);
       __syncthreads();
     }
+  }
+
+  const int rb = m0 + wm * WM, cb = n0 + wn * WN;
+  if constexpr (SPLIT) {
+    float* P = ws + (int64_t)z * M * N;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) store_partial(P, M, N, rb + 16 * i, cb + 16 * j, lane, acc[i][j]);
+  } else if constexpr (EPI == EPI_SWIGLU) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; j += 2)
+        store_swiglu((bf16_t*)C, ldc, M, rb + 16 * i, cb + 16 * j, lane, acc[i][j], acc[i][j + 1]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) store_tile<EPI>(C, ldc, M, rb + 16 * i, cb + 16 * j, lane, acc[i][j]);
+  }
+}
+
+// ------------------------------------------------------- tiled, LDS DMA
+// Same tile math as above, but operand tiles travel global -> LDS with
+// direct 16-byte LDS loads (no staging registers) through a STAGES-deep ring
+// of LDS buffers.  A 64-wide K slice of a row is 8 chunks of 16 bytes; chunk
+// c of row r is stored at chunk position c ^ (r & 7) of that row so that the
+// 16-byte fragment reads of 8 consecutive rows hit distinct banks.  Rows of A
+// past M load row M-1 (their results are never stored).
+// s_waitcnt vmcnt(N) (gfx9 encoding: vmcnt bits 3:0 and 15:14; expcnt and
+// lgkmcnt left at their "don't wait" maxima)
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+template <int BM, int BN, int WGM, int WGN, int STAGES, int EPI, bool SPLIT>
+__global__ void __launch_bounds__(256) gemm_dma_kernel(const bf16_t* __restrict__ A, int lda,
+                                                       const bf16_t* __restrict__ W, int ldw,
+                                                       void* __restrict__ C, int ldc, int M,
+                                                       int N, int K, int k_chunk, int mt, int nt,
+                                                       float* __restrict__ ws) {
+  constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 16, TN = WN / 16;
+  constexpr int AI = BM / 32, WI = BN / 32;       // 1 KB load instructions per wave per stage
+  constexpr int STAGE_ELEMS = (BM + BN) * BK;      // bf16 elements per stage
+  extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int nb = gridDim.x;
+  int b = blockIdx.x;
+  const int full = (nb / 8) * 8;
+  if (b < full) b = (b % 8) * (full / 8) + b / 8;
+  const int mi = b % mt, ni = (b / mt) % nt, z = b / (mt * nt);
+  const int m0 = mi * BM, n0 = ni * BN;
+  const int kbeg = z * k_chunk;
+  const int nk = k_chunk / BK;
+
+  // per-lane global source rows for this wave's load instructions
+  const int lrow = lane >> 3;                     // row within an 8-row instruction
+  const int gchunk = (lane & 7) ^ lrow;           // swizzled source chunk
+  const bf16_t* asrc[AI];
+  const bf16_t* wsrc[WI];
+#pragma unroll
+  for (int j = 0; j < AI; ++j) {
+    int r = m0 + wave * (BM / 4) + 8 * j + lrow;
+    r = r < M ? r : M - 1;
+    asrc[j] = A + (int64_t)r * lda + kbeg + gchunk * 8;
+  }
+#pragma unroll
+  for (int j = 0; j < WI; ++j)
+    wsrc[j] = W + (int64_t)(n0 + wave * (BN / 4) + 8 * j + lrow) * ldw + kbeg + gchunk * 8;
+
+  auto issue = [&](int kt, int buf) {
+    bf16_t* sa = smem + buf * STAGE_ELEMS;
+    bf16_t* sw = sa + BM * BK;
+#pragma unroll
+    for (int j = 0; j < AI; ++j)
+      __builtin_amdgcn_global_load_lds((const void*)(asrc[j] + kt * BK),
+                                       (lds_void_t*)(sa + (wave * (BM / 4) + 8 * j) * BK), 16, 0, 0);
+#pragma unroll
+    for (int j = 0; j < WI; ++j)
+      __builtin_amdgcn_global_load_lds((const void*)(wsrc[j] + kt * BK),
+                                       (lds_void_t*)(sw + (wave * (BN / 4) + 8 * j) * BK), 16, 0, 0);
+  };
+
+  f32x4_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nk) issue(s, s);
+
+  const int fr = lane & 15, fq = lane >> 4;
+  for (int kt = 0; kt < nk; ++kt) {
+    // this wave's loads of stage kt are done once at most the (STAGES-2) later
+    // stages' loads are outstanding (all outstanding in the last stages); the
+    // raw barrier then publishes every wave's stage kt (no memory fence: it
+    // would drain the prefetches still in flight)
+    if (kt + STAGES - 2 < nk) vm_wait<(STAGES - 2) * (AI + WI)>();
+    else vm_wait<0>();
+    __builtin_amdgcn_s_barrier();
+    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
+    const bf16_t* sa = smem + (kt % STAGES) * STAGE_ELEMS;
+    const bf16_t* sw = sa + BM * BK;
+    // fragments of both 32-wide K halves are read before the MFMAs of the
+    // first half, so LDS latency overlaps matrix work
+    bf16x8_t a[2][TM], bb[2][TN];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int r = wm * WM + 16 * i + fr;
+        a[ks][i] = *(const bf16x8_t*)(sa + r * BK + (((ks * 4 + fq) ^ (r & 7)) * 8));
+      }
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int r = wn * WN + 16 * j + fr;
+        bb[ks][j] = *(const bf16x8_t*)(sw + r * BK + (((ks * 4 + fq) ^ (r & 7)) * 8));
+      }
+    }
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks][i], bb[ks][j], acc[i][j], 0, 0, 0);
   }
 
   const int rb = m0 + wm * WM, cb = n0 + wn * WN;
@@ -381,6 +516,31 @@ static void skinny_go(const Plan& p, const void* A, int lda, const void* W, int 
                        lda, (const bf16_t*)W, ldw, C, ldc, M, N, K, K / p.S, p.nt, (float*)ws);
 }
 
+template <int EPI, int BM_, int BN_, int WGM, int WGN, int ST>
+static void dma_go(const Plan& p, const void* A, int lda, const void* W, int ldw, void* C, int ldc,
+                   int M, int N, int K, void* ws, hipStream_t st) {
+  const dim3 grid(p.mt * p.nt * p.S), blk(256);
+  const size_t lds = (size_t)ST * (BM_ + BN_) * BK * sizeof(bf16_t);
+  static bool attr_done[2] = {false, false};
+  if (p.S == 1) {
+    auto kern = gemm_dma_kernel<BM_, BN_, WGM, WGN, ST, EPI, false>;
+    if (!attr_done[0]) {
+      (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      attr_done[0] = true;
+    }
+    hipLaunchKernelGGL(kern, grid, blk, lds, st, (const bf16_t*)A, lda, (const bf16_t*)W, ldw, C,
+                       ldc, M, N, K, K, p.mt, p.nt, (float*)nullptr);
+  } else {
+    auto kern = gemm_dma_kernel<BM_, BN_, WGM, WGN, ST, EPI, true>;
+    if (!attr_done[1]) {
+      (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      attr_done[1] = true;
+    }
+    hipLaunchKernelGGL(kern, grid, blk, lds, st, (const bf16_t*)A, lda, (const bf16_t*)W, ldw, C,
+                       ldc, M, N, K, K / p.S, p.mt, p.nt, (float*)ws);
+  }
+}
+
 template <int EPI, int BM_, int BN_, int WGM, int WGN>
 static void tiled_go(const Plan& p, const void* A, int lda, const void* W, int ldw, void* C,
                      int ldc, int M, int N, int K, void* ws, hipStream_t st) {
@@ -420,9 +580,9 @@ static hipError_t gemm_bf16_launch(const void* A, int lda, const void* W, int ld
   } else {
     switch (p.kind) {
       case 1: tiled_go<EPI, 64, 128, 1, 4>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
-      case 2: tiled_go<EPI, 128, 128, 2, 2>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
-      case 3: tiled_go<EPI, 128, 256, 2, 2>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
-      default: tiled_go<EPI, 256, 128, 2, 2>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+      case 2: dma_go<EPI, 128, 128, 2, 2, 4>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+      case 3: dma_go<EPI, 128, 256, 2, 2, 3>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+      default: dma_go<EPI, 256, 128, 2, 2, 3>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
     }
   }
   hipError_t e = hipGetLastError();
