@@ -4,9 +4,11 @@
 // keys; key j sits in page page_table[pt_row][j/16], slot j%16, kv head
 // h / G (G = Hq/Hkv).
 //
-// Work unit = (row, kv head, chunk of C pages), one wavefront each, taken
-// from a device-built work list with a grid-stride loop (no host round trip,
-// no idle blocks for ragged contexts).  Per pair of pages (32 keys):
+// Work unit = (row, kv head, chunk of C pages), one wavefront each, with a
+// grid-stride loop.  Rows of equal context (every decode step) map units
+// arithmetically; ragged contexts use a work list built on the device (no
+// host round trip, no idle blocks).  Contexts are split into chunks only when
+// there are too few (row, kv head) units to fill the GPU.  Per pair of pages (32 keys):
 //   S[16 x 32]  = Q[16 x hd] . K^T      MFMA 16x16x32 bf16 (the G query heads
 //                                       sharing the kv head fill rows 0..G-1)
 //   online softmax per head row (16-lane shuffles)
@@ -69,36 +71,54 @@ __global__ void attn_plan_kernel(CtxSpec cs, int n_rows, int chunk_tokens, int32
   if (tid == 0) info[0] = running;
 }
 
+struct AttnBf16Args {
+  const bf16_t* q; const bf16_t* kpool; const bf16_t* vpool;
+  const int32_t* page_table; int pt_stride; CtxSpec cs; int hq, hkv, chunk_pages;
+  int n_rows;
+  int uniform_nch;            // > 0: every row has this many chunks, no work list
+  const int2* work; const int32_t* chunk_off; const int32_t* info;
+  float* ws_o; float2* ws_ml; bf16_t* out;
+};
+
+// K and V of one pair of pages (32 keys) for one kv head, in MFMA operand layout
 template <int HD>
-__global__ void __launch_bounds__(256) attn_bf16_kernel(
-    const bf16_t* __restrict__ q, const bf16_t* __restrict__ kpool, const bf16_t* __restrict__ vpool,
-    const int32_t* __restrict__ page_table, int pt_stride, CtxSpec cs, int hq, int hkv,
-    int chunk_pages, const int2* __restrict__ work, const int32_t* __restrict__ chunk_off,
-    const int32_t* __restrict__ info, float* __restrict__ ws_o, float2* __restrict__ ws_ml,
-    bf16_t* __restrict__ out) {
+struct PagePair {
+  bf16x8_t ka[HD / 32], kb[HD / 32], vv[HD / 16];
+  bool hasb;
+};
+
+template <int HD>
+__global__ void __launch_bounds__(256) attn_bf16_kernel(AttnBf16Args A) {
   constexpr int NKK = HD / 32, NNB = HD / 16, PST = 40;   // P row stride (bf16), 80 B
   __shared__ __attribute__((aligned(16))) bf16_t plds[4][16 * PST];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int hq = A.hq, hkv = A.hkv;
   const int G = hq / hkv;
   const int quad = lane >> 4, col = lane & 15;
   const float scale = 1.0f / sqrtf((float)HD);
-  const int total = info[0] * hkv;
+  const int total = (A.uniform_nch > 0 ? A.n_rows * A.uniform_nch : A.info[0]) * hkv;
   bf16_t* P = plds[w];
   for (int item = blockIdx.x * 4 + w; item < total; item += gridDim.x * 4) {
     const int wi = item / hkv, kvh = item - wi * hkv;
-    const int2 rc = work[wi];
-    const int row = rc.x, chunk = rc.y;
-    const int ctx = ctx_of(cs, row);
-    const int ptr = cs.row_pt ? cs.row_pt[row] : row;
-    const int32_t* pt = page_table + (int64_t)ptr * pt_stride;
+    int row, chunk, cid;
+    if (A.uniform_nch > 0) {
+      row = wi / A.uniform_nch; chunk = wi - row * A.uniform_nch; cid = wi;
+    } else {
+      const int2 rc = A.work[wi];
+      row = rc.x; chunk = rc.y; cid = A.chunk_off[row] + chunk;
+    }
+    const int ctx = ctx_of(A.cs, row);
+    const int ptr = A.cs.row_pt ? A.cs.row_pt[row] : row;
+    const int32_t* pt = A.page_table + (int64_t)ptr * A.pt_stride;
     const int npg = (ctx + kPage - 1) / kPage;
-    const int pbeg = chunk * chunk_pages;
-    const int pend = min(pbeg + chunk_pages, npg);
+    const int nch = (npg + A.chunk_pages - 1) / A.chunk_pages;
+    const int pbeg = chunk * A.chunk_pages;
+    const int pend = min(pbeg + A.chunk_pages, npg);
 
     bf16x8_t qa[NKK];
     {
       const bool valid = col < G;
-      const bf16_t* qrow = q + ((int64_t)row * hq + kvh * G + (valid ? col : 0)) * HD + quad * 8;
+      const bf16_t* qrow = A.q + ((int64_t)row * hq + kvh * G + (valid ? col : 0)) * HD + quad * 8;
 #pragma unroll
       for (int kk = 0; kk < NKK; ++kk) {
         u32x4_t v = valid ? *(const u32x4_t*)(qrow + 32 * kk) : (u32x4_t){0u, 0u, 0u, 0u};
@@ -112,35 +132,33 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(
 #pragma unroll
     for (int nb = 0; nb < NNB; ++nb) O[nb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 
-    for (int p = pbeg; p < pend; p += 2) {
-      const int pa = clamp_page(cs, pt[p]);
-      const bool hasb = (p + 1) < pend;
-      const int pb = hasb ? clamp_page(cs, pt[p + 1]) : pa;
-      bf16x8_t ka[NKK], kb[NKK], vv[NNB];
-      const bf16_t* kpa = kpool + k_off(pa, kvh, col, quad * 8, hkv, HD);
-      const bf16_t* kpb = kpool + k_off(pb, kvh, col, quad * 8, hkv, HD);
+    auto load = [&](int p, PagePair<HD>& F, int ida, int idb) {
+      const int pa = clamp_page(A.cs, ida);
+      F.hasb = (p + 1) < pend;
+      const int pb = F.hasb ? clamp_page(A.cs, idb) : pa;
+      const bf16_t* kpa = A.kpool + k_off(pa, kvh, col, quad * 8, hkv, HD);
+      const bf16_t* kpb = A.kpool + k_off(pb, kvh, col, quad * 8, hkv, HD);
 #pragma unroll
       for (int kk = 0; kk < NKK; ++kk) {
-        ka[kk] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(kpa + 32 * kk));
-        kb[kk] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(kpb + 32 * kk));
+        F.ka[kk] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(kpa + 32 * kk));
+        F.kb[kk] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(kpb + 32 * kk));
       }
-      {
-        const int vpage = quad < 2 ? pa : pb;
-        const int slot0 = (quad & 1) * 8;
-        const bf16_t* vb = vpool + v_off(vpage, kvh, slot0, col, hkv, HD);
+      const int vpage = quad < 2 ? pa : pb;
+      const bf16_t* vb = A.vpool + v_off(vpage, kvh, (quad & 1) * 8, col, hkv, HD);
 #pragma unroll
-        for (int nb = 0; nb < NNB; ++nb)
-          vv[nb] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(vb + nb * 16 * 8));
-      }
+      for (int nb = 0; nb < NNB; ++nb)
+        F.vv[nb] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(vb + nb * 16 * 8));
+    };
+    auto compute = [&](int p, const PagePair<HD>& F) {
       f32x4_t sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kk = 0; kk < NKK; ++kk) {
-        sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kk], ka[kk], sa, 0, 0, 0);
-        sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kk], kb[kk], sb, 0, 0, 0);
+        sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kk], F.ka[kk], sa, 0, 0, 0);
+        sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kk], F.kb[kk], sb, 0, 0, 0);
       }
-      // lane holds S[head 4*quad+i][token p*16+col] (sa) and [(p+1)*16+col] (sb)
+      // lane holds S[head 4*quad+i][key p*16+col] (sa) and [(p+1)*16+col] (sb)
       const bool va = p * kPage + col < ctx;
-      const bool vb2 = hasb && ((p + 1) * kPage + col < ctx);
+      const bool vb2 = F.hasb && ((p + 1) * kPage + col < ctx);
       float pva[4], pvb[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -171,12 +189,28 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
       const bf16x8_t pa8 = *(const bf16x8_t*)(&P[col * PST + quad * 8]);
 #pragma unroll
-      for (int nb = 0; nb < NNB; ++nb) O[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa8, vv[nb], O[nb], 0, 0, 0);
-      __builtin_amdgcn_wave_barrier();   // P is rewritten next iteration
+      for (int nb = 0; nb < NNB; ++nb)
+        O[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa8, F.vv[nb], O[nb], 0, 0, 0);
+      __builtin_amdgcn_wave_barrier();   // P is rewritten by the next pair
+    };
+
+    // page ids of the next pair are fetched one iteration ahead so that the
+    // dependent page-id -> key/value load chain is not serial
+    PagePair<HD> F;
+    int nxa = pbeg < pend ? pt[pbeg] : 0;
+    int nxb = pbeg + 1 < pend ? pt[pbeg + 1] : nxa;
+    for (int p = pbeg; p < pend; p += 2) {
+      const int ca = nxa, cb = nxb;
+      if (p + 2 < pend) {
+        nxa = pt[p + 2];
+        nxb = p + 3 < pend ? pt[p + 3] : nxa;
+      }
+      load(p, F, ca, cb);
+      compute(p, F);
     }
-    // finish: per head row, total softmax denominator over the 16 lanes
-    const int nch = (npg + chunk_pages - 1) / chunk_pages;
-    const int cid = chunk_off[row] + chunk;
+
+    // per head row: softmax denominator over the 16 lanes of the row
+    float lrow[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       float l = lpart[i];
@@ -184,20 +218,31 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(
       l += __shfl_xor(l, 2, 64);
       l += __shfl_xor(l, 4, 64);
       l += __shfl_xor(l, 8, 64);
+      lrow[i] = l;
+    }
+    if (nch == 1) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int h = 4 * quad + i;
+        if (h >= G) continue;
+        const float inv = 1.0f / lrow[i];
+        bf16_t* orow = A.out + ((int64_t)row * hq + kvh * G + h) * HD + col;
+#pragma unroll
+        for (int nb = 0; nb < NNB; ++nb) orow[nb * 16] = f32_to_bf16(O[nb][i] * inv);
+      }
+      continue;
+    }
+    // several chunks: write this chunk's unnormalised partial; the combine
+    // kernel merges the chunks of a row
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
       const int h = 4 * quad + i;
       if (h >= G) continue;
       const int qh = kvh * G + h;
-      if (nch == 1) {
-        const float inv = 1.0f / l;
-        bf16_t* orow = out + ((int64_t)row * hq + qh) * HD + col;
+      float* po = A.ws_o + ((int64_t)cid * hq + qh) * HD + col;
 #pragma unroll
-        for (int nb = 0; nb < NNB; ++nb) orow[nb * 16] = f32_to_bf16(O[nb][i] * inv);
-      } else {
-        float* po = ws_o + ((int64_t)cid * hq + qh) * HD + col;
-#pragma unroll
-        for (int nb = 0; nb < NNB; ++nb) po[nb * 16] = O[nb][i];
-        if (col == 0) ws_ml[(int64_t)cid * hq + qh] = make_float2(mrun[i], l);
-      }
+      for (int nb = 0; nb < NNB; ++nb) po[nb * 16] = O[nb][i];
+      if (col == 0) A.ws_ml[(int64_t)cid * hq + qh] = make_float2(mrun[i], lrow[i]);
     }
   }
 }
@@ -296,17 +341,24 @@ __global__ void attn_combine_kernel(CtxSpec cs, int n_rows, int hq, int hd, int 
   }
 }
 
+// Pages per chunk: the whole context while there are at least ~8 (row, kv
+// head) units per CU, otherwise the context is cut so that about 4096
+// wavefronts run (an even page count, at least 8 pages per chunk).
 static int choose_chunk_pages(int n_rows, int hkv, int max_ctx) {
-  const int64_t pages = (int64_t)n_rows * ((max_ctx + kPage - 1) / kPage) * hkv;
-  int c = 2;
-  while (c < 64 && pages / c > 8192) c *= 2;
-  return c;
+  const int64_t units = (int64_t)n_rows * hkv;
+  const int npg = (max_ctx + kPage - 1) / kPage;
+  if (units >= 2048) return npg + (npg & 1);
+  int64_t nch = (4096 + units - 1) / units;
+  int c = (int)((npg + nch - 1) / nch);
+  if (c < 8) c = 8;
+  return c + (c & 1);
 }
 
 struct AttnWs {
   int32_t* chunk_off; int2* work; int32_t* info; float* ws_o; float2* ws_ml;
 };
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+// Workspace: [chunk_off | work list | info | partial o | partial (m, l)].
 static size_t ws_layout(int n_rows, int hq, int hkv, int hd, int max_ctx, char* base, AttnWs* w) {
   const int cp = choose_chunk_pages(n_rows, hkv, max_ctx);
   const int64_t maxch = (int64_t)n_rows * ((max_ctx + cp * kPage - 1) / (cp * kPage));
@@ -329,14 +381,6 @@ size_t attn_workspace_bytes(int n_rows, int hq, int hkv, int hd, int max_ctx) {
 }
 
 template <int HD>
-static void attn_bf16_go(dim3 grid, hipStream_t st, const void* q, const void* k, const void* v,
-                         const int32_t* pt, int pts, CtxSpec cs, int hq, int hkv, int cp, AttnWs w,
-                         void* out) {
-  hipLaunchKernelGGL(attn_bf16_kernel<HD>, grid, dim3(256), 0, st, (const bf16_t*)q,
-                     (const bf16_t*)k, (const bf16_t*)v, pt, pts, cs, hq, hkv, cp, w.work,
-                     w.chunk_off, w.info, w.ws_o, w.ws_ml, (bf16_t*)out);
-}
-template <int HD>
 static void attn_f32_go(dim3 grid, hipStream_t st, const void* q, const void* k, const void* v,
                         const int32_t* pt, int pts, CtxSpec cs, int hq, int hkv, int cp, AttnWs w,
                         void* out) {
@@ -345,6 +389,7 @@ static void attn_f32_go(dim3 grid, hipStream_t st, const void* q, const void* k,
                      w.chunk_off, w.info, w.ws_o, w.ws_ml, (float*)out);
 }
 
+// uniform: every row has the same context (cs.ctx_len == NULL, cs.mod == 0)
 hipError_t launch_attention_spec(const void* q, const void* k_pool, const void* v_pool,
                                  const int32_t* page_table, int pt_stride, CtxSpec cs, int n_rows,
                                  int hq, int hkv, int hd, int max_ctx, bool bf16, void* out,
@@ -355,35 +400,49 @@ hipError_t launch_attention_spec(const void* q, const void* k_pool, const void* 
   const size_t need = ws_layout(n_rows, hq, hkv, hd, max_ctx, (char*)ws, &w);
   if (ws == nullptr || ws_bytes < need) return hipErrorInvalidValue;
   const int cp = choose_chunk_pages(n_rows, hkv, max_ctx);
-  hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(1024), 0, st, cs, n_rows, cp * kPage,
-                     w.chunk_off, w.work, w.info);
-  const int64_t maxch = (int64_t)n_rows * ((max_ctx + cp * kPage - 1) / (cp * kPage));
+  const bool uniform = bf16 && cs.ctx_len == nullptr && cs.mod == 0;
+  const int uni_nch = uniform ? ((min(cs.base, max_ctx) + cp * kPage - 1) / (cp * kPage)) : 0;
+  if (!uniform)
+    hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(1024), 0, st, cs, n_rows, cp * kPage,
+                       w.chunk_off, w.work, w.info);
+  const int64_t maxch = uniform ? (int64_t)n_rows * uni_nch
+                                : (int64_t)n_rows * ((max_ctx + cp * kPage - 1) / (cp * kPage));
   const int64_t items = maxch * (bf16 ? hkv : hq);
   int64_t blocks = (items + 3) / 4;
   if (blocks > 2048) blocks = 2048;
   if (blocks < 1) blocks = 1;
   const dim3 grid((unsigned)blocks);
   if (bf16) {
-    if (hd == 128) attn_bf16_go<128>(grid, st, q, k_pool, v_pool, page_table, pt_stride, cs, hq, hkv, cp, w, out);
-    else if (hd == 64) attn_bf16_go<64>(grid, st, q, k_pool, v_pool, page_table, pt_stride, cs, hq, hkv, cp, w, out);
-    else if (hd == 32) attn_bf16_go<32>(grid, st, q, k_pool, v_pool, page_table, pt_stride, cs, hq, hkv, cp, w, out);
+    AttnBf16Args a;
+    a.q = (const bf16_t*)q; a.kpool = (const bf16_t*)k_pool; a.vpool = (const bf16_t*)v_pool;
+    a.page_table = page_table; a.pt_stride = pt_stride; a.cs = cs; a.hq = hq; a.hkv = hkv;
+    a.chunk_pages = cp; a.n_rows = n_rows; a.uniform_nch = uni_nch;
+    a.work = w.work; a.chunk_off = w.chunk_off; a.info = w.info;
+    a.ws_o = w.ws_o; a.ws_ml = w.ws_ml; a.out = (bf16_t*)out;
+    if (hd == 128) hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, dim3(256), 0, st, a);
+    else if (hd == 64) hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, dim3(256), 0, st, a);
+    else if (hd == 32) hipLaunchKernelGGL(attn_bf16_kernel<32>, grid, dim3(256), 0, st, a);
     else return hipErrorInvalidValue;
-  } else {
-    if (hd == 128) attn_f32_go<128>(grid, st, q, k_pool, v_pool, page_table, pt_stride, cs, hq, hkv, cp, w, out);
-    else if (hd == 64) attn_f32_go<64>(grid, st, q, k_pool, v_pool, page_table, pt_stride, cs, hq, hkv, cp, w, out);
-    else if (hd == 32) attn_f32_go<32>(grid, st, q, k_pool, v_pool, page_table, pt_stride, cs, hq, hkv, cp, w, out);
-    else return hipErrorInvalidValue;
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if ((max_ctx + cp * kPage - 1) / (cp * kPage) > 1) {
+      const int64_t nb = ((int64_t)n_rows * hq + 3) / 4;
+      hipLaunchKernelGGL(attn_combine_kernel<bf16_t>, dim3((unsigned)nb), dim3(256), 0, st, cs,
+                         n_rows, hq, hd, cp * kPage, w.chunk_off, w.ws_o, w.ws_ml, (bf16_t*)out);
+      e = hipGetLastError();
+    }
+    return e;
   }
+  if (hd == 128) attn_f32_go<128>(grid, st, q, k_pool, v_pool, page_table, pt_stride, cs, hq, hkv, cp, w, out);
+  else if (hd == 64) attn_f32_go<64>(grid, st, q, k_pool, v_pool, page_table, pt_stride, cs, hq, hkv, cp, w, out);
+  else if (hd == 32) attn_f32_go<32>(grid, st, q, k_pool, v_pool, page_table, pt_stride, cs, hq, hkv, cp, w, out);
+  else return hipErrorInvalidValue;
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if ((max_ctx + cp * kPage - 1) / (cp * kPage) > 1) {
     const int64_t nb = ((int64_t)n_rows * hq + 3) / 4;
-    if (bf16)
-      hipLaunchKernelGGL(attn_combine_kernel<bf16_t>, dim3((unsigned)nb), dim3(256), 0, st, cs,
-                         n_rows, hq, hd, cp * kPage, w.chunk_off, w.ws_o, w.ws_ml, (bf16_t*)out);
-    else
-      hipLaunchKernelGGL(attn_combine_kernel<float>, dim3((unsigned)nb), dim3(256), 0, st, cs,
-                         n_rows, hq, hd, cp * kPage, w.chunk_off, w.ws_o, w.ws_ml, (float*)out);
+    hipLaunchKernelGGL(attn_combine_kernel<float>, dim3((unsigned)nb), dim3(256), 0, st, cs,
+                       n_rows, hq, hd, cp * kPage, w.chunk_off, w.ws_o, w.ws_ml, (float*)out);
     e = hipGetLastError();
   }
   return e;
