@@ -99,6 +99,79 @@ def cpu_baseline(model, run, budget_s=20.0):
                        f"{time.perf_counter() - t_start:.1f} s of CPU work")}
 
 
+def kernel_sweep(B, steps, warmup):
+    """Stateless kernels on the sweep's inputs (bf16, data seed 1): decode
+    attention over 1024 trajectories with lognormal(1500, 1.0) contexts clipped
+    to [16, 32768] in a shuffled page pool; the fused sampler on 1024 x 151936
+    logits ~ N(0, 3); selection over 65536 trajectories in groups of 16."""
+    import numpy as np
+    import torch
+    from workload import sweep_attention_inputs, sweep_sampler_logits, sweep_selection_inputs
+    from workload.gen import sweep_page_table
+    from workload.configs import SWEEP
+    out = {"metric": "kernel sweep", "data": "synthetic (sweep inputs, seed 1)"}
+    seed = SWEEP["seed"]
+    hq, hkv, hd = SWEEP["attn_hq"], SWEEP["attn_hkv"], SWEEP["attn_hd"]
+    ctx, rng = sweep_attention_inputs()
+    pt, n_pages = sweep_page_table(ctx.astype(np.int64), 16, rng)
+    rows = len(ctx)
+    q = torch.empty(rows * hq * hd, dtype=torch.bfloat16, device="cuda")
+    kp = torch.empty(n_pages * hkv * 16 * hd, dtype=torch.bfloat16, device="cuda")
+    vp = torch.empty_like(kp)
+    B.darts_fill_uniform(q, 0, seed, B.DARTS_BF16)
+    B.darts_fill_kv_pool(kp, vp, n_pages, hkv, hd, seed, B.DARTS_BF16)
+    ptd = torch.from_numpy(pt).cuda()
+    ctxd = torch.from_numpy(ctx.astype(np.int32)).cuda()
+    o = torch.empty_like(q)
+    max_ctx = int(ctx.max())
+    ws = torch.empty(B.darts_attn_workspace_bytes(rows, hq, hkv, hd, max_ctx), dtype=torch.uint8, device="cuda")
+    alg = float(ctx.sum()) * hkv * hd * 2 * 2 + rows * 2 * hq * hd * 2 + float(np.ceil(ctx / 16).sum()) * 4
+
+    def timed(fn, n):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n * 1e3   # us
+
+    n = max(steps, 10)
+    us = timed(lambda: B.darts_attn_decode(q, kp, vp, n_pages, ptd, ctxd, hq, hkv, hd, max_ctx,
+                                           B.DARTS_BF16, o, ws), n)
+    out["attention"] = {"rows": rows, "sum_ctx": int(ctx.sum()), "algorithmic_bytes": alg, "us": us,
+                        "achieved_GBs": alg / (us * 1e-6) / 1e9,
+                        "frac_of_hbm_peak": alg / (us * 1e-6) / 1e9 / HBM_PEAK_GBS}
+    del kp, vp
+    bits = sweep_sampler_logits()
+    lg = torch.from_numpy(bits.view(np.int16)).cuda().view(torch.bfloat16)
+    R, V = bits.shape
+    traj = torch.arange(R, dtype=torch.int32, device="cuda")
+    stp = torch.zeros(R, dtype=torch.int32, device="cuda")
+    tok = torch.empty(R, dtype=torch.int32, device="cuda")
+    lp = torch.empty(R, dtype=torch.float32, device="cuda")
+    en = torch.empty(R, dtype=torch.float32, device="cuda")
+    us = timed(lambda: B.darts_sample(lg, B.DARTS_BF16, seed, traj, stp, 1.0, None, tok, lp, en), n)
+    out["sampler"] = {"rows": R, "vocab": V, "us": us, "logit_bytes": R * V * 2,
+                      "achieved_GBs": R * V * 2 / (us * 1e-6) / 1e9}
+    raw, mlp = sweep_selection_inputs()
+    cap = SWEEP["sel_cap"]
+    ln = np.minimum(raw, cap).astype(np.int32)
+    st0 = np.where(raw > cap, 2, 1).astype(np.uint8)
+    std = torch.from_numpy(st0).cuda()
+    lnd = torch.from_numpy(ln).cuda()
+    mld = torch.from_numpy(mlp).cuda()
+    m, k = SWEEP["sel_m"], SWEEP["sel_k"]
+    kept = torch.empty((len(ln) // m, k), dtype=torch.int32, device="cuda")
+    comp = torch.empty(len(ln) // m, dtype=torch.uint8, device="cuda")
+    us = timed(lambda: B.darts_select_groups(std, lnd, mld, m, k, 1, 2 * k, 1, kept, comp), n)
+    out["selection"] = {"trajectories": len(ln), "groups": len(ln) // m, "us": us}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -107,7 +180,22 @@ def main():
     ap.add_argument("--config", default="qwen3-8b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-abort", action="store_true", help="counterfactual without early stop")
+    ap.add_argument("--sweep", action="store_true",
+                    help="kernel sweep instead of the rollout: decode attention (1024 rows, 32/8 heads, "
+                         "hd 128, lognormal contexts), fused sampler (1024 x 151936), selection (65536)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="three 1 GiB device copies (reference for HBM byte counters), then exit")
     args = ap.parse_args()
+    if args.copy_calibration:
+        import torch
+        x = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+        y = torch.empty_like(x)
+        x.fill_(1.0)
+        for _ in range(3):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": 1 << 30, "copies": 3}))
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build runs the rollout of one data-parallel "
               "rank (prompt groups are independent); multi-GPU runs are not part of it.",
@@ -121,6 +209,9 @@ def main():
 
     torch.cuda.set_device(0)
     B.load_library()
+    if args.sweep:
+        print(json.dumps(kernel_sweep(B, args.steps, args.warmup)), flush=True)
+        return
     model, run = get_config(args.config)
     prompts, forced = rollout_inputs(model, run)
     flags = B.FLAG_TIMING | (B.FLAG_NO_ABORT if args.no_abort else 0)
@@ -173,7 +264,7 @@ def main():
     peak_mm = BF16_PEAK_TFLOPS if model.dtype == "bf16" else FP32_PEAK_TFLOPS
     gemm_tf = gemm_f / (gemm_ms * 1e-3) / 1e12 if gemm_ms > 0 else 0.0
     cls = {}
-    for i, name in enumerate(["qkv", "o", "gate_up", "down", "lm_head"]):
+    for i, name in enumerate(["qkv", "o", "gate_up", "down", "lm_head", "moe_block"]):
         ms = sum(s["gemm_cls_ms"][i] for s in stats)
         fl = sum(s["gemm_cls_flop"][i] for s in stats)
         cls[name] = {"ms": ms, "tflops": fl / (ms * 1e-3) / 1e12 if ms > 0 else 0.0}

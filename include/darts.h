@@ -71,11 +71,11 @@ typedef struct {
   int32_t n_q_heads;
   int32_t n_kv_heads;    /* n_q_heads % n_kv_heads == 0 (GQA) */
   int32_t head_dim;      /* 32, 64 or 128 */
-  int32_t ffn_dim;       /* dense FFN hidden size */
+  int32_t ffn_dim;       /* dense FFN hidden size (ignored for MoE) */
   int32_t vocab;         /* multiple of 4; the end-of-sequence id is vocab-1 */
-  int32_t n_experts;     /* 0 for dense */
-  int32_t top_k;
-  int32_t expert_ffn;
+  int32_t n_experts;     /* 0 for dense; MoE needs BF16, d_model % 256 == 0 */
+  int32_t top_k;         /* experts per token (renormalised softmax weights) */
+  int32_t expert_ffn;    /* expert SwiGLU hidden size, multiple of 256 */
   float rope_theta;
   float rms_eps;
   int32_t dtype;         /* darts_dtype: F32 (all fp32) or BF16 (bf16 operands,
@@ -129,8 +129,9 @@ typedef struct {
   double gemm_ms;            /* with DARTS_FLAG_TIMING: summed GEMM time (decode and prefill) */
   double gemm_flop;          /* 2*M*N*K summed over those launches */
   int64_t gemm_launches;
-  double gemm_cls_ms[5];     /* per GEMM class: QKV, O, gate-up, down, LM head */
-  double gemm_cls_flop[5];
+  double gemm_cls_ms[6];     /* per GEMM class: QKV, O, gate-up, down, LM head, MoE block
+                                (router + routing + grouped experts + combine) */
+  double gemm_cls_flop[6];
 } darts_stats;
 
 typedef struct darts_ctx darts_ctx;

@@ -154,10 +154,21 @@ def moe_route(cfg, router_w, h):
     return order, w, p
 
 
-def ffn(cfg, lw, h):
+def route_margin(cfg, p):
+    """Per row: probability gap between the k-th and (k+1)-th expert (how far
+    the top-k decision is from a tie)."""
+    srt = -np.sort(-p, axis=-1)
+    if cfg.top_k >= p.shape[-1]:
+        return np.full(p.shape[0], np.inf)
+    return srt[:, cfg.top_k - 1] - srt[:, cfg.top_k]
+
+
+def ffn(cfg, lw, h, margins=None):
     if cfg.n_experts == 0:
         return (silu(h @ lw.wgate.T) * (h @ lw.wup.T)) @ lw.wdown.T
-    ids, w, _ = moe_route(cfg, lw.router, h)
+    ids, w, p = moe_route(cfg, lw.router, h)
+    if margins is not None:
+        margins.append(route_margin(cfg, p))
     out = np.zeros_like(h)
     for r in range(h.shape[0]):
         for j in range(cfg.top_k):
@@ -181,7 +192,7 @@ def attention(q, K, V, n_kv):
     return out
 
 
-def forward_sequence(cfg, W, tokens, cache=None):
+def forward_sequence(cfg, W, tokens, cache=None, margins=None):
     """Causal forward over ``tokens`` appended after an optional cache.
 
     cache: list per layer of (K [ctx, Hkv, hd], V [ctx, Hkv, hd]) or None.
@@ -210,15 +221,17 @@ def forward_sequence(cfg, W, tokens, cache=None):
             o[t] = attention(q[t], K[:ctx], V[:ctx], hkv)
         x = x + o.reshape(n, hq * hd) @ lw.wo.T
         h = rmsnorm(x, cfg.rms_eps)
-        x = x + ffn(cfg, lw, h)
+        x = x + ffn(cfg, lw, h, margins)
     logits = rmsnorm(x, cfg.rms_eps) @ W.lm_head.T
     return logits, new_cache
 
 
-def decode_batch(cfg, W, tokens, caches):
+def decode_batch(cfg, W, tokens, caches, margins=None):
     """One decode step for B sequences that all have the same cached length.
 
     tokens: [B]; caches: list per layer of (K [B, ctx, Hkv, hd], V [B, ctx, Hkv, hd]).
+    margins: optional list; for MoE models one array [B] of routing margins
+    per layer is appended.
     Returns (logits [B, V], caches extended by one position).
     """
     hq, hkv, hd = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
@@ -245,6 +258,6 @@ def decode_batch(cfg, W, tokens, caches):
         o = np.einsum("bhc,bchd->bhd", p, Vx)
         x = x + o.reshape(B, hq * hd) @ lw.wo.T
         h = rmsnorm(x, cfg.rms_eps)
-        x = x + ffn(cfg, lw, h)
+        x = x + ffn(cfg, lw, h, margins)
     logits = rmsnorm(x, cfg.rms_eps) @ W.lm_head.T
     return logits, out_caches

@@ -43,6 +43,7 @@ class RolloutResult:
     logprobs: dict               # g -> list (float64)
     entropies: dict
     margins: dict                # g -> list of top-2 perturbed-score margins
+    route_margins: dict          # g -> list of min MoE routing margin (over layers) per token
     logits: dict                 # g -> list of logit rows (float64) if kept
     status: dict
     length: dict
@@ -81,6 +82,7 @@ def rollout(cfg, W, prompts, forced, m, k, cap, seed, temperature=1.0, L=1, m_up
     ents = {g: [] for g in trajs}
     margins = {g: [] for g in trajs}
     lgs = {g: [] for g in trajs}
+    rmar = {g: [] for g in trajs}
     slp = {g: np.float32(0.0) for g in trajs}
     freed = {g: False for g in trajs}
     refcnt = {i: m for i in ids}
@@ -89,10 +91,13 @@ def rollout(cfg, W, prompts, forced, m, k, cap, seed, temperature=1.0, L=1, m_up
     # prefill
     caches = {}
     last_logits = {}
+    prompt_rmar = {}
     for i in ids:
-        lg, cache = M.forward_sequence(cfg, W, prompts[i])
+        mar = []
+        lg, cache = M.forward_sequence(cfg, W, prompts[i], margins=mar)
         caches[i] = cache
         last_logits[i] = lg[-1]
+        prompt_rmar[i] = float(np.min([m[-1] for m in mar])) if mar else float("inf")
     pages_used = prompt_pages * len(ids)
     hwm = pages_used
     trace, live_trace = [], []
@@ -148,6 +153,7 @@ def rollout(cfg, W, prompts, forced, m, k, cap, seed, temperature=1.0, L=1, m_up
     # step 1: token 0 from the prompt's logits
     for g in trajs:
         emit(g, last_logits[g // m], 0)
+        rmar[g].append(prompt_rmar[g // m])
     trace.append((len(trajs), pages_used, None))
     live_trace.append(len(trajs))
     select_and_free(1)
@@ -171,10 +177,13 @@ def rollout(cfg, W, prompts, forced, m, k, cap, seed, temperature=1.0, L=1, m_up
             tok_in = [toks[g][-1] for g in live]
             Lc = [np.stack([tcache[g][l][0] for g in live]) for l in range(cfg.n_layers)]
             Vc = [np.stack([tcache[g][l][1] for g in live]) for l in range(cfg.n_layers)]
-            logits, newc = M.decode_batch(cfg, W, tok_in, list(zip(Lc, Vc)))
+            mar = []
+            logits, newc = M.decode_batch(cfg, W, tok_in, list(zip(Lc, Vc)), margins=mar)
+            rm = np.min(np.stack(mar), axis=0) if mar else np.full(len(live), np.inf)
             for b, g in enumerate(live):
                 tcache[g] = [(newc[l][0][b], newc[l][1][b]) for l in range(cfg.n_layers)]
                 emit(g, logits[b], gen[g])
+                rmar[g].append(float(rm[b]))
         select_and_free(step)
         for g in trajs:
             if st[g] != LIVE and g in tcache:
@@ -185,6 +194,7 @@ def rollout(cfg, W, prompts, forced, m, k, cap, seed, temperature=1.0, L=1, m_up
     length = {g: gen[g] for g in trajs}
     mean = {g: np.float32(slp[g] / np.float32(max(gen[g], 1))) for g in trajs}
     return RolloutResult(tokens=toks, sampled=samp, logprobs=lps, entropies=ents, margins=margins,
+                         route_margins=rmar,
                          logits=lgs, status=st, length=length, sum_lp32=slp, mean_lp32=mean,
                          kept=kept, done_step=done_step, steps=step,
                          tokens_decoded=sum(length.values()), pages_hwm=hwm,

@@ -48,8 +48,8 @@ class Stats(C.Structure):
                 ("pages_used", C.c_int64), ("pages_hwm", C.c_int64), ("n_live", C.c_int32),
                 ("n_done", C.c_int32), ("attn_ms", C.c_double), ("attn_bytes", C.c_double),
                 ("attn_launches", C.c_int64), ("gemm_ms", C.c_double), ("gemm_flop", C.c_double),
-                ("gemm_launches", C.c_int64), ("gemm_cls_ms", C.c_double * 5),
-                ("gemm_cls_flop", C.c_double * 5)]
+                ("gemm_launches", C.c_int64), ("gemm_cls_ms", C.c_double * 6),
+                ("gemm_cls_flop", C.c_double * 6)]
 
 
 _P = C.c_void_p

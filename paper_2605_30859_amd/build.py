@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libdarts.so")
 SOURCES = ["api.hip", "k_init.hip", "k_gemm.hip", "k_elem.hip", "k_attn.hip", "k_sample.hip",
-           "k_select.hip"]
+           "k_select.hip", "k_moe.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          # no packed-fp32 instructions anywhere in this library

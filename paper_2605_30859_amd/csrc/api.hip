@@ -24,8 +24,11 @@ namespace {
 struct LayerW {
   void* wqkv = nullptr;   // [(hq + 2 hkv) hd][d]
   void* wo = nullptr;     // [d][hq hd]
-  void* wgu = nullptr;    // [2F][d], gate/up interleaved in groups of 16 rows
-  void* wdown = nullptr;  // [d][F]
+  void* wgu = nullptr;    // [2F][d], gate/up interleaved in groups of 16 rows (dense)
+  void* wdown = nullptr;  // [d][F] (dense)
+  void* wrouter = nullptr;  // [E][d] (MoE)
+  void* wegu = nullptr;     // [E][2Fe][d], per expert gate/up interleaved in groups of 16
+  void* wedown = nullptr;   // [E][d][Fe]
 };
 
 struct TimedLaunch {
@@ -45,6 +48,15 @@ struct darts_ctx {
   int P = 0, Lp = 0, cap = 0, pp = 0, max_pages = 0, n_traj = 0;
   int64_t n_pages = 0;
   int d = 0, hq = 0, hkv = 0, hd = 0, F = 0, V = 0, nl = 0, qkv_w = 0;
+  bool moe = false;
+  int E = 0, topk = 0, Fe = 0;
+  int32_t* m_topk_id = nullptr;
+  float* m_topk_w = nullptr;
+  int32_t* m_pos_of = nullptr;
+  int32_t* m_cnt = nullptr;       // counts | offsets | cursors, E each
+  void* m_a_perm = nullptr;
+  void* m_h_perm = nullptr;
+  float* m_y_perm = nullptr;
   // device memory
   std::vector<void*> allocs;
   void* embed = nullptr;
@@ -104,7 +116,7 @@ struct darts_ctx {
   int64_t attn_launches = 0;
   double gemm_ms = 0.0, gemm_flop = 0.0;
   int64_t gemm_launches = 0;
-  double cls_ms[5] = {0, 0, 0, 0, 0}, cls_flop[5] = {0, 0, 0, 0, 0};
+  double cls_ms[6] = {0, 0, 0, 0, 0, 0}, cls_flop[6] = {0, 0, 0, 0, 0, 0};
 };
 
 #define HIPCHK(ctx, expr)                                                      \
@@ -157,6 +169,18 @@ static int tbegin(darts_ctx* c, int kind, double units) {
   c->pending.push_back(TimedLaunch{kind, units});
   return (int)i;
 }
+// Reserve an event pair without recording (the launcher records it).
+static int treserve(darts_ctx* c, int kind, double units) {
+  if (!timing_on(c)) return -1;
+  const size_t i = c->pending.size();
+  while (c->events.size() < 2 * (i + 1)) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return -1;
+    c->events.push_back(e);
+  }
+  c->pending.push_back(TimedLaunch{kind, units});
+  return (int)i;
+}
 static void tend(darts_ctx* c, int i) {
   if (i >= 0) (void)hipEventRecord(c->events[2 * i + 1], c->st);
 }
@@ -177,6 +201,16 @@ static int init_weights(darts_ctx* c) {
                                   rowmap_plain(hkv * hd, (hq + hkv) * hd), c->st));
     HIPCHK(c, launch_init_weights(w.wo, b, d, (int64_t)hq * hd, (int64_t)hq * hd, T_WO, l, seed,
                                   rowmap_plain(d, 0), c->st));
+    if (c->moe) {
+      const int E = c->E, Fe = c->Fe;
+      HIPCHK(c, launch_init_weights(w.wrouter, b, E, d, d, T_ROUTER, l, seed, rowmap_plain(E, 0), c->st));
+      RowMap eg{Fe, 2 * (int64_t)Fe, 16, 32, 0}, eu{Fe, 2 * (int64_t)Fe, 16, 32, 16};
+      HIPCHK(c, launch_init_weights(w.wegu, b, (int64_t)E * Fe, d, d, T_EGATE, l, seed, eg, c->st));
+      HIPCHK(c, launch_init_weights(w.wegu, b, (int64_t)E * Fe, d, d, T_EUP, l, seed, eu, c->st));
+      HIPCHK(c, launch_init_weights(w.wedown, b, (int64_t)E * d, Fe, Fe, T_EDOWN, l, seed,
+                                    rowmap_plain((int64_t)E * d, 0), c->st));
+      continue;
+    }
     RowMap gate{F, 0, 16, 32, 0}, up{F, 0, 16, 32, 16};
     HIPCHK(c, launch_init_weights(w.wgu, b, F, d, d, T_WGATE, l, seed, gate, c->st));
     HIPCHK(c, launch_init_weights(w.wgu, b, F, d, d, T_WUP, l, seed, up, c->st));
@@ -196,8 +230,10 @@ static size_t gemm_ws_need(const darts_ctx* c) {
   for (int M : ms) {
     need = std::max(need, gemm_workspace_bytes(M, c->qkv_w, c->d));
     need = std::max(need, gemm_workspace_bytes(M, c->d, c->hq * c->hd));
-    need = std::max(need, gemm_workspace_bytes(M, 2 * c->F, c->d));
-    need = std::max(need, gemm_workspace_bytes(M, c->d, c->F));
+    if (!c->moe) {
+      need = std::max(need, gemm_workspace_bytes(M, 2 * c->F, c->d));
+      need = std::max(need, gemm_workspace_bytes(M, c->d, c->F));
+    }
     need = std::max(need, gemm_workspace_bytes(M, c->V, c->d));
   }
   return need;
@@ -235,13 +271,21 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
   if (!(mc.head_dim == 32 || mc.head_dim == 64 || mc.head_dim == 128)) return DARTS_EINVAL;
   if (mc.vocab < 8 || mc.vocab % 4 != 0) return DARTS_EINVAL;
   if (mc.dtype != DARTS_F32 && mc.dtype != DARTS_BF16) return DARTS_EINVAL;
-  if (mc.n_experts != 0) return DARTS_EINVAL;   // MoE decoder: not in this build yet
-  if (mc.ffn_dim < 16 || mc.ffn_dim % 16 != 0) return DARTS_EINVAL;
+  const bool moe = mc.n_experts > 0;
+  if (moe) {
+    // grouped expert GEMMs: K/8 a multiple of 32 for both d and expert_ffn; bf16 only
+    if (mc.dtype != DARTS_BF16 || mc.n_experts > 1024 || mc.top_k < 1 || mc.top_k > 64 ||
+        mc.top_k > mc.n_experts || mc.expert_ffn < 256 || mc.expert_ffn % 256 != 0 ||
+        mc.d_model % 256 != 0)
+      return DARTS_EINVAL;
+  } else if (mc.ffn_dim < 16 || mc.ffn_dim % 16 != 0) {
+    return DARTS_EINVAL;
+  }
   const int qkv_w = (mc.n_q_heads + 2 * mc.n_kv_heads) * mc.head_dim;
   if (mc.dtype == DARTS_BF16) {
     const int K1 = mc.d_model, K2 = mc.n_q_heads * mc.head_dim, K3 = mc.ffn_dim;
-    if (K1 % 64 || K2 % 64 || K3 % 64) return DARTS_EINVAL;
-    if (qkv_w % 128 || mc.d_model % 128 || (2 * mc.ffn_dim) % 128 || mc.vocab % 128)
+    if (K1 % 256 || K2 % 256 || (!moe && K3 % 256)) return DARTS_EINVAL;
+    if (qkv_w % 128 || mc.d_model % 128 || (!moe && (2 * mc.ffn_dim) % 128) || mc.vocab % 128)
       return DARTS_EINVAL;
   }
   const int64_t n_traj64 = (int64_t)rc.n_prompts * m;
@@ -258,7 +302,8 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
   c->max_pages = c->pp + (c->cap + kPage - 1) / kPage;
   c->n_traj = (int)n_traj64;
   c->d = mc.d_model; c->hq = mc.n_q_heads; c->hkv = mc.n_kv_heads; c->hd = mc.head_dim;
-  c->F = mc.ffn_dim; c->V = mc.vocab; c->nl = mc.n_layers; c->qkv_w = qkv_w;
+  c->F = moe ? 0 : mc.ffn_dim; c->V = mc.vocab; c->nl = mc.n_layers; c->qkv_w = qkv_w;
+  c->moe = moe; c->E = mc.n_experts; c->topk = mc.top_k; c->Fe = mc.expert_ffn;
 
   const int64_t page_bytes_all = (int64_t)c->nl * c->hkv * kPage * c->hd * 2 * c->esz;
   const int64_t worst = (int64_t)c->P * c->pp + (int64_t)c->n_traj * ((c->cap + kPage - 1) / kPage);
@@ -272,9 +317,11 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
   if (hipMemGetInfo(&free_b, &total_b) != hipSuccess) { delete c; return DARTS_EHIP; }
   const int rows_pf = c->P * c->Lp;
   const int rows_max = std::max(rows_pf, c->n_traj);
+  const size_t ffn_elems = moe ? (size_t)c->E * c->d + (size_t)3 * c->E * c->Fe * c->d
+                                : (size_t)3 * c->F * c->d;
   const size_t wbytes = ((size_t)c->V * c->d * 2 +
                          (size_t)c->nl * ((size_t)qkv_w * c->d + (size_t)c->d * c->hq * c->hd +
-                                          (size_t)3 * c->F * c->d)) * c->esz;
+                                          ffn_elems)) * c->esz;
   const size_t poolb = (size_t)n_pages * page_bytes_all;
   if (wbytes + poolb + (size_t)rows_max * c->V * 0 > free_b) { delete c; return DARTS_ENOMEM; }
 
@@ -286,8 +333,14 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
   for (auto& w : c->layers) {
     A(&w.wqkv, (size_t)qkv_w * c->d * c->esz);
     A(&w.wo, (size_t)c->d * c->hq * c->hd * c->esz);
-    A(&w.wgu, (size_t)2 * c->F * c->d * c->esz);
-    A(&w.wdown, (size_t)c->d * c->F * c->esz);
+    if (moe) {
+      A(&w.wrouter, (size_t)c->E * c->d * c->esz);
+      A(&w.wegu, (size_t)c->E * 2 * c->Fe * c->d * c->esz);
+      A(&w.wedown, (size_t)c->E * c->d * c->Fe * c->esz);
+    } else {
+      A(&w.wgu, (size_t)2 * c->F * c->d * c->esz);
+      A(&w.wdown, (size_t)c->d * c->F * c->esz);
+    }
   }
   A(&c->kpool, (size_t)c->nl * c->pool_layer_elems * c->esz);
   A(&c->vpool, (size_t)c->nl * c->pool_layer_elems * c->esz);
@@ -318,7 +371,17 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
   A(&c->qkv, (size_t)rows_max * qkv_w * 4);
   A(&c->q, (size_t)rows_max * c->hq * c->hd * c->esz);
   A(&c->attn, (size_t)rows_max * c->hq * c->hd * c->esz);
-  A(&c->hbuf, (size_t)rows_max * c->F * c->esz);
+  A(&c->hbuf, (size_t)rows_max * std::max(c->F, 1) * c->esz);
+  if (moe) {
+    const size_t pairs = (size_t)rows_max * c->topk;
+    A(&c->m_topk_id, pairs * 4);
+    A(&c->m_topk_w, pairs * 4);
+    A(&c->m_pos_of, pairs * 4);
+    A(&c->m_cnt, (size_t)3 * c->E * 4);
+    A(&c->m_a_perm, pairs * c->d * 2);
+    A(&c->m_h_perm, pairs * c->Fe * 2);
+    A(&c->m_y_perm, pairs * c->d * 4);
+  }
   A(&c->xlast, (size_t)c->P * c->d * 4);
   A(&c->logits, (size_t)c->n_traj * c->V * 4);
   c->gemm_ws_bytes = gemm_ws_need(c);
@@ -402,7 +465,7 @@ int darts_reset(darts_ctx* c) {
   c->pending.clear();
   c->attn_ms = c->attn_bytes = 0.0; c->attn_launches = 0;
   c->gemm_ms = c->gemm_flop = 0.0; c->gemm_launches = 0;
-  for (int i = 0; i < 5; ++i) c->cls_ms[i] = c->cls_flop[i] = 0.0;
+  for (int i = 0; i < 6; ++i) c->cls_ms[i] = c->cls_flop[i] = 0.0;
   return DARTS_OK;
 }
 
@@ -426,15 +489,17 @@ static int run_attention(darts_ctx* c, int layer, int n_rows, const int32_t* row
   const double ctx = ctx_base;
   const double bytes = (double)n_rows * (ctx * c->hkv * c->hd * 2.0 * c->esz +
                                          2.0 * c->hq * c->hd * c->esz + std::ceil(ctx / kPage) * 4.0);
-  const int ti = ctx_mod == 0 ? tbegin(c, 0, bytes) : -1;
+  // decode launches are timed around the attention kernel itself (events
+  // recorded inside the launcher, before and after that kernel only)
+  const int ti = ctx_mod == 0 ? treserve(c, 0, bytes) : -1;
+  hipEvent_t e0 = ti >= 0 ? c->events[2 * ti] : nullptr, e1 = ti >= 0 ? c->events[2 * ti + 1] : nullptr;
   HIPCHK(c, launch_attention(c->q, kp, vp, c->n_pages, c->page_table, c->max_pages, row_pt, nullptr,
                              ctx_mod, ctx_base, n_rows, c->hq, c->hkv, c->hd, max_ctx, c->bf16,
-                             c->attn, c->attn_ws, c->attn_ws_bytes, c->st));
-  tend(c, ti);
+                             c->attn, c->attn_ws, c->attn_ws_bytes, c->st, e0, e1));
   return DARTS_OK;
 }
 
-enum { G_QKV = 0, G_O, G_GU, G_DOWN, G_LM };
+enum { G_QKV = 0, G_O, G_GU, G_DOWN, G_LM, G_MOE };
 static hipError_t gemm_t(darts_ctx* c, int cls, const void* A, int lda, const void* W, int ldw,
                          void* C, int ldc, int M, int N, int K, int epi) {
   const int ti = tbegin(c, 1 + cls, 2.0 * M * N * K);
@@ -462,6 +527,20 @@ static int run_layers(darts_ctx* c, int n, const int32_t* row_pt, int pos_mod, i
     if (r != DARTS_OK) return r;
     HIPCHK(c, gemm_t(c, G_O, c->attn, hqd, w.wo, hqd, c->x, d, n, d, hqd, EPI_ADD_F32));
     HIPCHK(c, launch_rmsnorm(c->x, n, d, c->mc.rms_eps, c->xn, b, c->st));
+    if (c->moe) {
+      MoeArgs m;
+      m.xn = (const bf16_t*)c->xn; m.x = c->x; m.n_rows = n; m.d = d; m.E = c->E; m.k = c->topk;
+      m.Fe = c->Fe; m.w_router = (const bf16_t*)w.wrouter; m.w_gu = (const bf16_t*)w.wegu;
+      m.w_down = (const bf16_t*)w.wedown; m.topk_id = c->m_topk_id; m.topk_w = c->m_topk_w;
+      m.pos_of = c->m_pos_of; m.counts = c->m_cnt; m.offsets = c->m_cnt + c->E;
+      m.cursors = c->m_cnt + 2 * c->E; m.a_perm = (bf16_t*)c->m_a_perm;
+      m.h_perm = (bf16_t*)c->m_h_perm; m.y_perm = c->m_y_perm;
+      const double flop = 2.0 * n * ((double)c->E * d + (double)c->topk * 3.0 * c->Fe * d);
+      const int ti = tbegin(c, 1 + G_MOE, flop);
+      HIPCHK(c, launch_moe_ffn(m, c->st));
+      tend(c, ti);
+      continue;
+    }
     HIPCHK(c, gemm_t(c, G_GU, c->xn, d, w.wgu, d, c->hbuf, c->F, n, 2 * c->F, d, EPI_SWIGLU));
     HIPCHK(c, gemm_t(c, G_DOWN, c->hbuf, c->F, w.wdown, c->F, c->x, d, n, d, c->F, EPI_ADD_F32));
   }
@@ -615,7 +694,7 @@ int darts_get_stats(const darts_ctx* c, darts_stats* s) {
   s->gemm_ms = c->gemm_ms;
   s->gemm_flop = c->gemm_flop;
   s->gemm_launches = c->gemm_launches;
-  for (int i = 0; i < 5; ++i) { s->gemm_cls_ms[i] = c->cls_ms[i]; s->gemm_cls_flop[i] = c->cls_flop[i]; }
+  for (int i = 0; i < 6; ++i) { s->gemm_cls_ms[i] = c->cls_ms[i]; s->gemm_cls_flop[i] = c->cls_flop[i]; }
   return DARTS_OK;
 }
 

@@ -20,6 +20,8 @@
 // kernel merges them.
 #include <math.h>
 
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -341,12 +343,14 @@ __global__ void attn_combine_kernel(CtxSpec cs, int n_rows, int hq, int hd, int 
   }
 }
 
-// Pages per chunk: the whole context while there are at least ~8 (row, kv
-// head) units per CU, otherwise the context is cut so that about 4096
-// wavefronts run (an even page count, at least 8 pages per chunk).
-static int choose_chunk_pages(int n_rows, int hkv, int max_ctx) {
+// Pages per chunk.  Equal contexts: the whole context while there are at
+// least ~8 (row, kv head) units per CU, otherwise cut so that about 4096
+// wavefronts run.  Ragged contexts: 32 pages (512 keys), so that the longest
+// rows are spread over many wavefronts instead of one.  Even, >= 8 pages.
+static int choose_chunk_pages(int n_rows, int hkv, int max_ctx, bool uniform) {
   const int64_t units = (int64_t)n_rows * hkv;
   const int npg = (max_ctx + kPage - 1) / kPage;
+  if (!uniform) return npg <= 32 ? npg + (npg & 1) : 32;
   if (units >= 2048) return npg + (npg & 1);
   int64_t nch = (4096 + units - 1) / units;
   int c = (int)((npg + nch - 1) / nch);
@@ -360,7 +364,9 @@ struct AttnWs {
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // Workspace: [chunk_off | work list | info | partial o | partial (m, l)].
 static size_t ws_layout(int n_rows, int hq, int hkv, int hd, int max_ctx, char* base, AttnWs* w) {
-  const int cp = choose_chunk_pages(n_rows, hkv, max_ctx);
+  // sized for the larger of the two chunkings (ragged chunks are never longer)
+  const int cp = std::min(choose_chunk_pages(n_rows, hkv, max_ctx, true),
+                          choose_chunk_pages(n_rows, hkv, max_ctx, false));
   const int64_t maxch = (int64_t)n_rows * ((max_ctx + cp * kPage - 1) / (cp * kPage));
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off = align256(off + bytes); return base ? base + o : nullptr; };
@@ -393,14 +399,15 @@ static void attn_f32_go(dim3 grid, hipStream_t st, const void* q, const void* k,
 hipError_t launch_attention_spec(const void* q, const void* k_pool, const void* v_pool,
                                  const int32_t* page_table, int pt_stride, CtxSpec cs, int n_rows,
                                  int hq, int hkv, int hd, int max_ctx, bool bf16, void* out,
-                                 void* ws, size_t ws_bytes, hipStream_t st) {
+                                 void* ws, size_t ws_bytes, hipStream_t st, hipEvent_t ev0,
+                                 hipEvent_t ev1) {
   if (n_rows <= 0) return hipSuccess;
   cs.max_ctx = max_ctx;
   AttnWs w;
   const size_t need = ws_layout(n_rows, hq, hkv, hd, max_ctx, (char*)ws, &w);
   if (ws == nullptr || ws_bytes < need) return hipErrorInvalidValue;
-  const int cp = choose_chunk_pages(n_rows, hkv, max_ctx);
   const bool uniform = bf16 && cs.ctx_len == nullptr && cs.mod == 0;
+  const int cp = choose_chunk_pages(n_rows, hkv, max_ctx, uniform);
   const int uni_nch = uniform ? ((min(cs.base, max_ctx) + cp * kPage - 1) / (cp * kPage)) : 0;
   if (!uniform)
     hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(1024), 0, st, cs, n_rows, cp * kPage,
@@ -419,10 +426,12 @@ hipError_t launch_attention_spec(const void* q, const void* k_pool, const void* 
     a.chunk_pages = cp; a.n_rows = n_rows; a.uniform_nch = uni_nch;
     a.work = w.work; a.chunk_off = w.chunk_off; a.info = w.info;
     a.ws_o = w.ws_o; a.ws_ml = w.ws_ml; a.out = (bf16_t*)out;
+    if (ev0) (void)hipEventRecord(ev0, st);
     if (hd == 128) hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, dim3(256), 0, st, a);
     else if (hd == 64) hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, dim3(256), 0, st, a);
     else if (hd == 32) hipLaunchKernelGGL(attn_bf16_kernel<32>, grid, dim3(256), 0, st, a);
     else return hipErrorInvalidValue;
+    if (ev1) (void)hipEventRecord(ev1, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if ((max_ctx + cp * kPage - 1) / (cp * kPage) > 1) {
@@ -452,12 +461,13 @@ hipError_t launch_attention(const void* q, const void* k_pool, const void* v_poo
                             int64_t n_pages, const int32_t* page_table, int pt_stride,
                             const int32_t* row_pt, const int32_t* ctx_len, int ctx_mod,
                             int ctx_base, int n_rows, int hq, int hkv, int hd, int max_ctx,
-                            bool bf16, void* out, void* ws, size_t ws_bytes, hipStream_t st) {
+                            bool bf16, void* out, void* ws, size_t ws_bytes, hipStream_t st,
+                            hipEvent_t ev0, hipEvent_t ev1) {
   CtxSpec cs;
   cs.ctx_len = ctx_len; cs.mod = ctx_mod; cs.base = ctx_base; cs.row_pt = row_pt;
   cs.max_ctx = max_ctx; cs.n_pages = n_pages;
   return launch_attention_spec(q, k_pool, v_pool, page_table, pt_stride, cs, n_rows, hq, hkv, hd,
-                               max_ctx, bf16, out, ws, ws_bytes, st);
+                               max_ctx, bf16, out, ws, ws_bytes, st, ev0, ev1);
 }
 
 }  // namespace darts

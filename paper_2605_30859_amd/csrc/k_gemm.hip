@@ -10,7 +10,7 @@
 //    runs are neighbours in (m, n) and share operand tiles in that XCD's L2.
 //    The 64x128 tile uses a register-staged double buffer; the larger tiles
 //    use direct global->LDS loads through a 3-4 deep ring of LDS stages.
-//  * skinny (M <= 64, weight-bandwidth bound): no LDS for operands; each
+//  * skinny (M <= 32, weight-bandwidth bound): no LDS for operands; each
 //    wavefront loads W and A fragments straight into MFMA operand registers,
 //    8 wavefronts of a block split K and are reduced through LDS.
 // Either family may split K across blocks; partial sums then go to a
@@ -451,7 +451,7 @@ static const int kTiles[4][2] = {{64, 128}, {128, 128}, {128, 256}, {256, 128}};
 static Plan plan_gemm(int M, int N, int K) {
   Plan p{};
   const int cus = cu_count();
-  if (M <= 64) {
+  if (M <= 32) {
     p.kind = 0;
     p.MT = (M + 15) / 16;
     p.NS = (M <= 16) ? 2 : 4;
@@ -463,22 +463,24 @@ static Plan plan_gemm(int M, int N, int K) {
     while (p.nt * p.S < 2 * cus && K % (p.S * 2 * 8 * 32) == 0 && K / (p.S * 2) >= 8 * 256) p.S *= 2;
     return p;
   }
-  // tiled: pick the config with the best estimated time = rounds * tile work,
-  // tile work ~ BM*BN*(K/S) / efficiency(config)
+  // tiled: estimated time (us) = rounds * tile time at the config's measured
+  // per-CU MFMA efficiency, plus, for a K split, the partial-sum round trip
+  // through HBM (S*M*N fp32 written and read) and the reduce launch.
+  const double cu_tflops = 2500.0 / cus;                    // dense bf16 per CU
+  const double eff[4] = {0.12, 0.35, 0.42, 0.42};   // measured on MI355X (decode shapes)
   double best = 1e30;
   for (int c = 0; c < 4; ++c) {
     const int BMc = kTiles[c][0], BNc = kTiles[c][1];
     if (N % BNc) continue;
     if (BMc > 128 && M <= 128) continue;
     const int mt = (M + BMc - 1) / BMc, nt = N / BNc;
-    const double eff = (c == 0) ? 0.55 : (c == 1 ? 0.8 : 1.0);   // larger register tiles feed MFMA better
     for (int S = 1; S <= 8; S *= 2) {
       if (K % (S * BK) || K / S < 4 * BK) break;
       const int tiles = mt * nt * S;
       const int rounds = (tiles + cus - 1) / cus;
-      double t = (double)rounds * BMc * BNc * (double)(K / S) / eff;
-      if (S > 1) t += 4.0 * S * (double)M * N / 64.0;   // partial-sum traffic penalty
-      if (t < best * 0.98) {
+      double t = rounds * (2.0 * BMc * BNc * (K / S)) / (cu_tflops * eff[c] * 1e6);
+      if (S > 1) t += (2.0 * S * (double)M * N * 4.0) / 4.0e6 + 4.0;
+      if (t < best * 0.97) {
         best = t;
         p.kind = 1 + c; p.mt = mt; p.nt = nt; p.S = S;
       }

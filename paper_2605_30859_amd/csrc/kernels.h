@@ -53,7 +53,8 @@ hipError_t launch_attention(const void* q, const void* k_pool, const void* v_poo
                             int64_t n_pages, const int32_t* page_table, int pt_stride,
                             const int32_t* row_pt, const int32_t* ctx_len, int ctx_mod,
                             int ctx_base, int n_rows, int hq, int hkv, int hd, int max_ctx,
-                            bool bf16, void* out, void* ws, size_t ws_bytes, hipStream_t st);
+                            bool bf16, void* out, void* ws, size_t ws_bytes, hipStream_t st,
+                            hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 
 // ---- sampler (k_sample.hip)
 struct SampleArgs {
@@ -97,5 +98,17 @@ hipError_t launch_alloc_pages(const int32_t* live, int n_live, const int32_t* ge
 hipError_t launch_prefill_pages(int n_prompts, int m, int prompt_pages, int32_t* page_table,
                                 int pt_stride, int32_t* free_stack, int32_t* free_top,
                                 int32_t* refcnt, hipStream_t st);
+
+// ---- MoE FFN (k_moe.hip): x += sum over the top-k experts of w_e * expert_e(xn)
+struct MoeArgs {
+  const bf16_t* xn; float* x; int n_rows, d, E, k, Fe;
+  const bf16_t* w_router;   // [E][d]
+  const bf16_t* w_gu;       // [E][2Fe][d], gate/up rows interleaved in groups of 16
+  const bf16_t* w_down;     // [E][d][Fe]
+  int32_t* topk_id; float* topk_w; int32_t* pos_of;            // [n_rows*k]
+  int32_t* counts; int32_t* offsets; int32_t* cursors;         // [E]
+  bf16_t* a_perm; bf16_t* h_perm; float* y_perm;               // [n_rows*k][d | Fe | d]
+};
+hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st);
 
 }  // namespace darts
