@@ -174,13 +174,15 @@ __device__ __forceinline__ void vm_wait() {
 typedef __attribute__((address_space(3))) void lds_void_t;
 
 template <int BM, int BN, int WGM, int WGN, int STAGES, int EPI, bool SPLIT>
-__global__ void __launch_bounds__(256) gemm_dma_kernel(const bf16_t* __restrict__ A, int lda,
+__global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_kernel(const bf16_t* __restrict__ A, int lda,
                                                        const bf16_t* __restrict__ W, int ldw,
                                                        void* __restrict__ C, int ldc, int M,
                                                        int N, int K, int k_chunk, int mt, int nt,
                                                        float* __restrict__ ws) {
+  constexpr int NW = WGM * WGN;                    // wavefronts per block
   constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 16, TN = WN / 16;
-  constexpr int AI = BM / 32, WI = BN / 32;       // 1 KB load instructions per wave per stage
+  constexpr int AI = BM / (8 * NW), WI = BN / (8 * NW);   // 1 KB load instructions per wave per stage
+  static_assert(AI * 8 * NW == BM && WI * 8 * NW == BN, "tile rows must split over the waves");
   constexpr int STAGE_ELEMS = (BM + BN) * BK;      // bf16 elements per stage
   extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -201,13 +203,13 @@ __global__ void __launch_bounds__(256) gemm_dma_kernel(const bf16_t* __restrict_
   const bf16_t* wsrc[WI];
 #pragma unroll
   for (int j = 0; j < AI; ++j) {
-    int r = m0 + wave * (BM / 4) + 8 * j + lrow;
+    int r = m0 + wave * (BM / NW) + 8 * j + lrow;
     r = r < M ? r : M - 1;
     asrc[j] = A + (int64_t)r * lda + kbeg + gchunk * 8;
   }
 #pragma unroll
   for (int j = 0; j < WI; ++j)
-    wsrc[j] = W + (int64_t)(n0 + wave * (BN / 4) + 8 * j + lrow) * ldw + kbeg + gchunk * 8;
+    wsrc[j] = W + (int64_t)(n0 + wave * (BN / NW) + 8 * j + lrow) * ldw + kbeg + gchunk * 8;
 
   auto issue = [&](int kt, int buf) {
     bf16_t* sa = smem + buf * STAGE_ELEMS;
@@ -215,11 +217,11 @@ __global__ void __launch_bounds__(256) gemm_dma_kernel(const bf16_t* __restrict_
 #pragma unroll
     for (int j = 0; j < AI; ++j)
       __builtin_amdgcn_global_load_lds((const void*)(asrc[j] + kt * BK),
-                                       (lds_void_t*)(sa + (wave * (BM / 4) + 8 * j) * BK), 16, 0, 0);
+                                       (lds_void_t*)(sa + (wave * (BM / NW) + 8 * j) * BK), 16, 0, 0);
 #pragma unroll
     for (int j = 0; j < WI; ++j)
       __builtin_amdgcn_global_load_lds((const void*)(wsrc[j] + kt * BK),
-                                       (lds_void_t*)(sw + (wave * (BN / 4) + 8 * j) * BK), 16, 0, 0);
+                                       (lds_void_t*)(sw + (wave * (BN / NW) + 8 * j) * BK), 16, 0, 0);
   };
 
   f32x4_t acc[TM][TN];
@@ -446,7 +448,7 @@ struct Plan {
 static int cu_count() { return 256; }
 
 // Tiled configs: (BM, BN)
-static const int kTiles[4][2] = {{64, 128}, {128, 128}, {128, 256}, {256, 128}};
+static const int kTiles[5][2] = {{64, 128}, {128, 128}, {128, 256}, {256, 128}, {256, 256}};
 
 static Plan plan_gemm(int M, int N, int K) {
   Plan p{};
@@ -467,9 +469,9 @@ static Plan plan_gemm(int M, int N, int K) {
   // per-CU MFMA efficiency, plus, for a K split, the partial-sum round trip
   // through HBM (S*M*N fp32 written and read) and the reduce launch.
   const double cu_tflops = 2500.0 / cus;                    // dense bf16 per CU
-  const double eff[4] = {0.12, 0.35, 0.42, 0.42};   // measured on MI355X (decode shapes)
+  const double eff[5] = {0.12, 0.35, 0.42, 0.42, 0.55};   // measured on MI355X (decode shapes)
   double best = 1e30;
-  for (int c = 0; c < 4; ++c) {
+  for (int c = 0; c < 5; ++c) {
     const int BMc = kTiles[c][0], BNc = kTiles[c][1];
     if (N % BNc) continue;
     if (BMc > 128 && M <= 128) continue;
@@ -521,7 +523,7 @@ static void skinny_go(const Plan& p, const void* A, int lda, const void* W, int 
 template <int EPI, int BM_, int BN_, int WGM, int WGN, int ST>
 static void dma_go(const Plan& p, const void* A, int lda, const void* W, int ldw, void* C, int ldc,
                    int M, int N, int K, void* ws, hipStream_t st) {
-  const dim3 grid(p.mt * p.nt * p.S), blk(256);
+  const dim3 grid(p.mt * p.nt * p.S), blk(64 * WGM * WGN);
   const size_t lds = (size_t)ST * (BM_ + BN_) * BK * sizeof(bf16_t);
   static bool attr_done[2] = {false, false};
   if (p.S == 1) {
@@ -584,7 +586,8 @@ static hipError_t gemm_bf16_launch(const void* A, int lda, const void* W, int ld
       case 1: tiled_go<EPI, 64, 128, 1, 4>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
       case 2: dma_go<EPI, 128, 128, 2, 2, 4>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
       case 3: dma_go<EPI, 128, 256, 2, 2, 3>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
-      default: dma_go<EPI, 256, 128, 2, 2, 3>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+      case 4: dma_go<EPI, 256, 128, 2, 2, 3>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+      default: dma_go<EPI, 256, 256, 2, 4, 2>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
     }
   }
   hipError_t e = hipGetLastError();
