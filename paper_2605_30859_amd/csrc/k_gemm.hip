@@ -5,23 +5,30 @@
 // rows; output silu(gate) * up as bf16).
 //
 // Two kernel families, chosen per launch from (M, N, K):
-//  * tiled: BM x BN block tile staged through LDS, 4 wavefronts each owning
-//    a WM x WN register tile; blocks are renumbered so that the blocks an XCD
-//    runs are neighbours in (m, n) and share operand tiles in that XCD's L2.
-//    The 64x128 tile uses a register-staged double buffer; the larger tiles
-//    use direct global->LDS loads through a 3-4 deep ring of LDS stages.
-//  * skinny (M <= 32, weight-bandwidth bound): no LDS for operands; each
-//    wavefront loads W and A fragments straight into MFMA operand registers,
-//    8 wavefronts of a block split K and are reduced through LDS.
+//  * tiled: BM x BN block tile whose A and W slices are copied global -> LDS
+//    by direct loads (no register staging) through a ring of 2-4 LDS stages;
+//    4 or 8 wavefronts each own a WM x WN register tile.  Blocks are
+//    renumbered so that the blocks an XCD runs are neighbours in (m, n) and
+//    share operand tiles in that XCD's L2.  Configs: 128x128 with 2 stages
+//    (64 KB, two blocks per CU: one block's barrier wait is covered by the
+//    other), 128x128 with 4 stages (one block per CU, deepest prefetch: for
+//    weight streaming over very wide N), 256x128 and 256x256 with 8
+//    wavefronts (half the operand bytes per flop: large M).
+//  * skinny (M <= 32 with small W): no LDS for operands; each wavefront loads
+//    W and A fragments straight into MFMA operand registers, 8 wavefronts of a
+//    block split K and are reduced through LDS.
 // Either family may split K across blocks; partial sums then go to a
 // workspace and a reduce kernel adds them in a fixed order (bitwise
-// deterministic).
+// deterministic).  The plan is a pure function of (M, N, K), so results do
+// not depend on the device or on earlier calls.
+#include <algorithm>
+#include <cmath>
+
 #include "common.h"
 #include "kernels.h"
 
 namespace darts {
 
-constexpr int BK = 64, LDSK = BK + 8;  // +8 bf16 row pad: conflict-free 16-byte fragment reads
 
 __device__ __forceinline__ float silu_f(float g) { return g / (1.0f + __expf(-g)); }
 
@@ -61,108 +68,13 @@ __device__ __forceinline__ void store_partial(float* P, int M, int N, int r0, in
 }
 
 // ------------------------------------------------------------------ tiled
-template <int BM, int BN, int WGM, int WGN, int EPI, bool SPLIT>
-__global__ void __launch_bounds__(256) gemm_tiled_kernel(const bf16_t* __restrict__ A, int lda,
-                                                         const bf16_t* __restrict__ W, int ldw,
-                                                         void* __restrict__ C, int ldc, int M,
-                                                         int N, int K, int k_chunk, int mt, int nt,
-                                                         float* __restrict__ ws) {
-  constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 16, TN = WN / 16;
-  constexpr int ALD = BM / 32, WLD = BN / 32;   // 16-byte chunks per thread per k-tile
-  __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * LDSK];
-  __shared__ __attribute__((aligned(16))) bf16_t Ws[2][BN * LDSK];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WGN, wn = wave % WGN;
-  // XCD-aware renumbering: hardware block b runs on XCD b % 8; give each XCD a
-  // contiguous range of logical tiles (m fastest, then n, then the K split).
-  const int nb = gridDim.x;
-  int b = blockIdx.x;
-  const int full = (nb / 8) * 8;
-  if (b < full) b = (b % 8) * (full / 8) + b / 8;
-  const int mi = b % mt, ni = (b / mt) % nt, z = b / (mt * nt);
-  const int m0 = mi * BM, n0 = ni * BN;
-  const int kbeg = z * k_chunk;
-  const int nk = k_chunk / BK;
-
-  const int lr = tid >> 3, lc = (tid & 7) * 8;
-  u32x4_t ra[ALD], rw[WLD];
-  auto gload = [&](int kt) {
-    const int kk = kbeg + kt * BK + lc;
-#pragma unroll
-    for (int i = 0; i < ALD; ++i) {
-      const int r = m0 + lr + 32 * i;
-      ra[i] = r < M ? *(const u32x4_t*)(A + (int64_t)r * lda + kk) : (u32x4_t){0u, 0u, 0u, 0u};
-    }
-#pragma unroll
-    for (int i = 0; i < WLD; ++i) rw[i] = *(const u32x4_t*)(W + (int64_t)(n0 + lr + 32 * i) * ldw + kk);
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < ALD; ++i) *(u32x4_t*)(&As[buf][(lr + 32 * i) * LDSK + lc]) = ra[i];
-#pragma unroll
-    for (int i = 0; i < WLD; ++i) *(u32x4_t*)(&Ws[buf][(lr + 32 * i) * LDSK + lc]) = rw[i];
-  };
-
-  f32x4_t acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) acc[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
-
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  const int arow = wm * WM + (lane & 15), brow = wn * WN + (lane & 15), kq = (lane >> 4) * 8;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
-#pragma unroll
-    for (int ks = 0; ks < BK; ks += 32) {
-      bf16x8_t a[TM], bb[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) a[i] = *(const bf16x8_t*)(&As[buf][(arow + 16 * i) * LDSK + ks + kq]);
-#pragma unroll
-      for (int j = 0; j < TN; ++j) bb[j] = *(const bf16x8_t*)(&Ws[buf][(brow + 16 * j) * LDSK + ks + kq]);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bb[j], acc[i][j], 0, 0, 0);
-    }
-    if (kt + 1 < nk) {
-      sstore(buf ^ 1);
-      __syncthreads();
-    }
-  }
-
-  const int rb = m0 + wm * WM, cb = n0 + wn * WN;
-  if constexpr (SPLIT) {
-    float* P = ws + (int64_t)z * M * N;
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j) store_partial(P, M, N, rb + 16 * i, cb + 16 * j, lane, acc[i][j]);
-  } else if constexpr (EPI == EPI_SWIGLU) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; j += 2)
-        store_swiglu((bf16_t*)C, ldc, M, rb + 16 * i, cb + 16 * j, lane, acc[i][j], acc[i][j + 1]);
-  } else {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j) store_tile<EPI>(C, ldc, M, rb + 16 * i, cb + 16 * j, lane, acc[i][j]);
-  }
-}
-
-// ------------------------------------------------------- tiled, LDS DMA
-// Same tile math as above, but operand tiles travel global -> LDS with
-// direct 16-byte LDS loads (no staging registers) through a STAGES-deep ring
-// of LDS buffers.  A 64-wide K slice of a row is 8 chunks of 16 bytes; chunk
-// c of row r is stored at chunk position c ^ (r & 7) of that row so that the
-// 16-byte fragment reads of 8 consecutive rows hit distinct banks.  Rows of A
-// past M load row M-1 (their results are never stored).
+// Operand tiles travel global -> LDS with direct 16-byte LDS loads (no
+// staging registers) through a STAGES-deep ring of LDS buffers.  A KB-wide K
+// slice of a row is KB/8 chunks of 16 bytes, stored in a swizzled chunk order
+// (dma_swz) so that the 16-byte fragment reads of consecutive rows hit
+// distinct banks.  Rows of A past M load row M-1 (their results are never
+// stored).  Each wavefront owns a (BM/WGM) x (BN/WGN) register tile of
+// 16x16 MFMA accumulators.
 // s_waitcnt vmcnt(N) (gfx9 encoding: vmcnt bits 3:0 and 15:14; expcnt and
 // lgkmcnt left at their "don't wait" maxima)
 template <int N>
@@ -173,17 +85,29 @@ __device__ __forceinline__ void vm_wait() {
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-template <int BM, int BN, int WGM, int WGN, int STAGES, int EPI, bool SPLIT>
+// LDS chunk swizzle for a tile row of KB bf16 (KB/8 chunks of 16 bytes): the
+// chunk order of row r is permuted so that the 8 rows a 16-byte fragment read
+// touches in one LDS pass land in distinct banks.
+template <int KB>
+__device__ __forceinline__ int dma_swz(int r) {
+  if constexpr (KB == 64) return r & 7;
+  else return (r >> 1) & 3;
+}
+
+template <int BM, int BN, int KB, int WGM, int WGN, int STAGES, int EPI, bool SPLIT>
 __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_kernel(const bf16_t* __restrict__ A, int lda,
                                                        const bf16_t* __restrict__ W, int ldw,
                                                        void* __restrict__ C, int ldc, int M,
                                                        int N, int K, int k_chunk, int mt, int nt,
                                                        float* __restrict__ ws) {
+  static_assert(KB == 32 || KB == 64, "K tile");
   constexpr int NW = WGM * WGN;                    // wavefronts per block
   constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 16, TN = WN / 16;
-  constexpr int AI = BM / (8 * NW), WI = BN / (8 * NW);   // 1 KB load instructions per wave per stage
-  static_assert(AI * 8 * NW == BM && WI * 8 * NW == BN, "tile rows must split over the waves");
-  constexpr int STAGE_ELEMS = (BM + BN) * BK;      // bf16 elements per stage
+  constexpr int CH = KB / 8, RPI = 64 / CH;        // chunks per row, rows per 1 KB load instruction
+  constexpr int AI = BM / (RPI * NW), WI = BN / (RPI * NW);   // load instructions per wave per stage
+  static_assert(AI * RPI * NW == BM && WI * RPI * NW == BN, "tile rows must split over the waves");
+  constexpr int KH = KB / 32;                      // 32-wide MFMA K steps per tile
+  constexpr int STAGE_ELEMS = (BM + BN) * KB;      // bf16 elements per stage
   extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
@@ -194,34 +118,36 @@ __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_kernel(const bf16_t* 
   const int mi = b % mt, ni = (b / mt) % nt, z = b / (mt * nt);
   const int m0 = mi * BM, n0 = ni * BN;
   const int kbeg = z * k_chunk;
-  const int nk = k_chunk / BK;
+  const int nk = k_chunk / KB;
 
-  // per-lane global source rows for this wave's load instructions
-  const int lrow = lane >> 3;                     // row within an 8-row instruction
-  const int gchunk = (lane & 7) ^ lrow;           // swizzled source chunk
+  // per-lane global source rows for this wave's load instructions: lane i fills
+  // LDS bytes [16i, 16i+16) of the instruction's RPI rows, which hold source
+  // chunk (i % CH) ^ swizzle(row)
+  const int lrow = lane / CH;
+  const int gchunk = (lane % CH) ^ dma_swz<KB>(lrow);
   const bf16_t* asrc[AI];
   const bf16_t* wsrc[WI];
 #pragma unroll
   for (int j = 0; j < AI; ++j) {
-    int r = m0 + wave * (BM / NW) + 8 * j + lrow;
+    int r = m0 + wave * (BM / NW) + RPI * j + lrow;
     r = r < M ? r : M - 1;
     asrc[j] = A + (int64_t)r * lda + kbeg + gchunk * 8;
   }
 #pragma unroll
   for (int j = 0; j < WI; ++j)
-    wsrc[j] = W + (int64_t)(n0 + wave * (BN / NW) + 8 * j + lrow) * ldw + kbeg + gchunk * 8;
+    wsrc[j] = W + (int64_t)(n0 + wave * (BN / NW) + RPI * j + lrow) * ldw + kbeg + gchunk * 8;
 
   auto issue = [&](int kt, int buf) {
     bf16_t* sa = smem + buf * STAGE_ELEMS;
-    bf16_t* sw = sa + BM * BK;
+    bf16_t* sw = sa + BM * KB;
 #pragma unroll
     for (int j = 0; j < AI; ++j)
-      __builtin_amdgcn_global_load_lds((const void*)(asrc[j] + kt * BK),
-                                       (lds_void_t*)(sa + (wave * (BM / NW) + 8 * j) * BK), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const void*)(asrc[j] + kt * KB),
+                                       (lds_void_t*)(sa + (wave * (BM / NW) + RPI * j) * KB), 16, 0, 0);
 #pragma unroll
     for (int j = 0; j < WI; ++j)
-      __builtin_amdgcn_global_load_lds((const void*)(wsrc[j] + kt * BK),
-                                       (lds_void_t*)(sw + (wave * (BN / NW) + 8 * j) * BK), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const void*)(wsrc[j] + kt * KB),
+                                       (lds_void_t*)(sw + (wave * (BN / NW) + RPI * j) * KB), 16, 0, 0);
   };
 
   f32x4_t acc[TM][TN];
@@ -245,25 +171,25 @@ __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_kernel(const bf16_t* 
     __builtin_amdgcn_s_barrier();
     if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
     const bf16_t* sa = smem + (kt % STAGES) * STAGE_ELEMS;
-    const bf16_t* sw = sa + BM * BK;
-    // fragments of both 32-wide K halves are read before the MFMAs of the
-    // first half, so LDS latency overlaps matrix work
-    bf16x8_t a[2][TM], bb[2][TN];
+    const bf16_t* sw = sa + BM * KB;
+    // fragments of every 32-wide K step are read before the first MFMA, so
+    // LDS latency overlaps matrix work
+    bf16x8_t a[KH][TM], bb[KH][TN];
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
+    for (int ks = 0; ks < KH; ++ks) {
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int r = wm * WM + 16 * i + fr;
-        a[ks][i] = *(const bf16x8_t*)(sa + r * BK + (((ks * 4 + fq) ^ (r & 7)) * 8));
+        a[ks][i] = *(const bf16x8_t*)(sa + r * KB + (((ks * 4 + fq) ^ dma_swz<KB>(r)) * 8));
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int r = wn * WN + 16 * j + fr;
-        bb[ks][j] = *(const bf16x8_t*)(sw + r * BK + (((ks * 4 + fq) ^ (r & 7)) * 8));
+        bb[ks][j] = *(const bf16x8_t*)(sw + r * KB + (((ks * 4 + fq) ^ dma_swz<KB>(r)) * 8));
       }
     }
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
+    for (int ks = 0; ks < KH; ++ks)
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -440,20 +366,64 @@ __global__ void gemm_f32_swiglu_kernel(const float* __restrict__ A, int lda, con
 
 // ------------------------------------------------------------ dispatch
 struct Plan {
-  int kind;        // 0 skinny, 1..4 tiled configs
+  int kind;        // 0 skinny; tiled: 1 = 128x128 4 stages, 2 = 128x128 2 stages,
+                   // 3 = 256x128 8 waves, 4 = 256x256 8 waves
   int mt, nt, S;   // tiles and K splits
   int MT, NS;      // skinny shape
 };
 
-static int cu_count() { return 256; }
+// Planning assumes MI355X's 256 CUs whatever device runs the call, so a
+// shape always gets the same plan (and the same summation order).
+static constexpr int kCus = 256;
 
-// Tiled configs: (BM, BN)
-static const int kTiles[5][2] = {{64, 128}, {128, 128}, {128, 256}, {256, 128}, {256, 256}};
+static void set_tiled(Plan& p, int kind, int bm, int bn, int M, int N, int S) {
+  p.kind = kind; p.mt = (M + bm - 1) / bm; p.nt = N / bn; p.S = S;
+}
 
+// Tiled configs with the throughput model fitted to MI355X timings of every
+// projection of the supported models (M = 1..512, weights streamed from HBM,
+// not cache-resident): per-CU MFMA rate of one block (TFLOP/s), the weight
+// streaming rate (GB/s) and blocks resident per CU.
+struct TileCfg {
+  int kind, bm, bn, occ;
+  double rate, bw;
+};
+static const TileCfg kTileCfgs[4] = {
+    {1, 128, 128, 1, 3.38, 6425.0},
+    {2, 128, 128, 2, 2.26, 6423.0},
+    {3, 256, 128, 1, 4.89, 6325.0},
+    {4, 256, 256, 1, 6.68, 6298.0},
+};
+static constexpr double kOcc2Gain = 1.76;   // CU throughput with two co-resident blocks / one block
+static constexpr double kLaunchUs = 0.16;
+static constexpr double kSplitGBs = 4106.0;  // partial sums: written once, read once by the reduce
+static constexpr double kReduceUs = 3.19;
+
+// Estimated time (us): rounds of resident blocks at the config's rate, at
+// least the weight bytes at its streaming rate, plus the K-split partial-sum
+// round trip and reduce launch.
+static double tile_estimate(const TileCfg& c, int S, int M, int N, int K) {
+  const int mt = (M + c.bm - 1) / c.bm, nt = N / c.bn;
+  const double blocks = (double)mt * nt * S;
+  const double mflop = 2.0 * c.bm * c.bn * ((double)K / S) * 1e-6;
+  double t;
+  if (blocks <= kCus) t = mflop / c.rate;
+  else {
+    const double rounds = std::ceil(blocks / (c.occ * kCus));
+    t = rounds * c.occ * mflop / (c.occ == 2 ? c.rate * kOcc2Gain : c.rate);
+  }
+  t = std::max(t, 2.0 * N * (double)K / (c.bw * 1e3)) + kLaunchUs;
+  if (S > 1) t += 2.0 * S * (double)M * N * 4.0 / (kSplitGBs * 1e3) + kReduceUs;
+  return t;
+}
+
+//  * M <= 32 with W up to 40 MB (and K <= 2048 beyond 16 rows): skinny.
+//  * otherwise the tiled config and K split with the least estimated time
+//    (256-row tiles only above 128 rows).
 static Plan plan_gemm(int M, int N, int K) {
   Plan p{};
-  const int cus = cu_count();
-  if (M <= 32) {
+  const double wbytes = 2.0 * N * K;
+  if (M <= 32 && wbytes <= 40e6 && (M <= 16 || K <= 2048) && N % 32 == 0) {
     p.kind = 0;
     p.MT = (M + 15) / 16;
     p.NS = (M <= 16) ? 2 : 4;
@@ -462,33 +432,18 @@ static Plan plan_gemm(int M, int N, int K) {
     p.mt = 1;
     // split K across blocks until there are ~2 blocks per CU (each wave keeps >= 256 of K)
     p.S = 1;
-    while (p.nt * p.S < 2 * cus && K % (p.S * 2 * 8 * 32) == 0 && K / (p.S * 2) >= 8 * 256) p.S *= 2;
+    while (p.nt * p.S < 2 * kCus && K % (p.S * 2 * 8 * 32) == 0 && K / (p.S * 2) >= 8 * 256) p.S *= 2;
     return p;
   }
-  // tiled: estimated time (us) = rounds * tile time at the config's measured
-  // per-CU MFMA efficiency, plus, for a K split, the partial-sum round trip
-  // through HBM (S*M*N fp32 written and read) and the reduce launch.
-  const double cu_tflops = 2500.0 / cus;                    // dense bf16 per CU
-  const double eff[5] = {0.12, 0.35, 0.42, 0.42, 0.55};   // measured on MI355X (decode shapes)
   double best = 1e30;
-  for (int c = 0; c < 5; ++c) {
-    const int BMc = kTiles[c][0], BNc = kTiles[c][1];
-    if (N % BNc) continue;
-    if (BMc > 128 && M <= 128) continue;
-    const int mt = (M + BMc - 1) / BMc, nt = N / BNc;
+  for (const TileCfg& c : kTileCfgs) {
+    if (N % c.bn != 0 || (c.bm > 128 && M <= 128)) continue;
     for (int S = 1; S <= 8; S *= 2) {
-      if (K % (S * BK) || K / S < 4 * BK) break;
-      const int tiles = mt * nt * S;
-      const int rounds = (tiles + cus - 1) / cus;
-      double t = rounds * (2.0 * BMc * BNc * (K / S)) / (cu_tflops * eff[c] * 1e6);
-      if (S > 1) t += (2.0 * S * (double)M * N * 4.0) / 4.0e6 + 4.0;
-      if (t < best * 0.97) {
-        best = t;
-        p.kind = 1 + c; p.mt = mt; p.nt = nt; p.S = S;
-      }
+      if (K % (S * 256) != 0 || K / S < 256) break;
+      const double t = tile_estimate(c, S, M, N, K);
+      if (t < best) { best = t; set_tiled(p, c.kind, c.bm, c.bn, M, N, S); }
     }
   }
-  if (p.kind == 0) { p.kind = 1; p.mt = (M + 63) / 64; p.nt = N / 128; p.S = 1; }
   return p;
 }
 
@@ -520,14 +475,14 @@ static void skinny_go(const Plan& p, const void* A, int lda, const void* W, int 
                        lda, (const bf16_t*)W, ldw, C, ldc, M, N, K, K / p.S, p.nt, (float*)ws);
 }
 
-template <int EPI, int BM_, int BN_, int WGM, int WGN, int ST>
+template <int EPI, int BM_, int BN_, int KB, int WGM, int WGN, int ST>
 static void dma_go(const Plan& p, const void* A, int lda, const void* W, int ldw, void* C, int ldc,
                    int M, int N, int K, void* ws, hipStream_t st) {
   const dim3 grid(p.mt * p.nt * p.S), blk(64 * WGM * WGN);
-  const size_t lds = (size_t)ST * (BM_ + BN_) * BK * sizeof(bf16_t);
+  const size_t lds = (size_t)ST * (BM_ + BN_) * KB * sizeof(bf16_t);
   static bool attr_done[2] = {false, false};
   if (p.S == 1) {
-    auto kern = gemm_dma_kernel<BM_, BN_, WGM, WGN, ST, EPI, false>;
+    auto kern = gemm_dma_kernel<BM_, BN_, KB, WGM, WGN, ST, EPI, false>;
     if (!attr_done[0]) {
       (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       attr_done[0] = true;
@@ -535,7 +490,7 @@ static void dma_go(const Plan& p, const void* A, int lda, const void* W, int ldw
     hipLaunchKernelGGL(kern, grid, blk, lds, st, (const bf16_t*)A, lda, (const bf16_t*)W, ldw, C,
                        ldc, M, N, K, K, p.mt, p.nt, (float*)nullptr);
   } else {
-    auto kern = gemm_dma_kernel<BM_, BN_, WGM, WGN, ST, EPI, true>;
+    auto kern = gemm_dma_kernel<BM_, BN_, KB, WGM, WGN, ST, EPI, true>;
     if (!attr_done[1]) {
       (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       attr_done[1] = true;
@@ -543,20 +498,6 @@ static void dma_go(const Plan& p, const void* A, int lda, const void* W, int ldw
     hipLaunchKernelGGL(kern, grid, blk, lds, st, (const bf16_t*)A, lda, (const bf16_t*)W, ldw, C,
                        ldc, M, N, K, K / p.S, p.mt, p.nt, (float*)ws);
   }
-}
-
-template <int EPI, int BM_, int BN_, int WGM, int WGN>
-static void tiled_go(const Plan& p, const void* A, int lda, const void* W, int ldw, void* C,
-                     int ldc, int M, int N, int K, void* ws, hipStream_t st) {
-  const dim3 grid(p.mt * p.nt * p.S), blk(256);
-  if (p.S == 1)
-    hipLaunchKernelGGL((gemm_tiled_kernel<BM_, BN_, WGM, WGN, EPI, false>), grid, blk, 0, st,
-                       (const bf16_t*)A, lda, (const bf16_t*)W, ldw, C, ldc, M, N, K, K, p.mt, p.nt,
-                       (float*)nullptr);
-  else
-    hipLaunchKernelGGL((gemm_tiled_kernel<BM_, BN_, WGM, WGN, EPI, true>), grid, blk, 0, st,
-                       (const bf16_t*)A, lda, (const bf16_t*)W, ldw, C, ldc, M, N, K, K / p.S, p.mt,
-                       p.nt, (float*)ws);
 }
 
 template <int EPI>
@@ -583,11 +524,10 @@ static hipError_t gemm_bf16_launch(const void* A, int lda, const void* W, int ld
     }
   } else {
     switch (p.kind) {
-      case 1: tiled_go<EPI, 64, 128, 1, 4>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
-      case 2: dma_go<EPI, 128, 128, 2, 2, 4>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
-      case 3: dma_go<EPI, 128, 256, 2, 2, 3>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
-      case 4: dma_go<EPI, 256, 128, 2, 2, 3>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
-      default: dma_go<EPI, 256, 256, 2, 4, 2>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+      case 1: dma_go<EPI, 128, 128, 64, 2, 2, 4>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+      case 2: dma_go<EPI, 128, 128, 64, 2, 2, 2>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+      case 3: dma_go<EPI, 256, 128, 64, 4, 2, 3>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+      default: dma_go<EPI, 256, 256, 64, 2, 4, 2>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
     }
   }
   hipError_t e = hipGetLastError();
