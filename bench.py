@@ -9,7 +9,9 @@ Inputs (weights, prompts, forced lengths) are resident in HBM before timing.
 Prints ONE JSON line: rollout tokens/s (all generated tokens, including the
 ones of trajectories later aborted) over the timed steps, time-to-kept-set,
 the decode-attention roofline (HBM), GEMM MFMA utilisation, and the CPU
-oracle timed on a bounded sample of the same workload.
+oracle timed on a bounded sample of the same workload.  Kernel durations come
+from HIP events the library records around each attention and GEMM launch of
+the prefill and of every 8th decode step (totals are scaled to the whole run).
 """
 import argparse
 import json
@@ -172,6 +174,93 @@ def kernel_sweep(B, steps, warmup):
     return out
 
 
+ATTN_SOURCES = ("paper_2605_30859_amd/csrc/k_attn.hip", "paper_2605_30859_amd/csrc/common.h")
+
+
+def attn_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for rel in ATTN_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def _counter_rows(d):
+    """Per-dispatch counter sums from the one *_counter_collection.csv under d."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if len(files) != 1:
+        raise SystemExit(f"expected one counter_collection.csv under {d}, found {len(files)}")
+    per = {}
+    with open(files[0]) as f:
+        for r in csv.DictReader(f):
+            key = int(r["Dispatch_Id"])
+            name, v = r["Kernel_Name"], float(r["Counter_Value"])
+            per[key] = (name, per.get(key, (name, 0.0))[1] + v)
+    return list(per.values())
+
+
+def summarize_pmc(d):
+    """HBM traffic of the decode-attention kernel from four rocprofv3 --pmc
+    runs under d (pmc_copy_FETCH_SIZE, pmc_copy_WRITE_SIZE: bench.py
+    --copy-calibration; pmc_attn_FETCH_SIZE, pmc_attn_WRITE_SIZE: the rollout
+    with --kernel-include-regex attn_bf16) and the rollout's bench line in
+    d/bench_attn_fetch.json.  Each counter is scaled by what it reads for a
+    plain 1 GiB device copy."""
+    out = {"kernel": "attn_bf16_kernel", "kernel_source_sha256": attn_source_hash()}
+    cal = {}
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        rows = [v for n, v in _counter_rows(os.path.join(d, f"pmc_copy_{c}")) if "copyBuffer" in n]
+        kib = sum(rows) / len(rows)
+        cal[c] = {"KiB_per_1GiB_copy": kib, "scale": (1 << 30) / (kib * 1024.0), "copies": len(rows)}
+    out["copy_calibration"] = cal
+    with open(os.path.join(d, "bench_attn_fetch.json")) as f:
+        line = [l for l in f.read().splitlines() if l.startswith("{")][-1]
+    b = json.loads(line)
+    out["workload"] = b["config"]["workload"]
+    out["algorithmic_bytes_per_launch"] = b["roofline"]["algorithmic_bytes_per_launch"]
+    for c, key in (("FETCH_SIZE", "fetch_bytes_per_launch"), ("WRITE_SIZE", "write_bytes_per_launch")):
+        rows = [v for n, v in _counter_rows(os.path.join(d, f"pmc_attn_{c}")) if "attn_bf16" in n]
+        out[key] = sum(rows) / len(rows) * 1024.0 * cal[c]["scale"]
+        out[f"launches_{c}"] = len(rows)
+    out["traffic_bytes_per_launch"] = out["fetch_bytes_per_launch"] + out["write_bytes_per_launch"]
+    out["measured_over_algorithmic"] = out["traffic_bytes_per_launch"] / out["algorithmic_bytes_per_launch"]
+    return out
+
+
+def summarize_stats(path, top=16):
+    """Markdown table of a rocprofv3 --stats kernel_stats.csv."""
+    import csv
+    with open(path) as f:
+        rows = list(csv.DictReader(f))
+    tot = sum(float(r["TotalDurationNs"]) for r in rows)
+    rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    lines = ["| kernel | calls | total ms | avg us | share |", "|---|---:|---:|---:|---:|"]
+    for r in rows[:top]:
+        name = r["Name"].replace("|", "\\|")
+        name = name if len(name) < 90 else name[:87] + "..."
+        lines.append(f"| `{name}` | {int(r['Calls'])} | {float(r['TotalDurationNs']) / 1e6:.1f} | "
+                     f"{float(r['AverageNs']) / 1e3:.1f} | {100 * float(r['TotalDurationNs']) / tot:.1f}% |")
+    lines.append(f"| all kernels | {sum(int(r['Calls']) for r in rows)} | {tot / 1e6:.1f} | | 100% |")
+    return "\n".join(lines)
+
+
+def measured_traffic(config):
+    """Per-launch HBM bytes of the attention kernel from the committed counter
+    summary, or None when there is none for this workload or the kernel's
+    source changed since the counters were taken."""
+    p = os.path.join(ROOT, "profiles", f"attn_traffic_{config}_rollout.json")
+    if not os.path.exists(p):
+        return None
+    with open(p) as f:
+        t = json.load(f)
+    if t.get("kernel_source_sha256") != attn_source_hash():
+        return None
+    return t["traffic_bytes_per_launch"]
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -185,7 +274,17 @@ def main():
                          "hd 128, lognormal contexts), fused sampler (1024 x 151936), selection (65536)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="three 1 GiB device copies (reference for HBM byte counters), then exit")
+    ap.add_argument("--summarize-pmc", metavar="DIR",
+                    help="print the attention traffic summary (JSON) of the rocprofv3 counter runs in DIR")
+    ap.add_argument("--summarize-stats", metavar="CSV",
+                    help="print a markdown table of a rocprofv3 kernel_stats.csv")
     args = ap.parse_args()
+    if args.summarize_pmc:
+        print(json.dumps(summarize_pmc(args.summarize_pmc), indent=1))
+        return
+    if args.summarize_stats:
+        print(summarize_stats(args.summarize_stats))
+        return
     if args.copy_calibration:
         import torch
         x = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
@@ -293,8 +392,9 @@ def main():
         "kv_pool_pages": stats[-1]["n_pages"],
         "roofline": {"bound": "hbm", "kernel": "attn_bf16_kernel (paged GQA decode attention)",
                      "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": ach / HBM_PEAK_GBS, "traffic": None,
+                     "frac": ach / HBM_PEAK_GBS, "traffic": measured_traffic(args.config),
                      "launches": attn_n, "avg_launch_us": 1e3 * attn_ms / max(attn_n, 1),
+                     "timed": "HIP events on the context stream around every launch of every 8th decode step",
                      "algorithmic_bytes_per_launch": attn_b / max(attn_n, 1),
                      "share_of_step_time": attn_ms * 1e-3 / total},
         "gemm": {"bound": "mfma", "achieved": gemm_tf, "peak": peak_mm, "unit": "TFLOP/s",

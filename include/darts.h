@@ -59,8 +59,9 @@ typedef enum { DARTS_F32 = 0, DARTS_BF16 = 1 } darts_dtype;
 #define DARTS_FLAG_PERMUTE_PAGES 0x2u  /* initial free list in a seeded random order
                                           (physical page ids must not change any output) */
 #define DARTS_FLAG_TIMING        0x4u  /* record HIP events around decode-attention and
-                                          GEMM launches on the context's stream
-                                          (darts_get_stats reports them) */
+                                          GEMM launches on the context's stream, in the
+                                          prefill and in every 8th decode step (steps
+                                          8, 16, ...); darts_get_stats reports them */
 
 /* Decoder shape.  Weights are generated on the device from weight_seed
  * (Philox uniform, variance 1/fan_in, rounded to bf16 for DARTS_BF16).
@@ -123,10 +124,14 @@ typedef struct {
   int64_t pages_hwm;         /* high-water mark of pages in use */
   int32_t n_live;
   int32_t n_done;            /* prompts whose kept set is complete */
-  double attn_ms;            /* with DARTS_FLAG_TIMING: summed decode-attention time */
+  /* With DARTS_FLAG_TIMING, estimates for the whole run from the timed
+   * launches: each launch of a timed decode step counts 8 times (the steps
+   * between timed ones), a prefill launch once.  Ratios (bytes / ms,
+   * FLOP / ms) are those of the timed launches.                            */
+  double attn_ms;            /* decode-attention time */
   double attn_bytes;         /* algorithmic bytes of those launches */
   int64_t attn_launches;
-  double gemm_ms;            /* with DARTS_FLAG_TIMING: summed GEMM time (decode and prefill) */
+  double gemm_ms;            /* GEMM time (decode and prefill) */
   double gemm_flop;          /* 2*M*N*K summed over those launches */
   int64_t gemm_launches;
   double gemm_cls_ms[6];     /* per GEMM class: QKV, O, gate-up, down, LM head, MoE block

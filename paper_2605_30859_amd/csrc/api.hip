@@ -34,7 +34,13 @@ struct LayerW {
 struct TimedLaunch {
   int kind;        // 0 attention (decode), 1.. GEMM class + 1 (QKV, O, gate-up, down, LM head)
   double units;    // algorithmic bytes (attention) or FLOP (GEMM)
+  double weight;   // launches of the whole run this one stands for
 };
+
+// With timing on, events are recorded in the prefill and in every
+// kTimingStride-th decode step only (an event pair per launch costs about a
+// tenth of the decode time); each timed decode launch stands for kTimingStride.
+constexpr int kTimingStride = 8;
 
 }  // namespace
 
@@ -109,6 +115,7 @@ struct darts_ctx {
   int64_t hwm = 0;
   int last_rows_out = 0;
   bool poisoned = false;
+  double timed_weight = 0.0;       // > 0 while the current step's launches are timed
   std::string err;
   std::vector<TimedLaunch> pending;
   std::vector<hipEvent_t> events;  // pool, two per pending launch
@@ -158,7 +165,7 @@ static bool timing_on(const darts_ctx* c) { return (c->rc.flags & DARTS_FLAG_TIM
 
 // Record the start event of a timed launch; returns its index or -1.
 static int tbegin(darts_ctx* c, int kind, double units) {
-  if (!timing_on(c)) return -1;
+  if (c->timed_weight <= 0.0) return -1;
   const size_t i = c->pending.size();
   while (c->events.size() < 2 * (i + 1)) {
     hipEvent_t e;
@@ -166,19 +173,19 @@ static int tbegin(darts_ctx* c, int kind, double units) {
     c->events.push_back(e);
   }
   if (hipEventRecord(c->events[2 * i], c->st) != hipSuccess) return -1;
-  c->pending.push_back(TimedLaunch{kind, units});
+  c->pending.push_back(TimedLaunch{kind, units, c->timed_weight});
   return (int)i;
 }
 // Reserve an event pair without recording (the launcher records it).
 static int treserve(darts_ctx* c, int kind, double units) {
-  if (!timing_on(c)) return -1;
+  if (c->timed_weight <= 0.0) return -1;
   const size_t i = c->pending.size();
   while (c->events.size() < 2 * (i + 1)) {
     hipEvent_t e;
     if (hipEventCreate(&e) != hipSuccess) return -1;
     c->events.push_back(e);
   }
-  c->pending.push_back(TimedLaunch{kind, units});
+  c->pending.push_back(TimedLaunch{kind, units, c->timed_weight});
   return (int)i;
 }
 static void tend(darts_ctx* c, int i) {
@@ -563,6 +570,7 @@ int darts_prefill(darts_ctx* c, const int32_t* d_prompts, const int32_t* d_force
   if (!out->traj_id || !out->token || !out->logprob || !out->entropy || !out->finished)
     return DARTS_EINVAL;
   const bool b = c->bf16;
+  c->timed_weight = timing_on(c) ? 1.0 : 0.0;
   const int rows = c->P * c->Lp;
   HIPCHK(c, hipMemcpyAsync(c->forced_len, d_forced_len, (size_t)c->n_traj * 4,
                            hipMemcpyDeviceToDevice, c->st));
@@ -608,6 +616,7 @@ int darts_decode_step(darts_ctx* c, const int32_t* d_force_tokens, darts_step_ou
   if (pos + 1 > c->Lp + c->cap) return DARTS_ESTATE;
   const bool need_pages = ((s_before - 1) % kPage) == 0;
   if (need_pages && n > c->free_top) return DARTS_ENOMEM;
+  c->timed_weight = (timing_on(c) && s_before % kTimingStride == 0) ? (double)kTimingStride : 0.0;
   int32_t* live = c->live[c->cur];
   if (need_pages) {
     HIPCHK(c, launch_alloc_pages(live, n, c->gen, c->pp, c->page_table, c->max_pages, c->free_stack,
@@ -667,10 +676,11 @@ int darts_select_and_prune(darts_ctx* c, int32_t* d_kept, int32_t* d_done_step, 
     float ms = 0.f;
     HIPCHK(c, hipEventElapsedTime(&ms, c->events[2 * i], c->events[2 * i + 1]));
     const TimedLaunch& t = c->pending[i];
-    if (t.kind == 0) { c->attn_ms += ms; c->attn_bytes += t.units; c->attn_launches += 1; }
+    const double w = t.weight;
+    if (t.kind == 0) { c->attn_ms += w * ms; c->attn_bytes += w * t.units; c->attn_launches += (int64_t)w; }
     else {
-      c->gemm_ms += ms; c->gemm_flop += t.units; c->gemm_launches += 1;
-      c->cls_ms[t.kind - 1] += ms; c->cls_flop[t.kind - 1] += t.units;
+      c->gemm_ms += w * ms; c->gemm_flop += w * t.units; c->gemm_launches += (int64_t)w;
+      c->cls_ms[t.kind - 1] += w * ms; c->cls_flop[t.kind - 1] += w * t.units;
     }
   }
   c->pending.clear();
