@@ -269,6 +269,8 @@ def main():
     ap.add_argument("--config", default="qwen3-8b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-abort", action="store_true", help="counterfactual without early stop")
+    ap.add_argument("--shared-prefix", action="store_true",
+                    help="decode attention reads each prompt's shared pages once per group")
     ap.add_argument("--sweep", action="store_true",
                     help="kernel sweep instead of the rollout: decode attention (1024 rows, 32/8 heads, "
                          "hd 128, lognormal contexts), fused sampler (1024 x 151936), selection (65536)")
@@ -313,7 +315,8 @@ def main():
         return
     model, run = get_config(args.config)
     prompts, forced = rollout_inputs(model, run)
-    flags = B.FLAG_TIMING | (B.FLAG_NO_ABORT if args.no_abort else 0)
+    flags = (B.FLAG_TIMING | (B.FLAG_NO_ABORT if args.no_abort else 0) |
+             (B.FLAG_SHARED_PREFIX if args.shared_prefix else 0))
     t_init = time.perf_counter()
     ro = B.Rollout(model, run, flags=flags)
     pr = torch.from_numpy(prompts.reshape(-1).copy()).cuda()
@@ -384,7 +387,8 @@ def main():
         "data": "synthetic (seeded uniform prompt tokens, lognormal forced lengths, Philox random-init weights)",
         "config": {"workload": workload_desc(model, run), "name": args.config,
                    "prompts": run.n_prompts, "m": run.m, "k": run.k, "cap": run.cap,
-                   "early_stop": not args.no_abort},
+                   "early_stop": not args.no_abort,
+                   "decode_attention": "shared-prefix" if args.shared_prefix else "per-row"},
         "time_to_kept_set_s": float(np.mean(walls)),
         "tokens_per_rollout": stats[-1]["tokens_decoded"],
         "sampling_steps": stats[-1]["steps"],

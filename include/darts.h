@@ -62,6 +62,9 @@ typedef enum { DARTS_F32 = 0, DARTS_BF16 = 1 } darts_dtype;
                                           GEMM launches on the context's stream, in the
                                           prefill and in every 8th decode step (steps
                                           8, 16, ...); darts_get_stats reports them */
+#define DARTS_FLAG_SHARED_PREFIX 0x8u  /* bf16 models: decode attention reads a prompt's
+                                          shared pages once per group of its live members
+                                          (a prefix kernel) instead of once per row */
 
 /* Decoder shape.  Weights are generated on the device from weight_seed
  * (Philox uniform, variance 1/fan_in, rounded to bf16 for DARTS_BF16).
@@ -129,7 +132,9 @@ typedef struct {
    * between timed ones), a prefill launch once.  Ratios (bytes / ms,
    * FLOP / ms) are those of the timed launches.                            */
   double attn_ms;            /* decode-attention time */
-  double attn_bytes;         /* algorithmic bytes of those launches */
+  double attn_bytes;         /* algorithmic bytes of those launches: each distinct key and
+                                value once per kv head (a prompt's shared pages once per
+                                live group), q and out, page ids */
   int64_t attn_launches;
   double gemm_ms;            /* GEMM time (decode and prefill) */
   double gemm_flop;          /* 2*M*N*K summed over those launches */
@@ -137,6 +142,9 @@ typedef struct {
   double gemm_cls_ms[6];     /* per GEMM class: QKV, O, gate-up, down, LM head, MoE block
                                 (router + routing + grouped experts + combine) */
   double gemm_cls_flop[6];
+  double attn_traj_bytes;    /* the same launches' bytes if every row read its whole
+                                context itself (equal to attn_bytes unless
+                                DARTS_FLAG_SHARED_PREFIX) */
 } darts_stats;
 
 typedef struct darts_ctx darts_ctx;
@@ -253,6 +261,31 @@ int darts_attn_decode(const void* d_q, const void* d_k_pool, const void* d_v_poo
                       const int32_t* d_ctx_len, int32_t n_rows, int32_t n_q_heads,
                       int32_t n_kv_heads, int32_t head_dim, int32_t max_ctx, int32_t dtype,
                       void* d_out, void* d_workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace darts_attn_decode_shared needs for these sizes.       */
+size_t darts_attn_shared_workspace_bytes(int32_t n_rows, int32_t n_q_heads, int32_t n_kv_heads,
+                                         int32_t head_dim, int32_t ctx_len, int32_t prefix_pages);
+
+/* The same decode attention for rows that share a prompt prefix, as the m
+ * trajectories of one prompt do in the rollout (their prompt's KV pages are
+ * shared, Alg. 2 samples them from one prompt): the shared pages are read
+ * once per group of rows instead of once per row.  bf16 only.
+ *   d_row_traj    [n_rows] int32: row r uses page-table row d_row_traj[r]
+ *                 (clamped into [0, pt_rows)); rows r with equal
+ *                 d_row_traj[r] / m that are consecutive form a group
+ *   d_page_table  [pt_rows][pt_stride] int32, pt_stride >= ceil(ctx_len/16);
+ *                 the members of a group must have equal first prefix_pages
+ *                 entries (the prefix is read through the group's first row)
+ *   ctx_len       every row's context, > 16 * prefix_pages
+ *   d_q, d_out, pools, page ids: as for darts_attn_decode
+ *   d_workspace   darts_attn_shared_workspace_bytes(...) bytes, 256-byte aligned
+ * Returns DARTS_EINVAL for inconsistent sizes or dtype != DARTS_BF16.       */
+int darts_attn_decode_shared(const void* d_q, const void* d_k_pool, const void* d_v_pool,
+                             int64_t n_pages, const int32_t* d_page_table, int32_t pt_stride,
+                             int32_t pt_rows, const int32_t* d_row_traj, int32_t m,
+                             int32_t prefix_pages, int32_t ctx_len, int32_t n_rows, int32_t n_q_heads,
+                             int32_t n_kv_heads, int32_t head_dim, int32_t dtype, void* d_out,
+                             void* d_workspace, size_t workspace_bytes, void* stream);
 
 /* Fused sampler: for each row, Gumbel-max token with counter (traj, step),
  * log-prob of the taken token (d_force[r] if d_force != NULL and >= 0, else

@@ -6,8 +6,10 @@ and KV page reclaim -- all in hand-written HIP kernels behind a C ABI
 """
 from .binding import (DARTS_OK, DARTS_EINVAL, DARTS_ENOMEM, DARTS_ESTATE, DARTS_EHIP,
                       DARTS_F32, DARTS_BF16, FLAG_NO_ABORT, FLAG_PERMUTE_PAGES, FLAG_TIMING,
+                      FLAG_SHARED_PREFIX,
                       DartsError, load_library, lib_path, Rollout)
 
 __all__ = ["DARTS_OK", "DARTS_EINVAL", "DARTS_ENOMEM", "DARTS_ESTATE", "DARTS_EHIP",
            "DARTS_F32", "DARTS_BF16", "FLAG_NO_ABORT", "FLAG_PERMUTE_PAGES", "FLAG_TIMING",
+           "FLAG_SHARED_PREFIX",
            "DartsError", "load_library", "lib_path", "Rollout"]

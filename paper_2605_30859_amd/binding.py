@@ -9,7 +9,7 @@ import numpy as np
 
 DARTS_OK, DARTS_EINVAL, DARTS_ENOMEM, DARTS_ESTATE, DARTS_EHIP = 0, 1, 2, 3, 4
 DARTS_F32, DARTS_BF16 = 0, 1
-FLAG_NO_ABORT, FLAG_PERMUTE_PAGES, FLAG_TIMING = 0x1, 0x2, 0x4
+FLAG_NO_ABORT, FLAG_PERMUTE_PAGES, FLAG_TIMING, FLAG_SHARED_PREFIX = 0x1, 0x2, 0x4, 0x8
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 lib_path = os.path.join(_HERE, "libdarts.so")
@@ -49,7 +49,7 @@ class Stats(C.Structure):
                 ("n_done", C.c_int32), ("attn_ms", C.c_double), ("attn_bytes", C.c_double),
                 ("attn_launches", C.c_int64), ("gemm_ms", C.c_double), ("gemm_flop", C.c_double),
                 ("gemm_launches", C.c_int64), ("gemm_cls_ms", C.c_double * 6),
-                ("gemm_cls_flop", C.c_double * 6)]
+                ("gemm_cls_flop", C.c_double * 6), ("attn_traj_bytes", C.c_double)]
 
 
 _P = C.c_void_p
@@ -70,6 +70,10 @@ _SIGS = {
     "darts_attn_workspace_bytes": (C.c_size_t, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32]),
     "darts_attn_decode": (C.c_int, [_P, _P, _P, C.c_int64, _P, C.c_int32, _P, C.c_int32, C.c_int32,
                                     C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P, _P, C.c_size_t, _P]),
+    "darts_attn_shared_workspace_bytes": (C.c_size_t, [C.c_int32] * 6),
+    "darts_attn_decode_shared": (C.c_int, [_P, _P, _P, C.c_int64, _P, C.c_int32, C.c_int32, _P,
+                                           C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                           C.c_int32, C.c_int32, C.c_int32, _P, _P, C.c_size_t, _P]),
     "darts_sample": (C.c_int, [_P, C.c_int32, C.c_int32, C.c_int32, C.c_uint64, _P, _P, C.c_float,
                                _P, _P, _P, _P, _P]),
     "darts_debug_gumbel": (C.c_int, [_P, _P, C.c_int64, _P]),
@@ -146,6 +150,22 @@ def darts_attn_decode(q, k_pool, v_pool, n_pages, page_table, ctx_len, n_q_heads
         _ptr(q), _ptr(k_pool), _ptr(v_pool), n_pages, _ptr(page_table), page_table.shape[1],
         _ptr(ctx_len), n_rows, n_q_heads, n_kv_heads, head_dim, max_ctx, dtype, _ptr(out),
         _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def darts_attn_shared_workspace_bytes(n_rows, n_q_heads, n_kv_heads, head_dim, ctx_len, prefix_pages):
+    return int(load_library().darts_attn_shared_workspace_bytes(n_rows, n_q_heads, n_kv_heads,
+                                                                head_dim, ctx_len, prefix_pages))
+
+
+def darts_attn_decode_shared(q, k_pool, v_pool, n_pages, page_table, row_traj, m, prefix_pages,
+                             ctx_len, n_q_heads, n_kv_heads, head_dim, dtype, out, workspace,
+                             stream=None):
+    n_rows = row_traj.numel()
+    _check(load_library().darts_attn_decode_shared(
+        _ptr(q), _ptr(k_pool), _ptr(v_pool), n_pages, _ptr(page_table), page_table.shape[1],
+        page_table.shape[0], _ptr(row_traj), m, prefix_pages, ctx_len, n_rows, n_q_heads, n_kv_heads,
+        head_dim, dtype, _ptr(out), _ptr(workspace), workspace.numel() * workspace.element_size(),
+        _stream(stream)))
 
 
 def darts_sample(logits, dtype, seed, traj, step, temperature, force, token, logprob, entropy,

@@ -35,6 +35,8 @@ struct TimedLaunch {
   int kind;        // 0 attention (decode), 1.. GEMM class + 1 (QKV, O, gate-up, down, LM head)
   double units;    // algorithmic bytes (attention) or FLOP (GEMM)
   double weight;   // launches of the whole run this one stands for
+  double units_grp = 0.0;   // attention with a shared prefix: bytes per live prompt group
+  double traj_units = 0.0;  // attention: bytes if every row read its whole context itself
 };
 
 // With timing on, events are recorded in the prefill and in every
@@ -103,6 +105,7 @@ struct darts_ctx {
   size_t gemm_ws_bytes = 0;
   void* attn_ws = nullptr;
   size_t attn_ws_bytes = 0;
+  bool share_prefix = false;      // decode attention reads each prompt's pages once per group
   int32_t* h_info = nullptr;       // pinned host
   // host state
   int phase = 0;                   // 0 init, 1 decoding, 2 done
@@ -119,7 +122,7 @@ struct darts_ctx {
   std::string err;
   std::vector<TimedLaunch> pending;
   std::vector<hipEvent_t> events;  // pool, two per pending launch
-  double attn_ms = 0.0, attn_bytes = 0.0;
+  double attn_ms = 0.0, attn_bytes = 0.0, attn_traj_bytes = 0.0;
   int64_t attn_launches = 0;
   double gemm_ms = 0.0, gemm_flop = 0.0;
   int64_t gemm_launches = 0;
@@ -393,8 +396,12 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
   A(&c->logits, (size_t)c->n_traj * c->V * 4);
   c->gemm_ws_bytes = gemm_ws_need(c);
   A(&c->gemm_ws, c->gemm_ws_bytes);
+  c->share_prefix = c->bf16 && c->m > 1 && c->pp > 0 && (c->rc.flags & DARTS_FLAG_SHARED_PREFIX);
   c->attn_ws_bytes = std::max(attn_workspace_bytes(c->n_traj, c->hq, c->hkv, c->hd, c->Lp + c->cap),
                               attn_workspace_bytes(rows_pf, c->hq, c->hkv, c->hd, c->Lp));
+  if (c->share_prefix)
+    c->attn_ws_bytes = std::max(c->attn_ws_bytes, attn_shared_workspace_bytes(c->n_traj, c->hq, c->hkv,
+                                                                               c->hd, c->Lp + c->cap, c->pp));
   A(&c->attn_ws, c->attn_ws_bytes);
   if (e == hipSuccess) e = hipHostMalloc((void**)&c->h_info, 64, hipHostMallocDefault);
   if (e != hipSuccess) {
@@ -470,7 +477,7 @@ int darts_reset(darts_ctx* c) {
   c->phase = 0; c->cur = 0; c->n_live = 0; c->n_done = 0; c->free_top = (int)c->n_pages;
   c->step = 0; c->tokens = 0; c->hwm = 0; c->last_rows_out = 0;
   c->pending.clear();
-  c->attn_ms = c->attn_bytes = 0.0; c->attn_launches = 0;
+  c->attn_ms = c->attn_bytes = c->attn_traj_bytes = 0.0; c->attn_launches = 0;
   c->gemm_ms = c->gemm_flop = 0.0; c->gemm_launches = 0;
   for (int i = 0; i < 6; ++i) c->cls_ms[i] = c->cls_flop[i] = 0.0;
   return DARTS_OK;
@@ -491,15 +498,31 @@ static int run_attention(darts_ctx* c, int layer, int n_rows, const int32_t* row
                          int ctx_base, int max_ctx) {
   void* kp = (char*)c->kpool + (size_t)layer * c->pool_layer_elems * c->esz;
   void* vp = (char*)c->vpool + (size_t)layer * c->pool_layer_elems * c->esz;
-  // algorithmic bytes: every key and value of the context once per kv head,
-  // q and out once, one page id per 16 keys
+  // algorithmic bytes: every distinct key and value once per kv head (with a
+  // shared prefix, a prompt's prefix once per live group), q and out once,
+  // one page id per 16 keys of each row
   const double ctx = ctx_base;
-  const double bytes = (double)n_rows * (ctx * c->hkv * c->hd * 2.0 * c->esz +
-                                         2.0 * c->hq * c->hd * c->esz + std::ceil(ctx / kPage) * 4.0);
-  // decode launches are timed around the attention kernel itself (events
-  // recorded inside the launcher, before and after that kernel only)
+  const double kv_tok = (double)c->hkv * c->hd * 2.0 * c->esz;
+  const double per_row_fixed = 2.0 * c->hq * c->hd * c->esz + std::ceil(ctx / kPage) * 4.0;
+  const double traj_bytes = (double)n_rows * (ctx * kv_tok + per_row_fixed);
+  const bool shared = c->share_prefix && ctx_mod == 0 && ctx_base > c->pp * kPage;
+  double bytes = traj_bytes, grp_bytes = 0.0;
+  if (shared) {
+    bytes = (double)n_rows * ((ctx - c->pp * kPage) * kv_tok + per_row_fixed);
+    grp_bytes = (double)c->pp * kPage * kv_tok;
+  }
+  // decode launches are timed around the attention kernels themselves (events
+  // recorded inside the launcher)
   const int ti = ctx_mod == 0 ? treserve(c, 0, bytes) : -1;
+  if (ti >= 0) { c->pending[ti].units_grp = grp_bytes; c->pending[ti].traj_units = traj_bytes; }
   hipEvent_t e0 = ti >= 0 ? c->events[2 * ti] : nullptr, e1 = ti >= 0 ? c->events[2 * ti + 1] : nullptr;
+  if (shared) {
+    HIPCHK(c, launch_attention_shared(c->q, kp, vp, c->n_pages, c->page_table, c->max_pages, row_pt,
+                                      c->n_traj, c->m, c->pp, layer == 0, ctx_base, n_rows, c->hq,
+                                      c->hkv, c->hd, c->attn,
+                                      c->attn_ws, c->attn_ws_bytes, c->st, e0, e1, c->dcnt + 8));
+    return DARTS_OK;
+  }
   HIPCHK(c, launch_attention(c->q, kp, vp, c->n_pages, c->page_table, c->max_pages, row_pt, nullptr,
                              ctx_mod, ctx_base, n_rows, c->hq, c->hkv, c->hd, max_ctx, c->bf16,
                              c->attn, c->attn_ws, c->attn_ws_bytes, c->st, e0, e1));
@@ -665,7 +688,7 @@ int darts_select_and_prune(darts_ctx* c, int32_t* d_kept, int32_t* d_done_step, 
     HIPCHK(c, hipMemcpyAsync(d_kept, c->kept, (size_t)c->P * c->k * 4, hipMemcpyDeviceToDevice, c->st));
   if (d_done_step)
     HIPCHK(c, hipMemcpyAsync(d_done_step, c->done_step, (size_t)c->P * 4, hipMemcpyDeviceToDevice, c->st));
-  HIPCHK(c, hipMemcpyAsync(c->h_info, c->dcnt + 4, 16, hipMemcpyDeviceToHost, c->st));
+  HIPCHK(c, hipMemcpyAsync(c->h_info, c->dcnt + 4, 32, hipMemcpyDeviceToHost, c->st));
   HIPCHK(c, hipStreamSynchronize(c->st));
   c->cur ^= 1;
   c->n_live = c->h_info[0];
@@ -677,7 +700,12 @@ int darts_select_and_prune(darts_ctx* c, int32_t* d_kept, int32_t* d_done_step, 
     HIPCHK(c, hipEventElapsedTime(&ms, c->events[2 * i], c->events[2 * i + 1]));
     const TimedLaunch& t = c->pending[i];
     const double w = t.weight;
-    if (t.kind == 0) { c->attn_ms += w * ms; c->attn_bytes += w * t.units; c->attn_launches += (int64_t)w; }
+    if (t.kind == 0) {
+      // h_info[4]: live prompt groups of the step (written by the shared-prefix launch)
+      const double units = t.units + (t.units_grp > 0.0 ? t.units_grp * c->h_info[4] : 0.0);
+      c->attn_ms += w * ms; c->attn_bytes += w * units; c->attn_traj_bytes += w * t.traj_units;
+      c->attn_launches += (int64_t)w;
+    }
     else {
       c->gemm_ms += w * ms; c->gemm_flop += w * t.units; c->gemm_launches += (int64_t)w;
       c->cls_ms[t.kind - 1] += w * ms; c->cls_flop[t.kind - 1] += w * t.units;
@@ -700,6 +728,7 @@ int darts_get_stats(const darts_ctx* c, darts_stats* s) {
   s->n_done = c->n_done;
   s->attn_ms = c->attn_ms;
   s->attn_bytes = c->attn_bytes;
+  s->attn_traj_bytes = c->attn_traj_bytes;
   s->attn_launches = c->attn_launches;
   s->gemm_ms = c->gemm_ms;
   s->gemm_flop = c->gemm_flop;
@@ -784,6 +813,36 @@ int darts_attn_decode(const void* d_q, const void* d_k_pool, const void* d_v_poo
                                   d_ctx_len, 0, 0, n_rows, n_q_heads, n_kv_heads, head_dim, max_ctx,
                                   dtype == DARTS_BF16, d_out, d_workspace, workspace_bytes,
                                   (hipStream_t)stream);
+  return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
+}
+
+size_t darts_attn_shared_workspace_bytes(int32_t n_rows, int32_t n_q_heads, int32_t n_kv_heads,
+                                         int32_t head_dim, int32_t ctx_len, int32_t prefix_pages) {
+  if (n_rows < 1 || n_q_heads < 1 || n_kv_heads < 1 || ctx_len < 1 || prefix_pages < 1) return 0;
+  return attn_shared_workspace_bytes(n_rows, n_q_heads, n_kv_heads, head_dim, ctx_len, prefix_pages);
+}
+
+int darts_attn_decode_shared(const void* d_q, const void* d_k_pool, const void* d_v_pool,
+                             int64_t n_pages, const int32_t* d_page_table, int32_t pt_stride,
+                             int32_t pt_rows, const int32_t* d_row_traj, int32_t m,
+                             int32_t prefix_pages, int32_t ctx_len, int32_t n_rows, int32_t n_q_heads,
+                             int32_t n_kv_heads, int32_t head_dim, int32_t dtype, void* d_out,
+                             void* d_workspace, size_t workspace_bytes, void* stream) {
+  if (!d_q || !d_k_pool || !d_v_pool || !d_page_table || !d_row_traj || !d_out) return DARTS_EINVAL;
+  if (n_rows < 0 || n_q_heads < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads ||
+      n_q_heads / n_kv_heads > 16 || n_pages < 1 || pt_rows < 1 || m < 1 || prefix_pages < 1)
+    return DARTS_EINVAL;
+  if (!(head_dim == 32 || head_dim == 64 || head_dim == 128)) return DARTS_EINVAL;
+  if (dtype != DARTS_BF16) return DARTS_EINVAL;
+  if (ctx_len <= prefix_pages * kPage || pt_stride < (ctx_len + kPage - 1) / kPage) return DARTS_EINVAL;
+  if (n_rows == 0) return DARTS_OK;
+  if (workspace_bytes <
+      attn_shared_workspace_bytes(n_rows, n_q_heads, n_kv_heads, head_dim, ctx_len, prefix_pages))
+    return DARTS_EINVAL;
+  hipError_t e = launch_attention_shared(d_q, d_k_pool, d_v_pool, n_pages, d_page_table, pt_stride,
+                                         d_row_traj, pt_rows, m, prefix_pages, true, ctx_len, n_rows,
+                                         n_q_heads, n_kv_heads, head_dim, d_out, d_workspace,
+                                         workspace_bytes, (hipStream_t)stream);
   return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
 }
 

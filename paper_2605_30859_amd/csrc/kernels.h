@@ -55,6 +55,21 @@ hipError_t launch_attention(const void* q, const void* k_pool, const void* v_poo
                             int ctx_base, int n_rows, int hq, int hkv, int hd, int max_ctx,
                             bool bf16, void* out, void* ws, size_t ws_bytes, hipStream_t st,
                             hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+// Shared-prefix decode attention (bf16): every row has context ctx; row r
+// uses page-table row row_traj[r] (clamped into [0, pt_rows) when pt_rows >
+// 0); consecutive rows of one group (row_traj[r] / m) share their first
+// prefix_pages pages.  build_groups: derive the group table from row_traj
+// (else reuse the one in ws from an earlier call with the same rows); the
+// group count is also written to *n_groups_out when given.  Requires
+// ctx > 16 * prefix_pages.
+size_t attn_shared_workspace_bytes(int n_rows, int hq, int hkv, int hd, int ctx, int prefix_pages);
+hipError_t launch_attention_shared(const void* q, const void* k_pool, const void* v_pool,
+                                   int64_t n_pages, const int32_t* page_table, int pt_stride,
+                                   const int32_t* row_traj, int pt_rows, int m, int prefix_pages,
+                                   bool build_groups, int ctx, int n_rows, int hq, int hkv, int hd,
+                                   void* out, void* ws,
+                                   size_t ws_bytes, hipStream_t st, hipEvent_t ev0 = nullptr,
+                                   hipEvent_t ev1 = nullptr, int32_t* n_groups_out = nullptr);
 
 // ---- sampler (k_sample.hip)
 struct SampleArgs {

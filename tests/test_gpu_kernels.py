@@ -15,7 +15,7 @@ from oracle.sampler import sample_row
 from oracle.selection import group_decision, LIVE, EOS, TRUNC, ABORTED
 from oracle import sweep as OS
 from workload import sweep_attention_inputs, sweep_sampler_logits, sweep_selection_inputs
-from workload.gen import sweep_page_table, f32_from_bf16_bits
+from workload.gen import sweep_page_table, shared_prefix_page_table, f32_from_bf16_bits
 from workload.configs import SWEEP
 
 pytestmark = pytest.mark.gpu
@@ -169,6 +169,73 @@ def test_attention_full_sweep_sampled_rows():
         err = np.max(np.abs(got[r] - ref))
         assert err <= 2e-2 * max(1.0, np.max(np.abs(ref))), (r, ctx[r], err)
     assert np.isfinite(got).all()
+
+
+@pytest.mark.parametrize("hq,hkv,hd,m,prefix_pages,extra,groups", [
+    (32, 8, 128, 16, 32, 600, (16, 5, 1, 16, 9)),     # Qwen3-8B heads; suffix split in chunks
+    (32, 4, 128, 16, 13, 1, (3, 16)),                # G = 8; prefix chunks 8 + 5; one suffix key
+    (16, 4, 64, 16, 2, 37, (16, 16, 7)),             # dense-small heads
+    (8, 8, 128, 8, 3, 20, (8, 2)),                   # G = 1
+    (32, 8, 128, 16, 32, 100, (16,) * 32),           # 512 rows (the rollout's first steps)
+    (32, 8, 128, 16, 32, 7687, (8,)),                # few rows, long suffix: 61 chunks per row
+])
+def test_attention_shared_prefix(hq, hkv, hd, m, prefix_pages, extra, groups):
+    """Rows of prompt groups sharing their prompt pages: the shared-prefix
+    path against the oracle (sampled rows for the 512-row case) and against
+    the per-row path on the same inputs."""
+    B = _b()
+    seed = 91
+    ctx = prefix_pages * 16 + extra
+    say(f"shared-prefix attention hq={hq} hkv={hkv} hd={hd} m={m} pp={prefix_pages} ctx={ctx} groups={groups}")
+    rng = np.random.default_rng(seed)
+    row_traj, pt, n_pages = shared_prefix_page_table(groups, m, prefix_pages, ctx, 16, rng, spare=5)
+    rows = len(row_traj)
+    q = torch.empty(rows * hq * hd, dtype=torch.bfloat16, device=DEV)
+    kp = torch.empty(n_pages * hkv * 16 * hd, dtype=torch.bfloat16, device=DEV)
+    vp = torch.empty_like(kp)
+    B.darts_fill_uniform(q, OS.T_Q, seed, B.DARTS_BF16)
+    B.darts_fill_kv_pool(kp, vp, n_pages, hkv, hd, seed, B.DARTS_BF16)
+    ptd = torch.from_numpy(pt).to(DEV)
+    rtd = torch.from_numpy(row_traj).to(DEV)
+    out = torch.zeros(rows * hq * hd, dtype=torch.bfloat16, device=DEV)
+    ws = torch.empty(B.darts_attn_shared_workspace_bytes(rows, hq, hkv, hd, ctx, prefix_pages),
+                     dtype=torch.uint8, device=DEV)
+    B.darts_attn_decode_shared(q, kp, vp, n_pages, ptd, rtd, m, prefix_pages, ctx, hq, hkv, hd,
+                               B.DARTS_BF16, out, ws)
+    # the per-row path on the same rows (page-table rows gathered per row)
+    pt_rows = torch.from_numpy(np.ascontiguousarray(pt[row_traj])).to(DEV)
+    ctxd = torch.full((rows,), ctx, dtype=torch.int32, device=DEV)
+    out2 = torch.zeros_like(out)
+    ws2 = torch.empty(B.darts_attn_workspace_bytes(rows, hq, hkv, hd, ctx), dtype=torch.uint8, device=DEV)
+    B.darts_attn_decode(q, kp, vp, n_pages, pt_rows, ctxd, hq, hkv, hd, ctx, B.DARTS_BF16, out2, ws2)
+    torch.cuda.synchronize()
+    got = out.float().cpu().numpy().reshape(rows, hq, hd)
+    got2 = out2.float().cpu().numpy().reshape(rows, hq, hd)
+    assert np.isfinite(got).all()
+    assert np.max(np.abs(got - got2)) <= 2e-2 * max(1.0, np.max(np.abs(got2)))
+    if ctx > 4096:
+        sample = [0, rows - 1]
+    else:
+        sample = range(rows) if rows <= 64 else list(range(0, rows, 37)) + [rows - 1]
+    for r in sample:
+        ref = OS.attention_row(r, ctx, pt[row_traj[r]], seed, hq, hkv, hd)
+        err = np.max(np.abs(got[r] - ref))
+        assert err <= 2e-2 * max(1.0, np.max(np.abs(ref))), (r, err)
+
+
+def test_attention_shared_prefix_errors():
+    B = _b()
+    q = torch.zeros(4 * 32 * 128, dtype=torch.bfloat16, device=DEV)
+    kp = torch.zeros(64 * 8 * 16 * 128, dtype=torch.bfloat16, device=DEV)
+    pt = torch.zeros((16, 8), dtype=torch.int32, device=DEV)
+    rt = torch.arange(4, dtype=torch.int32, device=DEV)
+    ws = torch.empty(1 << 20, dtype=torch.uint8, device=DEV)
+    with pytest.raises(B.DartsError):   # context not beyond the prefix
+        B.darts_attn_decode_shared(q, kp, kp, 64, pt, rt, 4, 2, 32, 32, 8, 128, B.DARTS_BF16, q, ws)
+    with pytest.raises(B.DartsError):   # fp32 is not supported on this path
+        B.darts_attn_decode_shared(q, kp, kp, 64, pt, rt, 4, 2, 40, 32, 8, 128, B.DARTS_F32, q, ws)
+    with pytest.raises(B.DartsError):   # workspace too small
+        B.darts_attn_decode_shared(q, kp, kp, 64, pt, rt, 4, 2, 40, 32, 8, 128, B.DARTS_BF16, q, ws[:64])
 
 
 def _oracle_select(status, length, mlp, m, k, L, m_up, early_stop):

@@ -230,11 +230,10 @@ def dense_small_reduced():
     return model, run, ref, got
 
 
-def test_dense_small_bf16_parity(dense_small_reduced):
+def _check_bf16(name, run, ref, got):
     """bf16 configuration: logits within 2e-2 of the row's max |logit|; the
     log-prob / entropy deviation is bounded by the logit deviation (|d lp| <= 2 max|d z|);
     sampled tokens bit-exact where the top-2 margin is >= 0.1."""
-    model, run, ref, got = dense_small_reduced
     excused = mism = checked = 0
     worst = 0.0
     for s, rec in enumerate(got["steps"]):
@@ -255,10 +254,48 @@ def test_dense_small_bf16_parity(dense_small_reduced):
                     excused += 1
                 else:
                     mism += 1
-    say(f"dense-small: {checked} rows, worst logit dev {worst:.3e}, {excused} excused")
+    say(f"{name}: {checked} rows, worst logit dev {worst:.3e}, {excused} excused")
     assert mism == 0
     assert excused <= checked // 5
     for i in range(run.n_prompts):
         assert got["done"][i] == ref.done_step[i]
     assert got["stats"]["steps"] == ref.steps
     assert got["stats"]["pages_used"] == 0
+
+
+def test_dense_small_bf16_parity(dense_small_reduced):
+    model, run, ref, got = dense_small_reduced
+    _check_bf16("dense-small", run, ref, got)
+
+
+@pytest.fixture(scope="module")
+def dense_small_prompt256():
+    """dense-small's model on 2 prompts of 256 tokens (16 shared prompt pages
+    each), m=16, k=8, cap 48; the GPU runs twice: with the shared-prefix decode
+    attention and with the per-row kernel (which splits each row's 17-19 pages
+    into chunks that the combine kernel merges: 32 rows x 4 kv heads leave
+    most of the GPU idle otherwise)."""
+    from dataclasses import replace
+    model, run = get_config("dense-small")
+    run = replace(run, n_prompts=2, prompt_len=256, cap=48, len_median=20.0, kv_pool_gb=0.0)
+    prompts, forced = rollout_inputs(model, run)
+    say("dense-small prompt 256: oracle")
+    W = OM.init_weights(model)
+    ref = rollout(model, W, prompts, forced, run.m, run.k, run.cap, run.sample_seed, keep_logits=True)
+    B = _b()
+    say("dense-small prompt 256: GPU, shared prefix")
+    shared = run_gpu(model, run, prompts, forced, force_tokens=ref.tokens, keep_logits=True,
+                     flags=B.FLAG_SHARED_PREFIX)
+    say("dense-small prompt 256: GPU, per-row attention")
+    rows = run_gpu(model, run, prompts, forced, force_tokens=ref.tokens, keep_logits=True)
+    return run, ref, shared, rows
+
+
+def test_dense_small_shared_prefix_parity(dense_small_prompt256):
+    run, ref, shared, rows = dense_small_prompt256
+    _check_bf16("dense-small prompt 256, shared prefix", run, ref, shared)
+
+
+def test_dense_small_chunked_rows_parity(dense_small_prompt256):
+    run, ref, shared, rows = dense_small_prompt256
+    _check_bf16("dense-small prompt 256, per-row attention", run, ref, rows)

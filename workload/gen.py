@@ -64,6 +64,35 @@ def sweep_page_table(ctx: np.ndarray, page: int, rng, spare: int = 0):
     return pt, total
 
 
+def shared_prefix_page_table(group_sizes, m, prefix_pages, ctx, page, rng, spare=0):
+    """Rows of prompt groups that share their first ``prefix_pages`` pages.
+
+    Group i has ``group_sizes[i]`` members (a sorted random subset of the m
+    trajectory slots, traj = i*m + j); every member's page-table row starts
+    with the group's prefix pages, then holds private pages for the rest of
+    ``ctx`` keys.  Page ids come from a shuffled pool.  Returns (row_traj
+    [n_rows] int32, page table [n_groups*m, max_pages] int32 (-1 for unused),
+    pool size)."""
+    npg = (int(ctx) + page - 1) // page
+    priv = npg - prefix_pages
+    n_rows = int(sum(group_sizes))
+    total = len(group_sizes) * prefix_pages + n_rows * priv + spare
+    perm = rng.permutation(total).astype(np.int32)
+    pt = np.full((len(group_sizes) * m, npg), -1, dtype=np.int32)
+    rows = []
+    off = 0
+    for i, n in enumerate(group_sizes):
+        shared = perm[off:off + prefix_pages]
+        off += prefix_pages
+        for j in np.sort(rng.choice(m, size=n, replace=False)):
+            g = i * m + int(j)
+            pt[g, :prefix_pages] = shared
+            pt[g, prefix_pages:] = perm[off:off + priv]
+            off += priv
+            rows.append(g)
+    return np.asarray(rows, dtype=np.int32), pt, total
+
+
 def sweep_sampler_logits(rows=None, vocab=None, seed=None) -> np.ndarray:
     """bf16 logits ~ N(0, std) as uint16 bit patterns [rows, vocab]."""
     s = SWEEP
