@@ -57,7 +57,7 @@ struct darts_ctx {
   int64_t n_pages = 0;
   int d = 0, hq = 0, hkv = 0, hd = 0, F = 0, V = 0, nl = 0, qkv_w = 0;
   bool moe = false;
-  int E = 0, topk = 0, Fe = 0;
+  int E = 0, topk = 0, Fe = 0, Epad = 0;   // Epad: router rows padded to a multiple of 128
   int32_t* m_topk_id = nullptr;
   float* m_topk_w = nullptr;
   int32_t* m_pos_of = nullptr;
@@ -65,6 +65,7 @@ struct darts_ctx {
   void* m_a_perm = nullptr;
   void* m_h_perm = nullptr;
   float* m_y_perm = nullptr;
+  float* m_logits = nullptr;      // router logits [rows][Epad]
   // device memory
   std::vector<void*> allocs;
   void* embed = nullptr;
@@ -214,6 +215,9 @@ static int init_weights(darts_ctx* c) {
     if (c->moe) {
       const int E = c->E, Fe = c->Fe;
       HIPCHK(c, launch_init_weights(w.wrouter, b, E, d, d, T_ROUTER, l, seed, rowmap_plain(E, 0), c->st));
+      if (c->Epad > E)   // padding rows of the router: zero logits, never selected
+        HIPCHK(c, hipMemsetAsync((char*)w.wrouter + (size_t)E * d * c->esz, 0,
+                                 (size_t)(c->Epad - E) * d * c->esz, c->st));
       RowMap eg{Fe, 2 * (int64_t)Fe, 16, 32, 0}, eu{Fe, 2 * (int64_t)Fe, 16, 32, 16};
       HIPCHK(c, launch_init_weights(w.wegu, b, (int64_t)E * Fe, d, d, T_EGATE, l, seed, eg, c->st));
       HIPCHK(c, launch_init_weights(w.wegu, b, (int64_t)E * Fe, d, d, T_EUP, l, seed, eu, c->st));
@@ -243,6 +247,8 @@ static size_t gemm_ws_need(const darts_ctx* c) {
     if (!c->moe) {
       need = std::max(need, gemm_workspace_bytes(M, 2 * c->F, c->d));
       need = std::max(need, gemm_workspace_bytes(M, c->d, c->F));
+    } else {
+      need = std::max(need, gemm_workspace_bytes(M, c->Epad, c->d));   // router
     }
     need = std::max(need, gemm_workspace_bytes(M, c->V, c->d));
   }
@@ -314,6 +320,7 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
   c->d = mc.d_model; c->hq = mc.n_q_heads; c->hkv = mc.n_kv_heads; c->hd = mc.head_dim;
   c->F = moe ? 0 : mc.ffn_dim; c->V = mc.vocab; c->nl = mc.n_layers; c->qkv_w = qkv_w;
   c->moe = moe; c->E = mc.n_experts; c->topk = mc.top_k; c->Fe = mc.expert_ffn;
+  c->Epad = (c->E + 127) / 128 * 128;
 
   const int64_t page_bytes_all = (int64_t)c->nl * c->hkv * kPage * c->hd * 2 * c->esz;
   const int64_t worst = (int64_t)c->P * c->pp + (int64_t)c->n_traj * ((c->cap + kPage - 1) / kPage);
@@ -344,7 +351,7 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
     A(&w.wqkv, (size_t)qkv_w * c->d * c->esz);
     A(&w.wo, (size_t)c->d * c->hq * c->hd * c->esz);
     if (moe) {
-      A(&w.wrouter, (size_t)c->E * c->d * c->esz);
+      A(&w.wrouter, (size_t)c->Epad * c->d * c->esz);
       A(&w.wegu, (size_t)c->E * 2 * c->Fe * c->d * c->esz);
       A(&w.wedown, (size_t)c->E * c->d * c->Fe * c->esz);
     } else {
@@ -388,6 +395,7 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
     A(&c->m_topk_w, pairs * 4);
     A(&c->m_pos_of, pairs * 4);
     A(&c->m_cnt, (size_t)3 * c->E * 4);
+    A(&c->m_logits, (size_t)rows_max * c->Epad * 4);
     A(&c->m_a_perm, pairs * c->d * 2);
     A(&c->m_h_perm, pairs * c->Fe * 2);
     A(&c->m_y_perm, pairs * c->d * 4);
@@ -561,6 +569,8 @@ static int run_layers(darts_ctx* c, int n, const int32_t* row_pt, int pos_mod, i
       MoeArgs m;
       m.xn = (const bf16_t*)c->xn; m.x = c->x; m.n_rows = n; m.d = d; m.E = c->E; m.k = c->topk;
       m.Fe = c->Fe; m.w_router = (const bf16_t*)w.wrouter; m.w_gu = (const bf16_t*)w.wegu;
+      m.E_pad = c->Epad; m.logits = c->m_logits; m.gemm_ws = c->gemm_ws;
+      m.gemm_ws_bytes = c->gemm_ws_bytes;
       m.w_down = (const bf16_t*)w.wedown; m.topk_id = c->m_topk_id; m.topk_w = c->m_topk_w;
       m.pos_of = c->m_pos_of; m.counts = c->m_cnt; m.offsets = c->m_cnt + c->E;
       m.cursors = c->m_cnt + 2 * c->E; m.a_perm = (bf16_t*)c->m_a_perm;

@@ -94,12 +94,13 @@ __device__ __forceinline__ int dma_swz(int r) {
   else return (r >> 1) & 3;
 }
 
+// One BM x BN output tile (rows m0.., cols n0.., K range [z*k_chunk, +k_chunk)).
 template <int BM, int BN, int KB, int WGM, int WGN, int STAGES, int EPI, bool SPLIT>
-__global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_kernel(const bf16_t* __restrict__ A, int lda,
-                                                       const bf16_t* __restrict__ W, int ldw,
-                                                       void* __restrict__ C, int ldc, int M,
-                                                       int N, int K, int k_chunk, int mt, int nt,
-                                                       float* __restrict__ ws) {
+__device__ __forceinline__ void dma_gemm_tile(const bf16_t* __restrict__ A, int lda,
+                                              const bf16_t* __restrict__ W, int ldw,
+                                              void* __restrict__ C, int ldc, int M, int N,
+                                              int k_chunk, int mi, int ni, int z,
+                                              float* __restrict__ ws) {
   static_assert(KB == 32 || KB == 64, "K tile");
   constexpr int NW = WGM * WGN;                    // wavefronts per block
   constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 16, TN = WN / 16;
@@ -111,11 +112,6 @@ __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_kernel(const bf16_t* 
   extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
-  const int nb = gridDim.x;
-  int b = blockIdx.x;
-  const int full = (nb / 8) * 8;
-  if (b < full) b = (b % 8) * (full / 8) + b / 8;
-  const int mi = b % mt, ni = (b / mt) % nt, z = b / (mt * nt);
   const int m0 = mi * BM, n0 = ni * BN;
   const int kbeg = z * k_chunk;
   const int nk = k_chunk / KB;
@@ -216,6 +212,48 @@ __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_kernel(const bf16_t* 
 #pragma unroll
       for (int j = 0; j < TN; ++j) store_tile<EPI>(C, ldc, M, rb + 16 * i, cb + 16 * j, lane, acc[i][j]);
   }
+}
+
+// Blocks are renumbered so that the blocks one XCD runs (dispatch is round
+// robin over the 8 XCDs) are consecutive tiles and share operands in its L2.
+__device__ __forceinline__ int xcd_block() {
+  const int nb = gridDim.x;
+  int b = blockIdx.x;
+  const int full = (nb / 8) * 8;
+  if (b < full) b = (b % 8) * (full / 8) + b / 8;
+  return b;
+}
+
+template <int BM, int BN, int KB, int WGM, int WGN, int STAGES, int EPI, bool SPLIT>
+__global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_kernel(const bf16_t* __restrict__ A, int lda,
+                                                       const bf16_t* __restrict__ W, int ldw,
+                                                       void* __restrict__ C, int ldc, int M,
+                                                       int N, int K, int k_chunk, int mt, int nt,
+                                                       float* __restrict__ ws) {
+  const int b = xcd_block();
+  const int mi = b % mt, ni = (b / mt) % nt, z = b / (mt * nt);
+  dma_gemm_tile<BM, BN, KB, WGM, WGN, STAGES, EPI, SPLIT>(A, lda, W, ldw, C, ldc, M, N, k_chunk, mi,
+                                                          ni, z, ws);
+}
+
+// Grouped GEMM (mixture-of-experts): group e owns rows [off[e], off[e] +
+// cnt[e]) of A and C and the weight matrix W + e * w_stride ([N][K]).  Block
+// -> (group, n tile, m tile), m tile fastest; blocks past a group's row count
+// return at once (the grid covers mt_max row tiles per group).
+template <int BM, int BN, int KB, int WGM, int WGN, int STAGES, int EPI>
+__global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_grouped_kernel(
+    const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ W, int64_t w_stride, int ldw,
+    void* __restrict__ C, int ldc, int N, int K, const int32_t* __restrict__ g_off,
+    const int32_t* __restrict__ g_cnt, int mt_max, int nt) {
+  const int b = xcd_block();
+  const int mi = b % mt_max, ni = (b / mt_max) % nt, e = b / (mt_max * nt);
+  const int cnt = g_cnt[e];
+  if (mi * BM >= cnt) return;
+  const int64_t off = g_off[e];
+  constexpr int esz = (EPI == EPI_F32 || EPI == EPI_ADD_F32) ? 4 : 2;
+  void* Ce = (char*)C + off * ldc * esz;
+  dma_gemm_tile<BM, BN, KB, WGM, WGN, STAGES, EPI, false>(A + off * lda, lda, W + (int64_t)e * w_stride,
+                                                          ldw, Ce, ldc, cnt, N, K, mi, ni, 0, nullptr);
 }
 
 // ----------------------------------------------------------------- skinny
@@ -497,6 +535,41 @@ static void dma_go(const Plan& p, const void* A, int lda, const void* W, int ldw
     }
     hipLaunchKernelGGL(kern, grid, blk, lds, st, (const bf16_t*)A, lda, (const bf16_t*)W, ldw, C,
                        ldc, M, N, K, K / p.S, p.mt, p.nt, (float*)ws);
+  }
+}
+
+template <int EPI>
+static hipError_t grouped_launch(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
+                                 void* C, int ldc, int N, int K, const int32_t* g_off,
+                                 const int32_t* g_cnt, int n_groups, int max_rows, hipStream_t st) {
+  // 128x128 tiles, 4-stage ring: expert weights are streamed once per row tile
+  constexpr int BM_ = 128, BN_ = 128, KB = 64, ST = 4;
+  const int mt_max = (max_rows + BM_ - 1) / BM_, nt = N / BN_;
+  const int64_t blocks = (int64_t)n_groups * nt * mt_max;
+  if (blocks <= 0) return hipSuccess;
+  if (blocks > (1ll << 31) - 1) return hipErrorInvalidValue;
+  const size_t lds = (size_t)ST * (BM_ + BN_) * KB * sizeof(bf16_t);
+  auto kern = gemm_dma_grouped_kernel<BM_, BN_, KB, 2, 2, ST, EPI>;
+  static bool attr_done = false;
+  if (!attr_done) {
+    (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    attr_done = true;
+  }
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(256), lds, st, (const bf16_t*)A, lda,
+                     (const bf16_t*)W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mt_max, nt);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_grouped(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
+                               void* C, int ldc, int N, int K, int epi, const int32_t* g_off,
+                               const int32_t* g_cnt, int n_groups, int max_rows, hipStream_t st) {
+  if (N % 128 != 0 || K % 64 != 0 || K < 64 || n_groups < 0 || max_rows < 0) return hipErrorInvalidValue;
+  switch (epi) {
+    case EPI_F32: return grouped_launch<EPI_F32>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, n_groups, max_rows, st);
+    case EPI_BF16: return grouped_launch<EPI_BF16>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, n_groups, max_rows, st);
+    case EPI_ADD_F32: return grouped_launch<EPI_ADD_F32>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, n_groups, max_rows, st);
+    case EPI_SWIGLU: return grouped_launch<EPI_SWIGLU>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, n_groups, max_rows, st);
+    default: return hipErrorInvalidValue;
   }
 }
 

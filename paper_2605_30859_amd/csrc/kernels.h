@@ -46,6 +46,13 @@ hipError_t launch_rope_append2(const float* qkv, int n_rows, int hq, int hkv, in
 hipError_t launch_gather_rows(const float* src, const int32_t* rows, int n, int d, float* dst,
                               hipStream_t st);
 
+// Grouped bf16 GEMM (mixture of experts): for each group e < n_groups, rows
+// [g_off[e], g_off[e] + g_cnt[e]) of A and C against W + e * w_stride
+// ([N][K], row stride ldw); g_cnt[e] <= max_rows.  N % 128 == 0, K % 64 == 0.
+hipError_t launch_gemm_grouped(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
+                               void* C, int ldc, int N, int K, int epi, const int32_t* g_off,
+                               const int32_t* g_cnt, int n_groups, int max_rows, hipStream_t st);
+
 // ---- attention (k_attn.hip)
 size_t attn_workspace_bytes(int n_rows, int hq, int hkv, int hd, int max_ctx);
 // ctx(r) = ctx_len ? ctx_len[r] : (ctx_mod ? r % ctx_mod : 0) + ctx_base
@@ -117,7 +124,10 @@ hipError_t launch_prefill_pages(int n_prompts, int m, int prompt_pages, int32_t*
 // ---- MoE FFN (k_moe.hip): x += sum over the top-k experts of w_e * expert_e(xn)
 struct MoeArgs {
   const bf16_t* xn; float* x; int n_rows, d, E, k, Fe;
-  const bf16_t* w_router;   // [E][d]
+  int E_pad;                // router rows padded to a multiple of 128 (zero rows)
+  const bf16_t* w_router;   // [E_pad][d]
+  float* logits;            // [n_rows][E_pad] router logits
+  void* gemm_ws; size_t gemm_ws_bytes;   // workspace of the router GEMM
   const bf16_t* w_gu;       // [E][2Fe][d], gate/up rows interleaved in groups of 16
   const bf16_t* w_down;     // [E][d][Fe]
   int32_t* topk_id; float* topk_w; int32_t* pos_of;            // [n_rows*k]
