@@ -66,6 +66,7 @@ struct darts_ctx {
   void* m_h_perm = nullptr;
   float* m_y_perm = nullptr;
   float* m_logits = nullptr;      // router logits [rows][Epad]
+  int32_t* m_mtiles = nullptr;    // n_mtiles | non-empty expert row tiles
   // device memory
   std::vector<void*> allocs;
   void* embed = nullptr;
@@ -396,6 +397,7 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
     A(&c->m_pos_of, pairs * 4);
     A(&c->m_cnt, (size_t)3 * c->E * 4);
     A(&c->m_logits, (size_t)rows_max * c->Epad * 4);
+    A(&c->m_mtiles, (pairs / kGroupedTileRows + c->E + 1) * 4);
     A(&c->m_a_perm, pairs * c->d * 2);
     A(&c->m_h_perm, pairs * c->Fe * 2);
     A(&c->m_y_perm, pairs * c->d * 4);
@@ -570,6 +572,7 @@ static int run_layers(darts_ctx* c, int n, const int32_t* row_pt, int pos_mod, i
       m.xn = (const bf16_t*)c->xn; m.x = c->x; m.n_rows = n; m.d = d; m.E = c->E; m.k = c->topk;
       m.Fe = c->Fe; m.w_router = (const bf16_t*)w.wrouter; m.w_gu = (const bf16_t*)w.wegu;
       m.E_pad = c->Epad; m.logits = c->m_logits; m.gemm_ws = c->gemm_ws;
+      m.n_mtiles = c->m_mtiles; m.mtiles = c->m_mtiles + 1;
       m.gemm_ws_bytes = c->gemm_ws_bytes;
       m.w_down = (const bf16_t*)w.wedown; m.topk_id = c->m_topk_id; m.topk_w = c->m_topk_w;
       m.pos_of = c->m_pos_of; m.counts = c->m_cnt; m.offsets = c->m_cnt + c->E;

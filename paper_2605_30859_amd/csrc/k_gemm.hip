@@ -237,23 +237,32 @@ __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_kernel(const bf16_t* 
 }
 
 // Grouped GEMM (mixture-of-experts): group e owns rows [off[e], off[e] +
-// cnt[e]) of A and C and the weight matrix W + e * w_stride ([N][K]).  Block
-// -> (group, n tile, m tile), m tile fastest; blocks past a group's row count
-// return at once (the grid covers mt_max row tiles per group).
+// cnt[e]) of A and C and the weight matrix W + e * w_stride ([N][K]).  The
+// non-empty row tiles are listed on the device (mtiles[i] = e << 16 | m tile,
+// *n_mtiles of them); persistent blocks take items (row tile, n tile), n tile
+// fastest, in a grid-stride loop.
 template <int BM, int BN, int KB, int WGM, int WGN, int STAGES, int EPI>
 __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_grouped_kernel(
     const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ W, int64_t w_stride, int ldw,
     void* __restrict__ C, int ldc, int N, int K, const int32_t* __restrict__ g_off,
-    const int32_t* __restrict__ g_cnt, int mt_max, int nt) {
-  const int b = xcd_block();
-  const int mi = b % mt_max, ni = (b / mt_max) % nt, e = b / (mt_max * nt);
-  const int cnt = g_cnt[e];
-  if (mi * BM >= cnt) return;
-  const int64_t off = g_off[e];
+    const int32_t* __restrict__ g_cnt, const int32_t* __restrict__ mtiles,
+    const int32_t* __restrict__ n_mtiles, int nt) {
+  const int total = n_mtiles[0] * nt;
   constexpr int esz = (EPI == EPI_F32 || EPI == EPI_ADD_F32) ? 4 : 2;
-  void* Ce = (char*)C + off * ldc * esz;
-  dma_gemm_tile<BM, BN, KB, WGM, WGN, STAGES, EPI, false>(A + off * lda, lda, W + (int64_t)e * w_stride,
-                                                          ldw, Ce, ldc, cnt, N, K, mi, ni, 0, nullptr);
+  for (int it = blockIdx.x; it < total; it += gridDim.x) {
+    const int mt = mtiles[it / nt], ni = it % nt;
+    const int e = mt >> 16, mi = mt & 0xffff;
+    const int cnt = g_cnt[e];
+    const int64_t off = g_off[e];
+    // other waves may still read the previous item's last LDS stage: a raw
+    // barrier (their LDS reads have retired once their MFMAs issued); no
+    // memory fence, which would also wait for the previous item's stores
+    __builtin_amdgcn_s_barrier();
+    void* Ce = (char*)C + off * ldc * esz;
+    dma_gemm_tile<BM, BN, KB, WGM, WGN, STAGES, EPI, false>(A + off * lda, lda,
+                                                            W + (int64_t)e * w_stride, ldw, Ce, ldc,
+                                                            cnt, N, K, mi, ni, 0, nullptr);
+  }
 }
 
 // ----------------------------------------------------------------- skinny
@@ -541,13 +550,13 @@ static void dma_go(const Plan& p, const void* A, int lda, const void* W, int ldw
 template <int EPI>
 static hipError_t grouped_launch(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
                                  void* C, int ldc, int N, int K, const int32_t* g_off,
-                                 const int32_t* g_cnt, int n_groups, int max_rows, hipStream_t st) {
-  // 128x128 tiles, 4-stage ring: expert weights are streamed once per row tile
+                                 const int32_t* g_cnt, const int32_t* mtiles,
+                                 const int32_t* n_mtiles, hipStream_t st) {
+  // 128x128 tiles, 4-stage ring (one block per CU): expert weights are
+  // streamed once per row tile
   constexpr int BM_ = 128, BN_ = 128, KB = 64, ST = 4;
-  const int mt_max = (max_rows + BM_ - 1) / BM_, nt = N / BN_;
-  const int64_t blocks = (int64_t)n_groups * nt * mt_max;
-  if (blocks <= 0) return hipSuccess;
-  if (blocks > (1ll << 31) - 1) return hipErrorInvalidValue;
+  static_assert(BM_ == kGroupedTileRows, "row tile of the m-tile list");
+  const int nt = N / BN_;
   const size_t lds = (size_t)ST * (BM_ + BN_) * KB * sizeof(bf16_t);
   auto kern = gemm_dma_grouped_kernel<BM_, BN_, KB, 2, 2, ST, EPI>;
   static bool attr_done = false;
@@ -555,20 +564,21 @@ static hipError_t grouped_launch(const void* A, int lda, const void* W, int64_t 
     (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     attr_done = true;
   }
-  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(256), lds, st, (const bf16_t*)A, lda,
-                     (const bf16_t*)W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mt_max, nt);
+  hipLaunchKernelGGL(kern, dim3(kCus), dim3(256), lds, st, (const bf16_t*)A, lda, (const bf16_t*)W,
+                     w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, nt);
   return hipGetLastError();
 }
 
 hipError_t launch_gemm_grouped(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
                                void* C, int ldc, int N, int K, int epi, const int32_t* g_off,
-                               const int32_t* g_cnt, int n_groups, int max_rows, hipStream_t st) {
-  if (N % 128 != 0 || K % 64 != 0 || K < 64 || n_groups < 0 || max_rows < 0) return hipErrorInvalidValue;
+                               const int32_t* g_cnt, const int32_t* mtiles, const int32_t* n_mtiles,
+                               hipStream_t st) {
+  if (N % 128 != 0 || K % 64 != 0 || K < 64) return hipErrorInvalidValue;
   switch (epi) {
-    case EPI_F32: return grouped_launch<EPI_F32>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, n_groups, max_rows, st);
-    case EPI_BF16: return grouped_launch<EPI_BF16>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, n_groups, max_rows, st);
-    case EPI_ADD_F32: return grouped_launch<EPI_ADD_F32>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, n_groups, max_rows, st);
-    case EPI_SWIGLU: return grouped_launch<EPI_SWIGLU>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, n_groups, max_rows, st);
+    case EPI_F32: return grouped_launch<EPI_F32>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, st);
+    case EPI_BF16: return grouped_launch<EPI_BF16>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, st);
+    case EPI_ADD_F32: return grouped_launch<EPI_ADD_F32>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, st);
+    case EPI_SWIGLU: return grouped_launch<EPI_SWIGLU>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, st);
     default: return hipErrorInvalidValue;
   }
 }

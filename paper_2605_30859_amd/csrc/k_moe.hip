@@ -83,13 +83,32 @@ __global__ void __launch_bounds__(256) moe_topk_kernel(const float* __restrict__
   }
 }
 
+__device__ __forceinline__ int block_excl_scan1024(int v, int32_t* sh, int* total) {
+  const int tid = threadIdx.x;
+  sh[tid] = v;
+  __syncthreads();
+  for (int o = 1; o < 1024; o <<= 1) {
+    const int x = tid >= o ? sh[tid - o] : 0;
+    __syncthreads();
+    sh[tid] += x;
+    __syncthreads();
+  }
+  const int incl = sh[tid];
+  *total = sh[1023];
+  __syncthreads();
+  return incl - v;
+}
+
 // Single block: per-expert counts of the n_pairs routed (row, slot) pairs
-// (LDS histogram), their exclusive scan into offsets, cursors reset to 0.
+// (LDS histogram), their exclusive scan into offsets, cursors reset to 0, and
+// the list of non-empty expert row tiles (e << 16 | tile) for the grouped GEMMs.
 __global__ void __launch_bounds__(1024) moe_offsets_kernel(const int32_t* __restrict__ topk_id,
                                                            int n_pairs, int E,
                                                            int32_t* __restrict__ counts,
                                                            int32_t* __restrict__ offsets,
-                                                           int32_t* __restrict__ cursors) {
+                                                           int32_t* __restrict__ cursors,
+                                                           int32_t* __restrict__ mtiles,
+                                                           int32_t* __restrict__ n_mtiles) {
   __shared__ int32_t hist[1024];
   __shared__ int32_t sh[1024];
   const int tid = threadIdx.x;
@@ -101,19 +120,18 @@ __global__ void __launch_bounds__(1024) moe_offsets_kernel(const int32_t* __rest
   }
   __syncthreads();
   const int v = tid < E ? hist[tid] : 0;
-  sh[tid] = v;
-  __syncthreads();
-  for (int o = 1; o < 1024; o <<= 1) {
-    const int x = tid >= o ? sh[tid - o] : 0;
-    __syncthreads();
-    sh[tid] += x;
-    __syncthreads();
-  }
+  int total;
+  const int ex = block_excl_scan1024(v, sh, &total);
+  const int nt = (v + kGroupedTileRows - 1) / kGroupedTileRows;
+  int ntiles;
+  const int tex = block_excl_scan1024(nt, sh, &ntiles);
   if (tid < E) {
     counts[tid] = v;
-    offsets[tid] = sh[tid] - v;
+    offsets[tid] = ex;
     cursors[tid] = 0;
+    for (int j = 0; j < nt; ++j) mtiles[tex + j] = (tid << 16) | j;
   }
+  if (tid == 0) *n_mtiles = ntiles;
 }
 
 // One block per row: place its k pairs and copy the input row into each.
@@ -171,24 +189,25 @@ __global__ void __launch_bounds__(256) moe_combine_kernel(const float* __restric
 
 hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st) {
   if (a.n_rows <= 0) return hipSuccess;
-  if (a.E > 64 * kMoeMaxPerLane || a.E > 1024 || a.k > 64 || a.k > a.E || a.d % 4) return hipErrorInvalidValue;
+  if (a.E > 64 * kMoeMaxPerLane || a.E > 1024 || a.k > 64 || a.k > a.E || a.d % 4 ||
+      a.n_rows > 65536 * kGroupedTileRows)
+    return hipErrorInvalidValue;
   hipError_t e = launch_gemm(true, a.xn, a.d, a.w_router, a.d, a.logits, a.E_pad, a.n_rows, a.E_pad, a.d,
                              EPI_F32, a.gemm_ws, a.gemm_ws_bytes, st);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(moe_topk_kernel, dim3((a.n_rows + 3) / 4), dim3(256), 0, st, a.logits, a.E_pad,
                      a.n_rows, a.E, a.k, a.topk_id, a.topk_w);
   hipLaunchKernelGGL(moe_offsets_kernel, dim3(1), dim3(1024), 0, st, a.topk_id, a.n_rows * a.k, a.E,
-                     a.counts, a.offsets, a.cursors);
+                     a.counts, a.offsets, a.cursors, a.mtiles, a.n_mtiles);
   hipLaunchKernelGGL(moe_scatter_kernel, dim3(a.n_rows), dim3(256), 0, st, a.xn, a.d, a.k, a.topk_id,
                      a.offsets, a.cursors, a.pos_of, a.a_perm);
   const int Fe = a.Fe, d = a.d;
-  // gate/up: N = 2*Fe, K = d (SwiGLU into h_perm); down: N = d, K = Fe.
-  // An expert receives each row at most once: at most n_rows rows.
+  // gate/up: N = 2*Fe, K = d (SwiGLU into h_perm); down: N = d, K = Fe
   e = launch_gemm_grouped(a.a_perm, d, a.w_gu, (int64_t)2 * Fe * d, d, a.h_perm, Fe, 2 * Fe, d,
-                          EPI_SWIGLU, a.offsets, a.counts, a.E, a.n_rows, st);
+                          EPI_SWIGLU, a.offsets, a.counts, a.mtiles, a.n_mtiles, st);
   if (e != hipSuccess) return e;
   e = launch_gemm_grouped(a.h_perm, Fe, a.w_down, (int64_t)d * Fe, Fe, a.y_perm, d, d, Fe, EPI_F32,
-                          a.offsets, a.counts, a.E, a.n_rows, st);
+                          a.offsets, a.counts, a.mtiles, a.n_mtiles, st);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(moe_combine_kernel, dim3(a.n_rows), dim3(256), 0, st, a.y_perm, d, a.k,
                      a.pos_of, a.topk_w, a.x);

@@ -46,12 +46,16 @@ hipError_t launch_rope_append2(const float* qkv, int n_rows, int hq, int hkv, in
 hipError_t launch_gather_rows(const float* src, const int32_t* rows, int n, int d, float* dst,
                               hipStream_t st);
 
-// Grouped bf16 GEMM (mixture of experts): for each group e < n_groups, rows
-// [g_off[e], g_off[e] + g_cnt[e]) of A and C against W + e * w_stride
-// ([N][K], row stride ldw); g_cnt[e] <= max_rows.  N % 128 == 0, K % 64 == 0.
+// Grouped bf16 GEMM (mixture of experts): group e owns rows [g_off[e],
+// g_off[e] + g_cnt[e]) of A and C and the weights W + e * w_stride ([N][K],
+// row stride ldw).  mtiles lists the non-empty row tiles of
+// kGroupedTileRows rows, e << 16 | tile, *n_mtiles of them (device values).
+// N % 128 == 0, K % 64 == 0.
+constexpr int kGroupedTileRows = 128;
 hipError_t launch_gemm_grouped(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
                                void* C, int ldc, int N, int K, int epi, const int32_t* g_off,
-                               const int32_t* g_cnt, int n_groups, int max_rows, hipStream_t st);
+                               const int32_t* g_cnt, const int32_t* mtiles, const int32_t* n_mtiles,
+                               hipStream_t st);
 
 // ---- attention (k_attn.hip)
 size_t attn_workspace_bytes(int n_rows, int hq, int hkv, int hd, int max_ctx);
@@ -132,6 +136,8 @@ struct MoeArgs {
   const bf16_t* w_down;     // [E][d][Fe]
   int32_t* topk_id; float* topk_w; int32_t* pos_of;            // [n_rows*k]
   int32_t* counts; int32_t* offsets; int32_t* cursors;         // [E]
+  int32_t* mtiles;          // [n_rows*k / kGroupedTileRows + E] non-empty expert row tiles
+  int32_t* n_mtiles;        // [1]
   bf16_t* a_perm; bf16_t* h_perm; float* y_perm;               // [n_rows*k][d | Fe | d]
 };
 hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st);
