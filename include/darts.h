@@ -27,7 +27,9 @@
  *   - After DARTS_EHIP the context is poisoned: every call except
  *     darts_destroy returns DARTS_EHIP again; darts_last_error has the text.
  *
- * Trajectory ids: trajectory j of prompt i has global id g = i*m + j.
+ * Trajectory ids: trajectory j of prompt i has global id g = i*m + j, where
+ * m is the context's largest group size; with a redundancy plan (Alg. 1,
+ * darts_set_plan) prompt i has candidates j < M'_i <= m only.
  * Random numbers: Philox4x32-10 (Salmon et al., SC'11), key = 64-bit seed,
  * so every trajectory's tokens depend only on (seed, g, step), never on batch
  * composition, row order or physical page ids.
@@ -162,6 +164,15 @@ typedef struct darts_ctx darts_ctx;
 int darts_init(const darts_model_cfg* model, int32_t m, int32_t k,
                const darts_run_cfg* run, darts_ctx** out);
 
+/* Set the redundancy plan of the next batch (paper Sec. 4.2.2, Alg. 1 output
+ * M' = {M'_i}): prompt i gets h_plan[i] candidates, k <= h_plan[i] <= m, and
+ * its group is selected shortest-only with early stop when h_plan[i] >=
+ * m_up, dual-end otherwise (Alg. 2).  Valid only before darts_prefill
+ * (after darts_init or darts_reset, which both restore the uniform plan
+ * h_plan[i] = m).  Errors: DARTS_EINVAL for a size out of [k, m],
+ * DARTS_ESTATE after the prefill.  Synchronises the stream.                */
+int darts_set_plan(darts_ctx* ctx, const int32_t* h_plan);
+
 /* Prefill every prompt and sample generated token 0 of every trajectory
  * (paper Alg. 2: rollout of the candidate pool T_i).
  *   d_prompts      [n_prompts * prompt_len] int32 token ids in [0, vocab)
@@ -170,7 +181,8 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k,
  *                  d <= cap; d > cap means it is truncated at cap
  *   d_force_tokens NULL or [n_prompts * m] int32 teacher-forced token 0 per
  *                  trajectory (-1: no force)
- * Writes `out` (n_rows = n_prompts*m).  DARTS_ESTATE if called twice.      */
+ * Writes `out` (n_rows = the number of candidates of the plan, n_prompts*m
+ * for the uniform one).  DARTS_ESTATE if called twice.                      */
 int darts_prefill(darts_ctx* ctx, const int32_t* d_prompts, const int32_t* d_forced_len,
                   const int32_t* d_force_tokens, darts_step_out* out);
 
@@ -210,7 +222,8 @@ int darts_reset(darts_ctx* ctx);
 
 /* Final per-trajectory scores (device buffers of n_prompts*m, each may be
  * NULL): generated length, float32 sum of log-probs in step order, mean
- * = sum / length, status (0 live, 1 eos, 2 truncated, 3 aborted).          */
+ * = sum / length, status (0 live, 1 eos, 2 truncated, 3 aborted, 4 not a
+ * candidate of the plan: length 0).                                        */
 int darts_get_traj_scores(darts_ctx* ctx, int32_t* d_len, float* d_sum_lp, float* d_mean_lp,
                           uint8_t* d_status);
 
@@ -221,6 +234,41 @@ int darts_debug_logits(darts_ctx* ctx, float* d_dst, int32_t* h_n_rows);
 int darts_destroy(darts_ctx* ctx);
 const char* darts_strerror(int status);
 const char* darts_last_error(const darts_ctx* ctx);
+
+/* ------------------------------------------------------- batch planning   */
+/* Host-only calls (no device work, no context): they decide the redundancy
+ * plan of the next batch from the previous rollouts.  All arithmetic is
+ * float64; results are bitwise reproducible.                               */
+
+/* Population standard deviation of each prompt's candidate lengths, the
+ * per-prompt long-tail signal of Sec. 4.2.2: h_std[i] over h_len[i*m + j],
+ * j < h_plan[i] (h_plan NULL: j < m).  h_len as from darts_get_traj_scores
+ * (aborted candidates count with the length they reached).                 */
+int darts_prompt_length_std(const int32_t* h_len, const int32_t* h_plan, int32_t n_prompts,
+                            int32_t m, double* h_std);
+
+/* Exponential moving average of a per-prompt statistic (the smoothed
+ * historical variance of Sec. 4.2.2 / App. C): for every i with h_obs[i]
+ * not NaN, h_est[i] = h_obs[i] if !h_seen[i] else alpha*h_obs[i] +
+ * (1-alpha)*h_est[i], and h_seen[i] = 1.  0 < alpha <= 1.                   */
+int darts_ema_update(double* h_est, uint8_t* h_seen, const double* h_obs, int32_t n, double alpha);
+
+/* Adaptive total budget (App. B): the utility rho*ln(M) - lambda*(k_cost*M
+ * + c) peaks at M* = rho / (lambda*k_cost); *h_m_total = clip(floor(M*),
+ * M*n_prompts, 2*M*n_prompts).  rho = sigma_L / mean_L of recent response
+ * lengths, k_cost = rollout seconds per extra candidate (cost model of
+ * Sec. 4.2.1).  lambda <= 0 or k_cost <= 0 gives the upper bound.           */
+int darts_redundancy_budget(double rho, double lambda, double k_cost, int32_t n_prompts, int32_t M,
+                            int64_t* h_m_total);
+
+/* Variance-based allocation (Alg. 1): w_i = min-max normalised h_sigma[i]
+ * (all equal: 1; prompts with h_seen[i] == 0 first take the mean of the
+ * seen ones; h_seen NULL: all seen); every prompt starts at m_low and the
+ * remaining m_total - n*m_low candidates go one at a time to the prompt
+ * with the largest w_i*(1/M'_i - 1/(M'_i+1)) still below m_up (ties: lowest
+ * index).  A surplus beyond n*m_up stays unallocated.  Writes h_plan[n].    */
+int darts_allocate_redundancy(const double* h_sigma, const uint8_t* h_seen, int32_t n_prompts,
+                              int32_t m_low, int32_t m_up, int64_t m_total, int32_t* h_plan);
 
 /* ----------------------------------------------------- stateless kernels  */
 /* These run one kernel of the path on caller-provided device buffers, for

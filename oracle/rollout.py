@@ -59,12 +59,16 @@ class RolloutResult:
 
 
 def rollout(cfg, W, prompts, forced, m, k, cap, seed, temperature=1.0, L=1, m_up=None,
-            page=16, early_stop=True, prompt_ids=None, keep_logits=False):
+            page=16, early_stop=True, prompt_ids=None, keep_logits=False, alloc=None):
     """Run the rollout for prompts ``prompt_ids`` (default all) of the batch.
 
     prompts: [P, Lp] int; forced: [P*m] raw forced lengths (>= 1).
     Trajectory ids stay global (g = i*m + j) so a subset reproduces the same
     per-trajectory results as the full batch.
+    alloc: None (every prompt has m candidates) or the per-prompt redundancy
+    plan M'_i <= m of Alg. 1; prompt i then has candidates g = i*m + j,
+    j < M'_i, and its group runs shortest-only when M'_i >= m_up, dual-end
+    otherwise (Alg. 2).
     """
     prompts = np.asarray(prompts)
     P, Lp = prompts.shape
@@ -73,7 +77,8 @@ def rollout(cfg, W, prompts, forced, m, k, cap, seed, temperature=1.0, L=1, m_up
     eos = cfg.vocab - 1
     prompt_pages = -(-Lp // page)
 
-    trajs = [i * m + j for i in ids for j in range(m)]
+    size = [m] * P if alloc is None else [int(a) for a in alloc]
+    trajs = [i * m + j for i in ids for j in range(size[i])]
     st = {g: LIVE for g in trajs}
     gen = {g: 0 for g in trajs}
     toks = {g: [] for g in trajs}
@@ -85,7 +90,7 @@ def rollout(cfg, W, prompts, forced, m, k, cap, seed, temperature=1.0, L=1, m_up
     rmar = {g: [] for g in trajs}
     slp = {g: np.float32(0.0) for g in trajs}
     freed = {g: False for g in trajs}
-    refcnt = {i: m for i in ids}
+    refcnt = {i: size[i] for i in ids}
     kept, done_step = {}, {}
 
     # prefill
@@ -129,7 +134,7 @@ def rollout(cfg, W, prompts, forced, m, k, cap, seed, temperature=1.0, L=1, m_up
             if i in kept:
                 continue
             mem = []
-            for j in range(m):
+            for j in range(size[i]):
                 g = i * m + j
                 n = gen[g]
                 mem.append(dict(g=g, status=st[g], length=n, trunc=(st[g] == TRUNC),
@@ -141,7 +146,7 @@ def rollout(cfg, W, prompts, forced, m, k, cap, seed, temperature=1.0, L=1, m_up
                 for g in ab:
                     st[g] = ABORTED
         for i in ids:
-            for j in range(m):
+            for j in range(size[i]):
                 g = i * m + j
                 if st[g] != LIVE and not freed[g]:
                     freed[g] = True
@@ -202,16 +207,20 @@ def rollout(cfg, W, prompts, forced, m, k, cap, seed, temperature=1.0, L=1, m_up
 
 
 def schedule_only(forced, P, m, k, cap, Lp, L=1, m_up=None, page=16, early_stop=True,
-                  mean_lp=None):
+                  mean_lp=None, alloc=None):
     """Selection and page accounting without a model.  Termination is exogenous,
     so lengths, completion steps and page counts follow from the forced lengths
-    alone; ``mean_lp`` (per trajectory, float32) only breaks length ties."""
+    alone; ``mean_lp`` (per trajectory, float32) only breaks length ties.
+    ``alloc`` as for rollout(): candidates j >= M'_i of prompt i do not exist
+    (status None, length 0)."""
     m_up = 2 * k if m_up is None else m_up
+    size = [m] * P if alloc is None else [int(a) for a in alloc]
     n = P * m
-    st = [LIVE] * n
-    gen = [1] * n
-    freed = [False] * n
-    refcnt = [m] * P
+    exists = [g % m < size[g // m] for g in range(n)]
+    st = [LIVE if exists[g] else None for g in range(n)]
+    gen = [1 if exists[g] else 0 for g in range(n)]
+    freed = [not exists[g] for g in range(n)]
+    refcnt = list(size)
     kept, done_step = {}, {}
     prompt_pages = -(-Lp // page)
     pages = prompt_pages * P
@@ -231,7 +240,7 @@ def schedule_only(forced, P, m, k, cap, Lp, L=1, m_up=None, page=16, early_stop=
             if i in kept:
                 continue
             mem = [dict(g=g, status=st[g], length=gen[g], trunc=st[g] == TRUNC, mean_lp=mlp[g])
-                   for g in range(i * m, i * m + m)]
+                   for g in range(i * m, i * m + size[i])]
             c, kp, ab = group_decision(mem, k, L, m_up, early_stop)
             if c:
                 kept[i] = kp
@@ -239,7 +248,7 @@ def schedule_only(forced, P, m, k, cap, Lp, L=1, m_up=None, page=16, early_stop=
                 for g in ab:
                     st[g] = ABORTED
         for g in range(n):
-            if st[g] != LIVE and not freed[g]:
+            if exists[g] and st[g] != LIVE and not freed[g]:
                 freed[g] = True
                 pages -= -(-(gen[g] - 1) // page)
                 refcnt[g // m] -= 1
@@ -247,10 +256,11 @@ def schedule_only(forced, P, m, k, cap, Lp, L=1, m_up=None, page=16, early_stop=
                     pages -= prompt_pages
 
     for g in range(n):
-        term(g)
+        if exists[g]:
+            term(g)
     sel(1)
     step = 1
-    decoded = n
+    decoded = sum(size)
     while len(kept) < P:
         step += 1
         live = [g for g in range(n) if st[g] == LIVE]

@@ -63,6 +63,12 @@ _SIGS = {
     "darts_debug_logits": (C.c_int, [_P, _P, C.POINTER(C.c_int32)]),
     "darts_destroy": (C.c_int, [_P]),
     "darts_reset": (C.c_int, [_P]),
+    "darts_set_plan": (C.c_int, [_P, _P]),
+    "darts_prompt_length_std": (C.c_int, [_P, _P, C.c_int32, C.c_int32, _P]),
+    "darts_ema_update": (C.c_int, [_P, _P, _P, C.c_int32, C.c_double]),
+    "darts_redundancy_budget": (C.c_int, [C.c_double, C.c_double, C.c_double, C.c_int32, C.c_int32,
+                                          C.POINTER(C.c_int64)]),
+    "darts_allocate_redundancy": (C.c_int, [_P, _P, C.c_int32, C.c_int32, C.c_int32, C.c_int64, _P]),
     "darts_strerror": (C.c_char_p, [C.c_int]),
     "darts_last_error": (C.c_char_p, [_P]),
     "darts_fill_uniform": (C.c_int, [_P, C.c_uint64, C.c_int32, C.c_uint64, C.c_int32, _P]),
@@ -197,6 +203,45 @@ def darts_debug_gumbel(u, g, stream=None):
     _check(load_library().darts_debug_gumbel(_ptr(u), _ptr(g), u.numel(), _stream(stream)))
 
 
+# ---------------------------------------------------------------- planning
+def _np_ptr(a):
+    return None if a is None else C.c_void_p(a.ctypes.data)
+
+
+def darts_prompt_length_std(lengths, plan, n_prompts, m):
+    """lengths: int32 [n_prompts*m] host array; plan: None or int32 [n_prompts]."""
+    import numpy as np
+    ln = np.ascontiguousarray(lengths, dtype=np.int32)
+    pl = None if plan is None else np.ascontiguousarray(plan, dtype=np.int32)
+    out = np.zeros(n_prompts, dtype=np.float64)
+    _check(load_library().darts_prompt_length_std(_np_ptr(ln), _np_ptr(pl), n_prompts, m, _np_ptr(out)))
+    return out
+
+
+def darts_ema_update(est, seen, obs, alpha=0.5):
+    """In place on float64 `est` and uint8 `seen`; NaN in `obs` = not observed."""
+    import numpy as np
+    assert est.dtype == np.float64 and seen.dtype == np.uint8 and est.flags.c_contiguous
+    o = np.ascontiguousarray(obs, dtype=np.float64)
+    _check(load_library().darts_ema_update(_np_ptr(est), _np_ptr(seen), _np_ptr(o), len(est), alpha))
+
+
+def darts_redundancy_budget(rho, lam, k_cost, n_prompts, M):
+    out = C.c_int64()
+    _check(load_library().darts_redundancy_budget(rho, lam, k_cost, n_prompts, M, C.byref(out)))
+    return out.value
+
+
+def darts_allocate_redundancy(sigma, m_low, m_up, m_total, seen=None):
+    import numpy as np
+    sg = np.ascontiguousarray(sigma, dtype=np.float64)
+    sn = None if seen is None else np.ascontiguousarray(seen, dtype=np.uint8)
+    out = np.zeros(len(sg), dtype=np.int32)
+    _check(load_library().darts_allocate_redundancy(_np_ptr(sg), _np_ptr(sn), len(sg), m_low, m_up,
+                                                    m_total, _np_ptr(out)))
+    return out
+
+
 # ---------------------------------------------------------------- stateful
 def model_cfg_struct(model):
     return ModelCfg(model.n_layers, model.d_model, model.n_q_heads, model.n_kv_heads,
@@ -260,6 +305,14 @@ class Rollout:
         return dict(traj=self.o_traj[:n], token=self.o_tok[:n], sampled=self.o_samp[:n],
                     logprob=self.o_lp[:n], entropy=self.o_ent[:n], finished=self.o_fin[:n])
 
+    def darts_set_plan(self, plan):
+        """Per-prompt candidate counts M'_i (k <= M'_i <= m) for the next prefill."""
+        import numpy as np
+        pl = np.ascontiguousarray(plan, dtype=np.int32)
+        assert len(pl) == self.run.n_prompts
+        _check(self.lib.darts_set_plan(self.ctx, _np_ptr(pl)), self.ctx)
+        self.n_live = int(pl.sum())
+
     def darts_prefill(self, prompts, forced_len, force_tokens=None):
         _check(self.lib.darts_prefill(self.ctx, _ptr(prompts), _ptr(forced_len), _ptr(force_tokens),
                                       C.byref(self._out)), self.ctx)
@@ -308,10 +361,13 @@ class Rollout:
         _check(self.lib.darts_debug_logits(self.ctx, _ptr(buf), C.byref(n)), self.ctx)
         return buf[:n.value]
 
-    def run_to_completion(self, prompts, forced_len, on_step=None, force_fn=None):
+    def run_to_completion(self, prompts, forced_len, on_step=None, force_fn=None, plan=None):
         """prefill, then decode + select until every prompt's kept set is complete.
         on_step(step_index, rows) is called after every sampling step;
-        force_fn(step_index) may return a [n_traj] int32 device tensor."""
+        force_fn(step_index) may return a [n_traj] int32 device tensor;
+        plan: optional per-prompt candidate counts (darts_set_plan)."""
+        if plan is not None:
+            self.darts_set_plan(plan)
         rows = self.darts_prefill(prompts, forced_len, force_fn(0) if force_fn else None)
         if on_step:
             on_step(0, rows)

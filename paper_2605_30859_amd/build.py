@@ -11,6 +11,9 @@ CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libdarts.so")
 SOURCES = ["api.hip", "k_init.hip", "k_gemm.hip", "k_elem.hip", "k_attn.hip", "k_sample.hip",
            "k_select.hip", "k_moe.hip"]
+HOST_SOURCES = ["planner.cpp"]          # host-only C++ (no device code)
+CXX = os.environ.get("CXX", "g++")
+CXXFLAGS = ["-O2", "-std=c++17", "-fPIC", "-ffp-contract=off", "-Wall"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          # no packed-fp32 instructions anywhere in this library
@@ -30,6 +33,13 @@ def build(verbose: bool = False, jobs: int = 7) -> str:
         if len(procs) >= jobs:
             _wait(procs, verbose)
             procs = []
+    _wait(procs, verbose)
+    procs = []
+    for src in HOST_SOURCES:
+        obj = os.path.join(objdir, src.replace(".cpp", ".o"))
+        objs.append(obj)
+        cmd = [CXX, *CXXFLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+        procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))
     _wait(procs, verbose)
     tmp = OUT + ".tmp"
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]

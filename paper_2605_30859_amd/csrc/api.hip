@@ -90,6 +90,9 @@ struct darts_ctx {
   int32_t* done_step = nullptr;
   int32_t* kept = nullptr;
   int32_t* live[2] = {nullptr, nullptr};
+  int32_t* grp_m = nullptr;        // [P] candidates per prompt (redundancy plan M'_i)
+  std::vector<int32_t> plan;       // host copy of grp_m
+  int n_start = 0;                 // sum of the plan: trajectories started by the prefill
   int32_t* grp_cnt = nullptr;
   int32_t* grp_rel = nullptr;
   int32_t* trj_cnt = nullptr;
@@ -271,6 +274,27 @@ const char* darts_strerror(int s) {
 
 const char* darts_last_error(const darts_ctx* c) { return c ? c->err.c_str() : ""; }
 
+// Upload the redundancy plan: per-prompt candidate counts, the initial live
+// list (existing candidates g = i*m + j, j < M'_i, ascending) and statuses
+// (absent candidates j >= M'_i never run).  Synchronises the stream.
+static hipError_t upload_plan(darts_ctx* c) {
+  std::vector<int32_t> live;
+  std::vector<uint8_t> st((size_t)c->n_traj, 4);
+  live.reserve(c->n_traj);
+  for (int i = 0; i < c->P; ++i)
+    for (int j = 0; j < c->plan[i]; ++j) {
+      live.push_back(i * c->m + j);
+      st[(size_t)i * c->m + j] = 0;
+    }
+  c->n_start = (int)live.size();
+  hipError_t e = hipMemcpyAsync(c->grp_m, c->plan.data(), (size_t)c->P * 4, hipMemcpyHostToDevice, c->st);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(c->live[0], live.data(), live.size() * 4, hipMemcpyHostToDevice, c->st);
+  if (e == hipSuccess) e = hipMemcpyAsync(c->status, st.data(), st.size(), hipMemcpyHostToDevice, c->st);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->st);
+  return e;
+}
+
 int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_run_cfg* run,
                darts_ctx** out) {
   if (!model || !run || !out) return DARTS_EINVAL;
@@ -379,6 +403,7 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
   A(&c->kept, (size_t)c->P * k * 4);
   A(&c->live[0], (size_t)c->n_traj * 4);
   A(&c->live[1], (size_t)c->n_traj * 4);
+  A(&c->grp_m, (size_t)c->P * 4);
   A(&c->grp_cnt, (size_t)c->P * 4);
   A(&c->grp_rel, (size_t)c->P * 4);
   A(&c->trj_cnt, (size_t)c->n_traj * 4);
@@ -422,13 +447,11 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
   }
   // host-computed index tables (uploaded once)
   {
-    std::vector<int32_t> pf(rows_pf), lr(c->P), iota(c->n_traj);
+    std::vector<int32_t> pf(rows_pf), lr(c->P);
     for (int r = 0; r < rows_pf; ++r) pf[r] = (r / c->Lp) * c->m;
     for (int i = 0; i < c->P; ++i) lr[i] = i * c->Lp + c->Lp - 1;
-    for (int g = 0; g < c->n_traj; ++g) iota[g] = g;
     e = hipMemcpyAsync(c->prefill_pt, pf.data(), pf.size() * 4, hipMemcpyHostToDevice, c->st);
     if (e == hipSuccess) e = hipMemcpyAsync(c->last_rows, lr.data(), lr.size() * 4, hipMemcpyHostToDevice, c->st);
-    if (e == hipSuccess) e = hipMemcpyAsync(c->live[0], iota.data(), iota.size() * 4, hipMemcpyHostToDevice, c->st);
     if (e == hipSuccess) e = hipStreamSynchronize(c->st);
   }
   int rcode = DARTS_OK;
@@ -443,13 +466,14 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
     if (e == hipSuccess) e = hipMemcpyAsync(c->dcnt, &top, 4, hipMemcpyHostToDevice, c->st);
     if (e == hipSuccess) e = hipMemsetAsync(c->gen, 0, (size_t)c->n_traj * 4, c->st);
     if (e == hipSuccess) e = hipMemsetAsync(c->sum_lp, 0, (size_t)c->n_traj * 4, c->st);
-    if (e == hipSuccess) e = hipMemsetAsync(c->status, 0, (size_t)c->n_traj, c->st);
     if (e == hipSuccess) e = hipMemsetAsync(c->freed, 0, (size_t)c->n_traj, c->st);
     if (e == hipSuccess) e = hipMemsetAsync(c->group_done, 0, (size_t)c->P, c->st);
     if (e == hipSuccess) e = hipMemsetAsync(c->kept, 0xff, (size_t)c->P * c->k * 4, c->st);
     if (e == hipSuccess) e = hipMemsetAsync(c->done_step, 0xff, (size_t)c->P * 4, c->st);
     if (e == hipSuccess) e = hipMemsetAsync(c->page_table, 0xff, (size_t)c->n_traj * c->max_pages * 4, c->st);
     if (e == hipSuccess) e = hipStreamSynchronize(c->st);
+    c->plan.assign(c->P, c->m);
+    if (e == hipSuccess) e = upload_plan(c);
     if (e != hipSuccess) rcode = fail_hip(c, e, "init");
   }
   if (rcode != DARTS_OK) {
@@ -466,23 +490,21 @@ int darts_reset(darts_ctx* c) {
   if (!c) return DARTS_EINVAL;
   if (c->poisoned) return DARTS_EHIP;
   hipError_t e = hipStreamSynchronize(c->st);
-  std::vector<int32_t> iota(c->n_traj);
-  for (int g = 0; g < c->n_traj; ++g) iota[g] = g;
   const int32_t top = (int32_t)c->n_pages;
   if (e == hipSuccess)
     e = launch_iota_perm(c->free_stack, c->n_pages, c->rc.page_perm_seed,
                          (c->rc.flags & DARTS_FLAG_PERMUTE_PAGES) != 0, c->st);
   if (e == hipSuccess) e = hipMemcpyAsync(c->dcnt, &top, 4, hipMemcpyHostToDevice, c->st);
-  if (e == hipSuccess) e = hipMemcpyAsync(c->live[0], iota.data(), iota.size() * 4, hipMemcpyHostToDevice, c->st);
   if (e == hipSuccess) e = hipMemsetAsync(c->gen, 0, (size_t)c->n_traj * 4, c->st);
   if (e == hipSuccess) e = hipMemsetAsync(c->sum_lp, 0, (size_t)c->n_traj * 4, c->st);
-  if (e == hipSuccess) e = hipMemsetAsync(c->status, 0, (size_t)c->n_traj, c->st);
   if (e == hipSuccess) e = hipMemsetAsync(c->freed, 0, (size_t)c->n_traj, c->st);
   if (e == hipSuccess) e = hipMemsetAsync(c->group_done, 0, (size_t)c->P, c->st);
   if (e == hipSuccess) e = hipMemsetAsync(c->kept, 0xff, (size_t)c->P * c->k * 4, c->st);
   if (e == hipSuccess) e = hipMemsetAsync(c->done_step, 0xff, (size_t)c->P * 4, c->st);
   if (e == hipSuccess) e = hipMemsetAsync(c->page_table, 0xff, (size_t)c->n_traj * c->max_pages * 4, c->st);
   if (e == hipSuccess) e = hipStreamSynchronize(c->st);
+  c->plan.assign(c->P, c->m);
+  if (e == hipSuccess) e = upload_plan(c);
   if (e != hipSuccess) return fail_hip(c, e, "reset");
   c->phase = 0; c->cur = 0; c->n_live = 0; c->n_done = 0; c->free_top = (int)c->n_pages;
   c->step = 0; c->tokens = 0; c->hwm = 0; c->last_rows_out = 0;
@@ -490,6 +512,18 @@ int darts_reset(darts_ctx* c) {
   c->attn_ms = c->attn_bytes = c->attn_traj_bytes = 0.0; c->attn_launches = 0;
   c->gemm_ms = c->gemm_flop = 0.0; c->gemm_launches = 0;
   for (int i = 0; i < 6; ++i) c->cls_ms[i] = c->cls_flop[i] = 0.0;
+  return DARTS_OK;
+}
+
+int darts_set_plan(darts_ctx* c, const int32_t* h_plan) {
+  if (!c || !h_plan) return DARTS_EINVAL;
+  if (c->poisoned) return DARTS_EHIP;
+  if (c->phase != 0) return DARTS_ESTATE;
+  for (int i = 0; i < c->P; ++i)
+    if (h_plan[i] < c->k || h_plan[i] > c->m) return DARTS_EINVAL;
+  c->plan.assign(h_plan, h_plan + c->P);
+  hipError_t e = upload_plan(c);
+  if (e != hipSuccess) return fail_hip(c, e, "set plan");
   return DARTS_OK;
 }
 
@@ -610,8 +644,8 @@ int darts_prefill(darts_ctx* c, const int32_t* d_prompts, const int32_t* d_force
   const int rows = c->P * c->Lp;
   HIPCHK(c, hipMemcpyAsync(c->forced_len, d_forced_len, (size_t)c->n_traj * 4,
                            hipMemcpyDeviceToDevice, c->st));
-  HIPCHK(c, launch_prefill_pages(c->P, c->m, c->pp, c->page_table, c->max_pages, c->free_stack,
-                                 c->dcnt, c->refcnt, c->st));
+  HIPCHK(c, launch_prefill_pages(c->P, c->m, c->grp_m, c->pp, c->page_table, c->max_pages,
+                                 c->free_stack, c->dcnt, c->refcnt, c->st));
   HIPCHK(c, launch_embed_v(c->embed, b, d_prompts, nullptr, rows, c->d, c->V, c->x, c->st));
   int r = run_layers(c, rows, c->prefill_pt, c->Lp, 0, c->Lp, 1, c->Lp);
   if (r != DARTS_OK) return r;
@@ -620,7 +654,7 @@ int darts_prefill(darts_ctx* c, const int32_t* d_prompts, const int32_t* d_force
   HIPCHK(c, launch_gemm(b, c->xn, c->d, c->lm_head, c->d, c->logits, c->V, c->P, c->V, c->d,
                         EPI_F32, c->gemm_ws, c->gemm_ws_bytes, c->st));
   SampleArgs a{};
-  a.logits = c->logits; a.n_rows = c->n_traj; a.vocab = c->V; a.bf16 = false;
+  a.logits = c->logits; a.n_rows = c->n_start; a.vocab = c->V; a.bf16 = false;
   a.seed = c->rc.sample_seed; a.temperature = c->rc.temperature;
   a.row_logit = nullptr; a.logit_div = c->m;
   a.traj = c->live[c->cur]; a.step = nullptr; a.force = d_force_tokens;
@@ -633,10 +667,10 @@ int darts_prefill(darts_ctx* c, const int32_t* d_prompts, const int32_t* d_force
   c->hwm = std::max<int64_t>(c->hwm, c->n_pages - c->free_top);
   c->phase = 1;
   c->step = 1;
-  c->n_live = c->n_traj;
-  c->tokens += c->n_traj;
+  c->n_live = c->n_start;
+  c->tokens += c->n_start;
   HIPCHK(c, hipStreamSynchronize(c->st));
-  return write_out_rows(c, out, c->n_traj);
+  return write_out_rows(c, out, c->n_start);
 }
 
 int darts_decode_step(darts_ctx* c, const int32_t* d_force_tokens, darts_step_out* out) {
@@ -688,7 +722,7 @@ int darts_select_and_prune(darts_ctx* c, int32_t* d_kept, int32_t* d_done_step, 
   PruneArgs a{};
   a.status = c->status; a.gen = c->gen; a.sum_lp = c->sum_lp; a.freed = c->freed;
   a.refcnt = c->refcnt; a.group_done = c->group_done; a.done_step = c->done_step; a.kept = c->kept;
-  a.n_groups = c->P; a.m = c->m; a.k = c->k; a.L = c->L; a.m_up = c->m_up;
+  a.n_groups = c->P; a.m = c->m; a.k = c->k; a.L = c->L; a.m_up = c->m_up; a.grp_m = c->grp_m;
   a.early_stop = (c->rc.flags & DARTS_FLAG_NO_ABORT) ? 0 : 1;
   a.step = (int)c->step;
   a.page_table = c->page_table; a.pt_stride = c->max_pages; a.prompt_pages = c->pp;

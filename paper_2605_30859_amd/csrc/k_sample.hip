@@ -57,10 +57,10 @@ __global__ void __launch_bounds__(256) sample_kernel(SampleArgs a) {
   __shared__ Best sb[4];
   const int r = blockIdx.x;
   const int tid = threadIdx.x;
-  const int lrow = a.row_logit ? a.row_logit[r] : (a.logit_div > 0 ? r / a.logit_div : r);
+  const int g = a.traj[r];
+  const int lrow = a.row_logit ? a.row_logit[r] : (a.logit_div > 0 ? g / a.logit_div : r);
   const void* row = BF16 ? (const void*)((const bf16_t*)a.logits + (int64_t)lrow * a.vocab)
                          : (const void*)((const float*)a.logits + (int64_t)lrow * a.vocab);
-  const int g = a.traj[r];
   const int step = STATEFUL ? a.gen[g] : a.step[r];
   const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
   const bool tscale = a.temperature != 1.0f;

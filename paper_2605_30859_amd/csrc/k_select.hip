@@ -19,7 +19,7 @@
 
 namespace darts {
 
-enum { ST_LIVE = 0, ST_EOS = 1, ST_TRUNC = 2, ST_ABORT = 3 };
+enum { ST_LIVE = 0, ST_EOS = 1, ST_TRUNC = 2, ST_ABORT = 3, ST_ABSENT = 4 };
 
 __device__ __forceinline__ uint32_t ord_neg(float x) {
   float y = -x;
@@ -142,13 +142,14 @@ __global__ void __launch_bounds__(1024) prune_kernel(PruneArgs a) {
   // phase 1: decisions; pages each member / group releases now
   for (int grp = wv; grp < a.n_groups; grp += 16) {
     const int g = grp * a.m + lane;
-    const bool act = lane < a.m;
+    const int mi = a.grp_m[grp];              // this group's candidate count M'_i
+    const bool act = lane < mi;
     if (!a.group_done[grp]) {
       uint8_t dummy = ST_ABORT;
       uint8_t* stp = act ? &a.status[g] : &dummy;
       const int ln = act ? a.gen[g] : 0;
       const float ml = (act && ln > 0) ? __fdiv_rn(a.sum_lp[g], (float)ln) : 0.f;
-      const bool c = decide_group(lane, a.m, a.k, a.L, a.m_up, a.early_stop, stp, ln, ml, g,
+      const bool c = decide_group(lane, mi, a.k, a.L, a.m_up, a.early_stop, stp, ln, ml, g,
                                   a.kept + (int64_t)grp * a.k);
       if (c && lane == 0) { a.group_done[grp] = 1; a.done_step[grp] = a.step; }
     }
@@ -192,7 +193,7 @@ __global__ void __launch_bounds__(1024) prune_kernel(PruneArgs a) {
   // phase 3: push page ids: members in order, then the prompt's shared pages
   for (int grp = wv; grp < a.n_groups; grp += 16) {
     const int g = grp * a.m + lane;
-    const bool act = lane < a.m;
+    const bool act = lane < a.grp_m[grp];
     const int c = act ? a.trj_cnt[g] : 0;
     int incl = c;
 #pragma unroll
@@ -298,11 +299,12 @@ hipError_t launch_alloc_pages(const int32_t* live, int n_live, const int32_t* ge
 }
 
 // Prefill: prompt i takes pages top-1-(i*pp + t), t < pp; every member's
-// page-table row starts with them; refcount m.  Also resets per-trajectory
-// state.  Caller guarantees the stack holds n_prompts*pp pages.
-__global__ void prefill_pages_kernel(int n_prompts, int m, int pp, int32_t* page_table,
-                                     int pt_stride, const int32_t* free_stack,
-                                     const int32_t* free_top, int32_t* refcnt) {
+// page-table row starts with them; refcount = the prompt's candidate count.
+// Caller guarantees the stack holds n_prompts*pp pages.
+__global__ void prefill_pages_kernel(int n_prompts, int m, const int32_t* grp_m, int pp,
+                                     int32_t* page_table, int pt_stride,
+                                     const int32_t* free_stack, const int32_t* free_top,
+                                     int32_t* refcnt) {
   const int top = *free_top;
   const int64_t n = (int64_t)n_prompts * m * pp;
   for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n;
@@ -312,22 +314,22 @@ __global__ void prefill_pages_kernel(int n_prompts, int m, int pp, int32_t* page
     const int g = (int)gm;
     const int i = g / m;
     page_table[(int64_t)g * pt_stride + j] = free_stack[top - 1 - (i * pp + j)];
-    if (j == 0 && g % m == 0) refcnt[i] = m;
+    if (j == 0 && g % m == 0) refcnt[i] = grp_m[i];
   }
 }
 __global__ void set_top_kernel(int32_t* free_top, int delta) {
   if (threadIdx.x == 0 && blockIdx.x == 0) *free_top += delta;
 }
 
-hipError_t launch_prefill_pages(int n_prompts, int m, int prompt_pages, int32_t* page_table,
-                                int pt_stride, int32_t* free_stack, int32_t* free_top,
-                                int32_t* refcnt, hipStream_t st) {
+hipError_t launch_prefill_pages(int n_prompts, int m, const int32_t* grp_m, int prompt_pages,
+                                int32_t* page_table, int pt_stride, int32_t* free_stack,
+                                int32_t* free_top, int32_t* refcnt, hipStream_t st) {
   const int64_t n = (int64_t)n_prompts * m * prompt_pages;
   int64_t blocks = (n + 255) / 256;
   if (blocks < 1) blocks = 1;
   if (blocks > 4096) blocks = 4096;
   hipLaunchKernelGGL(prefill_pages_kernel, dim3((unsigned)blocks), dim3(256), 0, st, n_prompts, m,
-                     prompt_pages, page_table, pt_stride, free_stack, free_top, refcnt);
+                     grp_m, prompt_pages, page_table, pt_stride, free_stack, free_top, refcnt);
   hipLaunchKernelGGL(set_top_kernel, dim3(1), dim3(64), 0, st, free_top, -n_prompts * prompt_pages);
   return hipGetLastError();
 }

@@ -85,7 +85,7 @@ hipError_t launch_attention_shared(const void* q, const void* k_pool, const void
 // ---- sampler (k_sample.hip)
 struct SampleArgs {
   const void* logits; int n_rows; int vocab; bool bf16; uint64_t seed; float temperature;
-  const int32_t* row_logit;   // row r reads logits row row_logit[r], else r / logit_div, else r
+  const int32_t* row_logit;   // row r reads logits row row_logit[r], else traj[r] / logit_div, else r
   int logit_div;
   const int32_t* traj;        // [n_rows] trajectory id (counter word 1)
   const int32_t* step;        // NULL: use per-trajectory gen count (stateful)
@@ -110,6 +110,7 @@ struct PruneArgs {
   uint8_t* status; const int32_t* gen; const float* sum_lp; uint8_t* freed; int32_t* refcnt;
   uint8_t* group_done; int32_t* done_step; int32_t* kept;
   int n_groups, m, k, L, m_up, early_stop, step;
+  const int32_t* grp_m;   // [n_groups] candidates of each group (members j < grp_m[i] exist)
   const int32_t* page_table; int pt_stride; int prompt_pages;
   int32_t* free_stack; int32_t* free_top;     // free_top: device counter
   int n_pages;                                // stack capacity
@@ -121,7 +122,8 @@ hipError_t launch_prune(const PruneArgs& a, hipStream_t st);
 hipError_t launch_alloc_pages(const int32_t* live, int n_live, const int32_t* gen, int prompt_pages,
                               int32_t* page_table, int pt_stride, int32_t* free_stack,
                               int32_t* free_top, int32_t* info, hipStream_t st);
-hipError_t launch_prefill_pages(int n_prompts, int m, int prompt_pages, int32_t* page_table,
+hipError_t launch_prefill_pages(int n_prompts, int m, const int32_t* grp_m, int prompt_pages,
+                                int32_t* page_table,
                                 int pt_stride, int32_t* free_stack, int32_t* free_top,
                                 int32_t* refcnt, hipStream_t st);
 

@@ -71,3 +71,56 @@ def test_no_abort_counterfactual_same_kept(tiny_run):
                       mean_lp=mlp, early_stop=False)
     assert s["kept"] == r.kept
     assert s["steps"] >= r.steps and s["tokens_decoded"] >= r.tokens_decoded
+
+
+# ---------------------------------------------------------------- ragged plans
+def _ragged_plan(P, k, m):
+    """A redundancy plan with sizes in [k, m]: shortest-only and dual-end groups mixed."""
+    return [m if i % 2 == 0 else k + (i % (m - k + 1)) for i in range(P)]
+
+
+def test_ragged_schedule_equals_per_prompt_uniform_runs():
+    """A batch with per-prompt candidate counts decides every group exactly as a
+    batch holding only that prompt with a uniform size M'_i would (groups are
+    independent; pages are additive)."""
+    rng = np.random.default_rng(8)
+    P, m, k, cap, Lp = 6, 8, 4, 40, 32
+    forced = rng.integers(1, 60, P * m)
+    mlp = -(np.floor(rng.random(P * m) * 64) / 64).astype(np.float32)
+    plan = _ragged_plan(P, k, m)
+    r = schedule_only(forced, P, m, k, cap, Lp, mean_lp=mlp, alloc=plan)
+    tok = 0
+    for i in range(P):
+        mi = plan[i]
+        f = forced[i * m:i * m + mi]
+        s = schedule_only(f, 1, mi, k, cap, Lp, m_up=2 * k, mean_lp=mlp[i * m:i * m + mi])
+        assert r["kept"][i] == [i * m + g for g in s["kept"][0]]
+        assert r["done_step"][i] == s["done_step"][0]
+        assert r["length"][i * m:i * m + mi] == s["length"]
+        assert all(x == 0 for x in r["length"][i * m + mi:(i + 1) * m])
+        tok += s["tokens_decoded"]
+    assert r["tokens_decoded"] == tok
+    assert r["steps"] == max(r["done_step"].values())
+    assert r["pages_end"] == 0
+    # the uniform plan is the plain batch
+    u = schedule_only(forced, P, m, k, cap, Lp, mean_lp=mlp, alloc=[m] * P)
+    v = schedule_only(forced, P, m, k, cap, Lp, mean_lp=mlp)
+    assert u == v
+
+
+def test_ragged_model_rollout_matches_schedule(tiny_run):
+    cfg, run, W, prompts, forced, r = tiny_run
+    plan = _ragged_plan(run.n_prompts, run.k, run.m)
+    rr = rollout(cfg, W, prompts, forced, run.m, run.k, run.cap, run.sample_seed, alloc=plan)
+    assert sorted(rr.tokens) == [i * run.m + j for i in range(run.n_prompts) for j in range(plan[i])]
+    n = run.n_prompts * run.m
+    mlp = np.array([rr.mean_lp32.get(g, 0.0) for g in range(n)], np.float32)
+    s = schedule_only(forced, run.n_prompts, run.m, run.k, run.cap, run.prompt_len, mean_lp=mlp,
+                      alloc=plan)
+    assert s["kept"] == rr.kept and s["done_step"] == rr.done_step
+    assert s["steps"] == rr.steps and s["tokens_decoded"] == rr.tokens_decoded
+    assert s["pages_hwm"] == rr.pages_hwm
+    # a trajectory's tokens do not depend on the plan (counter-based sampling)
+    for g in rr.tokens:
+        L = min(len(rr.tokens[g]), len(r.tokens[g]))
+        assert rr.tokens[g][:L] == r.tokens[g][:L]
