@@ -269,6 +269,9 @@ def main():
     ap.add_argument("--config", default="qwen3-8b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-abort", action="store_true", help="counterfactual without early stop")
+    ap.add_argument("--cost-model-check", action="store_true",
+                    help="after the timed rollouts, run the no-abort counterfactual once and compare its "
+                         "measured decode time with Eq. 4 on the PTL curve fitted to the early-stop run")
     ap.add_argument("--shared-prefix", action="store_true",
                     help="decode attention reads each prompt's shared pages once per group")
     ap.add_argument("--sweep", action="store_true",
@@ -315,7 +318,7 @@ def main():
         return
     model, run = get_config(args.config)
     prompts, forced = rollout_inputs(model, run)
-    flags = (B.FLAG_TIMING | (B.FLAG_NO_ABORT if args.no_abort else 0) |
+    flags = (B.FLAG_TIMING | B.FLAG_STEP_TIMES | (B.FLAG_NO_ABORT if args.no_abort else 0) |
              (B.FLAG_SHARED_PREFIX if args.shared_prefix else 0))
     t_init = time.perf_counter()
     ro = B.Rollout(model, run, flags=flags)
@@ -365,12 +368,32 @@ def main():
     ach = attn_b / (attn_ms * 1e-3) / 1e9 if attn_ms > 0 else 0.0
     peak_mm = BF16_PEAK_TFLOPS if model.dtype == "bf16" else FP32_PEAK_TFLOPS
     gemm_tf = gemm_f / (gemm_ms * 1e-3) / 1e12 if gemm_ms > 0 else 0.0
+    # rollout cost model (Eq. 4) on this engine: PTL fitted to the last timed
+    # rollout's per-step (live rows, device ms) samples
+    rows, sms, pf_ms = ro.step_times()
+    lens = ro.traj_scores()[0].cpu().numpy()
+    ptl = B.darts_fit_ptl(rows, sms.astype(np.float64))
+    eq4 = B.darts_rollout_cost(np.maximum(lens[lens > 0] - 1, 0), ptl)
+    cost_model = {"ptl_ms": {"b1": ptl[0], "b2": ptl[1], "c0": ptl[2], "c1": ptl[3], "c2": ptl[4],
+                             "c3": ptl[5]},
+                  "decode_steps": int(len(rows)), "decode_ms_measured": float(sms.sum()),
+                  "decode_ms_eq4": eq4, "prefill_ms": pf_ms}
     cls = {}
     for i, name in enumerate(["qkv", "o", "gate_up", "down", "lm_head", "moe_block"]):
         ms = sum(s["gemm_cls_ms"][i] for s in stats)
-        fl = sum(s["gemm_cls_flop"][i] for s in stats)
-        cls[name] = {"ms": ms, "tflops": fl / (ms * 1e-3) / 1e12 if ms > 0 else 0.0}
+        fl_ = sum(s["gemm_cls_flop"][i] for s in stats)
+        cls[name] = {"ms": ms, "tflops": fl_ / (ms * 1e-3) / 1e12 if ms > 0 else 0.0}
     ro.close()
+    if args.cost_model_check and not args.no_abort:
+        ro2 = B.Rollout(model, run, flags=B.FLAG_STEP_TIMES | B.FLAG_NO_ABORT)
+        ro2.run_to_completion(pr, fl)
+        r2, ms2, _ = ro2.step_times()
+        l2 = ro2.traj_scores()[0].cpu().numpy()
+        ro2.close()
+        cost_model["no_abort"] = {"decode_ms_measured": float(ms2.sum()),
+                                  "decode_ms_eq4_from_early_stop_fit":
+                                      B.darts_rollout_cost(np.maximum(l2[l2 > 0] - 1, 0), ptl),
+                                  "decode_steps": int(len(r2))}
 
     out = {
         "metric": "rollout tokens/s + time-to-kept-set-complete; decode-attn HBM % of peak",
@@ -404,6 +427,7 @@ def main():
         "gemm": {"bound": "mfma", "achieved": gemm_tf, "peak": peak_mm, "unit": "TFLOP/s",
                  "frac": gemm_tf / peak_mm, "share_of_step_time": gemm_ms * 1e-3 / total,
                  "by_class": cls},
+        "cost_model": cost_model,
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:

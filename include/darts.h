@@ -68,6 +68,10 @@ typedef enum { DARTS_F32 = 0, DARTS_BF16 = 1 } darts_dtype;
                                           shared pages once per group of its live members
                                           (a prefix kernel) instead of once per row */
 
+#define DARTS_FLAG_STEP_TIMES    0x10u /* record device time of every sampling step (first
+                                          launch of the step to the end of its selection
+                                          kernel); darts_get_step_times reports them */
+
 /* Decoder shape.  Weights are generated on the device from weight_seed
  * (Philox uniform, variance 1/fan_in, rounded to bf16 for DARTS_BF16).
  * Dense SwiGLU when n_experts == 0, else top_k-of-n_experts MoE.            */
@@ -214,6 +218,16 @@ int darts_select_and_prune(darts_ctx* ctx, int32_t* d_kept, int32_t* d_done_step
 
 int darts_get_stats(const darts_ctx* ctx, darts_stats* out);
 
+/* Per decode step wall time on the device (DARTS_FLAG_STEP_TIMES): step i
+ * decoded h_rows[i] trajectories in h_ms[i] milliseconds, from its first
+ * launch to the end of the selection kernel that followed it; up to cap
+ * entries are written, *h_n = the number of decode steps recorded since the
+ * prefill.  *h_prefill_ms (may be NULL): the prefill step.  These are the
+ * (batch size, per-token latency) samples of the cost model (Sec. 4.2.1,
+ * App. A).  DARTS_ESTATE without the flag.                                 */
+int darts_get_step_times(const darts_ctx* ctx, int32_t* h_rows, float* h_ms, int32_t cap,
+                         int32_t* h_n, float* h_prefill_ms);
+
 /* Start a new batch on the same context: weights, pool and buffers are
  * kept; the free list, page tables, per-trajectory and per-prompt state and
  * the statistics are reset.  Synchronises the stream.  The next call must be
@@ -269,6 +283,23 @@ int darts_redundancy_budget(double rho, double lambda, double k_cost, int32_t n_
  * index).  A surplus beyond n*m_up stays unallocated.  Writes h_plan[n].    */
 int darts_allocate_redundancy(const double* h_sigma, const uint8_t* h_seen, int32_t n_prompts,
                               int32_t m_low, int32_t m_up, int64_t m_total, int32_t* h_plan);
+
+/* Rollout cost model, Eq. 4 (Sec. 4.2.1): with the n lengths sorted
+ * (l_[0] = 0), *h_T = sum_m (l_[m] - l_[m-1]) * PTL(n - m + 1), where
+ * PTL(b) = c0 + c1*b + c2*max(0, b-b1) + c3*max(0, b-b2) and
+ * h_ptl = {b1, b2, c0, c1, c2, c3}.  Lengths are the numbers of decode steps
+ * each trajectory takes part in; the result is in PTL's unit.  For data
+ * parallel ranks the batch cost is the maximum over ranks.                  */
+int darts_rollout_cost(const int32_t* h_len, int32_t n, const double* h_ptl, double* h_T);
+
+/* Three-stage piecewise-linear PTL fit (App. A): least squares of
+ * h_lat[i] ~ PTL(h_bsz[i]) over every breakpoint pair b1 = xs[i] < b2 = xs[j],
+ * 1 <= i < j <= D-2, of the D distinct batch sizes xs (ascending), the
+ * smallest residual winning (ties: the first pair).  D < 4: one line
+ * (b1 = b2 = largest size, c2 = c3 = 0); D = 1: the mean.  Writes
+ * h_ptl[6] = {b1, b2, c0, c1, c2, c3}.  DARTS_EINVAL for non-finite
+ * latencies.                                                               */
+int darts_fit_ptl(const int32_t* h_bsz, const double* h_lat, int32_t n, double* h_ptl);
 
 /* ----------------------------------------------------- stateless kernels  */
 /* These run one kernel of the path on caller-provided device buffers, for

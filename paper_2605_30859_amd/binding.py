@@ -9,7 +9,7 @@ import numpy as np
 
 DARTS_OK, DARTS_EINVAL, DARTS_ENOMEM, DARTS_ESTATE, DARTS_EHIP = 0, 1, 2, 3, 4
 DARTS_F32, DARTS_BF16 = 0, 1
-FLAG_NO_ABORT, FLAG_PERMUTE_PAGES, FLAG_TIMING, FLAG_SHARED_PREFIX = 0x1, 0x2, 0x4, 0x8
+FLAG_NO_ABORT, FLAG_PERMUTE_PAGES, FLAG_TIMING, FLAG_SHARED_PREFIX, FLAG_STEP_TIMES = 0x1, 0x2, 0x4, 0x8, 0x10
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 lib_path = os.path.join(_HERE, "libdarts.so")
@@ -69,6 +69,9 @@ _SIGS = {
     "darts_redundancy_budget": (C.c_int, [C.c_double, C.c_double, C.c_double, C.c_int32, C.c_int32,
                                           C.POINTER(C.c_int64)]),
     "darts_allocate_redundancy": (C.c_int, [_P, _P, C.c_int32, C.c_int32, C.c_int32, C.c_int64, _P]),
+    "darts_get_step_times": (C.c_int, [_P, _P, _P, C.c_int32, C.POINTER(C.c_int32), C.POINTER(C.c_float)]),
+    "darts_rollout_cost": (C.c_int, [_P, C.c_int32, _P, C.POINTER(C.c_double)]),
+    "darts_fit_ptl": (C.c_int, [_P, _P, C.c_int32, _P]),
     "darts_strerror": (C.c_char_p, [C.c_int]),
     "darts_last_error": (C.c_char_p, [_P]),
     "darts_fill_uniform": (C.c_int, [_P, C.c_uint64, C.c_int32, C.c_uint64, C.c_int32, _P]),
@@ -242,6 +245,24 @@ def darts_allocate_redundancy(sigma, m_low, m_up, m_total, seen=None):
     return out
 
 
+def darts_rollout_cost(lengths, ptl):
+    import numpy as np
+    ln = np.ascontiguousarray(lengths, dtype=np.int32)
+    p = np.ascontiguousarray(ptl, dtype=np.float64)
+    out = C.c_double()
+    _check(load_library().darts_rollout_cost(_np_ptr(ln), len(ln), _np_ptr(p), C.byref(out)))
+    return out.value
+
+
+def darts_fit_ptl(bsz, lat):
+    import numpy as np
+    b = np.ascontiguousarray(bsz, dtype=np.int32)
+    y = np.ascontiguousarray(lat, dtype=np.float64)
+    out = np.zeros(6, dtype=np.float64)
+    _check(load_library().darts_fit_ptl(_np_ptr(b), _np_ptr(y), len(b), _np_ptr(out)))
+    return tuple(float(x) for x in out)
+
+
 # ---------------------------------------------------------------- stateful
 def model_cfg_struct(model):
     return ModelCfg(model.n_layers, model.d_model, model.n_q_heads, model.n_kv_heads,
@@ -343,6 +364,18 @@ class Rollout:
             v = getattr(s, f)
             out[f] = list(v) if f.startswith("gemm_cls") else v
         return out
+
+    def step_times(self):
+        """(rows per decode step, ms per decode step, prefill ms); needs FLAG_STEP_TIMES."""
+        import numpy as np
+        n = C.c_int32()
+        pf = C.c_float()
+        _check(self.lib.darts_get_step_times(self.ctx, None, None, 0, C.byref(n), C.byref(pf)), self.ctx)
+        rows = np.zeros(n.value, np.int32)
+        ms = np.zeros(n.value, np.float32)
+        _check(self.lib.darts_get_step_times(self.ctx, _np_ptr(rows), _np_ptr(ms), n.value, C.byref(n),
+                                             C.byref(pf)), self.ctx)
+        return rows, ms, pf.value
 
     def traj_scores(self):
         t = self.torch

@@ -127,6 +127,13 @@ struct darts_ctx {
   std::string err;
   std::vector<TimedLaunch> pending;
   std::vector<hipEvent_t> events;  // pool, two per pending launch
+  // per-step wall time on the device (DARTS_FLAG_STEP_TIMES): from the start
+  // of a sampling step's first launch to the end of its selection kernel
+  hipEvent_t step_ev[2] = {nullptr, nullptr};
+  int step_rows = 0;               // rows of the open step, -1 for the prefill, 0 none
+  std::vector<int32_t> st_rows;
+  std::vector<float> st_ms;
+  float prefill_ms = 0.f;
   double attn_ms = 0.0, attn_bytes = 0.0, attn_traj_bytes = 0.0;
   int64_t attn_launches = 0;
   double gemm_ms = 0.0, gemm_flop = 0.0;
@@ -167,6 +174,19 @@ static void free_all(darts_ctx* c) {
   for (hipEvent_t e : c->events) (void)hipEventDestroy(e);
   c->events.clear();
   c->pending.clear();
+  for (hipEvent_t& e : c->step_ev) {
+    if (e) (void)hipEventDestroy(e);
+    e = nullptr;
+  }
+}
+
+static bool step_times_on(const darts_ctx* c) { return (c->rc.flags & DARTS_FLAG_STEP_TIMES) != 0; }
+
+// Open the timed interval of a sampling step (rows -1: the prefill).
+static hipError_t step_begin(darts_ctx* c, int rows) {
+  if (!step_times_on(c)) return hipSuccess;
+  c->step_rows = rows;
+  return hipEventRecord(c->step_ev[0], c->st);
 }
 
 static bool timing_on(const darts_ctx* c) { return (c->rc.flags & DARTS_FLAG_TIMING) != 0; }
@@ -439,6 +459,10 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
                                                                                c->hd, c->Lp + c->cap, c->pp));
   A(&c->attn_ws, c->attn_ws_bytes);
   if (e == hipSuccess) e = hipHostMalloc((void**)&c->h_info, 64, hipHostMallocDefault);
+  if (e == hipSuccess && (rc.flags & DARTS_FLAG_STEP_TIMES)) {
+    e = hipEventCreate(&c->step_ev[0]);
+    if (e == hipSuccess) e = hipEventCreate(&c->step_ev[1]);
+  }
   if (e != hipSuccess) {
     free_all(c);
     delete c;
@@ -509,6 +533,7 @@ int darts_reset(darts_ctx* c) {
   c->phase = 0; c->cur = 0; c->n_live = 0; c->n_done = 0; c->free_top = (int)c->n_pages;
   c->step = 0; c->tokens = 0; c->hwm = 0; c->last_rows_out = 0;
   c->pending.clear();
+  c->step_rows = 0; c->st_rows.clear(); c->st_ms.clear(); c->prefill_ms = 0.f;
   c->attn_ms = c->attn_bytes = c->attn_traj_bytes = 0.0; c->attn_launches = 0;
   c->gemm_ms = c->gemm_flop = 0.0; c->gemm_launches = 0;
   for (int i = 0; i < 6; ++i) c->cls_ms[i] = c->cls_flop[i] = 0.0;
@@ -642,6 +667,7 @@ int darts_prefill(darts_ctx* c, const int32_t* d_prompts, const int32_t* d_force
   const bool b = c->bf16;
   c->timed_weight = timing_on(c) ? 1.0 : 0.0;
   const int rows = c->P * c->Lp;
+  HIPCHK(c, step_begin(c, -1));
   HIPCHK(c, hipMemcpyAsync(c->forced_len, d_forced_len, (size_t)c->n_traj * 4,
                            hipMemcpyDeviceToDevice, c->st));
   HIPCHK(c, launch_prefill_pages(c->P, c->m, c->grp_m, c->pp, c->page_table, c->max_pages,
@@ -687,6 +713,7 @@ int darts_decode_step(darts_ctx* c, const int32_t* d_force_tokens, darts_step_ou
   const bool need_pages = ((s_before - 1) % kPage) == 0;
   if (need_pages && n > c->free_top) return DARTS_ENOMEM;
   c->timed_weight = (timing_on(c) && s_before % kTimingStride == 0) ? (double)kTimingStride : 0.0;
+  HIPCHK(c, step_begin(c, n));
   int32_t* live = c->live[c->cur];
   if (need_pages) {
     HIPCHK(c, launch_alloc_pages(live, n, c->gen, c->pp, c->page_table, c->max_pages, c->free_stack,
@@ -735,8 +762,17 @@ int darts_select_and_prune(darts_ctx* c, int32_t* d_kept, int32_t* d_done_step, 
     HIPCHK(c, hipMemcpyAsync(d_kept, c->kept, (size_t)c->P * c->k * 4, hipMemcpyDeviceToDevice, c->st));
   if (d_done_step)
     HIPCHK(c, hipMemcpyAsync(d_done_step, c->done_step, (size_t)c->P * 4, hipMemcpyDeviceToDevice, c->st));
+  const int timed_rows = c->step_rows;
+  if (timed_rows != 0) HIPCHK(c, hipEventRecord(c->step_ev[1], c->st));
   HIPCHK(c, hipMemcpyAsync(c->h_info, c->dcnt + 4, 32, hipMemcpyDeviceToHost, c->st));
   HIPCHK(c, hipStreamSynchronize(c->st));
+  if (timed_rows != 0) {
+    float ms = 0.f;
+    HIPCHK(c, hipEventElapsedTime(&ms, c->step_ev[0], c->step_ev[1]));
+    if (timed_rows < 0) c->prefill_ms += ms;
+    else { c->st_rows.push_back(timed_rows); c->st_ms.push_back(ms); }
+    c->step_rows = 0;
+  }
   c->cur ^= 1;
   c->n_live = c->h_info[0];
   c->n_done = c->h_info[1];
@@ -781,6 +817,17 @@ int darts_get_stats(const darts_ctx* c, darts_stats* s) {
   s->gemm_flop = c->gemm_flop;
   s->gemm_launches = c->gemm_launches;
   for (int i = 0; i < 6; ++i) { s->gemm_cls_ms[i] = c->cls_ms[i]; s->gemm_cls_flop[i] = c->cls_flop[i]; }
+  return DARTS_OK;
+}
+
+int darts_get_step_times(const darts_ctx* c, int32_t* h_rows, float* h_ms, int32_t cap, int32_t* h_n,
+                         float* h_prefill_ms) {
+  if (!c || !h_n || cap < 0 || (cap > 0 && (!h_rows || !h_ms))) return DARTS_EINVAL;
+  if (!step_times_on(c)) return DARTS_ESTATE;
+  const int32_t n = (int32_t)c->st_ms.size();
+  *h_n = n;
+  for (int32_t i = 0; i < std::min(n, cap); ++i) { h_rows[i] = c->st_rows[i]; h_ms[i] = c->st_ms[i]; }
+  if (h_prefill_ms) *h_prefill_ms = c->prefill_ms;
   return DARTS_OK;
 }
 

@@ -150,3 +150,29 @@ def test_plan_errors_and_reset():
     rows = ro.darts_prefill(pr, fl)
     assert len(rows["traj"]) == run.m * run.n_prompts
     ro.close()
+
+
+def test_step_times_and_cost_model_identity():
+    """DARTS_FLAG_STEP_TIMES records one (rows, ms) sample per decode step whose
+    row counts are the live counts the lengths imply; Eq. 4 with the PTL curve
+    fitted to those samples reproduces their total (least squares with an
+    intercept has zero-sum residuals), which checks the step accounting."""
+    B = _b()
+    model, run = get_config("dense-small")
+    run = replace(run, cap=512)
+    prompts, forced = rollout_inputs(model, run)
+    ro = B.Rollout(model, run, flags=B.FLAG_STEP_TIMES)
+    pr = torch.from_numpy(np.ascontiguousarray(prompts.reshape(-1))).to(DEV)
+    fl = torch.from_numpy(forced.astype(np.int32)).to(DEV)
+    st = ro.run_to_completion(pr, fl)
+    rows, ms, pf = ro.step_times()
+    ln = ro.traj_scores()[0].cpu().numpy()
+    ro.close()
+    assert len(rows) == st["steps"] - 1 and pf > 0 and (ms > 0).all()
+    exp_rows = [int((ln >= s).sum()) for s in range(2, st["steps"] + 1)]
+    assert list(rows) == exp_rows
+    p = B.darts_fit_ptl(rows, ms.astype(np.float64))
+    T = B.darts_rollout_cost(np.maximum(ln - 1, 0), p)
+    say(f"step times: {len(rows)} decode steps, {ms.sum():.1f} ms measured, Eq. 4 {T:.1f} ms; "
+        f"prefill {pf:.2f} ms; PTL {p}")
+    assert T == pytest.approx(float(ms.astype(np.float64).sum()), rel=1e-6)

@@ -86,3 +86,35 @@ def test_planning_argument_errors(B):
         B.darts_allocate_redundancy([1.0], 4, 2, 6)              # m_up < m_low
     with pytest.raises(B.DartsError):
         B.darts_ema_update(np.zeros(2), np.zeros(2, np.uint8), np.zeros(2), 0.0)
+
+
+# ---------------------------------------------------------------- cost model
+def test_rollout_cost_matches_oracle_bitwise(B):
+    from oracle.costmodel import rollout_cost, ptl_eval
+    rng = np.random.default_rng(13)
+    for _ in range(200):
+        n = int(rng.integers(0, 300))
+        ln = rng.integers(0, 5000, n).astype(np.int32)
+        p = (float(rng.integers(1, 200)), float(rng.integers(200, 600)), *rng.uniform(-1, 5, 4))
+        got = B.darts_rollout_cost(ln, p)
+        assert got == rollout_cost(list(ln), lambda b: ptl_eval(p, b))
+
+
+def test_ptl_fit_matches_oracle(B):
+    from oracle.costmodel import fit_ptl, ptl_eval
+    rng = np.random.default_rng(17)
+    for trial in range(30):
+        true = (float(rng.integers(20, 120)), float(rng.integers(150, 400)),
+                rng.uniform(1, 5), rng.uniform(0, 0.01), rng.uniform(0, 0.02), rng.uniform(0, 0.03))
+        b = rng.integers(1, 512, int(rng.integers(20, 120))).astype(np.int32)
+        y = np.array([ptl_eval(true, x) for x in b]) + rng.normal(0, 0.02, len(b))
+        got = B.darts_fit_ptl(b, y)
+        exp = fit_ptl(b, y)
+        assert got[:2] == exp[:2], trial
+        xs = np.unique(b)
+        assert np.allclose([ptl_eval(got, x) for x in xs], [ptl_eval(exp, x) for x in xs],
+                           rtol=1e-9, atol=1e-9)
+    # degenerate sizes
+    for b, y in (([8, 8, 8], [1.0, 2.0, 3.0]), ([4, 8, 8], [1.0, 2.0, 2.5]), ([], [])):
+        got, exp = B.darts_fit_ptl(b, y), fit_ptl(b, y)
+        assert got[:2] == exp[:2] and np.allclose(got[2:], exp[2:], rtol=1e-12, atol=1e-12)
