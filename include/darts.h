@@ -387,6 +387,15 @@ int darts_select_groups(uint8_t* d_status, const int32_t* d_len, const float* d_
                         int32_t n_traj, int32_t m, int32_t k, int32_t L, int32_t m_up,
                         int32_t early_stop, int32_t* d_kept, uint8_t* d_complete, void* stream);
 
+/* Group-normalised advantages of the kept training groups (Sec. 3.1, Eq. 2):
+ * for group i with kept ids d_kept[i*k + j] (as written by
+ * darts_select_and_prune), d_adv[i*k + j] = (r_j - mu_i) / (sigma_i + eps)
+ * with r_j = d_reward[kept id], mu_i and sigma_i the mean and population
+ * standard deviation of the group's k rewards, in float32.  A group holding
+ * an id outside [0, n_traj) (not complete) gets NaN.  k <= 64.             */
+int darts_group_advantages(const int32_t* d_kept, int32_t n_groups, int32_t k, const float* d_reward,
+                           int32_t n_traj, float eps, float* d_adv, void* stream);
+
 /* The decoder's dense projection (a plain GEMM with the decoder's fused
  * epilogues): C = A[M,K] . W[N,K]^T with fp32 accumulation.
  *   d_a  [M][K], d_w [N][K]: bf16 (DARTS_BF16) or f32 (DARTS_F32), row-major

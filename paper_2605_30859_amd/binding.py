@@ -72,6 +72,7 @@ _SIGS = {
     "darts_get_step_times": (C.c_int, [_P, _P, _P, C.c_int32, C.POINTER(C.c_int32), C.POINTER(C.c_float)]),
     "darts_rollout_cost": (C.c_int, [_P, C.c_int32, _P, C.POINTER(C.c_double)]),
     "darts_fit_ptl": (C.c_int, [_P, _P, C.c_int32, _P]),
+    "darts_group_advantages": (C.c_int, [_P, C.c_int32, C.c_int32, _P, C.c_int32, C.c_float, _P, _P]),
     "darts_strerror": (C.c_char_p, [C.c_int]),
     "darts_last_error": (C.c_char_p, [_P]),
     "darts_fill_uniform": (C.c_int, [_P, C.c_uint64, C.c_int32, C.c_uint64, C.c_int32, _P]),
@@ -190,6 +191,13 @@ def darts_select_groups(status, length, mean_lp, m, k, L, m_up, early_stop, kept
     _check(load_library().darts_select_groups(_ptr(status), _ptr(length), _ptr(mean_lp),
                                               status.numel(), m, k, L, m_up, int(early_stop),
                                               _ptr(kept), _ptr(complete), _stream(stream)))
+
+
+def darts_group_advantages(kept, reward, adv, eps=1e-6, stream=None):
+    """kept: int32 [n_groups, k] device tensor; reward: float32 [n_traj]; adv: like kept, float32."""
+    n_groups, k = kept.shape
+    _check(load_library().darts_group_advantages(_ptr(kept), n_groups, k, _ptr(reward), reward.numel(),
+                                                 eps, _ptr(adv), _stream(stream)))
 
 
 def darts_gemm_workspace_bytes(M, N, K):

@@ -982,6 +982,14 @@ int darts_debug_gumbel(const float* d_u, float* d_g, int64_t n, void* stream) {
   return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
 }
 
+int darts_group_advantages(const int32_t* d_kept, int32_t n_groups, int32_t k, const float* d_reward,
+                           int32_t n_traj, float eps, float* d_adv, void* stream) {
+  if (n_groups < 0 || k < 1 || k > 64 || n_traj < 0 || !(eps >= 0.f)) return DARTS_EINVAL;
+  if (n_groups > 0 && (!d_kept || !d_reward || !d_adv)) return DARTS_EINVAL;
+  hipError_t e = launch_advantages(d_kept, n_groups, k, d_reward, n_traj, eps, d_adv, (hipStream_t)stream);
+  return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
+}
+
 int darts_select_groups(uint8_t* d_status, const int32_t* d_len, const float* d_mean_lp,
                         int32_t n_traj, int32_t m, int32_t k, int32_t L, int32_t m_up,
                         int32_t early_stop, int32_t* d_kept, uint8_t* d_complete, void* stream) {

@@ -114,6 +114,33 @@ hipError_t launch_select(const GroupArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Group-normalised advantages of the kept groups (Sec. 3.1, Eq. 2): one
+// wavefront per group, lane j = kept slot j; mean and population standard
+// deviation by wavefront sums.  A group with an id outside [0, n_traj) (not
+// complete yet) gets NaN.
+__global__ void advantage_kernel(const int32_t* kept, int n_groups, int k, const float* reward,
+                                 int n_traj, float eps, float* adv) {
+  const int lane = threadIdx.x & 63;
+  const int grp = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (grp >= n_groups) return;
+  const bool act = lane < k;
+  const int g = act ? kept[(int64_t)grp * k + lane] : 0;
+  const bool bad = __ballot(act && (g < 0 || g >= n_traj)) != 0ull;
+  const float r = (act && !bad) ? reward[g] : 0.f;
+  const float mu = wave_sum(r) / (float)k;
+  const float dv = act ? r - mu : 0.f;
+  const float sd = sqrtf(wave_sum(dv * dv) / (float)k);
+  if (act) adv[(int64_t)grp * k + lane] = bad ? __int_as_float(0x7fc00000) : dv / (sd + eps);
+}
+
+hipError_t launch_advantages(const int32_t* kept, int n_groups, int k, const float* reward,
+                             int n_traj, float eps, float* adv, hipStream_t st) {
+  if (n_groups <= 0) return hipSuccess;
+  hipLaunchKernelGGL(advantage_kernel, dim3((n_groups + 3) / 4), dim3(256), 0, st, kept, n_groups,
+                     k, reward, n_traj, eps, adv);
+  return hipGetLastError();
+}
+
 // ---------------------------------------------------------------- stateful
 // One block of 1024 threads (16 wavefronts) does the whole select-and-prune
 // step: decide every open group, free the pages of members that ended or

@@ -119,6 +119,8 @@ struct PruneArgs {
   int32_t* info;    // out: [0] n_live, [1] n_done, [2] free_top
 };
 hipError_t launch_prune(const PruneArgs& a, hipStream_t st);
+hipError_t launch_advantages(const int32_t* kept, int n_groups, int k, const float* reward,
+                             int n_traj, float eps, float* adv, hipStream_t st);
 hipError_t launch_alloc_pages(const int32_t* live, int n_live, const int32_t* gen, int prompt_pages,
                               int32_t* page_table, int pt_stride, int32_t* free_stack,
                               int32_t* free_top, int32_t* info, hipStream_t st);

@@ -116,3 +116,9 @@ def sweep_selection_inputs(n=None, seed=None, cap=None, median=None):
     raw = np.maximum(1, np.rint(median * np.exp(rng.standard_normal(n)))).astype(np.int32)
     mlp = -(np.floor(rng.random(n) * 3 * 1024) / 1024).astype(np.float32)
     return raw, mlp
+
+
+def synthetic_rewards(n, seed, p_correct=0.5):
+    """Verifiable-reward stand-in: float32 {0, 1} per trajectory, Bernoulli(p_correct)."""
+    rng = np.random.default_rng([seed, 7])
+    return (rng.random(n) < p_correct).astype(np.float32)
