@@ -483,7 +483,10 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(
 }
 
 // Merge chunk partials: one wavefront per (row, q head); rows with a single
-// chunk were written directly by the attention kernel.
+// chunk were written directly by the attention kernel.  The chunk maxima and
+// denominators are reduced across lanes (lane = chunk), then each lane
+// accumulates its output dims over the chunks, taking each chunk's weight
+// exp(m_c - M) from the lane that computed it.
 template <typename OUT>
 __global__ void attn_combine_kernel(CtxSpec cs, int n_rows, int hq, int hd, int chunk_tokens,
                                     int uniform_nch, const int32_t* __restrict__ chunk_off,
@@ -497,21 +500,36 @@ __global__ void attn_combine_kernel(CtxSpec cs, int n_rows, int hq, int hd, int 
   if (nch <= 1) return;
   // equal contexts (no work list): row r's chunks are partial sets r*nch ..
   const int c0 = uniform_nch > 0 ? row * uniform_nch : chunk_off[row];
+  const float2* ml = ws_ml + (int64_t)c0 * hq + qh;          // chunk c at ml[c * hq]
   float M = -INFINITY;
-  for (int c = 0; c < nch; ++c) M = fmaxf(M, ws_ml[(int64_t)(c0 + c) * hq + qh].x);
+  for (int c = lane; c < nch; c += 64) M = fmaxf(M, ml[(int64_t)c * hq].x);
+  M = wave_max(M);
   float L = 0.f;
-  for (int c = 0; c < nch; ++c) {
-    const float2 ml = ws_ml[(int64_t)(c0 + c) * hq + qh];
-    L += ml.y * __expf(ml.x - M);
+  for (int c = lane; c < nch; c += 64) {
+    const float2 v = ml[(int64_t)c * hq];
+    L += v.y * __expf(v.x - M);
   }
+  L = wave_sum(L);
   const float invL = 1.0f / L;
-  for (int d = lane; d < hd; d += 64) {
-    float acc = 0.f;
-    for (int c = 0; c < nch; ++c) {
-      const float2 ml = ws_ml[(int64_t)(c0 + c) * hq + qh];
-      acc += ws_o[((int64_t)(c0 + c) * hq + qh) * hd + d] * __expf(ml.x - M);
+  const int nd = (hd + 63) / 64;                             // output dims per lane: lane + 64 t
+  float acc[2] = {0.f, 0.f};
+  const float* ob = ws_o + ((int64_t)c0 * hq + qh) * hd + lane;   // chunk c at ob[c * hq * hd]
+  const int64_t cstride = (int64_t)hq * hd;
+  for (int base = 0; base < nch; base += 64) {
+    const int nb = min(64, nch - base);
+    const float w = lane < nb ? __expf(ml[(int64_t)(base + lane) * hq].x - M) : 0.f;
+#pragma unroll 4
+    for (int j = 0; j < nb; ++j) {
+      const float wj = __shfl(w, j, 64);
+      const float* o = ob + (base + j) * cstride;
+      if (lane < hd) acc[0] += wj * o[0];
+      if (nd > 1) acc[1] += wj * o[64];
     }
-    const float v = acc * invL;
+  }
+  for (int t = 0; t < nd; ++t) {
+    const int d = lane + 64 * t;
+    if (d >= hd) break;
+    const float v = acc[t] * invL;
     if constexpr (sizeof(OUT) == 2) out[((int64_t)row * hq + qh) * hd + d] = f32_to_bf16(v);
     else out[((int64_t)row * hq + qh) * hd + d] = v;
   }
