@@ -12,7 +12,7 @@
 //    share operand tiles in that XCD's L2.  Configs: 128x128 with 2 stages
 //    (64 KB, two blocks per CU: one block's barrier wait is covered by the
 //    other), 128x128 with 4 stages (one block per CU, deepest prefetch: for
-//    weight streaming over very wide N), 256x128 and 256x256 with 8
+//    weight streaming over very wide N), 256x128, 256x192 and 256x256 with 8
 //    wavefronts (half the operand bytes per flop: large M).
 //  * skinny (M <= 32 with small W): no LDS for operands; each wavefront loads
 //    W and A fragments straight into MFMA operand registers, 8 wavefronts of a
@@ -414,7 +414,7 @@ __global__ void gemm_f32_swiglu_kernel(const float* __restrict__ A, int lda, con
 // ------------------------------------------------------------ dispatch
 struct Plan {
   int kind;        // 0 skinny; tiled: 1 = 128x128 4 stages, 2 = 128x128 2 stages,
-                   // 3 = 256x128 8 waves, 4 = 256x256 8 waves
+                   // 3 = 256x128 8 waves, 4 = 256x256 8 waves, 5 = 256x192 8 waves
   int mt, nt, S;   // tiles and K splits
   int MT, NS;      // skinny shape
 };
@@ -435,11 +435,15 @@ struct TileCfg {
   int kind, bm, bn, occ;
   double rate, bw;
 };
-static const TileCfg kTileCfgs[4] = {
+// The 256x192 tile (4 x 2 wavefronts of 64 x 96) fills all 256 CUs at
+// M in (256, 512] for the gate/up projection of the 8B shape (N = 128 * 192);
+// its rate is the 256x256 tile's scaled by their measured cache-cold ratio.
+static const TileCfg kTileCfgs[5] = {
     {1, 128, 128, 1, 3.38, 6425.0},
     {2, 128, 128, 2, 2.26, 6423.0},
     {3, 256, 128, 1, 4.89, 6325.0},
     {4, 256, 256, 1, 6.68, 6298.0},
+    {5, 256, 192, 1, 5.84, 6298.0},
 };
 static constexpr double kOcc2Gain = 1.76;   // CU throughput with two co-resident blocks / one block
 static constexpr double kLaunchUs = 0.16;
@@ -610,7 +614,8 @@ static hipError_t gemm_bf16_launch(const void* A, int lda, const void* W, int ld
       case 1: dma_go<EPI, 128, 128, 64, 2, 2, 4>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
       case 2: dma_go<EPI, 128, 128, 64, 2, 2, 2>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
       case 3: dma_go<EPI, 256, 128, 64, 4, 2, 3>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
-      default: dma_go<EPI, 256, 256, 64, 2, 4, 2>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+      case 4: dma_go<EPI, 256, 256, 64, 2, 4, 2>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
+      default: dma_go<EPI, 256, 192, 64, 4, 2, 2>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
     }
   }
   hipError_t e = hipGetLastError();
