@@ -14,11 +14,28 @@ __global__ void embed_kernel(const void* __restrict__ table, const int32_t* __re
   const int src = rows_traj ? rows_traj[r] : r;
   int tok = tokens[src];
   tok = tok < 0 ? 0 : (tok >= vocab ? vocab - 1 : tok);
+  float* xr = x + (int64_t)r * d;
+  if (BF16 && (d & 7) == 0) {
+    // 8 bf16 (16 bytes) per thread and step
+    const uint4* er = (const uint4*)((const bf16_t*)table + (int64_t)tok * d);
+    for (int c = threadIdx.x; c < d / 8; c += blockDim.x) {
+      const uint4 w = er[c];
+      const uint32_t q[4] = {w.x, w.y, w.z, w.w};
+      float4 lo, hi;
+      lo.x = __uint_as_float(q[0] << 16); lo.y = __uint_as_float(q[0] & 0xffff0000u);
+      lo.z = __uint_as_float(q[1] << 16); lo.w = __uint_as_float(q[1] & 0xffff0000u);
+      hi.x = __uint_as_float(q[2] << 16); hi.y = __uint_as_float(q[2] & 0xffff0000u);
+      hi.z = __uint_as_float(q[3] << 16); hi.w = __uint_as_float(q[3] & 0xffff0000u);
+      *(float4*)(xr + 8 * c) = lo;
+      *(float4*)(xr + 8 * c + 4) = hi;
+    }
+    return;
+  }
   for (int c = threadIdx.x; c < d; c += blockDim.x) {
     float v;
     if (BF16) v = bf16_to_f32(((const bf16_t*)table)[(int64_t)tok * d + c]);
     else v = ((const float*)table)[(int64_t)tok * d + c];
-    x[(int64_t)r * d + c] = v;
+    xr[c] = v;
   }
 }
 
@@ -35,24 +52,58 @@ hipError_t launch_embed_v(const void* table, bool bf16, const int32_t* tokens,
   return hipGetLastError();
 }
 
-// out[r] = x[r] / sqrt(mean(x[r]^2) + eps), one block of 256 per row
+// out[r] = x[r] / sqrt(mean(x[r]^2) + eps), one block of 256 per row.  Rows
+// with d % 4 == 0 and d <= 4096 are read once as float4 and kept in registers
+// between the sum of squares and the scaled store.
+constexpr int kRmsVec = 4;                      // float4 per thread: d <= 256 * 4 * 4
 template <bool BF16>
 __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ x, int d, float eps,
                                                       void* __restrict__ out) {
   __shared__ float red[4];
-  const int r = blockIdx.x;
+  const int r = blockIdx.x, tid = threadIdx.x;
   const float* xr = x + (int64_t)r * d;
+  const bool vec = (d & 3) == 0 && d <= 256 * 4 * kRmsVec;
+  float4 v[kRmsVec];
   float ss = 0.f;
-  for (int c = threadIdx.x; c < d; c += 256) ss = fmaf(xr[c], xr[c], ss);
+  if (vec) {
+#pragma unroll
+    for (int j = 0; j < kRmsVec; ++j) {
+      const int c = (tid + 256 * j) * 4;
+      v[j] = c < d ? *(const float4*)(xr + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+      ss = fmaf(v[j].x, v[j].x, ss);
+      ss = fmaf(v[j].y, v[j].y, ss);
+      ss = fmaf(v[j].z, v[j].z, ss);
+      ss = fmaf(v[j].w, v[j].w, ss);
+    }
+  } else {
+    for (int c = tid; c < d; c += 256) ss = fmaf(xr[c], xr[c], ss);
+  }
   ss = wave_sum(ss);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
   __syncthreads();
   const float tot = red[0] + red[1] + red[2] + red[3];
   const float inv = 1.0f / sqrtf(tot / (float)d + eps);
-  for (int c = threadIdx.x; c < d; c += 256) {
-    const float v = xr[c] * inv;
-    if (BF16) ((bf16_t*)out)[(int64_t)r * d + c] = f32_to_bf16(v);
-    else ((float*)out)[(int64_t)r * d + c] = v;
+  if (vec) {
+#pragma unroll
+    for (int j = 0; j < kRmsVec; ++j) {
+      const int c = (tid + 256 * j) * 4;
+      if (c >= d) break;
+      const float4 o = make_float4(v[j].x * inv, v[j].y * inv, v[j].z * inv, v[j].w * inv);
+      if (BF16) {
+        uint2 p;
+        p.x = (uint32_t)f32_to_bf16(o.x) | ((uint32_t)f32_to_bf16(o.y) << 16);
+        p.y = (uint32_t)f32_to_bf16(o.z) | ((uint32_t)f32_to_bf16(o.w) << 16);
+        *(uint2*)((bf16_t*)out + (int64_t)r * d + c) = p;
+      } else {
+        *(float4*)((float*)out + (int64_t)r * d + c) = o;
+      }
+    }
+  } else {
+    for (int c = tid; c < d; c += 256) {
+      const float o = xr[c] * inv;
+      if (BF16) ((bf16_t*)out)[(int64_t)r * d + c] = f32_to_bf16(o);
+      else ((float*)out)[(int64_t)r * d + c] = o;
+    }
   }
 }
 
@@ -87,33 +138,45 @@ __global__ void rope_append_kernel(const float* __restrict__ qkv, int hq, int hk
   const int width = (hq + 2 * hkv) * hd;
   const float* src = qkv + (int64_t)r * width;
   const float2* cs = rope + (int64_t)pos * half;
-  // rotated heads: hq query heads then hkv key heads
-  for (int t = threadIdx.x; t < (hq + hkv) * half; t += blockDim.x) {
-    const int h = t / half, i = t % half;
+  // rotated heads: hq query heads then hkv key heads; four consecutive
+  // rotation pairs (i .. i+3 with partners i+half ..) per thread
+  const int q4 = half / 4;
+  for (int t = threadIdx.x; t < (hq + hkv) * q4; t += blockDim.x) {
+    const int h = t / q4, i = (t % q4) * 4;
     const float* v = src + h * hd;
-    const float a = v[i], b = v[i + half];
-    const float2 c = cs[i];
-    const float o1 = a * c.x - b * c.y;
-    const float o2 = b * c.x + a * c.y;
+    const float4 a = *(const float4*)(v + i), b = *(const float4*)(v + i + half);
+    const float4 c01 = *(const float4*)(cs + i), c23 = *(const float4*)(cs + i + 2);
+    const float ca[4] = {c01.x, c01.z, c23.x, c23.z}, sa[4] = {c01.y, c01.w, c23.y, c23.w};
+    const float av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
+    float o1[4], o2[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      o1[e] = av[e] * ca[e] - bv[e] * sa[e];
+      o2[e] = bv[e] * ca[e] + av[e] * sa[e];
+    }
+    int64_t oa, ob;
+    void* dst;
     if (h < hq) {
-      const int64_t base = ((int64_t)r * hq + h) * hd;
-      if (BF16) {
-        ((bf16_t*)q_out)[base + i] = f32_to_bf16(o1);
-        ((bf16_t*)q_out)[base + i + half] = f32_to_bf16(o2);
-      } else {
-        ((float*)q_out)[base + i] = o1;
-        ((float*)q_out)[base + i + half] = o2;
-      }
+      oa = ((int64_t)r * hq + h) * hd + i;
+      ob = oa + half;
+      dst = q_out;
     } else {
       const int kh = h - hq;
-      const int64_t o_a = k_off(page, kh, slot, i, hkv, hd), o_b = k_off(page, kh, slot, i + half, hkv, hd);
-      if (BF16) {
-        ((bf16_t*)k_pool)[o_a] = f32_to_bf16(o1);
-        ((bf16_t*)k_pool)[o_b] = f32_to_bf16(o2);
-      } else {
-        ((float*)k_pool)[o_a] = o1;
-        ((float*)k_pool)[o_b] = o2;
-      }
+      oa = k_off(page, kh, slot, i, hkv, hd);
+      ob = k_off(page, kh, slot, i + half, hkv, hd);
+      dst = k_pool;
+    }
+    if (BF16) {
+      uint2 p1, p2;
+      p1.x = (uint32_t)f32_to_bf16(o1[0]) | ((uint32_t)f32_to_bf16(o1[1]) << 16);
+      p1.y = (uint32_t)f32_to_bf16(o1[2]) | ((uint32_t)f32_to_bf16(o1[3]) << 16);
+      p2.x = (uint32_t)f32_to_bf16(o2[0]) | ((uint32_t)f32_to_bf16(o2[1]) << 16);
+      p2.y = (uint32_t)f32_to_bf16(o2[2]) | ((uint32_t)f32_to_bf16(o2[3]) << 16);
+      *(uint2*)((bf16_t*)dst + oa) = p1;
+      *(uint2*)((bf16_t*)dst + ob) = p2;
+    } else {
+      *(float4*)((float*)dst + oa) = make_float4(o1[0], o1[1], o1[2], o1[3]);
+      *(float4*)((float*)dst + ob) = make_float4(o2[0], o2[1], o2[2], o2[3]);
     }
   }
   for (int t = threadIdx.x; t < hkv * hd; t += blockDim.x) {

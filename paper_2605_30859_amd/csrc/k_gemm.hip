@@ -346,24 +346,46 @@ __global__ void __launch_bounds__(512) gemm_skinny_kernel(const bf16_t* __restri
 template <int EPI>
 __global__ void splitk_reduce_kernel(const float* __restrict__ ws, int S, int M, int N, void* C,
                                      int ldc) {
-  const int64_t nout = (EPI == EPI_SWIGLU) ? (int64_t)M * (N / 2) : (int64_t)M * N;
-  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < nout;
+  // four consecutive output columns per thread (N % 128 == 0 and, for SwiGLU,
+  // four consecutive hidden columns stay inside one 16-column gate/up group)
+  const int64_t ncol = (EPI == EPI_SWIGLU) ? N / 2 : N;
+  const int64_t nout4 = (int64_t)M * ncol / 4;
+  const int64_t zs = (int64_t)M * N;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < nout4;
        t += (int64_t)gridDim.x * blockDim.x) {
+    const int m = (int)(t / (ncol / 4));
+    const int c = (int)(t % (ncol / 4)) * 4;
     if constexpr (EPI == EPI_SWIGLU) {
-      const int F = N / 2;
-      const int m = (int)(t / F), c = (int)(t % F);
       const int pg = (c >> 4) * 32 + (c & 15), pu = pg + 16;
-      float g = 0.f, u = 0.f;
+      float4 g = make_float4(0.f, 0.f, 0.f, 0.f), u = g;
       for (int z = 0; z < S; ++z) {
-        g += ws[((int64_t)z * M + m) * N + pg];
-        u += ws[((int64_t)z * M + m) * N + pu];
+        const float4 a = *(const float4*)(ws + z * zs + (int64_t)m * N + pg);
+        const float4 b = *(const float4*)(ws + z * zs + (int64_t)m * N + pu);
+        g.x += a.x; g.y += a.y; g.z += a.z; g.w += a.w;
+        u.x += b.x; u.y += b.y; u.z += b.z; u.w += b.w;
       }
-      ((bf16_t*)C)[(int64_t)m * ldc + c] = f32_to_bf16(silu_f(g) * u);
+      uint2 p;
+      p.x = (uint32_t)f32_to_bf16(silu_f(g.x) * u.x) | ((uint32_t)f32_to_bf16(silu_f(g.y) * u.y) << 16);
+      p.y = (uint32_t)f32_to_bf16(silu_f(g.z) * u.z) | ((uint32_t)f32_to_bf16(silu_f(g.w) * u.w) << 16);
+      *(uint2*)((bf16_t*)C + (int64_t)m * ldc + c) = p;
     } else {
-      const int m = (int)(t / N), n = (int)(t % N);
-      float s = 0.f;
-      for (int z = 0; z < S; ++z) s += ws[((int64_t)z * M + m) * N + n];
-      epi_store<EPI>(C, ldc, M, m, n, s);
+      float4 s4 = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int z = 0; z < S; ++z) {
+        const float4 a = *(const float4*)(ws + z * zs + (int64_t)m * N + c);
+        s4.x += a.x; s4.y += a.y; s4.z += a.z; s4.w += a.w;
+      }
+      if constexpr (EPI == EPI_F32) {
+        *(float4*)((float*)C + (int64_t)m * ldc + c) = s4;
+      } else if constexpr (EPI == EPI_ADD_F32) {
+        float4* o = (float4*)((float*)C + (int64_t)m * ldc + c);
+        const float4 x = *o;
+        *o = make_float4(x.x + s4.x, x.y + s4.y, x.z + s4.z, x.w + s4.w);
+      } else {
+        uint2 p;
+        p.x = (uint32_t)f32_to_bf16(s4.x) | ((uint32_t)f32_to_bf16(s4.y) << 16);
+        p.y = (uint32_t)f32_to_bf16(s4.z) | ((uint32_t)f32_to_bf16(s4.w) << 16);
+        *(uint2*)((bf16_t*)C + (int64_t)m * ldc + c) = p;
+      }
     }
   }
 }
@@ -506,7 +528,7 @@ size_t gemm_workspace_bytes(int M, int N, int K) {
 template <int EPI>
 static hipError_t reduce_launch(const void* ws, int S, int M, int N, void* C, int ldc,
                                 hipStream_t st) {
-  const int64_t nout = (EPI == EPI_SWIGLU) ? (int64_t)M * (N / 2) : (int64_t)M * N;
+  const int64_t nout = ((EPI == EPI_SWIGLU) ? (int64_t)M * (N / 2) : (int64_t)M * N) / 4;
   int64_t blocks = (nout + 255) / 256;
   if (blocks > 16384) blocks = 16384;
   hipLaunchKernelGGL(splitk_reduce_kernel<EPI>, dim3((unsigned)blocks), dim3(256), 0, st,
