@@ -608,24 +608,44 @@ static hipError_t gemm_t(darts_ctx* c, int cls, const void* A, int lda, const vo
   return e;
 }
 
-// Decoder layers over n rows whose residual stream is in c->x.
+// x += A . W^T (residual projection), then xn = RMSNorm(x) when the two can
+// be fused (bf16 dense models with a split-K plan): *normed reports it.
+static hipError_t gemm_add_t(darts_ctx* c, int cls, const void* A, int lda, const void* W, int ldw,
+                             int M, int K, bool* normed) {
+  const int ti = tbegin(c, 1 + cls, 2.0 * M * c->d * K);
+  hipError_t e;
+  if (c->bf16) {
+    e = launch_gemm_add_norm(A, lda, W, ldw, c->x, c->d, M, c->d, K, c->gemm_ws, c->gemm_ws_bytes,
+                             c->mc.rms_eps, c->xn, c->st, normed);
+  } else {
+    *normed = false;
+    e = launch_gemm(false, A, lda, W, ldw, c->x, c->d, M, c->d, K, EPI_ADD_F32, c->gemm_ws,
+                    c->gemm_ws_bytes, c->st);
+  }
+  tend(c, ti);
+  return e;
+}
+
+// Decoder layers over n rows whose residual stream is in c->x.  normed: c->xn
+// already holds RMSNorm(x) on entry; on return, whether it holds the final
+// residual's norm.
 static int run_layers(darts_ctx* c, int n, const int32_t* row_pt, int pos_mod, int pos_base,
-                      int ctx_mod, int ctx_base, int max_ctx) {
+                      int ctx_mod, int ctx_base, int max_ctx, bool* normed) {
   const bool b = c->bf16;
   const int d = c->d, hqd = c->hq * c->hd;
   for (int l = 0; l < c->nl; ++l) {
     LayerW& w = c->layers[l];
     void* kp = (char*)c->kpool + (size_t)l * c->pool_layer_elems * c->esz;
     void* vp = (char*)c->vpool + (size_t)l * c->pool_layer_elems * c->esz;
-    HIPCHK(c, launch_rmsnorm(c->x, n, d, c->mc.rms_eps, c->xn, b, c->st));
+    if (!*normed) HIPCHK(c, launch_rmsnorm(c->x, n, d, c->mc.rms_eps, c->xn, b, c->st));
     HIPCHK(c, gemm_t(c, G_QKV, c->xn, d, w.wqkv, d, c->qkv, c->qkv_w, n, c->qkv_w, d, EPI_F32));
     HIPCHK(c, launch_rope_append2(c->qkv, n, c->hq, c->hkv, c->hd, row_pt, pos_mod, pos_base,
                                   c->page_table, c->max_pages, c->n_pages, c->rope, c->q, kp, vp, b,
                                   c->st));
     int r = run_attention(c, l, n, row_pt, ctx_mod, ctx_base, max_ctx);
     if (r != DARTS_OK) return r;
-    HIPCHK(c, gemm_t(c, G_O, c->attn, hqd, w.wo, hqd, c->x, d, n, d, hqd, EPI_ADD_F32));
-    HIPCHK(c, launch_rmsnorm(c->x, n, d, c->mc.rms_eps, c->xn, b, c->st));
+    HIPCHK(c, gemm_add_t(c, G_O, c->attn, hqd, w.wo, hqd, n, hqd, normed));
+    if (!*normed) HIPCHK(c, launch_rmsnorm(c->x, n, d, c->mc.rms_eps, c->xn, b, c->st));
     if (c->moe) {
       MoeArgs m;
       m.xn = (const bf16_t*)c->xn; m.x = c->x; m.n_rows = n; m.d = d; m.E = c->E; m.k = c->topk;
@@ -641,10 +661,11 @@ static int run_layers(darts_ctx* c, int n, const int32_t* row_pt, int pos_mod, i
       const int ti = tbegin(c, 1 + G_MOE, flop);
       HIPCHK(c, launch_moe_ffn(m, c->st));
       tend(c, ti);
+      *normed = false;
       continue;
     }
     HIPCHK(c, gemm_t(c, G_GU, c->xn, d, w.wgu, d, c->hbuf, c->F, n, 2 * c->F, d, EPI_SWIGLU));
-    HIPCHK(c, gemm_t(c, G_DOWN, c->hbuf, c->F, w.wdown, c->F, c->x, d, n, d, c->F, EPI_ADD_F32));
+    HIPCHK(c, gemm_add_t(c, G_DOWN, c->hbuf, c->F, w.wdown, c->F, n, c->F, normed));
   }
   return DARTS_OK;
 }
@@ -672,8 +693,11 @@ int darts_prefill(darts_ctx* c, const int32_t* d_prompts, const int32_t* d_force
                            hipMemcpyDeviceToDevice, c->st));
   HIPCHK(c, launch_prefill_pages(c->P, c->m, c->grp_m, c->pp, c->page_table, c->max_pages,
                                  c->free_stack, c->dcnt, c->refcnt, c->st));
-  HIPCHK(c, launch_embed_v(c->embed, b, d_prompts, nullptr, rows, c->d, c->V, c->x, c->st));
-  int r = run_layers(c, rows, c->prefill_pt, c->Lp, 0, c->Lp, 1, c->Lp);
+  bool normed = b;
+  if (b) HIPCHK(c, launch_embed_norm(c->embed, d_prompts, nullptr, rows, c->d, c->V, c->mc.rms_eps,
+                                     c->x, c->xn, c->st));
+  else HIPCHK(c, launch_embed_v(c->embed, b, d_prompts, nullptr, rows, c->d, c->V, c->x, c->st));
+  int r = run_layers(c, rows, c->prefill_pt, c->Lp, 0, c->Lp, 1, c->Lp, &normed);
   if (r != DARTS_OK) return r;
   HIPCHK(c, launch_gather_rows(c->x, c->last_rows, c->P, c->d, c->xlast, c->st));
   HIPCHK(c, launch_rmsnorm(c->xlast, c->P, c->d, c->mc.rms_eps, c->xn, b, c->st));
@@ -721,10 +745,13 @@ int darts_decode_step(darts_ctx* c, const int32_t* d_force_tokens, darts_step_ou
     c->free_top -= n;
     c->hwm = std::max<int64_t>(c->hwm, c->n_pages - c->free_top);
   }
-  HIPCHK(c, launch_embed_v(c->embed, b, c->last_tok, live, n, c->d, c->V, c->x, c->st));
-  int r = run_layers(c, n, live, 0, pos, 0, pos + 1, pos + 1);
+  bool normed = b;
+  if (b) HIPCHK(c, launch_embed_norm(c->embed, c->last_tok, live, n, c->d, c->V, c->mc.rms_eps, c->x,
+                                     c->xn, c->st));
+  else HIPCHK(c, launch_embed_v(c->embed, b, c->last_tok, live, n, c->d, c->V, c->x, c->st));
+  int r = run_layers(c, n, live, 0, pos, 0, pos + 1, pos + 1, &normed);
   if (r != DARTS_OK) return r;
-  HIPCHK(c, launch_rmsnorm(c->x, n, c->d, c->mc.rms_eps, c->xn, b, c->st));
+  if (!normed) HIPCHK(c, launch_rmsnorm(c->x, n, c->d, c->mc.rms_eps, c->xn, b, c->st));
   HIPCHK(c, gemm_t(c, G_LM, c->xn, c->d, c->lm_head, c->d, c->logits, c->V, n, c->V, c->d, EPI_F32));
   SampleArgs a{};
   a.logits = c->logits; a.n_rows = n; a.vocab = c->V; a.bf16 = false;

@@ -515,15 +515,27 @@ __global__ void attn_combine_kernel(CtxSpec cs, int n_rows, int hq, int hd, int 
   float acc[2] = {0.f, 0.f};
   const float* ob = ws_o + ((int64_t)c0 * hq + qh) * hd + lane;   // chunk c at ob[c * hq * hd]
   const int64_t cstride = (int64_t)hq * hd;
+  // batches of up to kCB chunks: every partial of the batch is loaded before
+  // any is accumulated, so a lane keeps 2 * kCB loads in flight
+  constexpr int kCB = 16;
   for (int base = 0; base < nch; base += 64) {
     const int nb = min(64, nch - base);
     const float w = lane < nb ? __expf(ml[(int64_t)(base + lane) * hq].x - M) : 0.f;
-#pragma unroll 4
-    for (int j = 0; j < nb; ++j) {
-      const float wj = __shfl(w, j, 64);
-      const float* o = ob + (base + j) * cstride;
-      if (lane < hd) acc[0] += wj * o[0];
-      if (nd > 1) acc[1] += wj * o[64];
+    for (int j0 = 0; j0 < nb; j0 += kCB) {
+      float o0[kCB], o1[kCB];
+#pragma unroll
+      for (int j = 0; j < kCB; ++j) {
+        const float* o = ob + (int64_t)(base + j0 + j) * cstride;
+        const bool ok = j0 + j < nb;
+        o0[j] = (ok && lane < hd) ? o[0] : 0.f;
+        o1[j] = (ok && nd > 1) ? o[64] : 0.f;
+      }
+#pragma unroll
+      for (int j = 0; j < kCB; ++j) {
+        const float wj = __shfl(w, (j0 + j) & 63, 64);
+        acc[0] += wj * o0[j];
+        acc[1] += wj * o1[j];
+      }
     }
   }
   for (int t = 0; t < nd; ++t) {

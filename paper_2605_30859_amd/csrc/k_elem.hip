@@ -52,6 +52,58 @@ hipError_t launch_embed_v(const void* table, bool bf16, const int32_t* tokens,
   return hipGetLastError();
 }
 
+// Embedding gather fused with the first RMSNorm (bf16 tables, d % 8 == 0,
+// d <= 4096): x[r] = E[tok] (fp32), xn[r] = bf16(x[r] / sqrt(mean(x^2) + eps)).
+constexpr int kEmbVec = 2;                      // 8 bf16 per step, d <= 256 * 8 * 2
+__global__ void __launch_bounds__(256) embed_norm_kernel(const bf16_t* __restrict__ table,
+                                                         const int32_t* __restrict__ tokens,
+                                                         const int32_t* __restrict__ rows_traj,
+                                                         int d, int vocab, float eps,
+                                                         float* __restrict__ x,
+                                                         bf16_t* __restrict__ xn) {
+  __shared__ float red[4];
+  const int r = blockIdx.x, tid = threadIdx.x;
+  const int src = rows_traj ? rows_traj[r] : r;
+  int tok = tokens[src];
+  tok = tok < 0 ? 0 : (tok >= vocab ? vocab - 1 : tok);
+  const uint4* er = (const uint4*)(table + (int64_t)tok * d);
+  float* xr = x + (int64_t)r * d;
+  float v[kEmbVec][8];
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < kEmbVec; ++j) {
+    const int c = tid + 256 * j;
+    uint4 w = c < d / 8 ? er[c] : make_uint4(0u, 0u, 0u, 0u);
+    const uint32_t q[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[j][2 * e] = __uint_as_float(q[e] << 16);
+      v[j][2 * e + 1] = __uint_as_float(q[e] & 0xffff0000u);
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss = fmaf(v[j][e], v[j][e], ss);
+    if (c < d / 8) {
+      *(float4*)(xr + 8 * c) = make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
+      *(float4*)(xr + 8 * c + 4) = make_float4(v[j][4], v[j][5], v[j][6], v[j][7]);
+    }
+  }
+  ss = wave_sum(ss);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  const float inv = 1.0f / sqrtf((red[0] + red[1] + red[2] + red[3]) / (float)d + eps);
+#pragma unroll
+  for (int j = 0; j < kEmbVec; ++j) {
+    const int c = tid + 256 * j;
+    if (c >= d / 8) break;
+    uint4 p;
+    p.x = (uint32_t)f32_to_bf16(v[j][0] * inv) | ((uint32_t)f32_to_bf16(v[j][1] * inv) << 16);
+    p.y = (uint32_t)f32_to_bf16(v[j][2] * inv) | ((uint32_t)f32_to_bf16(v[j][3] * inv) << 16);
+    p.z = (uint32_t)f32_to_bf16(v[j][4] * inv) | ((uint32_t)f32_to_bf16(v[j][5] * inv) << 16);
+    p.w = (uint32_t)f32_to_bf16(v[j][6] * inv) | ((uint32_t)f32_to_bf16(v[j][7] * inv) << 16);
+    *(uint4*)(xn + (int64_t)r * d + 8 * c) = p;
+  }
+}
+
 // out[r] = x[r] / sqrt(mean(x[r]^2) + eps), one block of 256 per row.  Rows
 // with d % 4 == 0 and d <= 4096 are read once as float4 and kept in registers
 // between the sum of squares and the scaled store.
@@ -105,6 +157,19 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ 
       else ((float*)out)[(int64_t)r * d + c] = o;
     }
   }
+}
+
+hipError_t launch_embed_norm(const void* table, const int32_t* tokens, const int32_t* rows_traj,
+                             int n_rows, int d, int vocab, float eps, float* x, void* xn,
+                             hipStream_t st) {
+  if (n_rows <= 0) return hipSuccess;
+  if (d % 8 != 0 || d > 256 * 8 * kEmbVec) {
+    hipError_t e = launch_embed_v(table, true, tokens, rows_traj, n_rows, d, vocab, x, st);
+    return e != hipSuccess ? e : launch_rmsnorm(x, n_rows, d, eps, xn, true, st);
+  }
+  hipLaunchKernelGGL(embed_norm_kernel, dim3(n_rows), dim3(256), 0, st, (const bf16_t*)table, tokens,
+                     rows_traj, d, vocab, eps, x, (bf16_t*)xn);
+  return hipGetLastError();
 }
 
 hipError_t launch_rmsnorm(const float* x, int n_rows, int d, float eps, void* out, bool bf16,

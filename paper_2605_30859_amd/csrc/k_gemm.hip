@@ -390,6 +390,53 @@ __global__ void splitk_reduce_kernel(const float* __restrict__ ws, int S, int M,
   }
 }
 
+// Split-K reduce fused with the residual add and the next RMSNorm: one block
+// of 1024 threads per row, one float4 of the row per thread (N % 4 == 0,
+// N <= 4096); x[m] += sum_z ws[z][m] in z order (all S partial loads issued
+// together), then xn[m] = bf16(x[m] / sqrt(mean(x[m]^2) + eps)).
+constexpr int kAddNormMaxN = 4096;
+constexpr int kMaxSplits = 8;
+__global__ void __launch_bounds__(1024) splitk_add_norm_kernel(const float* __restrict__ ws, int S,
+                                                               int M, int N, float* __restrict__ x,
+                                                               int ldx, float eps,
+                                                               bf16_t* __restrict__ xn) {
+  __shared__ float red[16];
+  const int m = blockIdx.x, tid = threadIdx.x;
+  const int64_t zs = (int64_t)M * N;
+  const int c = tid * 4;
+  const bool act = c < N;
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (act) {
+    float4 p[kMaxSplits];
+#pragma unroll
+    for (int z = 0; z < kMaxSplits; ++z)
+      p[z] = z < S ? *(const float4*)(ws + z * zs + (int64_t)m * N + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+    a = *(const float4*)(x + (int64_t)m * ldx + c);
+#pragma unroll
+    for (int z = 0; z < kMaxSplits; ++z) {
+      a.x += p[z].x; a.y += p[z].y; a.z += p[z].z; a.w += p[z].w;
+    }
+    *(float4*)(x + (int64_t)m * ldx + c) = a;
+  }
+  float ss = a.x * a.x;
+  ss = fmaf(a.y, a.y, ss);
+  ss = fmaf(a.z, a.z, ss);
+  ss = fmaf(a.w, a.w, ss);
+  ss = wave_sum(ss);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < 16; ++w) tot += red[w];
+  const float inv = 1.0f / sqrtf(tot / (float)N + eps);
+  if (act) {
+    uint2 q;
+    q.x = (uint32_t)f32_to_bf16(a.x * inv) | ((uint32_t)f32_to_bf16(a.y * inv) << 16);
+    q.y = (uint32_t)f32_to_bf16(a.z * inv) | ((uint32_t)f32_to_bf16(a.w * inv) << 16);
+    *(uint2*)(xn + (int64_t)m * N + c) = q;
+  }
+}
+
 // fp32 GEMM (fp32 models): 16x16 output tile per block, K in steps of 16.
 template <int EPI>
 __global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__ A, int lda,
@@ -609,12 +656,10 @@ hipError_t launch_gemm_grouped(const void* A, int lda, const void* W, int64_t w_
   }
 }
 
+// Launch the GEMM kernel of plan p (partial sums into ws when p.S > 1).
 template <int EPI>
-static hipError_t gemm_bf16_launch(const void* A, int lda, const void* W, int ldw, void* C, int ldc,
-                                   int M, int N, int K, void* ws, size_t ws_bytes, hipStream_t st) {
-  Plan p = plan_gemm(M, N, K);
-  if (p.S > 1 && (ws == nullptr || ws_bytes < (size_t)p.S * M * N * sizeof(float)))
-    return hipErrorInvalidValue;
+static hipError_t launch_plan(const Plan& p, const void* A, int lda, const void* W, int ldw, void* C,
+                              int ldc, int M, int N, int K, void* ws, hipStream_t st) {
   if (p.kind == 0) {
     if (p.NS == 2) {
       switch (p.MT) {
@@ -640,7 +685,16 @@ static hipError_t gemm_bf16_launch(const void* A, int lda, const void* W, int ld
       default: dma_go<EPI, 256, 192, 64, 4, 2, 2>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st); break;
     }
   }
-  hipError_t e = hipGetLastError();
+  return hipGetLastError();
+}
+
+template <int EPI>
+static hipError_t gemm_bf16_launch(const void* A, int lda, const void* W, int ldw, void* C, int ldc,
+                                   int M, int N, int K, void* ws, size_t ws_bytes, hipStream_t st) {
+  const Plan p = plan_gemm(M, N, K);
+  if (p.S > 1 && (ws == nullptr || ws_bytes < (size_t)p.S * M * N * sizeof(float)))
+    return hipErrorInvalidValue;
+  hipError_t e = launch_plan<EPI>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st);
   if (e != hipSuccess || p.S == 1) return e;
   return reduce_launch<EPI>(ws, p.S, M, N, C, ldc, st);
 }
@@ -685,6 +739,28 @@ hipError_t launch_gemm(bool bf16, const void* A, int lda, const void* W, int ldw
       return gemm_bf16_launch<EPI_SWIGLU>(A, lda, W, ldw, C, ldc, M, N, K, ws, ws_bytes, st);
   }
   return hipErrorInvalidValue;
+}
+
+// x[M, N] += A . W^T followed by xn = bf16(RMSNorm(x)).  When the plan splits
+// K the add and the norm are fused into the reduce (returns *fused = true);
+// otherwise the GEMM adds in its epilogue and the caller normalises.
+hipError_t launch_gemm_add_norm(const void* A, int lda, const void* W, int ldw, float* x, int ldx,
+                                int M, int N, int K, void* ws, size_t ws_bytes, float eps,
+                                void* xn, hipStream_t st, bool* fused) {
+  *fused = false;
+  if (M <= 0) return hipSuccess;
+  if (N % 128 != 0 || K % 256 != 0) return hipErrorInvalidValue;
+  const Plan p = plan_gemm(M, N, K);
+  if (p.S == 1 || p.S > kMaxSplits || N > kAddNormMaxN)
+    return gemm_bf16_launch<EPI_ADD_F32>(A, lda, W, ldw, x, ldx, M, N, K, ws, ws_bytes, st);
+  if (ws == nullptr || ws_bytes < (size_t)p.S * M * N * sizeof(float)) return hipErrorInvalidValue;
+  // the partial-sum GEMM of the plan, then the fused reduce
+  hipError_t e = launch_plan<EPI_ADD_F32>(p, A, lda, W, ldw, x, ldx, M, N, K, ws, st);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(splitk_add_norm_kernel, dim3(M), dim3(1024), 0, st, (const float*)ws, p.S, M, N,
+                     x, ldx, eps, (bf16_t*)xn);
+  *fused = true;
+  return hipGetLastError();
 }
 
 }  // namespace darts

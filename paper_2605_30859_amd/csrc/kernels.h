@@ -28,10 +28,19 @@ hipError_t launch_iota_perm(int32_t* stack, int64_t n, uint64_t perm_seed, bool 
 // ---- GEMM (k_gemm.hip): C[M,N] (op)= A[M,K] * W[N,K]^T
 enum Epi { EPI_F32 = 0, EPI_BF16 = 1, EPI_ADD_F32 = 2, EPI_SWIGLU = 3 };
 size_t gemm_workspace_bytes(int M, int N, int K);
+// x += A . W^T and xn = bf16(RMSNorm(x)) (bf16 operands); *fused says whether
+// xn was written (split-K plans) or the caller must normalise
+hipError_t launch_gemm_add_norm(const void* A, int lda, const void* W, int ldw, float* x, int ldx,
+                                int M, int N, int K, void* ws, size_t ws_bytes, float eps,
+                                void* xn, hipStream_t st, bool* fused);
 hipError_t launch_gemm(bool bf16, const void* A, int lda, const void* W, int ldw, void* C, int ldc,
                        int M, int N, int K, int epi, void* ws, size_t ws_bytes, hipStream_t st);
 
 // ---- elementwise (k_elem.hip)
+// embedding gather; with xn != NULL (bf16 models) also xn = bf16(RMSNorm(x))
+hipError_t launch_embed_norm(const void* table, const int32_t* tokens, const int32_t* rows_traj,
+                             int n_rows, int d, int vocab, float eps, float* x, void* xn,
+                             hipStream_t st);
 hipError_t launch_embed_v(const void* table, bool bf16, const int32_t* tokens,
                           const int32_t* rows_traj, int n_rows, int d, int vocab, float* x,
                           hipStream_t st);
