@@ -72,6 +72,10 @@ typedef enum { DARTS_F32 = 0, DARTS_BF16 = 1 } darts_dtype;
                                           launch of the step to the end of its selection
                                           kernel); darts_get_step_times reports them */
 
+#define DARTS_FLAG_STREAM        0x20u /* keep every trajectory's token and log-prob history on
+                                          the device ([n_prompts*m][cap] each) for
+                                          darts_stream_chunks */
+
 /* Decoder shape.  Weights are generated on the device from weight_seed
  * (Philox uniform, variance 1/fan_in, rounded to bf16 for DARTS_BF16).
  * Dense SwiGLU when n_experts == 0, else top_k-of-n_experts MoE.            */
@@ -227,6 +231,25 @@ int darts_get_stats(const darts_ctx* ctx, darts_stats* out);
  * App. A).  DARTS_ESTATE without the flag.                                 */
 int darts_get_step_times(const darts_ctx* ctx, int32_t* h_rows, float* h_ms, int32_t cap,
                          int32_t* h_n, float* h_prefill_ms);
+
+/* Token-level streaming, producer side (Sec. 4.3.2, App. E).  Tokens generated
+ * since a trajectory's last dispatch are pending; when the pending total over
+ * all trajectories is >= threshold, or flush != 0 and anything is pending or
+ * some ended trajectory has not been marked final, every trajectory with
+ * pending tokens or an unsent final mark gets one descriptor, ascending id:
+ *   d_desc[4i .. 4i+3] = {trajectory id, first token index, token count,
+ *                         final status (1 eos, 2 truncated, 3 aborted; 0: more
+ *                         tokens will come)}
+ * and its tokens and log-probs are copied, in descriptor order, to
+ * d_tokens / d_logprobs (out_cap entries each).  Otherwise nothing is
+ * written and *h_n_desc = 0.  Kept sets come from darts_select_and_prune.
+ * d_desc holds n_prompts*m*4 int32.  Call after darts_select_and_prune; flush
+ * once every kept set is complete to deliver the rest.  Errors: DARTS_ESTATE
+ * without DARTS_FLAG_STREAM or before the prefill; DARTS_ENOMEM if the
+ * pending tokens exceed out_cap (nothing dispatched, state unchanged).       */
+int darts_stream_chunks(darts_ctx* ctx, int64_t threshold, int32_t flush, int32_t* d_desc,
+                        int32_t* d_tokens, float* d_logprobs, int64_t out_cap, int32_t* h_n_desc,
+                        int64_t* h_n_tokens);
 
 /* Start a new batch on the same context: weights, pool and buffers are
  * kept; the free list, page tables, per-trajectory and per-prompt state and

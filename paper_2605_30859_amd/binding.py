@@ -10,6 +10,7 @@ import numpy as np
 DARTS_OK, DARTS_EINVAL, DARTS_ENOMEM, DARTS_ESTATE, DARTS_EHIP = 0, 1, 2, 3, 4
 DARTS_F32, DARTS_BF16 = 0, 1
 FLAG_NO_ABORT, FLAG_PERMUTE_PAGES, FLAG_TIMING, FLAG_SHARED_PREFIX, FLAG_STEP_TIMES = 0x1, 0x2, 0x4, 0x8, 0x10
+FLAG_STREAM = 0x20
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 lib_path = os.path.join(_HERE, "libdarts.so")
@@ -72,6 +73,8 @@ _SIGS = {
     "darts_get_step_times": (C.c_int, [_P, _P, _P, C.c_int32, C.POINTER(C.c_int32), C.POINTER(C.c_float)]),
     "darts_rollout_cost": (C.c_int, [_P, C.c_int32, _P, C.POINTER(C.c_double)]),
     "darts_fit_ptl": (C.c_int, [_P, _P, C.c_int32, _P]),
+    "darts_stream_chunks": (C.c_int, [_P, C.c_int64, C.c_int32, _P, _P, _P, C.c_int64,
+                                      C.POINTER(C.c_int32), C.POINTER(C.c_int64)]),
     "darts_group_advantages": (C.c_int, [_P, C.c_int32, C.c_int32, _P, C.c_int32, C.c_float, _P, _P]),
     "darts_strerror": (C.c_char_p, [C.c_int]),
     "darts_last_error": (C.c_char_p, [_P]),
@@ -384,6 +387,28 @@ class Rollout:
         _check(self.lib.darts_get_step_times(self.ctx, _np_ptr(rows), _np_ptr(ms), n.value, C.byref(n),
                                              C.byref(pf)), self.ctx)
         return rows, ms, pf.value
+
+    def stream_chunks(self, threshold, flush=False, out_cap=None):
+        """Dispatch pending token chunks (FLAG_STREAM).  Returns None if nothing
+        was dispatched, else (descriptors [n, 4] int32, tokens, log-probs) on
+        the host; descriptor = (trajectory, start, count, final status)."""
+        t = self.torch
+        dev = self.o_tok.device
+        cap = self.n_traj * self.run.cap if out_cap is None else out_cap
+        if not hasattr(self, "_s_desc"):
+            self._s_desc = t.zeros(self.n_traj * 4, dtype=t.int32, device=dev)
+        if getattr(self, "_s_cap", -1) < cap:
+            self._s_tok = t.zeros(max(cap, 1), dtype=t.int32, device=dev)
+            self._s_lp = t.zeros(max(cap, 1), dtype=t.float32, device=dev)
+            self._s_cap = cap
+        nd, ntok = C.c_int32(), C.c_int64()
+        _check(self.lib.darts_stream_chunks(self.ctx, threshold, int(flush), _ptr(self._s_desc),
+                                            _ptr(self._s_tok), _ptr(self._s_lp), cap, C.byref(nd),
+                                            C.byref(ntok)), self.ctx)
+        if nd.value == 0:
+            return None
+        return (self._s_desc[:4 * nd.value].view(-1, 4).cpu().numpy(),
+                self._s_tok[:ntok.value].cpu().numpy(), self._s_lp[:ntok.value].cpu().numpy())
 
     def traj_scores(self):
         t = self.torch

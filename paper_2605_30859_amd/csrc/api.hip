@@ -91,6 +91,13 @@ struct darts_ctx {
   int32_t* kept = nullptr;
   int32_t* live[2] = {nullptr, nullptr};
   int32_t* grp_m = nullptr;        // [P] candidates per prompt (redundancy plan M'_i)
+  // token-chunk streaming (DARTS_FLAG_STREAM): per-trajectory token/log-prob
+  // history [n_traj][cap], tokens already dispatched, final marks sent
+  int32_t* hist_tok = nullptr;
+  float* hist_lp = nullptr;
+  int32_t* streamed = nullptr;
+  uint8_t* fin_sent = nullptr;
+  int32_t* stream_off = nullptr;
   std::vector<int32_t> plan;       // host copy of grp_m
   int n_start = 0;                 // sum of the plan: trajectories started by the prefill
   int32_t* grp_cnt = nullptr;
@@ -447,6 +454,13 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
     A(&c->m_h_perm, pairs * c->Fe * 2);
     A(&c->m_y_perm, pairs * c->d * 4);
   }
+  if (rc.flags & DARTS_FLAG_STREAM) {
+    A(&c->hist_tok, (size_t)c->n_traj * c->cap * 4);
+    A(&c->hist_lp, (size_t)c->n_traj * c->cap * 4);
+    A(&c->streamed, (size_t)c->n_traj * 4);
+    A(&c->fin_sent, (size_t)c->n_traj);
+    A(&c->stream_off, (size_t)c->n_traj * 4);
+  }
   A(&c->xlast, (size_t)c->P * c->d * 4);
   A(&c->logits, (size_t)c->n_traj * c->V * 4);
   c->gemm_ws_bytes = gemm_ws_need(c);
@@ -491,6 +505,8 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
     if (e == hipSuccess) e = hipMemsetAsync(c->gen, 0, (size_t)c->n_traj * 4, c->st);
     if (e == hipSuccess) e = hipMemsetAsync(c->sum_lp, 0, (size_t)c->n_traj * 4, c->st);
     if (e == hipSuccess) e = hipMemsetAsync(c->freed, 0, (size_t)c->n_traj, c->st);
+    if (e == hipSuccess && c->streamed) e = hipMemsetAsync(c->streamed, 0, (size_t)c->n_traj * 4, c->st);
+    if (e == hipSuccess && c->fin_sent) e = hipMemsetAsync(c->fin_sent, 0, (size_t)c->n_traj, c->st);
     if (e == hipSuccess) e = hipMemsetAsync(c->group_done, 0, (size_t)c->P, c->st);
     if (e == hipSuccess) e = hipMemsetAsync(c->kept, 0xff, (size_t)c->P * c->k * 4, c->st);
     if (e == hipSuccess) e = hipMemsetAsync(c->done_step, 0xff, (size_t)c->P * 4, c->st);
@@ -522,6 +538,8 @@ int darts_reset(darts_ctx* c) {
   if (e == hipSuccess) e = hipMemsetAsync(c->gen, 0, (size_t)c->n_traj * 4, c->st);
   if (e == hipSuccess) e = hipMemsetAsync(c->sum_lp, 0, (size_t)c->n_traj * 4, c->st);
   if (e == hipSuccess) e = hipMemsetAsync(c->freed, 0, (size_t)c->n_traj, c->st);
+  if (e == hipSuccess && c->streamed) e = hipMemsetAsync(c->streamed, 0, (size_t)c->n_traj * 4, c->st);
+  if (e == hipSuccess && c->fin_sent) e = hipMemsetAsync(c->fin_sent, 0, (size_t)c->n_traj, c->st);
   if (e == hipSuccess) e = hipMemsetAsync(c->group_done, 0, (size_t)c->P, c->st);
   if (e == hipSuccess) e = hipMemsetAsync(c->kept, 0xff, (size_t)c->P * c->k * 4, c->st);
   if (e == hipSuccess) e = hipMemsetAsync(c->done_step, 0xff, (size_t)c->P * 4, c->st);
@@ -712,6 +730,7 @@ int darts_prefill(darts_ctx* c, const int32_t* d_prompts, const int32_t* d_force
   a.entropy_out = out->entropy; a.gen = c->gen; a.sum_lp = c->sum_lp; a.status = c->status;
   a.last_tok = c->last_tok; a.forced_len = c->forced_len; a.finished_out = out->finished;
   a.traj_out = out->traj_id; a.cap = c->cap; a.eos = c->V - 1;
+  a.hist_tok = c->hist_tok; a.hist_lp = c->hist_lp;
   HIPCHK(c, launch_sample(a, c->st));
   c->free_top -= c->P * c->pp;
   c->hwm = std::max<int64_t>(c->hwm, c->n_pages - c->free_top);
@@ -762,6 +781,7 @@ int darts_decode_step(darts_ctx* c, const int32_t* d_force_tokens, darts_step_ou
   a.entropy_out = out->entropy; a.gen = c->gen; a.sum_lp = c->sum_lp; a.status = c->status;
   a.last_tok = c->last_tok; a.forced_len = c->forced_len; a.finished_out = out->finished;
   a.traj_out = out->traj_id; a.cap = c->cap; a.eos = c->V - 1;
+  a.hist_tok = c->hist_tok; a.hist_lp = c->hist_lp;
   HIPCHK(c, launch_sample(a, c->st));
   c->step += 1;
   c->tokens += n;
@@ -855,6 +875,27 @@ int darts_get_step_times(const darts_ctx* c, int32_t* h_rows, float* h_ms, int32
   *h_n = n;
   for (int32_t i = 0; i < std::min(n, cap); ++i) { h_rows[i] = c->st_rows[i]; h_ms[i] = c->st_ms[i]; }
   if (h_prefill_ms) *h_prefill_ms = c->prefill_ms;
+  return DARTS_OK;
+}
+
+int darts_stream_chunks(darts_ctx* c, int64_t threshold, int32_t flush, int32_t* d_desc,
+                        int32_t* d_tokens, float* d_logprobs, int64_t out_cap, int32_t* h_n_desc,
+                        int64_t* h_n_tokens) {
+  if (!c || !d_desc || !h_n_desc || threshold < 1 || out_cap < 0) return DARTS_EINVAL;
+  if (out_cap > 0 && (!d_tokens || !d_logprobs)) return DARTS_EINVAL;
+  if (c->poisoned) return DARTS_EHIP;
+  if (!c->hist_tok || c->phase == 0) return DARTS_ESTATE;
+  StreamArgs a{};
+  a.gen = c->gen; a.status = c->status; a.streamed = c->streamed; a.fin_sent = c->fin_sent;
+  a.hist_tok = c->hist_tok; a.hist_lp = c->hist_lp; a.cap = c->cap; a.n_traj = c->n_traj;
+  a.threshold = threshold; a.flush = flush ? 1 : 0; a.desc = d_desc; a.off = c->stream_off;
+  a.tok_out = d_tokens; a.lp_out = d_logprobs; a.out_cap = out_cap; a.info = c->dcnt + 12;
+  HIPCHK(c, launch_stream(a, c->st));
+  HIPCHK(c, hipMemcpyAsync(c->h_info + 8, c->dcnt + 12, 8, hipMemcpyDeviceToHost, c->st));
+  HIPCHK(c, hipStreamSynchronize(c->st));
+  if (c->h_info[8] < 0) return DARTS_ENOMEM;
+  *h_n_desc = c->h_info[8];
+  if (h_n_tokens) *h_n_tokens = c->h_info[9];
   return DARTS_OK;
 }
 

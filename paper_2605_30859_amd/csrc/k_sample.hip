@@ -134,6 +134,10 @@ __global__ void __launch_bounds__(256) sample_kernel(SampleArgs a) {
   if (a.logprob_out) a.logprob_out[r] = lp;
   if (a.entropy_out) a.entropy_out[r] = ent;
   if (STATEFUL) {
+    if (a.hist_tok && step < a.cap) {
+      a.hist_tok[(int64_t)g * a.cap + step] = taken;
+      a.hist_lp[(int64_t)g * a.cap + step] = lp;
+    }
     a.gen[g] = step + 1;
     a.sum_lp[g] = a.sum_lp[g] + lp;
     a.last_tok[g] = taken;

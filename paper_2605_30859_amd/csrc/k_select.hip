@@ -271,6 +271,86 @@ hipError_t launch_prune(const PruneArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Token-chunk streaming (Sec. 4.3.2, producer side): one block of 1024
+// threads.  Pending tokens of trajectory g are those generated since its last
+// dispatch (gen[g] - streamed[g]); when their total reaches the threshold (or
+// on a flush) every trajectory with pending tokens, or that ended and has not
+// been marked final yet, gets one descriptor (ascending g) and its tokens are
+// copied, in descriptor order, into the output buffers.
+__global__ void __launch_bounds__(1024) stream_kernel(StreamArgs a) {
+  __shared__ int32_t sh[1024];
+  __shared__ int s_emit, s_ndesc;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  // pass 1: pending total and whether some trajectory still owes a final mark
+  int64_t pend_tot = 0;
+  int owes = 0;
+  for (int base = 0; base < a.n_traj; base += 1024) {
+    const int g = base + tid;
+    int pend = 0, fin = 0;
+    if (g < a.n_traj && a.status[g] != ST_ABSENT) {
+      pend = a.gen[g] - a.streamed[g];
+      fin = (a.status[g] >= ST_EOS && a.status[g] <= ST_ABORT && !a.fin_sent[g]) ? 1 : 0;
+    }
+    int total, tf;
+    (void)block_excl_scan(pend, sh, &total);
+    (void)block_excl_scan(fin, sh, &tf);
+    pend_tot += total;
+    owes += tf;
+  }
+  if (tid == 0) {
+    const bool emit = pend_tot >= a.threshold || (a.flush && (pend_tot > 0 || owes > 0));
+    s_emit = !emit ? 0 : (pend_tot > a.out_cap ? -1 : 1);
+    if (s_emit <= 0) { a.info[0] = s_emit < 0 ? -1 : 0; a.info[1] = (int32_t)pend_tot; }
+  }
+  __syncthreads();
+  if (s_emit <= 0) return;
+  // pass 2: descriptors, token offsets, dispatch bookkeeping
+  int run_desc = 0, run_tok = 0;
+  for (int base = 0; base < a.n_traj; base += 1024) {
+    const int g = base + tid;
+    int pend = 0, fin = 0, stv = 0, start = 0;
+    if (g < a.n_traj && a.status[g] != ST_ABSENT) {
+      stv = a.status[g];
+      start = a.streamed[g];
+      pend = a.gen[g] - start;
+      fin = (stv >= ST_EOS && stv <= ST_ABORT && !a.fin_sent[g]) ? 1 : 0;
+    }
+    const int want = (pend > 0 || fin) ? 1 : 0;
+    int nd, nt;
+    const int di = block_excl_scan(want, sh, &nd);
+    const int to = block_excl_scan(pend, sh, &nt);
+    if (want) {
+      const int i = run_desc + di;
+      a.desc[4 * i] = g;
+      a.desc[4 * i + 1] = start;
+      a.desc[4 * i + 2] = pend;
+      a.desc[4 * i + 3] = fin ? stv : 0;
+      a.off[i] = run_tok + to;
+      a.streamed[g] = start + pend;
+      if (fin) a.fin_sent[g] = 1;
+    }
+    run_desc += nd;
+    run_tok += nt;
+  }
+  if (tid == 0) { s_ndesc = run_desc; a.info[0] = run_desc; a.info[1] = run_tok; }
+  __syncthreads();
+  // pass 3: copy each descriptor's tokens (one wavefront per descriptor)
+  for (int i = wv; i < s_ndesc; i += 16) {
+    const int g = a.desc[4 * i], start = a.desc[4 * i + 1], cnt = a.desc[4 * i + 2];
+    const int o = a.off[i];
+    const int64_t src = (int64_t)g * a.cap + start;
+    for (int t = lane; t < cnt; t += 64) {
+      a.tok_out[o + t] = a.hist_tok[src + t];
+      a.lp_out[o + t] = a.hist_lp[src + t];
+    }
+  }
+}
+
+hipError_t launch_stream(const StreamArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(stream_kernel, dim3(1), dim3(1024), 0, st, a);
+  return hipGetLastError();
+}
+
 // Pop a page for every live row whose next key/value write starts a page:
 // the token written this step has 0-based index gen-1 among the generated
 // tokens, so a page is needed when (gen-1) % 16 == 0.  Pages are taken from

@@ -104,6 +104,7 @@ struct SampleArgs {
   int32_t* gen; float* sum_lp; uint8_t* status; int32_t* last_tok; const int32_t* forced_len;
   uint8_t* finished_out; int32_t* traj_out; int cap; int eos;
   int64_t* tokens_counter;
+  int32_t* hist_tok; float* hist_lp;   // NULL or [n_traj][cap]: token t of trajectory g at g*cap + t
 };
 hipError_t launch_sample(const SampleArgs& a, hipStream_t st);
 hipError_t launch_gumbel_map(const float* u, float* g, int64_t n, hipStream_t st);
@@ -128,6 +129,16 @@ struct PruneArgs {
   int32_t* info;    // out: [0] n_live, [1] n_done, [2] free_top
 };
 hipError_t launch_prune(const PruneArgs& a, hipStream_t st);
+struct StreamArgs {
+  const int32_t* gen; const uint8_t* status; int32_t* streamed; uint8_t* fin_sent;
+  const int32_t* hist_tok; const float* hist_lp; int cap; int n_traj;
+  int64_t threshold; int flush;
+  int32_t* desc;        // [n_traj][4] out: traj, start, count, final status (0: more to come)
+  int32_t* off;         // [n_traj] scratch: token offset of each descriptor
+  int32_t* tok_out; float* lp_out; int64_t out_cap;
+  int32_t* info;        // out: [0] descriptors (-1: output capacity exceeded), [1] tokens
+};
+hipError_t launch_stream(const StreamArgs& a, hipStream_t st);
 hipError_t launch_advantages(const int32_t* kept, int n_groups, int k, const float* reward,
                              int n_traj, float eps, float* adv, hipStream_t st);
 hipError_t launch_alloc_pages(const int32_t* live, int n_live, const int32_t* gen, int prompt_pages,
