@@ -656,10 +656,22 @@ static int run_layers(darts_ctx* c, int n, const int32_t* row_pt, int pos_mod, i
     void* kp = (char*)c->kpool + (size_t)l * c->pool_layer_elems * c->esz;
     void* vp = (char*)c->vpool + (size_t)l * c->pool_layer_elems * c->esz;
     if (!*normed) HIPCHK(c, launch_rmsnorm(c->x, n, d, c->mc.rms_eps, c->xn, b, c->st));
-    HIPCHK(c, gemm_t(c, G_QKV, c->xn, d, w.wqkv, d, c->qkv, c->qkv_w, n, c->qkv_w, d, EPI_F32));
-    HIPCHK(c, launch_rope_append2(c->qkv, n, c->hq, c->hkv, c->hd, row_pt, pos_mod, pos_base,
-                                  c->page_table, c->max_pages, c->n_pages, c->rope, c->q, kp, vp, b,
-                                  c->st));
+    // QKV projection; with a split-K plan the partial sums go straight to the
+    // RoPE + KV-append kernel, which adds them
+    int n_split = 1;
+    const float* qkv_src = c->qkv;
+    if (b) {
+      const int ti = tbegin(c, 1 + G_QKV, 2.0 * n * c->qkv_w * d);
+      HIPCHK(c, launch_gemm_f32_or_partials(c->xn, d, w.wqkv, d, c->qkv, c->qkv_w, n, c->qkv_w, d,
+                                            c->gemm_ws, c->gemm_ws_bytes, c->st, &n_split));
+      tend(c, ti);
+      if (n_split > 1) qkv_src = (const float*)c->gemm_ws;
+    } else {
+      HIPCHK(c, gemm_t(c, G_QKV, c->xn, d, w.wqkv, d, c->qkv, c->qkv_w, n, c->qkv_w, d, EPI_F32));
+    }
+    HIPCHK(c, launch_rope_append2(qkv_src, n_split, (int64_t)n * c->qkv_w, n, c->hq, c->hkv, c->hd,
+                                  row_pt, pos_mod, pos_base, c->page_table, c->max_pages,
+                                  c->n_pages, c->rope, c->q, kp, vp, b, c->st));
     int r = run_attention(c, l, n, row_pt, ctx_mod, ctx_base, max_ctx);
     if (r != DARTS_OK) return r;
     HIPCHK(c, gemm_add_t(c, G_O, c->attn, hqd, w.wo, hqd, n, hqd, normed));

@@ -1,5 +1,7 @@
 // Elementwise kernels of the decoder step: embedding gather, RMSNorm,
 // RoPE + paged KV append, row gather.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -182,12 +184,15 @@ hipError_t launch_rmsnorm(const float* x, int n_rows, int d, float eps, void* ou
   return hipGetLastError();
 }
 
-// qkv[r] = [q (hq*hd) | k (hkv*hd) | v (hkv*hd)] fp32.  Rotate-half RoPE on q
+// qkv[r] = [q (hq*hd) | k (hkv*hd) | v (hkv*hd)] fp32, the sum of n_split
+// planes split_stride floats apart (split-K partials of the QKV projection,
+// summed here in plane order; n_split = 1 for a plain result).  Rotate-half RoPE on q
 // and k with the cos/sin table, write q (activation dtype) and append k, v
 // at position pos(r) into the pages of page-table row pt(r).
 //   pos(r) = pos_mod ? r % pos_mod + pos_base : pos_base
 template <bool BF16>
-__global__ void rope_append_kernel(const float* __restrict__ qkv, int hq, int hkv, int hd,
+__global__ void rope_append_kernel(const float* __restrict__ qkv, int n_split, int64_t split_stride,
+                                   int hq, int hkv, int hd,
                                    const int32_t* __restrict__ row_pt, int pos_mod, int pos_base,
                                    const int32_t* __restrict__ page_table, int pt_stride,
                                    int64_t n_pages, const float2* __restrict__ rope,
@@ -206,10 +211,18 @@ __global__ void rope_append_kernel(const float* __restrict__ qkv, int hq, int hk
   // rotated heads: hq query heads then hkv key heads; four consecutive
   // rotation pairs (i .. i+3 with partners i+half ..) per thread
   const int q4 = half / 4;
-  for (int t = threadIdx.x; t < (hq + hkv) * q4; t += blockDim.x) {
+  // blockIdx.y splits a row's work over several blocks (small batches)
+  const int t0 = blockIdx.y * blockDim.x + threadIdx.x, tstep = gridDim.y * blockDim.x;
+  for (int t = t0; t < (hq + hkv) * q4; t += tstep) {
     const int h = t / q4, i = (t % q4) * 4;
     const float* v = src + h * hd;
-    const float4 a = *(const float4*)(v + i), b = *(const float4*)(v + i + half);
+    float4 a = *(const float4*)(v + i), b = *(const float4*)(v + i + half);
+    for (int z = 1; z < n_split; ++z) {
+      const float4 a2 = *(const float4*)(v + z * split_stride + i);
+      const float4 b2 = *(const float4*)(v + z * split_stride + i + half);
+      a.x += a2.x; a.y += a2.y; a.z += a2.z; a.w += a2.w;
+      b.x += b2.x; b.y += b2.y; b.z += b2.z; b.w += b2.w;
+    }
     const float4 c01 = *(const float4*)(cs + i), c23 = *(const float4*)(cs + i + 2);
     const float ca[4] = {c01.x, c01.z, c23.x, c23.z}, sa[4] = {c01.y, c01.w, c23.y, c23.w};
     const float av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
@@ -244,29 +257,36 @@ __global__ void rope_append_kernel(const float* __restrict__ qkv, int hq, int hk
       *(float4*)((float*)dst + ob) = make_float4(o2[0], o2[1], o2[2], o2[3]);
     }
   }
-  for (int t = threadIdx.x; t < hkv * hd; t += blockDim.x) {
+  for (int t = t0; t < hkv * hd; t += tstep) {
     const int h = t / hd, dd = t % hd;
-    const float v = src[(hq + hkv) * hd + t];
+    float v = src[(hq + hkv) * hd + t];
+    for (int z = 1; z < n_split; ++z) v += src[z * split_stride + (hq + hkv) * hd + t];
     const int64_t o = v_off(page, h, slot, dd, hkv, hd);
     if (BF16) ((bf16_t*)v_pool)[o] = f32_to_bf16(v);
     else ((float*)v_pool)[o] = v;
   }
 }
 
-hipError_t launch_rope_append2(const float* qkv, int n_rows, int hq, int hkv, int hd,
-                               const int32_t* row_pt, int pos_mod, int pos_base,
-                               const int32_t* page_table, int pt_stride, int64_t n_pages,
-                               const float2* rope, void* q_out, void* k_pool, void* v_pool,
-                               bool bf16, hipStream_t st) {
+hipError_t launch_rope_append2(const float* qkv, int n_split, int64_t split_stride, int n_rows,
+                               int hq, int hkv, int hd, const int32_t* row_pt, int pos_mod,
+                               int pos_base, const int32_t* page_table, int pt_stride,
+                               int64_t n_pages, const float2* rope, void* q_out, void* k_pool,
+                               void* v_pool, bool bf16, hipStream_t st) {
   if (n_rows <= 0) return hipSuccess;
+  if (n_split < 1) return hipErrorInvalidValue;
+  // at least ~512 blocks when rows are few, at most one block per 256 items
+  const int items = std::max((hq + hkv) * (hd / 8), hkv * hd);
+  const int ymax = std::max(1, (items + 255) / 256);
+  const int y = std::min(ymax, std::max(1, (512 + n_rows - 1) / n_rows));
+  const dim3 grid(n_rows, y);
   if (bf16)
-    hipLaunchKernelGGL(rope_append_kernel<true>, dim3(n_rows), dim3(256), 0, st, qkv, hq, hkv, hd,
-                       row_pt, pos_mod, pos_base, page_table, pt_stride, n_pages, rope, q_out,
-                       k_pool, v_pool);
+    hipLaunchKernelGGL(rope_append_kernel<true>, grid, dim3(256), 0, st, qkv, n_split,
+                       split_stride, hq, hkv, hd, row_pt, pos_mod, pos_base, page_table, pt_stride,
+                       n_pages, rope, q_out, k_pool, v_pool);
   else
-    hipLaunchKernelGGL(rope_append_kernel<false>, dim3(n_rows), dim3(256), 0, st, qkv, hq, hkv, hd,
-                       row_pt, pos_mod, pos_base, page_table, pt_stride, n_pages, rope, q_out,
-                       k_pool, v_pool);
+    hipLaunchKernelGGL(rope_append_kernel<false>, grid, dim3(256), 0, st, qkv, n_split,
+                       split_stride, hq, hkv, hd, row_pt, pos_mod, pos_base, page_table, pt_stride,
+                       n_pages, rope, q_out, k_pool, v_pool);
   return hipGetLastError();
 }
 

@@ -741,6 +741,19 @@ hipError_t launch_gemm(bool bf16, const void* A, int lda, const void* W, int ldw
   return hipErrorInvalidValue;
 }
 
+hipError_t launch_gemm_f32_or_partials(const void* A, int lda, const void* W, int ldw, float* C,
+                                       int ldc, int M, int N, int K, void* ws, size_t ws_bytes,
+                                       hipStream_t st, int* n_split) {
+  *n_split = 1;
+  if (M <= 0) return hipSuccess;
+  if (N % 128 != 0 || K % 256 != 0) return hipErrorInvalidValue;
+  const Plan p = plan_gemm(M, N, K);
+  if (p.S == 1) return launch_plan<EPI_F32>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st);
+  if (ws == nullptr || ws_bytes < (size_t)p.S * M * N * sizeof(float)) return hipErrorInvalidValue;
+  *n_split = p.S;
+  return launch_plan<EPI_F32>(p, A, lda, W, ldw, C, ldc, M, N, K, ws, st);
+}
+
 // x[M, N] += A . W^T followed by xn = bf16(RMSNorm(x)).  When the plan splits
 // K the add and the norm are fused into the reduce (returns *fused = true);
 // otherwise the GEMM adds in its epilogue and the caller normalises.

@@ -30,6 +30,11 @@ enum Epi { EPI_F32 = 0, EPI_BF16 = 1, EPI_ADD_F32 = 2, EPI_SWIGLU = 3 };
 size_t gemm_workspace_bytes(int M, int N, int K);
 // x += A . W^T and xn = bf16(RMSNorm(x)) (bf16 operands); *fused says whether
 // xn was written (split-K plans) or the caller must normalise
+// bf16 C = A . W^T in fp32 when the plan keeps K whole (*n_split = 1), else
+// only the plan's split-K partial sums into ws (*n_split planes of M*N floats)
+hipError_t launch_gemm_f32_or_partials(const void* A, int lda, const void* W, int ldw, float* C,
+                                       int ldc, int M, int N, int K, void* ws, size_t ws_bytes,
+                                       hipStream_t st, int* n_split);
 hipError_t launch_gemm_add_norm(const void* A, int lda, const void* W, int ldw, float* x, int ldx,
                                 int M, int N, int K, void* ws, size_t ws_bytes, float eps,
                                 void* xn, hipStream_t st, bool* fused);
@@ -47,11 +52,11 @@ hipError_t launch_embed_v(const void* table, bool bf16, const int32_t* tokens,
 hipError_t launch_rmsnorm(const float* x, int n_rows, int d, float eps, void* out, bool bf16,
                           hipStream_t st);
 // pos(r) = pos_mod ? r % pos_mod + pos_base : pos_base
-hipError_t launch_rope_append2(const float* qkv, int n_rows, int hq, int hkv, int hd,
-                               const int32_t* row_pt, int pos_mod, int pos_base,
-                               const int32_t* page_table, int pt_stride, int64_t n_pages,
-                               const float2* rope, void* q_out, void* k_pool, void* v_pool,
-                               bool bf16, hipStream_t st);
+hipError_t launch_rope_append2(const float* qkv, int n_split, int64_t split_stride, int n_rows,
+                               int hq, int hkv, int hd, const int32_t* row_pt, int pos_mod,
+                               int pos_base, const int32_t* page_table, int pt_stride,
+                               int64_t n_pages, const float2* rope, void* q_out, void* k_pool,
+                               void* v_pool, bool bf16, hipStream_t st);
 hipError_t launch_gather_rows(const float* src, const int32_t* rows, int n, int d, float* dst,
                               hipStream_t st);
 
