@@ -299,3 +299,28 @@ def test_dense_small_shared_prefix_parity(dense_small_prompt256):
 def test_dense_small_chunked_rows_parity(dense_small_prompt256):
     run, ref, shared, rows = dense_small_prompt256
     _check_bf16("dense-small prompt 256, per-row attention", run, ref, rows)
+
+
+def test_qwen3_8b_full_size_schedule():
+    """Qwen3-8B shape at full size (36 layers, d 4096, 32/8 heads x 128, FFN
+    12288, vocab 151936; 32 prompts x 512, m 16, k 8, cap 8192), in the launch
+    configuration the benchmark times: the rollout completes with the steps,
+    tokens and page high-water mark the forced lengths imply, kept sets equal
+    the selection of its own scores, and every score is a valid log-prob /
+    entropy."""
+    model, run = get_config("qwen3-8b")
+    prompts, forced = rollout_inputs(model, run)
+    say("qwen3-8b full size: GPU rollout")
+    got = run_gpu(model, run, prompts, forced)
+    s = schedule_only(forced, run.n_prompts, run.m, run.k, run.cap, run.prompt_len,
+                      mean_lp=got["mean_lp"])
+    assert got["stats"]["steps"] == s["steps"]
+    assert got["stats"]["tokens_decoded"] == s["tokens_decoded"]
+    assert got["stats"]["pages_hwm"] == s["pages_hwm"] and got["stats"]["pages_used"] == 0
+    for i in range(run.n_prompts):
+        assert list(got["kept"][i]) == s["kept"][i]
+    assert list(got["length"]) == s["length"]
+    ent = np.concatenate([r["entropy"] for r in got["steps"]])
+    lp = np.concatenate([r["logprob"] for r in got["steps"]])
+    assert np.isfinite(ent).all() and np.isfinite(lp).all()
+    assert (ent >= 0).all() and (ent <= np.log(model.vocab) + 1e-3).all() and (lp <= 1e-5).all()
