@@ -62,7 +62,7 @@ struct darts_ctx {
   float* m_topk_w = nullptr;
   int32_t* m_pos_of = nullptr;
   int32_t* m_cnt = nullptr;       // counts | offsets | cursors, E each
-  void* m_a_perm = nullptr;
+  int32_t* m_row_of = nullptr;    // [pairs] input row of each expert-sorted position
   void* m_h_perm = nullptr;
   float* m_y_perm = nullptr;
   float* m_logits = nullptr;      // router logits [rows][Epad]
@@ -450,7 +450,7 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
     A(&c->m_cnt, (size_t)3 * c->E * 4);
     A(&c->m_logits, (size_t)rows_max * c->Epad * 4);
     A(&c->m_mtiles, (pairs / kGroupedTileRows + c->E + 1) * 4);
-    A(&c->m_a_perm, pairs * c->d * 2);
+    A(&c->m_row_of, pairs * 4);
     A(&c->m_h_perm, pairs * c->Fe * 2);
     A(&c->m_y_perm, pairs * c->d * 4);
   }
@@ -678,20 +678,20 @@ static int run_layers(darts_ctx* c, int n, const int32_t* row_pt, int pos_mod, i
     if (!*normed) HIPCHK(c, launch_rmsnorm(c->x, n, d, c->mc.rms_eps, c->xn, b, c->st));
     if (c->moe) {
       MoeArgs m;
-      m.xn = (const bf16_t*)c->xn; m.x = c->x; m.n_rows = n; m.d = d; m.E = c->E; m.k = c->topk;
+      m.xn = (bf16_t*)c->xn; m.x = c->x; m.n_rows = n; m.d = d; m.E = c->E; m.k = c->topk;
+      m.eps = c->mc.rms_eps; m.row_of = c->m_row_of;
       m.Fe = c->Fe; m.w_router = (const bf16_t*)w.wrouter; m.w_gu = (const bf16_t*)w.wegu;
       m.E_pad = c->Epad; m.logits = c->m_logits; m.gemm_ws = c->gemm_ws;
       m.n_mtiles = c->m_mtiles; m.mtiles = c->m_mtiles + 1;
       m.gemm_ws_bytes = c->gemm_ws_bytes;
       m.w_down = (const bf16_t*)w.wedown; m.topk_id = c->m_topk_id; m.topk_w = c->m_topk_w;
       m.pos_of = c->m_pos_of; m.counts = c->m_cnt; m.offsets = c->m_cnt + c->E;
-      m.cursors = c->m_cnt + 2 * c->E; m.a_perm = (bf16_t*)c->m_a_perm;
+      m.cursors = c->m_cnt + 2 * c->E;
       m.h_perm = (bf16_t*)c->m_h_perm; m.y_perm = c->m_y_perm;
       const double flop = 2.0 * n * ((double)c->E * d + (double)c->topk * 3.0 * c->Fe * d);
       const int ti = tbegin(c, 1 + G_MOE, flop);
-      HIPCHK(c, launch_moe_ffn(m, c->st));
+      HIPCHK(c, launch_moe_ffn(m, c->st, normed));
       tend(c, ti);
-      *normed = false;
       continue;
     }
     HIPCHK(c, gemm_t(c, G_GU, c->xn, d, w.wgu, d, c->hbuf, c->F, n, 2 * c->F, d, EPI_SWIGLU));

@@ -95,12 +95,14 @@ __device__ __forceinline__ int dma_swz(int r) {
 }
 
 // One BM x BN output tile (rows m0.., cols n0.., K range [z*k_chunk, +k_chunk)).
+// arow != NULL: row r of the tile's A operand is row arow[r] of A (a gather).
 template <int BM, int BN, int KB, int WGM, int WGN, int STAGES, int EPI, bool SPLIT>
 __device__ __forceinline__ void dma_gemm_tile(const bf16_t* __restrict__ A, int lda,
                                               const bf16_t* __restrict__ W, int ldw,
                                               void* __restrict__ C, int ldc, int M, int N,
                                               int k_chunk, int mi, int ni, int z,
-                                              float* __restrict__ ws) {
+                                              float* __restrict__ ws,
+                                              const int32_t* __restrict__ arow = nullptr) {
   static_assert(KB == 32 || KB == 64, "K tile");
   constexpr int NW = WGM * WGN;                    // wavefronts per block
   constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 16, TN = WN / 16;
@@ -127,6 +129,7 @@ __device__ __forceinline__ void dma_gemm_tile(const bf16_t* __restrict__ A, int 
   for (int j = 0; j < AI; ++j) {
     int r = m0 + wave * (BM / NW) + RPI * j + lrow;
     r = r < M ? r : M - 1;
+    if (arow) r = arow[r];
     asrc[j] = A + (int64_t)r * lda + kbeg + gchunk * 8;
   }
 #pragma unroll
@@ -237,7 +240,8 @@ __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_kernel(const bf16_t* 
 }
 
 // Grouped GEMM (mixture-of-experts): group e owns rows [off[e], off[e] +
-// cnt[e]) of A and C and the weight matrix W + e * w_stride ([N][K]).  The
+// cnt[e]) of C (and of A, or of the gather list arow into A) and the weight
+// matrix W + e * w_stride ([N][K]).  The
 // non-empty row tiles are listed on the device (mtiles[i] = e << 16 | m tile,
 // *n_mtiles of them); persistent blocks take items (row tile, n tile), n tile
 // fastest, in a grid-stride loop.
@@ -246,7 +250,7 @@ __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_grouped_kernel(
     const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ W, int64_t w_stride, int ldw,
     void* __restrict__ C, int ldc, int N, int K, const int32_t* __restrict__ g_off,
     const int32_t* __restrict__ g_cnt, const int32_t* __restrict__ mtiles,
-    const int32_t* __restrict__ n_mtiles, int nt) {
+    const int32_t* __restrict__ n_mtiles, int nt, const int32_t* __restrict__ arow) {
   const int total = n_mtiles[0] * nt;
   constexpr int esz = (EPI == EPI_F32 || EPI == EPI_ADD_F32) ? 4 : 2;
   for (int it = blockIdx.x; it < total; it += gridDim.x) {
@@ -259,9 +263,11 @@ __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_grouped_kernel(
     // memory fence, which would also wait for the previous item's stores
     __builtin_amdgcn_s_barrier();
     void* Ce = (char*)C + off * ldc * esz;
-    dma_gemm_tile<BM, BN, KB, WGM, WGN, STAGES, EPI, false>(A + off * lda, lda,
+    // with arow, A rows are gathered: segment row r is A row arow[off + r]
+    dma_gemm_tile<BM, BN, KB, WGM, WGN, STAGES, EPI, false>(arow ? A : A + off * lda, lda,
                                                             W + (int64_t)e * w_stride, ldw, Ce, ldc,
-                                                            cnt, N, K, mi, ni, 0, nullptr);
+                                                            cnt, N, K, mi, ni, 0, nullptr,
+                                                            arow ? arow + off : nullptr);
   }
 }
 
@@ -624,7 +630,7 @@ template <int EPI>
 static hipError_t grouped_launch(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
                                  void* C, int ldc, int N, int K, const int32_t* g_off,
                                  const int32_t* g_cnt, const int32_t* mtiles,
-                                 const int32_t* n_mtiles, hipStream_t st) {
+                                 const int32_t* n_mtiles, const int32_t* arow, hipStream_t st) {
   // 128x128 tiles, 4-stage ring (one block per CU): expert weights are
   // streamed once per row tile
   constexpr int BM_ = 128, BN_ = 128, KB = 64, ST = 4;
@@ -638,20 +644,20 @@ static hipError_t grouped_launch(const void* A, int lda, const void* W, int64_t 
     attr_done = true;
   }
   hipLaunchKernelGGL(kern, dim3(kCus), dim3(256), lds, st, (const bf16_t*)A, lda, (const bf16_t*)W,
-                     w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, nt);
+                     w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, nt, arow);
   return hipGetLastError();
 }
 
 hipError_t launch_gemm_grouped(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
                                void* C, int ldc, int N, int K, int epi, const int32_t* g_off,
                                const int32_t* g_cnt, const int32_t* mtiles, const int32_t* n_mtiles,
-                               hipStream_t st) {
+                               const int32_t* arow, hipStream_t st) {
   if (N % 128 != 0 || K % 64 != 0 || K < 64) return hipErrorInvalidValue;
   switch (epi) {
-    case EPI_F32: return grouped_launch<EPI_F32>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, st);
-    case EPI_BF16: return grouped_launch<EPI_BF16>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, st);
-    case EPI_ADD_F32: return grouped_launch<EPI_ADD_F32>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, st);
-    case EPI_SWIGLU: return grouped_launch<EPI_SWIGLU>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, st);
+    case EPI_F32: return grouped_launch<EPI_F32>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
+    case EPI_BF16: return grouped_launch<EPI_BF16>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
+    case EPI_ADD_F32: return grouped_launch<EPI_ADD_F32>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
+    case EPI_SWIGLU: return grouped_launch<EPI_SWIGLU>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
     default: return hipErrorInvalidValue;
   }
 }

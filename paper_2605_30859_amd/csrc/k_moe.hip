@@ -4,12 +4,13 @@
 //             zero-padded to a multiple of 128); per row r = softmax over the E
 //             logits, the k largest (ties to the lower expert id), weights
 //             renormalised over the k
-//   offsets:  per-expert counts (block histogram) and their exclusive scan
-//   scatter:  every (row, slot) pair gets a position in its expert's segment
-//             and its normalised input row is copied there
+//   offsets:  per-expert counts (block histogram), their exclusive scan, and
+//             a position in its expert's segment for every (row, slot) pair
 //   experts:  grouped tiled GEMMs over the expert segments: gate/up (+ SwiGLU
-//             epilogue), then down
-//   combine:  x[row] += sum_j w[row][j] * y[pos(row, j)]   (slot order)
+//             epilogue; its A rows are gathered from the normalised input
+//             through the position -> row list), then down
+//   combine:  x[row] += sum_j w[row][j] * y[pos(row, j)]   (slot order),
+//             then the next RMSNorm of the updated row
 // Positions inside a segment come from atomics, so their order varies from
 // run to run, but no value depends on it: every output row of an expert GEMM
 // depends only on its own input row, and the combine sums in slot order.
@@ -22,8 +23,10 @@ namespace darts {
 
 // One wavefront per row: softmax over the E router logits (fp32), then k
 // rounds of wavefront argmax (value descending, expert id ascending), each
-// winner removed; weights renormalised over the k.
+// winner removed; weights renormalised over the k.  NPL logits per lane
+// (E <= 64 * NPL).
 constexpr int kMoeMaxPerLane = 16;   // E <= 1024
+template <int NPL>
 __global__ void __launch_bounds__(256) moe_topk_kernel(const float* __restrict__ logits, int ld,
                                                        int n_rows, int E, int k,
                                                        int32_t* __restrict__ topk_id,
@@ -32,10 +35,10 @@ __global__ void __launch_bounds__(256) moe_topk_kernel(const float* __restrict__
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (r >= n_rows) return;
   const float* lg = logits + (int64_t)r * ld;
-  float p[kMoeMaxPerLane];
+  float p[NPL];
   float mx = -INFINITY;
 #pragma unroll
-  for (int j = 0; j < kMoeMaxPerLane; ++j) {
+  for (int j = 0; j < NPL; ++j) {
     const int e = lane + 64 * j;
     p[j] = e < E ? lg[e] : -INFINITY;
     mx = fmaxf(mx, p[j]);
@@ -43,7 +46,7 @@ __global__ void __launch_bounds__(256) moe_topk_kernel(const float* __restrict__
   mx = wave_max(mx);
   float sum = 0.f;
 #pragma unroll
-  for (int j = 0; j < kMoeMaxPerLane; ++j) {
+  for (int j = 0; j < NPL; ++j) {
     const int e = lane + 64 * j;
     const float v = e < E ? __expf(p[j] - mx) : 0.f;
     p[j] = v;
@@ -52,13 +55,15 @@ __global__ void __launch_bounds__(256) moe_topk_kernel(const float* __restrict__
   sum = wave_sum(sum);
   const float inv = 1.0f / sum;
 #pragma unroll
-  for (int j = 0; j < kMoeMaxPerLane; ++j) p[j] = (lane + 64 * j < E) ? p[j] * inv : -2.0f;
+  for (int j = 0; j < NPL; ++j) p[j] = (lane + 64 * j < E) ? p[j] * inv : -2.0f;
   float wsum = 0.f;
+  float my_w = 0.f;
+  int my_id = 0;
   for (int t = 0; t < k; ++t) {
     float bv = -3.0f;
     int bi = 0x7fffffff;
 #pragma unroll
-    for (int j = 0; j < kMoeMaxPerLane; ++j) {
+    for (int j = 0; j < NPL; ++j) {
       const int e = lane + 64 * j;
       if (p[j] > bv || (p[j] == bv && e < bi)) { bv = p[j]; bi = e; }
     }
@@ -69,17 +74,14 @@ __global__ void __launch_bounds__(256) moe_topk_kernel(const float* __restrict__
       if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
     }
 #pragma unroll
-    for (int j = 0; j < kMoeMaxPerLane; ++j)
+    for (int j = 0; j < NPL; ++j)
       if (lane + 64 * j == bi) p[j] = -2.0f;          // removed
-    if (lane == 0) {
-      topk_id[(int64_t)r * k + t] = bi;
-      topk_w[(int64_t)r * k + t] = bv;
-    }
+    if (lane == t) { my_w = bv; my_id = bi; }         // lane t keeps round t's winner
     wsum += bv;
   }
-  if (lane == 0) {
-    const float winv = 1.0f / wsum;
-    for (int t = 0; t < k; ++t) topk_w[(int64_t)r * k + t] *= winv;
+  if (lane < k) {
+    topk_id[(int64_t)r * k + lane] = my_id;
+    topk_w[(int64_t)r * k + lane] = my_w * (1.0f / wsum);
   }
 }
 
@@ -100,15 +102,18 @@ __device__ __forceinline__ int block_excl_scan1024(int v, int32_t* sh, int* tota
 }
 
 // Single block: per-expert counts of the n_pairs routed (row, slot) pairs
-// (LDS histogram), their exclusive scan into offsets, cursors reset to 0, and
-// the list of non-empty expert row tiles (e << 16 | tile) for the grouped GEMMs.
+// (LDS histogram), their exclusive scan into offsets, cursors reset to 0, the
+// list of non-empty expert row tiles (e << 16 | tile) for the grouped GEMMs,
+// and every pair's position (pos_of) with its inverse (row_of).
 __global__ void __launch_bounds__(1024) moe_offsets_kernel(const int32_t* __restrict__ topk_id,
-                                                           int n_pairs, int E,
+                                                           int n_pairs, int E, int k,
                                                            int32_t* __restrict__ counts,
                                                            int32_t* __restrict__ offsets,
                                                            int32_t* __restrict__ cursors,
                                                            int32_t* __restrict__ mtiles,
-                                                           int32_t* __restrict__ n_mtiles) {
+                                                           int32_t* __restrict__ n_mtiles,
+                                                           int32_t* __restrict__ pos_of,
+                                                           int32_t* __restrict__ row_of) {
   __shared__ int32_t hist[1024];
   __shared__ int32_t sh[1024];
   const int tid = threadIdx.x;
@@ -132,45 +137,40 @@ __global__ void __launch_bounds__(1024) moe_offsets_kernel(const int32_t* __rest
     for (int j = 0; j < nt; ++j) mtiles[tex + j] = (tid << 16) | j;
   }
   if (tid == 0) *n_mtiles = ntiles;
-}
-
-// One block per row: place its k pairs and copy the input row into each.
-__global__ void __launch_bounds__(256) moe_scatter_kernel(const bf16_t* __restrict__ xn, int d, int k,
-                                                          const int32_t* __restrict__ topk_id,
-                                                          const int32_t* __restrict__ offsets,
-                                                          int32_t* __restrict__ cursors,
-                                                          int32_t* __restrict__ pos_of,
-                                                          bf16_t* __restrict__ a_perm) {
-  __shared__ int32_t pos[64];
-  const int r = blockIdx.x, tid = threadIdx.x;
-  if (tid < k) {
-    const int e = topk_id[(int64_t)r * k + tid];
-    const int p = offsets[e] + atomicAdd(&cursors[e], 1);
-    pos[tid] = p;
-    pos_of[(int64_t)r * k + tid] = p;
-  }
+  // positions: pair i (row i / k) takes the next free slot of its expert's
+  // segment; hist becomes the per-expert cursor
+  hist[tid] = tid < E ? ex : 0;
   __syncthreads();
-  const uint32_t* src = (const uint32_t*)(xn + (int64_t)r * d);
-  for (int j = 0; j < k; ++j) {
-    uint32_t* dst = (uint32_t*)(a_perm + (int64_t)pos[j] * d);
-    for (int c = tid; c < d / 2; c += 256) dst[c] = src[c];
+  for (int i = tid; i < n_pairs; i += 1024) {
+    const int e = topk_id[i];
+    if (e < 0 || e >= E) continue;
+    const int p = atomicAdd(&hist[e], 1);
+    pos_of[i] = p;
+    row_of[p] = i / k;
   }
 }
 
-// x[r] += sum_j w[r][j] * y[pos(r, j)]   (slot order), 4 columns per thread
+// x[r] += sum_j w[r][j] * y[pos(r, j)]   (slot order), 4 columns per thread;
+// with xn (d <= 4096) also xn[r] = bf16(x[r] / sqrt(mean(x[r]^2) + eps)).
+constexpr int kCombVec = 4;
 __global__ void __launch_bounds__(256) moe_combine_kernel(const float* __restrict__ y, int d, int k,
                                                           const int32_t* __restrict__ pos_of,
                                                           const float* __restrict__ topk_w,
-                                                          float* __restrict__ x) {
+                                                          float* __restrict__ x, float eps,
+                                                          bf16_t* __restrict__ xn) {
   __shared__ int32_t sp[64];
   __shared__ float sw[64];
+  __shared__ float red[4];
   const int r = blockIdx.x, tid = threadIdx.x;
   if (tid < k) {
     sp[tid] = pos_of[(int64_t)r * k + tid];
     sw[tid] = topk_w[(int64_t)r * k + tid];
   }
   __syncthreads();
-  for (int c = tid * 4; c < d; c += 1024) {
+  float4 keep[kCombVec];
+  float ss = 0.f;
+  int t = 0;
+  for (int c = tid * 4; c < d; c += 1024, ++t) {
     float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int j = 0; j < k; ++j) {
       const float4 v = *(const float4*)(y + (int64_t)sp[j] * d + c);
@@ -184,10 +184,28 @@ __global__ void __launch_bounds__(256) moe_combine_kernel(const float* __restric
     float4 xv = *xp;
     xv.x += s.x; xv.y += s.y; xv.z += s.z; xv.w += s.w;
     *xp = xv;
+    if (t < kCombVec) keep[t] = xv;
+    ss = fmaf(xv.x, xv.x, ss);
+    ss = fmaf(xv.y, xv.y, ss);
+    ss = fmaf(xv.z, xv.z, ss);
+    ss = fmaf(xv.w, xv.w, ss);
+  }
+  if (xn == nullptr) return;
+  ss = wave_sum(ss);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  const float inv = 1.0f / sqrtf((red[0] + red[1] + red[2] + red[3]) / (float)d + eps);
+  t = 0;
+  for (int c = tid * 4; c < d && t < kCombVec; c += 1024, ++t) {
+    uint2 q;
+    q.x = (uint32_t)f32_to_bf16(keep[t].x * inv) | ((uint32_t)f32_to_bf16(keep[t].y * inv) << 16);
+    q.y = (uint32_t)f32_to_bf16(keep[t].z * inv) | ((uint32_t)f32_to_bf16(keep[t].w * inv) << 16);
+    *(uint2*)(xn + (int64_t)r * d + c) = q;
   }
 }
 
-hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st) {
+hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st, bool* normed) {
+  *normed = false;
   if (a.n_rows <= 0) return hipSuccess;
   if (a.E > 64 * kMoeMaxPerLane || a.E > 1024 || a.k > 64 || a.k > a.E || a.d % 4 ||
       a.n_rows > 65536 * kGroupedTileRows)
@@ -195,23 +213,31 @@ hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st) {
   hipError_t e = launch_gemm(true, a.xn, a.d, a.w_router, a.d, a.logits, a.E_pad, a.n_rows, a.E_pad, a.d,
                              EPI_F32, a.gemm_ws, a.gemm_ws_bytes, st);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(moe_topk_kernel, dim3((a.n_rows + 3) / 4), dim3(256), 0, st, a.logits, a.E_pad,
-                     a.n_rows, a.E, a.k, a.topk_id, a.topk_w);
-  hipLaunchKernelGGL(moe_offsets_kernel, dim3(1), dim3(1024), 0, st, a.topk_id, a.n_rows * a.k, a.E,
-                     a.counts, a.offsets, a.cursors, a.mtiles, a.n_mtiles);
-  hipLaunchKernelGGL(moe_scatter_kernel, dim3(a.n_rows), dim3(256), 0, st, a.xn, a.d, a.k, a.topk_id,
-                     a.offsets, a.cursors, a.pos_of, a.a_perm);
+  const dim3 gtk((a.n_rows + 3) / 4), btk(256);
+  if (a.E <= 128)
+    hipLaunchKernelGGL(moe_topk_kernel<2>, gtk, btk, 0, st, a.logits, a.E_pad, a.n_rows, a.E, a.k, a.topk_id, a.topk_w);
+  else if (a.E <= 256)
+    hipLaunchKernelGGL(moe_topk_kernel<4>, gtk, btk, 0, st, a.logits, a.E_pad, a.n_rows, a.E, a.k, a.topk_id, a.topk_w);
+  else
+    hipLaunchKernelGGL(moe_topk_kernel<kMoeMaxPerLane>, gtk, btk, 0, st, a.logits, a.E_pad, a.n_rows, a.E, a.k,
+                       a.topk_id, a.topk_w);
+  hipLaunchKernelGGL(moe_offsets_kernel, dim3(1), dim3(1024), 0, st, a.topk_id, a.n_rows * a.k, a.E, a.k,
+                     a.counts, a.offsets, a.cursors, a.mtiles, a.n_mtiles, a.pos_of, a.row_of);
   const int Fe = a.Fe, d = a.d;
-  // gate/up: N = 2*Fe, K = d (SwiGLU into h_perm); down: N = d, K = Fe
-  e = launch_gemm_grouped(a.a_perm, d, a.w_gu, (int64_t)2 * Fe * d, d, a.h_perm, Fe, 2 * Fe, d,
-                          EPI_SWIGLU, a.offsets, a.counts, a.mtiles, a.n_mtiles, st);
+  // gate/up: N = 2*Fe, K = d (SwiGLU into h_perm), A rows gathered from xn;
+  // down: N = d, K = Fe
+  e = launch_gemm_grouped(a.xn, d, a.w_gu, (int64_t)2 * Fe * d, d, a.h_perm, Fe, 2 * Fe, d,
+                          EPI_SWIGLU, a.offsets, a.counts, a.mtiles, a.n_mtiles, a.row_of, st);
   if (e != hipSuccess) return e;
   e = launch_gemm_grouped(a.h_perm, Fe, a.w_down, (int64_t)d * Fe, Fe, a.y_perm, d, d, Fe, EPI_F32,
-                          a.offsets, a.counts, a.mtiles, a.n_mtiles, st);
+                          a.offsets, a.counts, a.mtiles, a.n_mtiles, nullptr, st);
   if (e != hipSuccess) return e;
+  const bool fuse = d <= 1024 * kCombVec;
   hipLaunchKernelGGL(moe_combine_kernel, dim3(a.n_rows), dim3(256), 0, st, a.y_perm, d, a.k,
-                     a.pos_of, a.topk_w, a.x);
-  return hipGetLastError();
+                     a.pos_of, a.topk_w, a.x, a.eps, fuse ? a.xn : nullptr);
+  e = hipGetLastError();
+  if (e == hipSuccess) *normed = fuse;
+  return e;
 }
 
 }  // namespace darts

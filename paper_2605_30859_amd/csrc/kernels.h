@@ -69,7 +69,7 @@ constexpr int kGroupedTileRows = 128;
 hipError_t launch_gemm_grouped(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
                                void* C, int ldc, int N, int K, int epi, const int32_t* g_off,
                                const int32_t* g_cnt, const int32_t* mtiles, const int32_t* n_mtiles,
-                               hipStream_t st);
+                               const int32_t* arow, hipStream_t st);
 
 // ---- attention (k_attn.hip)
 size_t attn_workspace_bytes(int n_rows, int hq, int hkv, int hd, int max_ctx);
@@ -156,7 +156,9 @@ hipError_t launch_prefill_pages(int n_prompts, int m, const int32_t* grp_m, int 
 
 // ---- MoE FFN (k_moe.hip): x += sum over the top-k experts of w_e * expert_e(xn)
 struct MoeArgs {
-  const bf16_t* xn; float* x; int n_rows, d, E, k, Fe;
+  bf16_t* xn;               // in: RMSNorm(x) (bf16); out: RMSNorm of the updated x when *normed
+  float* x; int n_rows, d, E, k, Fe;
+  float eps;
   int E_pad;                // router rows padded to a multiple of 128 (zero rows)
   const bf16_t* w_router;   // [E_pad][d]
   float* logits;            // [n_rows][E_pad] router logits
@@ -164,11 +166,13 @@ struct MoeArgs {
   const bf16_t* w_gu;       // [E][2Fe][d], gate/up rows interleaved in groups of 16
   const bf16_t* w_down;     // [E][d][Fe]
   int32_t* topk_id; float* topk_w; int32_t* pos_of;            // [n_rows*k]
+  int32_t* row_of;          // [n_rows*k]: input row of each expert-sorted position
   int32_t* counts; int32_t* offsets; int32_t* cursors;         // [E]
   int32_t* mtiles;          // [n_rows*k / kGroupedTileRows + E] non-empty expert row tiles
   int32_t* n_mtiles;        // [1]
-  bf16_t* a_perm; bf16_t* h_perm; float* y_perm;               // [n_rows*k][d | Fe | d]
+  bf16_t* h_perm; float* y_perm;                               // [n_rows*k][Fe | d]
 };
-hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st);
+// *normed: the combine also wrote xn = bf16(RMSNorm(x)) (d <= 4096)
+hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st, bool* normed);
 
 }  // namespace darts
