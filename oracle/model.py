@@ -38,7 +38,7 @@ import math
 
 import numpy as np
 
-from .philox import philox_words
+from .philox import philox_range
 
 TAG_WEIGHT = 1
 T_EMBED, T_WQ, T_WK, T_WV, T_WO, T_WGATE, T_WUP, T_WDOWN, T_LM = range(9)
@@ -59,14 +59,14 @@ def init_tensor(seed, tensor_id, layer, n_out, n_in, fan_in, dtype, chunk=1 << 2
     total = n_out * n_in
     out = np.empty(total, dtype=np.float64)
     for s in range(0, total, chunk):
-        idx = np.arange(s, min(total, s + chunk), dtype=np.uint64)
-        w = philox_words(idx, tensor_id, layer, TAG_WEIGHT, seed)
+        n = min(total, s + chunk) - s
+        w = philox_range(s, n, tensor_id, layer, TAG_WEIGHT, seed)
         k = ((w >> np.uint32(8)) | np.uint32(1)).astype(np.float32)
         v = (k * np.float32(2.0 ** -23) - np.float32(1.0)).astype(np.float32)
         x = (v * a).astype(np.float32)
         if dtype == "bf16":
             x = round_bf16(x)
-        out[s:s + len(idx)] = x
+        out[s:s + n] = x
     return out.reshape(n_out, n_in)
 
 

@@ -43,6 +43,18 @@ def philox4x32_10(c0, c1, c2, c3, k0, k1):
             x2.astype(np.uint32), x3.astype(np.uint32))
 
 
+def philox_range(start, n, c1, c2, c3, seed):
+    """philox_words(arange(start, start + n), ...) for scalar c1, c2, c3 and a
+    start that is a multiple of 4: each counter block is evaluated once and its
+    four words are laid out in order (the same values, fewer evaluations)."""
+    assert start % 4 == 0
+    nb = (n + 3) // 4
+    blk = np.arange(start // 4, start // 4 + nb, dtype=np.uint64)
+    seed = int(seed)
+    w = philox4x32_10(blk, c1, c2, c3, seed & 0xFFFFFFFF, (seed >> 32) & 0xFFFFFFFF)
+    return np.stack(w, axis=1).reshape(-1)[:n].astype(np.uint32)
+
+
 def philox_words(idx, c1, c2, c3, seed):
     """Word ``idx & 3`` of Philox(counter=(idx >> 2, c1, c2, c3), key=(seed lo, seed hi))."""
     idx = np.asarray(idx, dtype=np.uint64)

@@ -59,7 +59,8 @@ class RolloutResult:
 
 
 def rollout(cfg, W, prompts, forced, m, k, cap, seed, temperature=1.0, L=1, m_up=None,
-            page=16, early_stop=True, prompt_ids=None, keep_logits=False, alloc=None):
+            page=16, early_stop=True, prompt_ids=None, keep_logits=False, alloc=None,
+            max_steps=None):
     """Run the rollout for prompts ``prompt_ids`` (default all) of the batch.
 
     prompts: [P, Lp] int; forced: [P*m] raw forced lengths (>= 1).
@@ -69,6 +70,8 @@ def rollout(cfg, W, prompts, forced, m, k, cap, seed, temperature=1.0, L=1, m_up
     plan M'_i <= m of Alg. 1; prompt i then has candidates g = i*m + j,
     j < M'_i, and its group runs shortest-only when M'_i >= m_up, dual-end
     otherwise (Alg. 2).
+    max_steps: stop after this many sampling steps even if groups are still
+    open (a prefix of the rollout, for checks on long configurations).
     """
     prompts = np.asarray(prompts)
     P, Lp = prompts.shape
@@ -169,7 +172,7 @@ def rollout(cfg, W, prompts, forced, m, k, cap, seed, temperature=1.0, L=1, m_up
     for g in trajs:
         tcache[g] = caches[g // m]
     step = 1
-    while len(kept) < len(ids):
+    while len(kept) < len(ids) and (max_steps is None or step < max_steps):
         step += 1
         live = [g for g in trajs if st[g] == LIVE]
         n_before = len(live)

@@ -62,3 +62,14 @@ def test_uniformity_chi_square():
     # 63 dof: the 99.99% quantile is about 117
     assert chi2 < 117
     assert abs(u.mean() - 0.5) < 2e-3
+
+
+def test_range_equals_per_word_evaluation():
+    """philox_range evaluates each counter block once; it must give exactly
+    the words philox_words gives element by element."""
+    import numpy as np
+    from oracle.philox import philox_range, philox_words
+    for start, n, seed in ((0, 1, 5), (0, 13, 7), (4096, 1000, 3), (1 << 24, 4097, 1 << 40)):
+        a = philox_range(start, n, 9, 2, 1, seed)
+        b = philox_words(np.arange(start, start + n, dtype=np.uint64), 9, 2, 1, seed)
+        assert np.array_equal(a, b)
