@@ -101,6 +101,27 @@ def cpu_baseline(model, run, budget_s=20.0):
                        f"{time.perf_counter() - t_start:.1f} s of CPU work")}
 
 
+def hbm_read_rate(B, gib=8, reps=10):
+    """HBM read rate this device sustains (GB/s): the library's streaming-read
+    kernel (16-byte loads, 2048 blocks, grid-stride) over a `gib` GiB buffer."""
+    import torch
+    src = torch.zeros(gib << 30, dtype=torch.uint8, device="cuda")
+    sink = torch.empty(8192, dtype=torch.float32, device="cuda")
+    for _ in range(2):
+        B.darts_stream_read(src, sink)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        B.darts_stream_read(src, sink)
+    e1.record()
+    torch.cuda.synchronize()
+    rate = src.numel() * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, sink
+    torch.cuda.empty_cache()
+    return rate
+
+
 def kernel_sweep(B, steps, warmup):
     """Stateless kernels on the sweep's inputs (bf16, data seed 1): decode
     attention over 1024 trajectories with lognormal(1500, 1.0) contexts clipped
@@ -148,6 +169,11 @@ def kernel_sweep(B, steps, warmup):
                         "achieved_GBs": alg / (us * 1e-6) / 1e9,
                         "frac_of_hbm_peak": alg / (us * 1e-6) / 1e9 / HBM_PEAK_GBS}
     del kp, vp
+    torch.cuda.empty_cache()
+    rd = hbm_read_rate(B)
+    out["hbm_read"] = {"GBs": rd, "frac_of_hbm_peak": rd / HBM_PEAK_GBS,
+                       "kernel": "darts_stream_read over 8 GiB"}
+    out["attention"]["frac_of_measured_read"] = out["attention"]["achieved_GBs"] / rd
     bits = sweep_sampler_logits()
     lg = torch.from_numpy(bits.view(np.int16)).cuda().view(torch.bfloat16)
     R, V = bits.shape
@@ -384,6 +410,7 @@ def main():
         fl_ = sum(s["gemm_cls_flop"][i] for s in stats)
         cls[name] = {"ms": ms, "tflops": fl_ / (ms * 1e-3) / 1e12 if ms > 0 else 0.0}
     ro.close()
+    read_gbs = hbm_read_rate(B)
     if args.cost_model_check and not args.no_abort:
         ro2 = B.Rollout(model, run, flags=B.FLAG_STEP_TIMES | B.FLAG_NO_ABORT)
         ro2.run_to_completion(pr, fl)
@@ -423,6 +450,7 @@ def main():
                      "launches": attn_n, "avg_launch_us": 1e3 * attn_ms / max(attn_n, 1),
                      "timed": "HIP events on the context stream around every launch of every 8th decode step",
                      "algorithmic_bytes_per_launch": attn_b / max(attn_n, 1),
+                     "measured_read_GBs": read_gbs, "frac_of_measured_read": ach / read_gbs,
                      "share_of_step_time": attn_ms * 1e-3 / total},
         "gemm": {"bound": "mfma", "achieved": gemm_tf, "peak": peak_mm, "unit": "TFLOP/s",
                  "frac": gemm_tf / peak_mm, "share_of_step_time": gemm_ms * 1e-3 / total,

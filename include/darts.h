@@ -334,6 +334,13 @@ int darts_fit_ptl(const int32_t* h_bsz, const double* h_lat, int32_t n, double* 
 int darts_fill_uniform(void* d_dst, uint64_t n, int32_t tensor, uint64_t seed, int32_t dtype,
                        void* stream);
 
+/* Read d_src[0..bytes) once with 16-byte loads (2048 blocks x 256 threads,
+ * grid-stride) and write 8192 wavefront sums to d_sink (caller-owned, 8192
+ * floats).  A streaming-read reference: the HBM read rate this device
+ * sustains, against which the bandwidth-bound kernels are also reported.
+ * bytes must be a multiple of 16 and d_src 16-byte aligned.                */
+int darts_stream_read(const void* d_src, int64_t bytes, float* d_sink, void* stream);
+
 /* Fill the paged K and V pools of the attention sweep with the values above
  * (tensor 1 for K, 2 for V) at logical index ((page*Hkv + h)*16 + slot)*hd + d,
  * written in the library's physical pool layouts (n_pages pages, dtype as
@@ -440,6 +447,19 @@ int darts_gemm(const void* d_a, const void* d_w, void* d_c, int32_t M, int32_t N
  * operations: atanh series on the reduced mantissa).  d_u in (0, 1).  For
  * bit-exact verification of the sampler's noise.                           */
 int darts_debug_gumbel(const float* d_u, float* d_g, int64_t n, void* stream);
+
+/* The sampler's fast Gumbel map (two hardware log2 evaluations), which only
+ * pre-selects candidates: d_g[i] = -ln(-ln(d_u[i])) approximately, d_u in
+ * [2^-24, 1 - 2^-24].  darts_sampler_gumbel_bound() is the distance from the
+ * exact map (darts_debug_gumbel) that the sampler's filter assumes; the
+ * token is the exact-noise argmax provided the fast map stays within it on
+ * every u = (2k+1) 2^-24, which callers can check exhaustively with these
+ * two entries.  The filter's soundness argument: a thread's best fast score
+ * more than twice that distance (plus float32 rounding of the sums) above
+ * its second best is its exact winner; nearer cases are rescanned exactly.
+ * Same stream and error semantics as darts_debug_gumbel.                   */
+int darts_debug_gumbel_fast(const float* d_u, float* d_g, int64_t n, void* stream);
+float darts_sampler_gumbel_bound(void);
 
 #ifdef __cplusplus
 }

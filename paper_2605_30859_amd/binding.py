@@ -90,6 +90,9 @@ _SIGS = {
     "darts_sample": (C.c_int, [_P, C.c_int32, C.c_int32, C.c_int32, C.c_uint64, _P, _P, C.c_float,
                                _P, _P, _P, _P, _P]),
     "darts_debug_gumbel": (C.c_int, [_P, _P, C.c_int64, _P]),
+    "darts_debug_gumbel_fast": (C.c_int, [_P, _P, C.c_int64, _P]),
+    "darts_stream_read": (C.c_int, [_P, C.c_int64, _P, _P]),
+    "darts_sampler_gumbel_bound": (C.c_float, []),
     "darts_gemm_workspace_bytes": (C.c_size_t, [C.c_int32, C.c_int32, C.c_int32]),
     "darts_gemm": (C.c_int, [_P, _P, _P, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                              _P, C.c_size_t, _P]),
@@ -215,6 +218,19 @@ def darts_gemm(a, w, c, M, N, K, dtype, epilogue, workspace=None, stream=None):
 
 def darts_debug_gumbel(u, g, stream=None):
     _check(load_library().darts_debug_gumbel(_ptr(u), _ptr(g), u.numel(), _stream(stream)))
+
+
+def darts_debug_gumbel_fast(u, g, stream=None):
+    _check(load_library().darts_debug_gumbel_fast(_ptr(u), _ptr(g), u.numel(), _stream(stream)))
+
+
+def darts_stream_read(src, sink, stream=None):
+    _check(load_library().darts_stream_read(_ptr(src), src.numel() * src.element_size(), _ptr(sink),
+                                            _stream(stream)))
+
+
+def darts_sampler_gumbel_bound():
+    return float(load_library().darts_sampler_gumbel_bound())
 
 
 # ---------------------------------------------------------------- planning

@@ -954,6 +954,13 @@ int darts_fill_uniform(void* d_dst, uint64_t n, int32_t tensor, uint64_t seed, i
   return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
 }
 
+int darts_stream_read(const void* d_src, int64_t bytes, float* d_sink, void* stream) {
+  if (bytes < 0 || bytes % 16 || (bytes && (!d_src || ((uintptr_t)d_src & 15))) || !d_sink)
+    return DARTS_EINVAL;
+  hipError_t e = launch_stream_read(d_src, bytes / 16, d_sink, (hipStream_t)stream);
+  return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
+}
+
 int darts_fill_kv_pool(void* d_k_pool, void* d_v_pool, int64_t n_pages, int32_t n_kv_heads,
                        int32_t head_dim, uint64_t seed, int32_t dtype, void* stream) {
   if (!d_k_pool || !d_v_pool || n_pages < 1 || n_kv_heads < 1 || head_dim % 8) return DARTS_EINVAL;
@@ -1058,9 +1065,17 @@ int darts_gemm(const void* d_a, const void* d_w, void* d_c, int32_t M, int32_t N
 
 int darts_debug_gumbel(const float* d_u, float* d_g, int64_t n, void* stream) {
   if ((!d_u || !d_g) && n > 0) return DARTS_EINVAL;
-  hipError_t e = launch_gumbel_map(d_u, d_g, n, (hipStream_t)stream);
+  hipError_t e = launch_gumbel_map(d_u, d_g, n, false, (hipStream_t)stream);
   return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
 }
+
+int darts_debug_gumbel_fast(const float* d_u, float* d_g, int64_t n, void* stream) {
+  if ((!d_u || !d_g) && n > 0) return DARTS_EINVAL;
+  hipError_t e = launch_gumbel_map(d_u, d_g, n, true, (hipStream_t)stream);
+  return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
+}
+
+float darts_sampler_gumbel_bound(void) { return gumbel_fast_bound(); }
 
 int darts_group_advantages(const int32_t* d_kept, int32_t n_groups, int32_t k, const float* d_reward,
                            int32_t n_traj, float eps, float* d_adv, void* stream) {

@@ -115,6 +115,26 @@ hipError_t launch_fill_uniform(void* dst, uint64_t n, uint32_t tensor, uint64_t 
   return hipGetLastError();
 }
 
+// Streaming read of n16 16-byte words (the HBM read rate that the attention
+// kernel's roofline is compared with): grid-stride float4 loads, one sum per
+// wavefront written to sink so the loads are not dead.
+__global__ void __launch_bounds__(256) stream_read_kernel(const float4* __restrict__ src, int64_t n16,
+                                                          float* __restrict__ sink) {
+  float s = 0.f;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += (int64_t)gridDim.x * 256) {
+    const float4 v = src[i];
+    s += (v.x + v.y) + (v.z + v.w);
+  }
+  s = wave_sum(s);
+  if ((threadIdx.x & 63) == 0) sink[blockIdx.x * 4 + (threadIdx.x >> 6)] = s;
+}
+
+hipError_t launch_stream_read(const void* src, int64_t n16, float* sink, hipStream_t st) {
+  hipLaunchKernelGGL(stream_read_kernel, dim3(kStreamReadBlocks), dim3(256), 0, st,
+                     (const float4*)src, n16, sink);
+  return hipGetLastError();
+}
+
 // Logical index ((page*Hkv + h)*16 + slot)*hd + d  ->  physical pool layouts.
 template <bool BF16>
 __global__ void fill_kv_kernel(void* k, void* v, int64_t n_pages, int hkv, int hd, uint32_t k0,

@@ -7,6 +7,19 @@
 // then the log-prob of the taken token.  In the stateful form the same block
 // applies the exogenous termination rule (forced end-of-sequence length,
 // truncation at cap) and accumulates the trajectory's score.
+//
+// Filtered argmax.  g_i is defined by the library's exact float32 logarithm
+// (two per element, each with a correctly rounded division), which would
+// dominate the kernel's arithmetic.  The scan instead scores every element
+// with a fast map (two hardware log2 evaluations) whose distance from the
+// exact map is at most kGumbelFastBound over all 2^23 possible u (checked
+// exhaustively on the device by the test suite), and each thread keeps its
+// two best fast scores.  If they are further apart than twice the bound on
+// |fast score - exact score| (noise error plus the float32 roundings of the
+// two sums), the thread's exact winner is its fast winner, whose exact score
+// is then computed once; otherwise (a near tie, probability ~1e-5 per thread)
+// the thread re-scans its elements with the exact map.  The token is
+// therefore the exact-map argmax, bit for bit, in every case.
 #include <math.h>
 
 #include "common.h"
@@ -51,6 +64,24 @@ __device__ __forceinline__ void load4(const void* row, int j, float z[4]) {
   }
 }
 
+// Fast Gumbel map: -ln(-ln u) from two hardware log2 evaluations (the only
+// approximation; products by ln 2 in float32).  u in [2^-24, 1 - 2^-24]
+// keeps both log2 arguments normal.
+__device__ __forceinline__ float gumbel_fast(float u) {
+  constexpr float kLn2 = 0.693147180559945309f;
+  const float a = -kLn2 * __builtin_amdgcn_logf(u);
+  return -kLn2 * __builtin_amdgcn_logf(a);
+}
+// |gumbel_fast(u) - gumbel_of(u)| <= kGumbelFastBound for every u the sampler
+// draws (measured maximum 1.9e-6; the bound is 2^-17)
+constexpr float kGumbelFastBound = 7.62939453125e-06f;
+
+template <bool BF16>
+__device__ __forceinline__ float logit_at(const void* row, int i, bool tscale, float temperature) {
+  float z = BF16 ? bf16_to_f32(((const bf16_t*)row)[i]) : ((const float*)row)[i];
+  return tscale ? __fdiv_rn(z, temperature) : z;
+}
+
 template <bool BF16, bool STATEFUL>
 __global__ void __launch_bounds__(256) sample_kernel(SampleArgs a) {
   __shared__ SoftState ss[4];
@@ -65,7 +96,8 @@ __global__ void __launch_bounds__(256) sample_kernel(SampleArgs a) {
   const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
   const bool tscale = a.temperature != 1.0f;
   SoftState st = {-INFINITY, 0.f, 0.f};
-  Best best = {-INFINITY, 0x7fffffff};
+  float b1 = -INFINITY, b2 = -INFINITY;   // this thread's two best fast scores
+  int i1 = 0x7fffffff;                     // index of the best
   const int n4 = a.vocab >> 2;
   for (int j = tid; j < n4; j += 256) {
     float z[4];
@@ -90,8 +122,33 @@ __global__ void __launch_bounds__(256) sample_kernel(SampleArgs a) {
       const float ez = __expf(d);
       st.s += ez;
       st.t = fmaf(ez, d, st.t);
-      const float sc = z[e] + gumbel_of(open_unit(p.x[e]));
-      if (sc > best.v) { best.v = sc; best.i = 4 * j + e; }
+      const float sf = z[e] + gumbel_fast(open_unit(p.x[e]));
+      const bool c1 = sf > b1, c2 = sf > b2;
+      b2 = c1 ? b1 : (c2 ? sf : b2);
+      b1 = c1 ? sf : b1;
+      i1 = c1 ? 4 * j + e : i1;
+    }
+  }
+  // exact score of this thread's winner, or an exact re-scan on a near tie
+  Best best = {-INFINITY, 0x7fffffff};
+  const float margin =
+      2.0f * (kGumbelFastBound + 2.384185791015625e-07f * fmaxf(fabsf(b1), fabsf(b2)));   // 2^-22 |s|
+  if (b1 - b2 > margin) {
+    const int j = i1 >> 2, e = i1 & 3;
+    const Philox4 p = philox4x32_10((uint32_t)j, (uint32_t)g, (uint32_t)step, kTagSample, k0, k1);
+    best.v = logit_at<BF16>(row, i1, tscale, a.temperature) + gumbel_of(open_unit(p.x[e]));
+    best.i = i1;
+  } else {
+    for (int j = tid; j < n4; j += 256) {
+      float z[4];
+      load4<BF16>(row, j, z);
+      const Philox4 p = philox4x32_10((uint32_t)j, (uint32_t)g, (uint32_t)step, kTagSample, k0, k1);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float zz = tscale ? __fdiv_rn(z[e], a.temperature) : z[e];
+        const float sc = zz + gumbel_of(open_unit(p.x[e]));
+        if (sc > best.v) { best.v = sc; best.i = 4 * j + e; }
+      }
     }
   }
   // wavefront merge
@@ -169,11 +226,18 @@ __global__ void gumbel_map_kernel(const float* __restrict__ u, float* __restrict
        i += (int64_t)gridDim.x * blockDim.x)
     g[i] = gumbel_of(u[i]);
 }
-hipError_t launch_gumbel_map(const float* u, float* g, int64_t n, hipStream_t st) {
+__global__ void gumbel_fast_map_kernel(const float* __restrict__ u, float* __restrict__ g, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    g[i] = gumbel_fast(u[i]);
+}
+hipError_t launch_gumbel_map(const float* u, float* g, int64_t n, bool fast, hipStream_t st) {
   if (n <= 0) return hipSuccess;
   int64_t blocks = (n + 255) / 256;
   if (blocks > 16384) blocks = 16384;
-  hipLaunchKernelGGL(gumbel_map_kernel, dim3((unsigned)blocks), dim3(256), 0, st, u, g, n);
+  if (fast) hipLaunchKernelGGL(gumbel_fast_map_kernel, dim3((unsigned)blocks), dim3(256), 0, st, u, g, n);
+  else hipLaunchKernelGGL(gumbel_map_kernel, dim3((unsigned)blocks), dim3(256), 0, st, u, g, n);
   return hipGetLastError();
 }
+float gumbel_fast_bound() { return kGumbelFastBound; }
 }  // namespace darts

@@ -18,6 +18,10 @@ hipError_t launch_init_weights(void* dst, bool bf16, int64_t n_out, int64_t n_in
                                uint32_t tensor_id, uint32_t layer, uint64_t seed, RowMap map,
                                hipStream_t st);
 hipError_t launch_rope_table(float2* table, int max_pos, int hd, double theta, hipStream_t st);
+// streaming read (HBM read-rate reference): kStreamReadBlocks x 256 threads,
+// one float per wavefront written to sink
+constexpr int kStreamReadBlocks = 2048;
+hipError_t launch_stream_read(const void* src, int64_t n16, float* sink, hipStream_t st);
 hipError_t launch_fill_uniform(void* dst, uint64_t n, uint32_t tensor, uint64_t seed, bool bf16,
                                hipStream_t st);
 hipError_t launch_fill_kv_pool(void* k, void* v, int64_t n_pages, int hkv, int hd, uint64_t seed,
@@ -112,7 +116,8 @@ struct SampleArgs {
   int32_t* hist_tok; float* hist_lp;   // NULL or [n_traj][cap]: token t of trajectory g at g*cap + t
 };
 hipError_t launch_sample(const SampleArgs& a, hipStream_t st);
-hipError_t launch_gumbel_map(const float* u, float* g, int64_t n, hipStream_t st);
+hipError_t launch_gumbel_map(const float* u, float* g, int64_t n, bool fast, hipStream_t st);
+float gumbel_fast_bound();   // the fast map's distance bound the sampler's filter assumes
 
 // ---- selection / pages (k_select.hip)
 struct GroupArgs {

@@ -48,6 +48,70 @@ def test_gumbel_map_bit_exact_all_u():
     assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
 
 
+def test_gumbel_fast_map_within_filter_bound_all_u():
+    """The sampler pre-selects candidates with a fast Gumbel map and only the
+    exact map decides; that is sound if the fast map stays within the bound
+    the filter assumes on every one of the 2^23 possible u."""
+    B = _b()
+    say("fast gumbel map: 2^23 inputs")
+    k = np.arange(1 << 23, dtype=np.uint64) * 2 + 1
+    u = (k.astype(np.float32) * np.float32(2.0 ** -24)).astype(np.float32)
+    ud = torch.from_numpy(u).to(DEV)
+    exact, fast = torch.empty_like(ud), torch.empty_like(ud)
+    B.darts_debug_gumbel(ud, exact)
+    B.darts_debug_gumbel_fast(ud, fast)
+    torch.cuda.synchronize()
+    err = (fast.double() - exact.double()).abs().max().item()
+    bound = B.darts_sampler_gumbel_bound()
+    say(f"fast gumbel map: max |fast - exact| = {err:.3e}, filter bound {bound:.3e}")
+    assert np.array_equal(exact.cpu().numpy().view(np.uint32), gumbel_f32(u).view(np.uint32))
+    assert err <= bound
+
+
+def test_sampler_filter_near_ties():
+    """Logits built from the oracle's own Gumbel noise so that several
+    perturbed scores tie exactly or within a few ulp: in one thread's
+    elements (4 consecutive ids, ids 1024 apart), across threads, and a
+    unique winner one ulp above a same-thread runner-up.  These take the
+    sampler's exact re-scan; the token must still be the oracle's
+    first-maximal index."""
+    from oracle.sampler import gumbel_noise
+    B = _b()
+    rows, vocab, seed = 16, 4096, 424242
+    rng = np.random.default_rng(3)
+    l32 = (rng.normal(0, 1, (rows, vocab)) - 30.0).astype(np.float32)
+    traj = np.arange(rows, dtype=np.int32) * 5 + 1
+    step = np.arange(rows, dtype=np.int32) % 3
+    C = np.float32(5.0)
+    for r in range(rows):
+        g = gumbel_noise(vocab, int(traj[r]), int(step[r]), seed)
+        kind = r % 4
+        if kind == 0:      # one thread: ids 4j..4j+3 and 4(j+256)+1
+            j = int(rng.integers(0, 256))
+            picks = [4 * j, 4 * j + 1, 4 * j + 2, 4 * j + 3, 4 * (j + 256) + 1]
+        elif kind == 1:    # several threads
+            picks = [int(x) for x in rng.choice(vocab, 6, replace=False)]
+        else:              # a runner-up within one ulp, same thread (2) or not (3)
+            j = int(rng.integers(0, 256))
+            picks = [4 * j + 2, 4 * (j + 512)] if kind == 2 else [4 * j + 2, 4 * ((j + 7) % 256) + 3]
+        for i in picks:
+            l32[r, i] = np.float32(C - g[i])
+        if kind >= 2:
+            l32[r, picks[1]] = np.nextafter(l32[r, picks[1]], np.float32(np.inf))
+    logits = torch.from_numpy(l32).to(DEV)
+    td, sd = torch.from_numpy(traj).to(DEV), torch.from_numpy(step).to(DEV)
+    tok = torch.empty(rows, dtype=torch.int32, device=DEV)
+    lp = torch.empty(rows, dtype=torch.float32, device=DEV)
+    ent = torch.empty(rows, dtype=torch.float32, device=DEV)
+    B.darts_sample(logits, B.DARTS_F32, seed, td, sd, 1.0, None, tok, lp, ent)
+    torch.cuda.synchronize()
+    tok, lp, ent = tok.cpu().numpy(), lp.cpu().numpy(), ent.cpu().numpy()
+    for r in range(rows):
+        stok, slp, sent = sample_row(l32[r], 1.0, int(traj[r]), int(step[r]), seed)
+        assert tok[r] == stok, (r, tok[r], stok)
+        assert abs(lp[r] - slp) < 1e-4 and abs(ent[r] - sent) < 1e-4
+
+
 def _bf16_tensor(bits):
     return torch.from_numpy(bits.view(np.int16)).to(DEV).view(torch.bfloat16)
 
@@ -88,8 +152,9 @@ def test_sampler_small(dtype, rows, vocab, temp):
 
 
 def test_sampler_full_sweep_size():
-    """1024 x 151936 bf16 logits ~ N(0, 3) (the sweep's shape); every row's
-    token checked bit-exact on a sample of rows."""
+    """1024 x 151936 bf16 logits ~ N(0, 3) (the sweep's shape); tokens
+    bit-exact on every 8th row and the last, log-prob and entropy within
+    1e-3."""
     B = _b()
     rows, vocab = SWEEP["samp_rows"], SWEEP["samp_vocab"]
     say(f"sampler sweep {rows}x{vocab}")
@@ -105,7 +170,7 @@ def test_sampler_full_sweep_size():
     torch.cuda.synchronize()
     tok, lp, ent = tok.cpu().numpy(), lp.cpu().numpy(), ent.cpu().numpy()
     l32 = None
-    for r in list(range(0, rows, 97)) + [rows - 1]:
+    for r in list(range(0, rows, 8)) + [rows - 1]:
         row = f32_from_bf16_bits(bits[r])
         stok, slp, sent = sample_row(row, 1.0, r, 0, seed)
         assert tok[r] == stok
