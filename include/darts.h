@@ -326,7 +326,10 @@ int darts_fit_ptl(const int32_t* h_bsz, const double* h_lat, int32_t n, double* 
 
 /* ----------------------------------------------------- stateless kernels  */
 /* These run one kernel of the path on caller-provided device buffers, for
- * kernel sweeps and parity checks "given the same inputs".                 */
+ * kernel sweeps and parity checks "given the same inputs".  A call whose
+ * work size (rows, M, trajectories, groups, bytes, elements) is zero checks
+ * its scalar arguments, does nothing and returns DARTS_OK; its device
+ * pointers may then be NULL.                                               */
 
 /* Fill d_dst[0..n) with element idx = bf16(((w>>8)|1)*2^-23 - 1),
  * w = Philox(key=seed, counter=(idx>>2, tensor, 0, 3)) word idx&3, stored as

@@ -49,14 +49,17 @@ def top2_margin(logits32, temperature, traj, step, seed):
 
 
 def logprob_entropy(logits, temperature, token):
-    """log p(token) and entropy of softmax(logits / T), evaluated in float64."""
+    """log p(token) and entropy of softmax(logits / T), evaluated in float64.
+    Logits of -inf (masked entries) have probability 0 and, with the usual
+    convention 0 log 0 = 0, contribute nothing to the entropy."""
     z = np.asarray(logits, dtype=np.float64) / float(temperature)
     mx = np.max(z)
     e = np.exp(z - mx)
     ssum = np.sum(e)
     lse = mx + np.log(ssum)
     p = e / ssum
-    ent = lse - np.sum(p * z)
+    live = p > 0                                    # 0 log 0 = 0 (masked -inf logits)
+    ent = lse - np.sum(p[live] * z[live])
     return float(z[token] - lse), float(ent)
 
 

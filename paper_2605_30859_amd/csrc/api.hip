@@ -955,8 +955,9 @@ int darts_fill_uniform(void* d_dst, uint64_t n, int32_t tensor, uint64_t seed, i
 }
 
 int darts_stream_read(const void* d_src, int64_t bytes, float* d_sink, void* stream) {
-  if (bytes < 0 || bytes % 16 || (bytes && (!d_src || ((uintptr_t)d_src & 15))) || !d_sink)
-    return DARTS_EINVAL;
+  if (bytes < 0 || bytes % 16) return DARTS_EINVAL;
+  if (bytes == 0) return DARTS_OK;
+  if (!d_src || ((uintptr_t)d_src & 15) || !d_sink) return DARTS_EINVAL;
   hipError_t e = launch_stream_read(d_src, bytes / 16, d_sink, (hipStream_t)stream);
   return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
 }
@@ -981,13 +982,14 @@ int darts_attn_decode(const void* d_q, const void* d_k_pool, const void* d_v_poo
                            const int32_t* d_ctx_len, int32_t n_rows, int32_t n_q_heads,
                            int32_t n_kv_heads, int32_t head_dim, int32_t max_ctx, int32_t dtype,
                            void* d_out, void* d_workspace, size_t workspace_bytes, void* stream) {
-  if (!d_q || !d_k_pool || !d_v_pool || !d_page_table || !d_ctx_len || !d_out) return DARTS_EINVAL;
   if (n_rows < 0 || n_q_heads < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads ||
       n_q_heads / n_kv_heads > 16 || max_ctx < 1 || n_pages < 1)
     return DARTS_EINVAL;
   if (!(head_dim == 32 || head_dim == 64 || head_dim == 128)) return DARTS_EINVAL;
   if (dtype != DARTS_F32 && dtype != DARTS_BF16) return DARTS_EINVAL;
   if (pt_stride < (max_ctx + kPage - 1) / kPage) return DARTS_EINVAL;
+  if (n_rows == 0) return DARTS_OK;
+  if (!d_q || !d_k_pool || !d_v_pool || !d_page_table || !d_ctx_len || !d_out) return DARTS_EINVAL;
   if (workspace_bytes < attn_workspace_bytes(n_rows, n_q_heads, n_kv_heads, head_dim, max_ctx))
     return DARTS_EINVAL;
   hipError_t e = launch_attention(d_q, d_k_pool, d_v_pool, n_pages, d_page_table, pt_stride, nullptr,
@@ -1009,7 +1011,6 @@ int darts_attn_decode_shared(const void* d_q, const void* d_k_pool, const void* 
                              int32_t prefix_pages, int32_t ctx_len, int32_t n_rows, int32_t n_q_heads,
                              int32_t n_kv_heads, int32_t head_dim, int32_t dtype, void* d_out,
                              void* d_workspace, size_t workspace_bytes, void* stream) {
-  if (!d_q || !d_k_pool || !d_v_pool || !d_page_table || !d_row_traj || !d_out) return DARTS_EINVAL;
   if (n_rows < 0 || n_q_heads < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads ||
       n_q_heads / n_kv_heads > 16 || n_pages < 1 || pt_rows < 1 || m < 1 || prefix_pages < 1)
     return DARTS_EINVAL;
@@ -1017,6 +1018,7 @@ int darts_attn_decode_shared(const void* d_q, const void* d_k_pool, const void* 
   if (dtype != DARTS_BF16) return DARTS_EINVAL;
   if (ctx_len <= prefix_pages * kPage || pt_stride < (ctx_len + kPage - 1) / kPage) return DARTS_EINVAL;
   if (n_rows == 0) return DARTS_OK;
+  if (!d_q || !d_k_pool || !d_v_pool || !d_page_table || !d_row_traj || !d_out) return DARTS_EINVAL;
   if (workspace_bytes <
       attn_shared_workspace_bytes(n_rows, n_q_heads, n_kv_heads, head_dim, ctx_len, prefix_pages))
     return DARTS_EINVAL;
@@ -1031,9 +1033,10 @@ int darts_sample(const void* d_logits, int32_t n_rows, int32_t vocab, int32_t dt
                  const int32_t* d_traj, const int32_t* d_step, float temperature,
                  const int32_t* d_force, int32_t* d_token, float* d_logprob, float* d_entropy,
                  void* stream) {
-  if (!d_logits || !d_traj || !d_step || n_rows < 0 || vocab < 4 || vocab % 4 || !(temperature > 0.f))
-    return DARTS_EINVAL;
+  if (n_rows < 0 || vocab < 4 || vocab % 4 || !(temperature > 0.f)) return DARTS_EINVAL;
   if (dtype != DARTS_F32 && dtype != DARTS_BF16) return DARTS_EINVAL;
+  if (n_rows == 0) return DARTS_OK;
+  if (!d_logits || !d_traj || !d_step) return DARTS_EINVAL;
   SampleArgs a{};
   a.logits = d_logits; a.n_rows = n_rows; a.vocab = vocab; a.bf16 = dtype == DARTS_BF16;
   a.seed = seed; a.temperature = temperature; a.traj = d_traj; a.step = d_step; a.force = d_force;
@@ -1050,11 +1053,13 @@ size_t darts_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K) {
 int darts_gemm(const void* d_a, const void* d_w, void* d_c, int32_t M, int32_t N, int32_t K,
                int32_t dtype, int32_t epilogue, void* d_workspace, size_t workspace_bytes,
                void* stream) {
-  if (!d_a || !d_w || !d_c || M < 0 || N < 1 || K < 1) return DARTS_EINVAL;
+  if (M < 0 || N < 1 || K < 1) return DARTS_EINVAL;
   if (dtype != DARTS_F32 && dtype != DARTS_BF16) return DARTS_EINVAL;
   if (epilogue < 0 || epilogue > 3) return DARTS_EINVAL;
   if (epilogue == 3 && N % 32) return DARTS_EINVAL;
   if (dtype == DARTS_BF16 && (N % 128 || K % 256)) return DARTS_EINVAL;
+  if (M == 0) return DARTS_OK;
+  if (!d_a || !d_w || !d_c) return DARTS_EINVAL;
   const int ldc = epilogue == 3 ? N / 2 : N;
   const size_t need = dtype == DARTS_BF16 ? gemm_workspace_bytes(M, N, K) : 0;
   if (need > workspace_bytes || (need && !d_workspace)) return DARTS_EINVAL;
@@ -1088,9 +1093,10 @@ int darts_group_advantages(const int32_t* d_kept, int32_t n_groups, int32_t k, c
 int darts_select_groups(uint8_t* d_status, const int32_t* d_len, const float* d_mean_lp,
                         int32_t n_traj, int32_t m, int32_t k, int32_t L, int32_t m_up,
                         int32_t early_stop, int32_t* d_kept, uint8_t* d_complete, void* stream) {
-  if (!d_status || !d_len || !d_mean_lp || !d_kept || !d_complete) return DARTS_EINVAL;
   if (m < 1 || m > 64 || k < 1 || k > m || n_traj < 0 || n_traj % m) return DARTS_EINVAL;
   if (m < m_up && (L < 1 || L >= k)) return DARTS_EINVAL;
+  if (n_traj == 0) return DARTS_OK;
+  if (!d_status || !d_len || !d_mean_lp || !d_kept || !d_complete) return DARTS_EINVAL;
   GroupArgs a{};
   a.status = d_status; a.len = d_len; a.mean_lp = d_mean_lp; a.n_groups = n_traj / m;
   a.m = m; a.k = k; a.L = L; a.m_up = m_up; a.early_stop = early_stop ? 1 : 0;

@@ -118,7 +118,9 @@ __global__ void __launch_bounds__(256) sample_kernel(SampleArgs a) {
     }
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const float d = z[e] - st.m;
+      // masked (-inf) logits add nothing: d clamps to -FLT_MAX (also when the
+      // running max is still -inf), so e^d = 0 and the entropy term 0 * d = 0
+      const float d = fmaxf(z[e] - st.m, -3.40282347e+38f);
       const float ez = __expf(d);
       st.s += ez;
       st.t = fmaf(ez, d, st.t);

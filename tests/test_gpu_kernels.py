@@ -112,6 +112,47 @@ def test_sampler_filter_near_ties():
         assert abs(lp[r] - slp) < 1e-4 and abs(ent[r] - sent) < 1e-4
 
 
+def test_sampler_edge_rows():
+    """Degenerate rows, each against the oracle: the smallest vocabulary
+    (V = 4), one logit 40 above the rest (entropy ~ 0, log-prob ~ 0), masked
+    rows with only 3 finite logits (the token is one of them, scores are
+    those of the finite sub-vocabulary), a row whose first 1024 logits are
+    masked (whole threads see only -inf), and equal logits."""
+    B = _b()
+    seed = 31337
+    cases = []
+    rng = np.random.default_rng(9)
+    cases.append(rng.normal(0, 2, 4).astype(np.float32))
+    z = rng.normal(0, 1, 2048).astype(np.float32)
+    z[777] = 40.0
+    cases.append(z)
+    z = np.full(4096, -np.inf, dtype=np.float32)
+    z[[5, 2049, 4095]] = [0.5, -1.0, 0.25]
+    cases.append(z)
+    z = rng.normal(0, 1, 4096).astype(np.float32)
+    z[:1024] = -np.inf
+    cases.append(z)
+    cases.append(np.zeros(4096, dtype=np.float32))
+    for ci, z in enumerate(cases):
+        V = len(z)
+        traj = torch.tensor([ci * 3 + 1], dtype=torch.int32, device=DEV)
+        step = torch.tensor([ci], dtype=torch.int32, device=DEV)
+        tok = torch.empty(1, dtype=torch.int32, device=DEV)
+        lp = torch.empty(1, dtype=torch.float32, device=DEV)
+        ent = torch.empty(1, dtype=torch.float32, device=DEV)
+        B.darts_sample(torch.from_numpy(z).to(DEV).view(1, V), B.DARTS_F32, seed, traj, step, 1.0, None,
+                       tok, lp, ent)
+        torch.cuda.synchronize()
+        stok, slp, sent = sample_row(z, 1.0, ci * 3 + 1, ci, seed)
+        assert int(tok.item()) == stok, (ci, int(tok.item()), stok)
+        assert np.isfinite(lp.item()) and np.isfinite(ent.item()), ci
+        assert abs(lp.item() - slp) < 1e-5 and abs(ent.item() - sent) < 1e-5, (ci, lp.item(), slp, ent.item(), sent)
+        if ci == 1:
+            assert stok == 777 and ent.item() < 1e-6
+        if ci == 2:
+            assert stok in (5, 2049, 4095)
+
+
 def _bf16_tensor(bits):
     return torch.from_numpy(bits.view(np.int16)).to(DEV).view(torch.bfloat16)
 

@@ -91,6 +91,23 @@ def test_closed_forms():
     assert abs(lp2 - lp1) < 1e-15 and abs(e2 - e1) < 1e-15
 
 
+def test_masked_logits():
+    """Entries at -inf have probability 0: the scores equal those of the
+    finite sub-vocabulary (0 log 0 = 0), and the sampled token is never a
+    masked one."""
+    z = np.full(64, -np.inf)
+    z[[3, 17, 40]] = [0.5, 0.5, 0.5]
+    lp, e = logprob_entropy(z, 1.0, 17)
+    assert abs(e - math.log(3)) < 1e-12 and abs(lp + math.log(3)) < 1e-12
+    sub = np.array([1.0, -2.0, 0.25])
+    z[[3, 17, 40]] = sub
+    lp, e = logprob_entropy(z, 1.0, 40)
+    lp_s, e_s = logprob_entropy(sub, 1.0, 2)
+    assert abs(lp - lp_s) < 1e-12 and abs(e - e_s) < 1e-12
+    for t in range(20):
+        assert sample_token(z.astype(np.float32), 1.0, t, 0, 5) in (3, 17, 40)
+
+
 def test_gumbel_max_frequencies_match_softmax():
     V = 8
     z = np.array([0.3, -1.2, 2.0, 0.0, 1.1, -0.4, 0.8, -2.5])
