@@ -76,7 +76,13 @@ def test_gemm_qkv_shape_all_batch_sizes(M):
 @pytest.mark.parametrize("M,N,K,epi", [(512, 4096, 4096, 2), (37, 4096, 4096, 2),
                                        (512, 24576, 4096, 3), (9, 24576, 4096, 3), (130, 24576, 4096, 3),
                                        (512, 4096, 12288, 2), (3, 4096, 12288, 2), (200, 4096, 12288, 2),
-                                       (64, 1536, 1024, 1), (300, 32000, 1024, 0), (1024, 5120, 2048, 0)])
+                                       (64, 1536, 1024, 1), (300, 32000, 1024, 0), (1024, 5120, 2048, 0),
+                                       # small-batch exact-fill tiles (64 and 128 rows, 64 and 96 wide),
+                                       # every epilogue, with and without a K split
+                                       (64, 4096, 4096, 2), (100, 4096, 4096, 2), (16, 4096, 12288, 2),
+                                       (64, 4096, 12288, 2), (50, 24576, 4096, 3), (128, 24576, 4096, 3),
+                                       (60, 6144, 4096, 1), (97, 6144, 4096, 1), (40, 8192, 1024, 3),
+                                       (33, 2048, 4096, 2)])
 def test_gemm_decoder_shapes(M, N, K, epi):
     print(f"gemm M={M} N={N} K={K} epi={epi}", flush=True)
     _run(M, N, K, epi)
