@@ -101,6 +101,31 @@ def cpu_baseline(model, run, budget_s=20.0):
                        f"{time.perf_counter() - t_start:.1f} s of CPU work")}
 
 
+def rollout_bound(model, run, rows, hbm_gbs, mfma_tflops):
+    """Roofline bound of the measured schedule: per decode step with B live
+    rows at context Lp + i, KV bytes / HBM + max(weight bytes / HBM, GEMM
+    FLOP / MFMA peak); the prefill adds the prompt tokens' GEMM FLOP (or its
+    weight read).  MoE weights count every expert (an upper bound on the
+    bytes, so the bound is optimistic there)."""
+    d, hq, hkv, hd, L = model.d_model, model.n_q_heads, model.n_kv_heads, model.head_dim, model.n_layers
+    eb = 2 if model.dtype == "bf16" else 4
+    attn_p = d * (hq + 2 * hkv) * hd + hq * hd * d
+    if model.is_moe:
+        ffn_all = model.n_experts * 3 * d * model.expert_ffn + d * model.n_experts
+        ffn_act = model.top_k * 3 * d * model.expert_ffn + d * model.n_experts
+    else:
+        ffn_all = ffn_act = 3 * d * model.ffn_dim
+    w_bytes = (L * (attn_p + ffn_all) + d * model.vocab) * eb
+    flop_tok = 2.0 * (L * (attn_p + ffn_act) + d * model.vocab)
+    kv_tok = 2 * L * hkv * hd * eb
+    hbm, mm = hbm_gbs * 1e9, mfma_tflops * 1e12
+    t = max(w_bytes / hbm, run.n_prompts * run.prompt_len * flop_tok / mm)
+    for i, b in enumerate(rows, start=1):
+        b = float(b)
+        t += b * (run.prompt_len + i) * kv_tok / hbm + max(w_bytes / hbm, b * flop_tok / mm)
+    return t
+
+
 def hbm_read_rate(B, gib=8, reps=10):
     """HBM read rate this device sustains (GB/s): the library's streaming-read
     kernel (16-byte loads, 2048 blocks, grid-stride) over a `gib` GiB buffer."""
@@ -411,6 +436,8 @@ def main():
         cls[name] = {"ms": ms, "tflops": fl_ / (ms * 1e-3) / 1e12 if ms > 0 else 0.0}
     ro.close()
     read_gbs = hbm_read_rate(B)
+    bound_peak = rollout_bound(model, run, rows, HBM_PEAK_GBS, peak_mm)
+    bound_read = rollout_bound(model, run, rows, read_gbs, peak_mm)
     if args.cost_model_check and not args.no_abort:
         ro2 = B.Rollout(model, run, flags=B.FLAG_STEP_TIMES | B.FLAG_NO_ABORT)
         ro2.run_to_completion(pr, fl)
@@ -456,6 +483,13 @@ def main():
                  "frac": gemm_tf / peak_mm, "share_of_step_time": gemm_ms * 1e-3 / total,
                  "by_class": cls},
         "cost_model": cost_model,
+        "rollout_bound": {
+            "what": "roofline bound of the measured schedule (per step: KV bytes / HBM + max(weights / HBM, "
+                    "GEMM FLOP / MFMA peak), plus the prefill)",
+            "bound_s_at_peak": bound_peak, "tokens_per_s_at_peak": stats[-1]["tokens_decoded"] / bound_peak,
+            "frac_at_peak": bound_peak / float(np.mean(walls)),
+            "bound_s_at_measured_read": bound_read,
+            "frac_at_measured_read": bound_read / float(np.mean(walls))},
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:
