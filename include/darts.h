@@ -315,6 +315,13 @@ int darts_allocate_redundancy(const double* h_sigma, const uint8_t* h_seen, int3
  * parallel ranks the batch cost is the maximum over ranks.                  */
 int darts_rollout_cost(const int32_t* h_len, int32_t n, const double* h_ptl, double* h_T);
 
+/* Eq. 4 under data parallelism (Sec. 4.2.1): trajectory i runs on rank
+ * h_rank[i] in [0, n_ranks); each rank's batch costs Eq. 4 over its own
+ * lengths and *h_T is the maximum over ranks (an empty rank costs 0).
+ * DARTS_EINVAL for a rank out of range.                                     */
+int darts_rollout_cost_dp(const int32_t* h_len, const int32_t* h_rank, int32_t n, int32_t n_ranks,
+                          const double* h_ptl, double* h_T);
+
 /* Three-stage piecewise-linear PTL fit (App. A): least squares of
  * h_lat[i] ~ PTL(h_bsz[i]) over every breakpoint pair b1 = xs[i] < b2 = xs[j],
  * 1 <= i < j <= D-2, of the D distinct batch sizes xs (ascending), the

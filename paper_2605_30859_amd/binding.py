@@ -72,6 +72,7 @@ _SIGS = {
     "darts_allocate_redundancy": (C.c_int, [_P, _P, C.c_int32, C.c_int32, C.c_int32, C.c_int64, _P]),
     "darts_get_step_times": (C.c_int, [_P, _P, _P, C.c_int32, C.POINTER(C.c_int32), C.POINTER(C.c_float)]),
     "darts_rollout_cost": (C.c_int, [_P, C.c_int32, _P, C.POINTER(C.c_double)]),
+    "darts_rollout_cost_dp": (C.c_int, [_P, _P, C.c_int32, C.c_int32, _P, C.POINTER(C.c_double)]),
     "darts_fit_ptl": (C.c_int, [_P, _P, C.c_int32, _P]),
     "darts_stream_chunks": (C.c_int, [_P, C.c_int64, C.c_int32, _P, _P, _P, C.c_int64,
                                       C.POINTER(C.c_int32), C.POINTER(C.c_int64)]),
@@ -278,6 +279,17 @@ def darts_rollout_cost(lengths, ptl):
     p = np.ascontiguousarray(ptl, dtype=np.float64)
     out = C.c_double()
     _check(load_library().darts_rollout_cost(_np_ptr(ln), len(ln), _np_ptr(p), C.byref(out)))
+    return out.value
+
+
+def darts_rollout_cost_dp(lengths, ranks, n_ranks, ptl):
+    import numpy as np
+    ln = np.ascontiguousarray(lengths, dtype=np.int32)
+    rk = np.ascontiguousarray(ranks, dtype=np.int32)
+    p = np.ascontiguousarray(ptl, dtype=np.float64)
+    out = C.c_double()
+    _check(load_library().darts_rollout_cost_dp(_np_ptr(ln), _np_ptr(rk), len(ln), n_ranks, _np_ptr(p),
+                                                C.byref(out)))
     return out.value
 
 

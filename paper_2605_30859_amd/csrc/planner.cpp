@@ -145,6 +145,26 @@ int darts_rollout_cost(const int32_t* h_len, int32_t n, const double* h_ptl, dou
   return DARTS_OK;
 }
 
+int darts_rollout_cost_dp(const int32_t* h_len, const int32_t* h_rank, int32_t n, int32_t n_ranks,
+                          const double* h_ptl, double* h_T) {
+  if (n < 0 || n_ranks < 1 || ((!h_len || !h_rank) && n > 0) || !h_ptl || !h_T) return DARTS_EINVAL;
+  std::vector<std::vector<int32_t>> per(n_ranks);
+  for (int32_t i = 0; i < n; ++i) {
+    if (h_rank[i] < 0 || h_rank[i] >= n_ranks) return DARTS_EINVAL;
+    per[h_rank[i]].push_back(h_len[i]);
+  }
+  // the slowest rank sets the batch cost (an empty rank costs 0)
+  double T = 0.0;
+  for (int32_t r = 0; r < n_ranks; ++r) {
+    double t = 0.0;
+    const int rc = darts_rollout_cost(per[r].data(), (int32_t)per[r].size(), h_ptl, &t);
+    if (rc != DARTS_OK) return rc;
+    T = r == 0 ? t : std::max(T, t);
+  }
+  *h_T = T;
+  return DARTS_OK;
+}
+
 namespace {
 // Weighted least squares of the hinge basis (1, x, (x-b1)+, (x-b2)+) on the
 // per-size mean latencies (weights = sample counts; the same solution as the

@@ -100,6 +100,22 @@ def test_rollout_cost_matches_oracle_bitwise(B):
         assert got == rollout_cost(list(ln), lambda b: ptl_eval(p, b))
 
 
+def test_rollout_cost_dp_matches_oracle_bitwise(B):
+    """Data-parallel Eq. 4: the maximum of the per-rank costs, ranks assigned
+    at random (some empty)."""
+    from oracle.costmodel import rollout_cost_dp, ptl_eval
+    rng = np.random.default_rng(29)
+    for _ in range(100):
+        n, R = int(rng.integers(0, 200)), int(rng.integers(1, 9))
+        ln = rng.integers(0, 5000, n).astype(np.int32)
+        rk = rng.integers(0, R, n).astype(np.int32)
+        p = (float(rng.integers(1, 200)), float(rng.integers(200, 600)), *rng.uniform(0, 5, 4))
+        groups = [list(ln[rk == r]) for r in range(R)]
+        assert B.darts_rollout_cost_dp(ln, rk, R, p) == rollout_cost_dp(groups, lambda b: ptl_eval(p, b))
+    with pytest.raises(B.DartsError):
+        B.darts_rollout_cost_dp(np.array([3], np.int32), np.array([2], np.int32), 2, (1.0, 2.0, 1, 0, 0, 0))
+
+
 def test_ptl_fit_matches_oracle(B):
     from oracle.costmodel import fit_ptl, ptl_eval
     rng = np.random.default_rng(17)
