@@ -24,10 +24,13 @@ namespace darts {
 // One wavefront per row: softmax over the E router logits (fp32), then k
 // rounds of wavefront argmax (value descending, expert id ascending), each
 // winner removed; weights renormalised over the k.  NPL logits per lane
-// (E <= 64 * NPL).
+// (E <= 64 * NPL).  The logits are the sum of n_split split-K partial planes
+// split_stride apart, added in plane order (the dense reduce's order), so the
+// router GEMM needs no separate reduce.
 constexpr int kMoeMaxPerLane = 16;   // E <= 1024
 template <int NPL>
 __global__ void __launch_bounds__(256) moe_topk_kernel(const float* __restrict__ logits, int ld,
+                                                       int n_split, int64_t split_stride,
                                                        int n_rows, int E, int k,
                                                        int32_t* __restrict__ topk_id,
                                                        float* __restrict__ topk_w) {
@@ -40,7 +43,12 @@ __global__ void __launch_bounds__(256) moe_topk_kernel(const float* __restrict__
 #pragma unroll
   for (int j = 0; j < NPL; ++j) {
     const int e = lane + 64 * j;
-    p[j] = e < E ? lg[e] : -INFINITY;
+    float v = -INFINITY;
+    if (e < E) {
+      v = 0.f;
+      for (int z = 0; z < n_split; ++z) v += lg[z * split_stride + e];
+    }
+    p[j] = v;
     mx = fmaxf(mx, p[j]);
   }
   mx = wave_max(mx);
@@ -210,17 +218,23 @@ hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st, bool* normed) {
   if (a.E > 64 * kMoeMaxPerLane || a.E > 1024 || a.k > 64 || a.k > a.E || a.d % 4 ||
       a.n_rows > 65536 * kGroupedTileRows)
     return hipErrorInvalidValue;
-  hipError_t e = launch_gemm(true, a.xn, a.d, a.w_router, a.d, a.logits, a.E_pad, a.n_rows, a.E_pad, a.d,
-                             EPI_F32, a.gemm_ws, a.gemm_ws_bytes, st);
+  // router logits, or their split-K partial planes (summed by the top-k kernel)
+  int n_split = 1;
+  hipError_t e = launch_gemm_f32_or_partials(a.xn, a.d, a.w_router, a.d, a.logits, a.E_pad, a.n_rows,
+                                             a.E_pad, a.d, a.gemm_ws, a.gemm_ws_bytes, st, &n_split);
   if (e != hipSuccess) return e;
+  const float* lg = n_split > 1 ? (const float*)a.gemm_ws : a.logits;
+  const int64_t zs = (int64_t)a.n_rows * a.E_pad;
   const dim3 gtk((a.n_rows + 3) / 4), btk(256);
   if (a.E <= 128)
-    hipLaunchKernelGGL(moe_topk_kernel<2>, gtk, btk, 0, st, a.logits, a.E_pad, a.n_rows, a.E, a.k, a.topk_id, a.topk_w);
-  else if (a.E <= 256)
-    hipLaunchKernelGGL(moe_topk_kernel<4>, gtk, btk, 0, st, a.logits, a.E_pad, a.n_rows, a.E, a.k, a.topk_id, a.topk_w);
-  else
-    hipLaunchKernelGGL(moe_topk_kernel<kMoeMaxPerLane>, gtk, btk, 0, st, a.logits, a.E_pad, a.n_rows, a.E, a.k,
+    hipLaunchKernelGGL(moe_topk_kernel<2>, gtk, btk, 0, st, lg, a.E_pad, n_split, zs, a.n_rows, a.E, a.k,
                        a.topk_id, a.topk_w);
+  else if (a.E <= 256)
+    hipLaunchKernelGGL(moe_topk_kernel<4>, gtk, btk, 0, st, lg, a.E_pad, n_split, zs, a.n_rows, a.E, a.k,
+                       a.topk_id, a.topk_w);
+  else
+    hipLaunchKernelGGL(moe_topk_kernel<kMoeMaxPerLane>, gtk, btk, 0, st, lg, a.E_pad, n_split, zs, a.n_rows,
+                       a.E, a.k, a.topk_id, a.topk_w);
   hipLaunchKernelGGL(moe_offsets_kernel, dim3(1), dim3(1024), 0, st, a.topk_id, a.n_rows * a.k, a.E, a.k,
                      a.counts, a.offsets, a.cursors, a.mtiles, a.n_mtiles, a.pos_of, a.row_of);
   const int Fe = a.Fe, d = a.d;
