@@ -565,16 +565,20 @@ static int attn_slots(int hd) {
   return cached[i];
 }
 
-// Pages per chunk.  Ragged contexts: 32 pages (512 keys), so that the longest
-// rows are spread over many wavefronts instead of one.  Equal contexts: the
+// Pages per chunk.  Ragged contexts: 128 pages (2048 keys), so that the
+// longest rows are spread over many wavefronts instead of one while short rows
+// stay whole (on the sweep's lognormal contexts, 32 / 64 / 128 / 256 pages
+// took 1.85 / 1.76 / 1.72 / 1.82 ms: fewer chunks mean fewer partial sums and
+// less per-item work, more mean better balance).  Equal contexts: the
 // chunk count that minimises the kernel's makespan, rounds of resident
 // wavefronts times pages per chunk (plus a page of fixed work per item), plus
 // the partial-sum round trip and combine launch when rows are split; at most
 // ~4 rounds of items and chunks of at least 4 pages.
+constexpr int kRaggedChunkPages = 128;
 static int choose_chunk_pages(int n_rows, int hkv, int max_ctx, bool uniform, int hd) {
   const int64_t units = (int64_t)n_rows * hkv;
   const int npg = (max_ctx + kPage - 1) / kPage;
-  if (!uniform) return npg <= 32 ? npg + (npg & 1) : 32;
+  if (!uniform) return npg <= kRaggedChunkPages ? npg + (npg & 1) : kRaggedChunkPages;
   const int slots = attn_slots(hd);
   const int64_t nmax = std::max<int64_t>(1, (4 * (int64_t)slots + units - 1) / units);
   double best = 1e30;
@@ -605,11 +609,11 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // with a shared prefix [prefix partial o | prefix (m, l) | group row0 | group n | n_groups].
 static size_t ws_layout(int n_rows, int hq, int hkv, int hd, int max_ctx, int prefix_pages, char* base,
                         AttnWs* w) {
-  // partial sets for either chunking: ragged rows split into 32-page chunks;
+  // partial sets for either chunking: ragged rows split into kRaggedChunkPages chunks;
   // equal contexts into at most max(1, ceil(4 * slots / units)) chunks per row
   // (choose_chunk_pages), i.e. at most n_rows + 4 * kAttnMaxSlots / hkv sets
   const int npg = (max_ctx + kPage - 1) / kPage;
-  const int64_t ragged = (int64_t)n_rows * ((npg + 31) / 32);
+  const int64_t ragged = (int64_t)n_rows * ((npg + kRaggedChunkPages - 1) / kRaggedChunkPages);
   const int64_t equal = (int64_t)n_rows + (4 * (int64_t)kAttnMaxSlots + hkv - 1) / hkv;
   const int64_t maxch = std::max(ragged, std::min<int64_t>(equal, (int64_t)n_rows * npg));
   (void)prefix_pages;
