@@ -28,6 +28,7 @@ namespace darts {
 // split_stride apart, added in plane order (the dense reduce's order), so the
 // router GEMM needs no separate reduce.
 constexpr int kMoeMaxPerLane = 16;   // E <= 1024
+constexpr int kMoeMaxSplits = 8;     // router GEMM K splits the top-k kernel sums
 template <int NPL>
 __global__ void __launch_bounds__(256) moe_topk_kernel(const float* __restrict__ logits, int ld,
                                                        int n_split, int64_t split_stride,
@@ -45,8 +46,14 @@ __global__ void __launch_bounds__(256) moe_topk_kernel(const float* __restrict__
     const int e = lane + 64 * j;
     float v = -INFINITY;
     if (e < E) {
+      // all planes' loads issued before the adds (in plane order)
+      float pz[kMoeMaxSplits];
+#pragma unroll
+      for (int z = 0; z < kMoeMaxSplits; ++z) pz[z] = z < n_split ? lg[z * split_stride + e] : 0.f;
       v = 0.f;
-      for (int z = 0; z < n_split; ++z) v += lg[z * split_stride + e];
+#pragma unroll
+      for (int z = 0; z < kMoeMaxSplits; ++z)
+        if (z < n_split) v += pz[z];
     }
     p[j] = v;
     mx = fmaxf(mx, p[j]);
@@ -223,6 +230,7 @@ hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st, bool* normed) {
   hipError_t e = launch_gemm_f32_or_partials(a.xn, a.d, a.w_router, a.d, a.logits, a.E_pad, a.n_rows,
                                              a.E_pad, a.d, a.gemm_ws, a.gemm_ws_bytes, st, &n_split);
   if (e != hipSuccess) return e;
+  if (n_split > kMoeMaxSplits) return hipErrorInvalidValue;
   const float* lg = n_split > 1 ? (const float*)a.gemm_ws : a.logits;
   const int64_t zs = (int64_t)a.n_rows * a.E_pad;
   const dim3 gtk((a.n_rows + 3) / 4), btk(256);
