@@ -187,6 +187,47 @@ def test_dual_mode_tiny():
     assert got["stats"]["pages_used"] == 0
 
 
+@pytest.mark.parametrize("shape", [
+    # (layers, d, hq, hkv, hd, ffn, vocab, prompts, prompt_len, m, k, cap, m_up)
+    (3, 64, 4, 1, 128, 256, 1000, 3, 32, 6, 3, 40, None),      # GQA 4:1, hd 128, hq*hd != d
+    (2, 96, 8, 2, 64, 192, 768, 2, 16, 5, 3, 48, None),        # m < 2k: dual-end groups
+    (1, 128, 2, 2, 32, 512, 516, 5, 48, 4, 4, 30, None),       # k = m (no redundancy), 3 prompt pages
+    (2, 128, 16, 4, 32, 256, 4096, 2, 16, 8, 2, 64, 9),        # G = 4 with 16 q heads, dual-end forced (m_up 9 > m)
+])
+def test_fp32_shape_variants(shape):
+    """fp32 models of other shapes than the tiny configuration through the
+    whole rollout (teacher-forced): schedule, kept sets, lengths and statuses
+    equal the oracle's; per step log-probs and entropies within 1e-5, tokens
+    bit-exact where the oracle's top-2 margin is at least 1e-4."""
+    from workload.configs import ModelCfg, RunCfg
+    L_, d, hq, hkv, hd, F, V, P, Lp, m, k, cap, m_up = shape
+    model = ModelCfg("fp32-variant", L_, d, hq, hkv, hd, F, V, "f32", 11)
+    run = RunCfg(P, Lp, m, k, cap, 16.0, 0.9, False, 5, 5, m_up=m_up)
+    say(f"fp32 variant {shape}: oracle")
+    prompts, forced = rollout_inputs(model, run)
+    W = OM.init_weights(model)
+    ref = rollout(model, W, prompts, forced, run.m, run.k, run.cap, run.sample_seed, m_up=run.m_up_eff)
+    say(f"fp32 variant {shape}: GPU")
+    got = run_gpu(model, run, prompts, forced, force_tokens=ref.tokens)
+    assert got["stats"]["steps"] == ref.steps
+    assert got["stats"]["tokens_decoded"] == ref.tokens_decoded
+    assert got["stats"]["pages_hwm"] == ref.pages_hwm and got["stats"]["pages_used"] == 0
+    for i in range(run.n_prompts):
+        assert list(got["kept"][i]) == ref.kept[i], i
+        assert got["done"][i] == ref.done_step[i], i
+    for g in range(run.n_prompts * run.m):
+        assert got["length"][g] == ref.length[g] and got["status"][g] == ref.status[g], g
+    mism = 0
+    for st, rec in enumerate(got["steps"]):
+        for r, g in enumerate(rec["traj"]):
+            g = int(g)
+            assert abs(rec["logprob"][r] - ref.logprobs[g][st]) <= 1e-5, (st, g)
+            assert abs(rec["entropy"][r] - ref.entropies[g][st]) <= 1e-5, (st, g)
+            if rec["sampled"][r] != ref.sampled[g][st] and ref.margins[g][st] >= 1e-4:
+                mism += 1
+    assert mism == 0
+
+
 def test_error_paths():
     B = _b()
     model, run = get_config("tiny")
