@@ -352,7 +352,7 @@ def main():
         print(json.dumps({"copy_calibration_bytes": 1 << 30, "copies": 3}))
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU: this build runs the rollout of one data-parallel "
+        print("bench.py measures one GPU: the library runs the rollout of one data-parallel "
               "rank (prompt groups are independent); multi-GPU runs are not part of it.",
               file=sys.stderr)
         sys.exit(2)

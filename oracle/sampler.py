@@ -1,7 +1,7 @@
 """Gumbel-max sampling with per-token log-probability and entropy.
 
-Definitions (spec rollout scoring; the paper itself uses its rollout
-engine's sampler and states no formula):
+Definitions (the per-token scoring of the rollout; the paper itself uses its
+rollout engine's sampler and states no formula):
     z_i      = logit_i / T                                  (float32 division)
     u_i      = Philox(key=seed, counter=(i>>2, g, s, TAG_SAMPLE)) word i&3 -> (0,1)
     token    = argmax_i fl32(z_i + g(u_i)), smallest i on ties (Gumbel-max)
