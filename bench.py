@@ -491,6 +491,9 @@ def main():
             "bound_s_at_measured_read": bound_read,
             "frac_at_measured_read": bound_read / float(np.mean(walls))},
         "cpu_baseline": None,
+        "paper_context": "the paper reports end-to-end RL training speedups only: up to 1.77x over VeRL "
+                         "(Sec. 5.2) on 8-node clusters of NVIDIA H20 GPUs, precision not stated; "
+                         "context, not a figure for this metric",
     }
     if not args.no_cpu_baseline:
         try:
