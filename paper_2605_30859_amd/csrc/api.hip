@@ -98,6 +98,9 @@ struct darts_ctx {
   int32_t* streamed = nullptr;
   uint8_t* fin_sent = nullptr;
   int32_t* stream_off = nullptr;
+  // sampler slice partials (rows split across blocks when few are live)
+  SamplePart* samp_parts = nullptr;
+  int64_t samp_part_cap = 0;
   std::vector<int32_t> plan;       // host copy of grp_m
   int n_start = 0;                 // sum of the plan: trajectories started by the prefill
   int32_t* grp_cnt = nullptr;
@@ -463,6 +466,8 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
   }
   A(&c->xlast, (size_t)c->P * c->d * 4);
   A(&c->logits, (size_t)c->n_traj * c->V * 4);
+  c->samp_part_cap = (int64_t)kSampleBlocks + c->n_traj;
+  A(&c->samp_parts, (size_t)c->samp_part_cap * sizeof(SamplePart));
   c->gemm_ws_bytes = gemm_ws_need(c);
   A(&c->gemm_ws, c->gemm_ws_bytes);
   c->share_prefix = c->bf16 && c->m > 1 && c->pp > 0 && (c->rc.flags & DARTS_FLAG_SHARED_PREFIX);
@@ -743,6 +748,7 @@ int darts_prefill(darts_ctx* c, const int32_t* d_prompts, const int32_t* d_force
   a.last_tok = c->last_tok; a.forced_len = c->forced_len; a.finished_out = out->finished;
   a.traj_out = out->traj_id; a.cap = c->cap; a.eos = c->V - 1;
   a.hist_tok = c->hist_tok; a.hist_lp = c->hist_lp;
+  a.part_out = c->samp_parts; a.part_cap = c->samp_part_cap;
   HIPCHK(c, launch_sample(a, c->st));
   c->free_top -= c->P * c->pp;
   c->hwm = std::max<int64_t>(c->hwm, c->n_pages - c->free_top);
@@ -794,6 +800,7 @@ int darts_decode_step(darts_ctx* c, const int32_t* d_force_tokens, darts_step_ou
   a.last_tok = c->last_tok; a.forced_len = c->forced_len; a.finished_out = out->finished;
   a.traj_out = out->traj_id; a.cap = c->cap; a.eos = c->V - 1;
   a.hist_tok = c->hist_tok; a.hist_lp = c->hist_lp;
+  a.part_out = c->samp_parts; a.part_cap = c->samp_part_cap;
   HIPCHK(c, launch_sample(a, c->st));
   c->step += 1;
   c->tokens += n;

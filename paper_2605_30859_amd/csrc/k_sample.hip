@@ -22,6 +22,8 @@
 // therefore the exact-map argmax, bit for bit, in every case.
 #include <math.h>
 
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -82,24 +84,89 @@ __device__ __forceinline__ float logit_at(const void* row, int i, bool tscale, f
   return tscale ? __fdiv_rn(z, temperature) : z;
 }
 
+// Per-row values every part of a row shares.
+struct RowCtx {
+  int g, step;
+  const void* row;
+};
+template <bool BF16, bool STATEFUL>
+__device__ __forceinline__ RowCtx row_ctx(const SampleArgs& a, int r) {
+  RowCtx c;
+  c.g = a.traj[r];
+  const int lrow = a.row_logit ? a.row_logit[r] : (a.logit_div > 0 ? c.g / a.logit_div : r);
+  c.row = BF16 ? (const void*)((const bf16_t*)a.logits + (int64_t)lrow * a.vocab)
+               : (const void*)((const float*)a.logits + (int64_t)lrow * a.vocab);
+  c.step = STATEFUL ? a.gen[c.g] : a.step[r];
+  return c;
+}
+
+// Row r's result from its merged softmax state and Gumbel-max winner: the
+// taken token (forced end of sequence, teacher forcing), its log-prob, the
+// entropy and, in the stateful form, termination and score accumulation.
+template <bool BF16, bool STATEFUL>
+__device__ __forceinline__ void finish_row(const SampleArgs& a, int r, const RowCtx& c, SoftState st,
+                                           Best best) {
+  const int g = c.g, step = c.step;
+  const float lse = st.m + logf(st.s);
+  const float ent = logf(st.s) - st.t / st.s;
+  const int sampled = best.i;
+  int taken = sampled;
+  uint8_t fin = 0;
+  if (STATEFUL) {
+    const int s_new = step + 1;
+    const int d = a.forced_len[g];
+    if (d <= a.cap && s_new == d) { taken = a.eos; fin = 1; }
+    else {
+      if (a.force && a.force[g] >= 0) taken = a.force[g];
+      if (s_new >= a.cap) fin = 2;
+    }
+  } else if (a.force && a.force[r] >= 0) {
+    taken = a.force[r];
+  }
+  if (taken < 0 || taken >= a.vocab) taken = sampled;
+  const float zt = logit_at<BF16>(c.row, taken, a.temperature != 1.0f, a.temperature);
+  const float lp = zt - lse;
+  if (a.token_out) a.token_out[r] = taken;
+  if (a.sampled_out) a.sampled_out[r] = sampled;
+  if (a.logprob_out) a.logprob_out[r] = lp;
+  if (a.entropy_out) a.entropy_out[r] = ent;
+  if (STATEFUL) {
+    if (a.hist_tok && step < a.cap) {
+      a.hist_tok[(int64_t)g * a.cap + step] = taken;
+      a.hist_lp[(int64_t)g * a.cap + step] = lp;
+    }
+    a.gen[g] = step + 1;
+    a.sum_lp[g] = a.sum_lp[g] + lp;
+    a.last_tok[g] = taken;
+    if (fin) a.status[g] = fin;
+    if (a.finished_out) a.finished_out[r] = fin;
+    if (a.traj_out) a.traj_out[r] = g;
+  }
+}
+
+// Block (r, part): part `part` of the a.parts contiguous slices of row r's
+// vocabulary.  With one part the block finishes the row; with several it
+// writes its partial (softmax state, winner) and the finalize kernel merges
+// the parts in part order.
 template <bool BF16, bool STATEFUL>
 __global__ void __launch_bounds__(256) sample_kernel(SampleArgs a) {
   __shared__ SoftState ss[4];
   __shared__ Best sb[4];
-  const int r = blockIdx.x;
+  const int parts = a.parts > 1 ? a.parts : 1;
+  const int r = blockIdx.x / parts, part = blockIdx.x - r * parts;
   const int tid = threadIdx.x;
-  const int g = a.traj[r];
-  const int lrow = a.row_logit ? a.row_logit[r] : (a.logit_div > 0 ? g / a.logit_div : r);
-  const void* row = BF16 ? (const void*)((const bf16_t*)a.logits + (int64_t)lrow * a.vocab)
-                         : (const void*)((const float*)a.logits + (int64_t)lrow * a.vocab);
-  const int step = STATEFUL ? a.gen[g] : a.step[r];
+  const RowCtx c = row_ctx<BF16, STATEFUL>(a, r);
+  const int g = c.g, step = c.step;
+  const void* row = c.row;
   const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
   const bool tscale = a.temperature != 1.0f;
   SoftState st = {-INFINITY, 0.f, 0.f};
   float b1 = -INFINITY, b2 = -INFINITY;   // this thread's two best fast scores
   int i1 = 0x7fffffff;                     // index of the best
   const int n4 = a.vocab >> 2;
-  for (int j = tid; j < n4; j += 256) {
+  const int span = (n4 + parts - 1) / parts;
+  const int jb = part * span, je = min(n4, jb + span);
+  for (int j = jb + tid; j < je; j += 256) {
     float z[4];
     load4<BF16>(row, j, z);
     if (tscale) {
@@ -141,7 +208,7 @@ __global__ void __launch_bounds__(256) sample_kernel(SampleArgs a) {
     best.v = logit_at<BF16>(row, i1, tscale, a.temperature) + gumbel_of(open_unit(p.x[e]));
     best.i = i1;
   } else {
-    for (int j = tid; j < n4; j += 256) {
+    for (int j = jb + tid; j < je; j += 256) {
       float z[4];
       load4<BF16>(row, j, z);
       const Philox4 p = philox4x32_10((uint32_t)j, (uint32_t)g, (uint32_t)step, kTagSample, k0, k1);
@@ -166,56 +233,61 @@ __global__ void __launch_bounds__(256) sample_kernel(SampleArgs a) {
   if (tid != 0) return;
   st = soft_merge(soft_merge(ss[0], ss[1]), soft_merge(ss[2], ss[3]));
   best = best_merge(best_merge(sb[0], sb[1]), best_merge(sb[2], sb[3]));
-  const float lse = st.m + logf(st.s);
-  const float ent = logf(st.s) - st.t / st.s;
-  const int sampled = best.i;
-  int taken = sampled;
-  uint8_t fin = 0;
-  if (STATEFUL) {
-    const int s_new = step + 1;
-    const int d = a.forced_len[g];
-    if (d <= a.cap && s_new == d) { taken = a.eos; fin = 1; }
-    else {
-      if (a.force && a.force[g] >= 0) taken = a.force[g];
-      if (s_new >= a.cap) fin = 2;
-    }
-  } else if (a.force && a.force[r] >= 0) {
-    taken = a.force[r];
+  if (parts > 1) {
+    SamplePart o;
+    o.m = st.m; o.s = st.s; o.t = st.t; o.v = best.v; o.i = best.i;
+    a.part_out[blockIdx.x] = o;
+    return;
   }
-  if (taken < 0 || taken >= a.vocab) taken = sampled;
-  float zt;
-  if (BF16) zt = bf16_to_f32(((const bf16_t*)row)[taken]);
-  else zt = ((const float*)row)[taken];
-  if (tscale) zt = __fdiv_rn(zt, a.temperature);
-  const float lp = zt - lse;
-  if (a.token_out) a.token_out[r] = taken;
-  if (a.sampled_out) a.sampled_out[r] = sampled;
-  if (a.logprob_out) a.logprob_out[r] = lp;
-  if (a.entropy_out) a.entropy_out[r] = ent;
-  if (STATEFUL) {
-    if (a.hist_tok && step < a.cap) {
-      a.hist_tok[(int64_t)g * a.cap + step] = taken;
-      a.hist_lp[(int64_t)g * a.cap + step] = lp;
-    }
-    a.gen[g] = step + 1;
-    a.sum_lp[g] = a.sum_lp[g] + lp;
-    a.last_tok[g] = taken;
-    if (fin) a.status[g] = fin;
-    if (a.finished_out) a.finished_out[r] = fin;
-    if (a.traj_out) a.traj_out[r] = g;
-  }
+  finish_row<BF16, STATEFUL>(a, r, c, st, best);
 }
 
-hipError_t launch_sample(const SampleArgs& a, hipStream_t st) {
-  if (a.n_rows <= 0) return hipSuccess;
+// One thread per row: merge the row's parts in part order, then finish it.
+template <bool BF16, bool STATEFUL>
+__global__ void __launch_bounds__(256) sample_finalize_kernel(SampleArgs a) {
+  const int r = blockIdx.x * 256 + threadIdx.x;
+  if (r >= a.n_rows) return;
+  SoftState st = {-INFINITY, 0.f, 0.f};
+  Best best = {-INFINITY, 0x7fffffff};
+  for (int p = 0; p < a.parts; ++p) {
+    const SamplePart o = a.part_out[(int64_t)r * a.parts + p];
+    st = soft_merge(st, SoftState{o.m, o.s, o.t});
+    best = best_merge(best, Best{o.v, o.i});
+  }
+  finish_row<BF16, STATEFUL>(a, r, row_ctx<BF16, STATEFUL>(a, r), st, best);
+}
+
+int sample_parts(int n_rows, int vocab) {
+  // about kSampleBlocks blocks in all, each part at least kSampleMinGroups
+  // groups of 4 logits (two per thread), at most kSampleMaxParts per row
+  const int n4 = vocab >> 2;
+  int parts = (kSampleBlocks + n_rows - 1) / n_rows;
+  parts = std::min(parts, std::max(1, n4 / kSampleMinGroups));
+  return std::max(1, std::min(parts, kSampleMaxParts));
+}
+
+hipError_t launch_sample(const SampleArgs& a0, hipStream_t st) {
+  if (a0.n_rows <= 0) return hipSuccess;
+  SampleArgs a = a0;
+  a.parts = a.part_out ? sample_parts(a.n_rows, a.vocab) : 1;
+  if (a.parts > 1 && (int64_t)a.n_rows * a.parts > a.part_cap) a.parts = 1;
   const bool stateful = a.gen != nullptr;
-  const dim3 grid(a.n_rows), blk(256);
+  const dim3 grid((unsigned)(a.n_rows * a.parts)), blk(256);
+  const dim3 gfin((unsigned)((a.n_rows + 255) / 256));
   if (a.bf16) {
     if (stateful) hipLaunchKernelGGL((sample_kernel<true, true>), grid, blk, 0, st, a);
     else hipLaunchKernelGGL((sample_kernel<true, false>), grid, blk, 0, st, a);
+    if (a.parts > 1) {
+      if (stateful) hipLaunchKernelGGL((sample_finalize_kernel<true, true>), gfin, blk, 0, st, a);
+      else hipLaunchKernelGGL((sample_finalize_kernel<true, false>), gfin, blk, 0, st, a);
+    }
   } else {
     if (stateful) hipLaunchKernelGGL((sample_kernel<false, true>), grid, blk, 0, st, a);
     else hipLaunchKernelGGL((sample_kernel<false, false>), grid, blk, 0, st, a);
+    if (a.parts > 1) {
+      if (stateful) hipLaunchKernelGGL((sample_finalize_kernel<false, true>), gfin, blk, 0, st, a);
+      else hipLaunchKernelGGL((sample_finalize_kernel<false, false>), gfin, blk, 0, st, a);
+    }
   }
   return hipGetLastError();
 }

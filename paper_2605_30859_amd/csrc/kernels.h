@@ -114,7 +114,21 @@ struct SampleArgs {
   uint8_t* finished_out; int32_t* traj_out; int cap; int eos;
   int64_t* tokens_counter;
   int32_t* hist_tok; float* hist_lp;   // NULL or [n_traj][cap]: token t of trajectory g at g*cap + t
+  // NULL: one block per row.  Otherwise room for part_cap partials: rows are
+  // split into sample_parts(n_rows, vocab) vocabulary slices, one block each,
+  // merged by a finalize kernel (set by the launcher; parts 1 without room)
+  struct SamplePart* part_out; int64_t part_cap;
+  int parts;
 };
+struct SamplePart {
+  float m, s, t;   // softmax state of the slice: max, sum e^(z-m), sum e^(z-m)(z-m)
+  float v; int i;  // its Gumbel-max winner (exact score, index)
+};
+// slices per row: about kSampleBlocks blocks in all, each slice at least
+// kSampleMinGroups groups of 4 logits, at most kSampleMaxParts per row, so
+// n_rows * parts <= kSampleBlocks + n_rows
+constexpr int kSampleBlocks = 1024, kSampleMinGroups = 512, kSampleMaxParts = 128;
+int sample_parts(int n_rows, int vocab);
 hipError_t launch_sample(const SampleArgs& a, hipStream_t st);
 hipError_t launch_gumbel_map(const float* u, float* g, int64_t n, bool fast, hipStream_t st);
 float gumbel_fast_bound();   // the fast map's distance bound the sampler's filter assumes
