@@ -147,7 +147,7 @@ __device__ __forceinline__ void finish_row(const SampleArgs& a, int r, const Row
 // Block (r, part): part `part` of the a.parts contiguous slices of row r's
 // vocabulary.  With one part the block finishes the row; with several it
 // writes its partial (softmax state, winner) and the finalize kernel merges
-// the parts in part order.
+// the parts.
 template <bool BF16, bool STATEFUL>
 __global__ void __launch_bounds__(256) sample_kernel(SampleArgs a) {
   __shared__ SoftState ss[4];
@@ -242,19 +242,29 @@ __global__ void __launch_bounds__(256) sample_kernel(SampleArgs a) {
   finish_row<BF16, STATEFUL>(a, r, c, st, best);
 }
 
-// One thread per row: merge the row's parts in part order, then finish it.
+// One wavefront per row: lane l merges parts l, l + 64 (in that order), the
+// lanes are then merged by a fixed butterfly (a fixed order, so the result
+// is reproducible), and lane 0 finishes the row.
 template <bool BF16, bool STATEFUL>
 __global__ void __launch_bounds__(256) sample_finalize_kernel(SampleArgs a) {
-  const int r = blockIdx.x * 256 + threadIdx.x;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
   if (r >= a.n_rows) return;
   SoftState st = {-INFINITY, 0.f, 0.f};
   Best best = {-INFINITY, 0x7fffffff};
-  for (int p = 0; p < a.parts; ++p) {
+  for (int p = lane; p < a.parts; p += 64) {
     const SamplePart o = a.part_out[(int64_t)r * a.parts + p];
     st = soft_merge(st, SoftState{o.m, o.s, o.t});
     best = best_merge(best, Best{o.v, o.i});
   }
-  finish_row<BF16, STATEFUL>(a, r, row_ctx<BF16, STATEFUL>(a, r), st, best);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    SoftState other = {__shfl_xor(st.m, o, 64), __shfl_xor(st.s, o, 64), __shfl_xor(st.t, o, 64)};
+    st = soft_merge(st, other);
+    Best ob = {__shfl_xor(best.v, o, 64), __shfl_xor(best.i, o, 64)};
+    best = best_merge(best, ob);
+  }
+  if (lane == 0) finish_row<BF16, STATEFUL>(a, r, row_ctx<BF16, STATEFUL>(a, r), st, best);
 }
 
 int sample_parts(int n_rows, int vocab) {
@@ -273,7 +283,7 @@ hipError_t launch_sample(const SampleArgs& a0, hipStream_t st) {
   if (a.parts > 1 && (int64_t)a.n_rows * a.parts > a.part_cap) a.parts = 1;
   const bool stateful = a.gen != nullptr;
   const dim3 grid((unsigned)(a.n_rows * a.parts)), blk(256);
-  const dim3 gfin((unsigned)((a.n_rows + 255) / 256));
+  const dim3 gfin((unsigned)((a.n_rows + 3) / 4));
   if (a.bf16) {
     if (stateful) hipLaunchKernelGGL((sample_kernel<true, true>), grid, blk, 0, st, a);
     else hipLaunchKernelGGL((sample_kernel<true, false>), grid, blk, 0, st, a);
