@@ -126,6 +126,29 @@ def rollout_bound(model, run, rows, hbm_gbs, mfma_tflops):
     return t
 
 
+def gemm_class_roofline(model, run, rows, hbm_gbs, mfma_tflops):
+    """Per dense GEMM class, the roofline time of the measured schedule in ms:
+    every launch costs max(2 M N K / MFMA peak, N K weight bytes / HBM), with
+    M = the live rows of each decode step (one launch per layer; the LM head
+    once per step) and the prefill's rows.  MoE expert GEMMs are not included."""
+    d, hq, hkv, hd, L = model.d_model, model.n_q_heads, model.n_kv_heads, model.head_dim, model.n_layers
+    eb = 2 if model.dtype == "bf16" else 4
+    shapes = {"qkv": ((hq + 2 * hkv) * hd, d), "o": (d, hq * hd), "lm_head": (model.vocab, d)}
+    if not model.is_moe:
+        shapes["gate_up"] = (2 * model.ffn_dim, d)
+        shapes["down"] = (d, model.ffn_dim)
+    hbm, mm = hbm_gbs * 1e9, mfma_tflops * 1e12
+    out = {}
+    for name, (N, K) in shapes.items():
+        per_step = 1 if name == "lm_head" else L
+        pre_m = run.n_prompts if name == "lm_head" else run.n_prompts * run.prompt_len
+        t = per_step * max(2.0 * pre_m * N * K / mm, N * K * eb / hbm)
+        for b in rows:
+            t += per_step * max(2.0 * float(b) * N * K / mm, N * K * eb / hbm)
+        out[name] = 1e3 * t
+    return out
+
+
 def hbm_read_rate(B, gib=8, reps=10):
     """HBM read rate this device sustains (GB/s): the library's streaming-read
     kernel (16-byte loads, 2048 blocks, grid-stride) over a `gib` GiB buffer."""
@@ -436,6 +459,11 @@ def main():
         cls[name] = {"ms": ms, "tflops": fl_ / (ms * 1e-3) / 1e12 if ms > 0 else 0.0}
     ro.close()
     read_gbs = hbm_read_rate(B)
+    roof = gemm_class_roofline(model, run, rows, HBM_PEAK_GBS, peak_mm)
+    for name, rms in roof.items():
+        if cls[name]["ms"] > 0:
+            cls[name]["roofline_ms"] = rms
+            cls[name]["frac_of_roofline"] = rms / cls[name]["ms"]
     bound_peak = rollout_bound(model, run, rows, HBM_PEAK_GBS, peak_mm)
     bound_read = rollout_bound(model, run, rows, read_gbs, peak_mm)
     if args.cost_model_check and not args.no_abort:
@@ -481,6 +509,10 @@ def main():
                      "share_of_step_time": attn_ms * 1e-3 / total},
         "gemm": {"bound": "mfma", "achieved": gemm_tf, "peak": peak_mm, "unit": "TFLOP/s",
                  "frac": gemm_tf / peak_mm, "share_of_step_time": gemm_ms * 1e-3 / total,
+                 "frac_of_roofline": (sum(v.get("roofline_ms", 0.0) for v in cls.values())
+                                      / max(sum(v["ms"] for v in cls.values() if "roofline_ms" in v), 1e-9)),
+                 "roofline_note": "per class: the schedule's max(FLOP / MFMA peak, weight bytes / HBM peak) "
+                                  "summed over launches, over the measured class time",
                  "by_class": cls},
         "cost_model": cost_model,
         "rollout_bound": {
