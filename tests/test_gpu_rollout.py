@@ -347,8 +347,8 @@ def test_qwen3_8b_full_size_schedule():
     12288, vocab 151936; 32 prompts x 512, m 16, k 8, cap 8192), in the launch
     configuration the benchmark times: the rollout completes with the steps,
     tokens and page high-water mark the forced lengths imply, kept sets equal
-    the selection of its own scores, and every score is a valid log-prob /
-    entropy."""
+    the selection of its own scores, every score is a valid log-prob /
+    entropy, and a second run on a permuted page pool is bitwise identical."""
     model, run = get_config("qwen3-8b")
     prompts, forced = rollout_inputs(model, run)
     say("qwen3-8b full size: GPU rollout")
@@ -365,6 +365,13 @@ def test_qwen3_8b_full_size_schedule():
     lp = np.concatenate([r["logprob"] for r in got["steps"]])
     assert np.isfinite(ent).all() and np.isfinite(lp).all()
     assert (ent >= 0).all() and (ent <= np.log(model.vocab) + 1e-3).all() and (lp <= 1e-5).all()
+    # reproducible at full size, whatever the physical pages: a second run
+    # with a permuted free list gives bitwise the same scores and kept sets
+    say("qwen3-8b full size: second GPU rollout, permuted page pool")
+    again = run_gpu(model, run, prompts, forced, perm_seed=7)
+    for key in ("length", "sum_lp", "mean_lp", "status", "kept", "done"):
+        assert np.array_equal(np.asarray(again[key]).view(np.uint8), np.asarray(got[key]).view(np.uint8)), key
+    assert again["stats"]["steps"] == got["stats"]["steps"]
 
 
 def test_dense_small_full_config_prompt_prefix():
