@@ -6,7 +6,10 @@
 //     state merged across lanes and wavefronts;
 // then the log-prob of the taken token.  In the stateful form the same block
 // applies the exogenous termination rule (forced end-of-sequence length,
-// truncation at cap) and accumulates the trajectory's score.
+// truncation at cap) and accumulates the trajectory's score.  When few rows
+// are live (given room for partials), a row's vocabulary is split into
+// slices, one block each, and a finalize kernel merges the slices' states
+// and winners before finishing the row.
 //
 // Filtered argmax.  g_i is defined by the library's exact float32 logarithm
 // (two per element, each with a correctly rounded division), which would
