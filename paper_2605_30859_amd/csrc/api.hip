@@ -395,7 +395,10 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
                          (size_t)c->nl * ((size_t)qkv_w * c->d + (size_t)c->d * c->hq * c->hd +
                                           ffn_elems)) * c->esz;
   const size_t poolb = (size_t)n_pages * page_bytes_all;
-  if (wbytes + poolb + (size_t)rows_max * c->V * 0 > free_b) { delete c; return DARTS_ENOMEM; }
+  // weights, the pool and the fp32 logits of a full batch (the largest
+  // buffers; a failing allocation of the rest is reported the same way)
+  const size_t logitb = (size_t)c->n_traj * c->V * 4;
+  if (wbytes + poolb + logitb > free_b) { delete c; return DARTS_ENOMEM; }
 
   hipError_t e = hipSuccess;
   auto A = [&](auto** p, size_t bytes) { if (e == hipSuccess) e = dalloc(c, p, bytes); };
