@@ -233,7 +233,7 @@ template <int BM, int BN, int KB, int WGM, int WGN, int STAGES, int EPI, bool SP
 __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_kernel(const bf16_t* __restrict__ A, int lda,
                                                        const bf16_t* __restrict__ W, int ldw,
                                                        void* __restrict__ C, int ldc, int M,
-                                                       int N, int K, int k_chunk, int mt, int nt,
+                                                       int N, int /*K*/, int k_chunk, int mt, int nt,
                                                        float* __restrict__ ws) {
   const int b = xcd_block();
   const int mi = b % mt, ni = (b / mt) % nt, z = b / (mt * nt);
@@ -280,7 +280,7 @@ template <int MT, int NS, int EPI, bool SPLIT>
 __global__ void __launch_bounds__(512) gemm_skinny_kernel(const bf16_t* __restrict__ A, int lda,
                                                           const bf16_t* __restrict__ W, int ldw,
                                                           void* __restrict__ C, int ldc, int M,
-                                                          int N, int K, int k_chunk, int nt,
+                                                          int N, int /*K*/, int k_chunk, int nt,
                                                           float* __restrict__ ws) {
   __shared__ f32x4_t red[8][MT * NS][64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -304,7 +304,6 @@ __global__ void __launch_bounds__(512) gemm_skinny_kernel(const bf16_t* __restri
     av[i] = (16 * i + r) < M;
     ap[i] = A + (int64_t)(av[i] ? 16 * i + r : 0) * lda + kbeg + kq;
   }
-#pragma unroll 4
   for (int k = 0; k < kw; k += 32) {
     bf16x8_t a[MT], b[NS];
 #pragma unroll
