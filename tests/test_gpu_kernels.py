@@ -402,3 +402,16 @@ def test_selection_sweep(mode):
         else:
             assert comp[grp] == 0 and (kept[grp] == -1).all()
     assert len(kept_ref) > 0
+
+
+def test_stream_read_reads_every_word():
+    """The streaming-read reference touches every 16-byte word exactly once:
+    the sum of its per-wavefront partial sums equals the buffer's sum (small
+    integers, exact in float32 at this size), with a ragged tail."""
+    B = _b()
+    n = (1 << 20) + 12                       # floats: 16-byte words plus a partial grid stride
+    x = (torch.arange(n, dtype=torch.int64, device=DEV) % 7).to(torch.float32)
+    sink = torch.zeros(8192, dtype=torch.float32, device=DEV)
+    B.darts_stream_read(x, sink)
+    torch.cuda.synchronize()
+    assert float(sink.double().sum().item()) == float(x.double().sum().item())
