@@ -248,6 +248,119 @@ def kernel_sweep(B, steps, warmup):
     return out
 
 
+def next_rows(B, model, run, threshold):
+    """The widened rows on one workload, each measured on the GPU:
+    * adaptive redundancy (Alg. 1, App. B): a uniform rollout gives each
+      prompt's length spread; the EMA of it (first observation as is)
+      weights Alg. 1, which spreads the paper's solved budget of 1.5 N M
+      candidates over M'_i in [M, 2M]; the planned rollout then runs on the
+      same prompts and forced lengths;
+    * token-chunk streaming: the uniform rollout again with chunks dispatched
+      after every step once `threshold` tokens are pending (host copies of
+      the descriptors and tokens included in the timed region);
+    * group advantages (Eq. 2) of the uniform rollout's kept groups with
+      Bernoulli(0.5) rewards.
+    The allocation is measured on the configuration's own lengths (drawn
+    alike for every prompt) and on lengths whose spread belongs to the prompt
+    (alternating lognormal sigma 0.3 / 1.2, the tail only on the wide ones)."""
+    import numpy as np
+    import torch
+    from workload import rollout_inputs
+    prompts, forced = rollout_inputs(model, run)
+    pr = torch.from_numpy(np.ascontiguousarray(prompts.reshape(-1))).cuda()
+    fl = torch.from_numpy(forced.astype(np.int32)).cuda()
+    P, m, k = run.n_prompts, run.m, run.k
+
+    def progress(s, rows):
+        if s % 1000 == 0:
+            print(f"[bench]   step {s}: live {len(rows['traj'])}", file=sys.stderr, flush=True)
+
+    def timed_rollout(lengths, flags=0, plan=None):
+        ro = B.Rollout(model, run, flags=flags)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        st = ro.run_to_completion(pr, lengths, plan=plan, on_step=progress)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        print(f"[bench] next: rollout ({'planned' if plan is not None else 'uniform'}) {dt:.1f} s, "
+              f"{st['steps']} steps", file=sys.stderr, flush=True)
+        return ro, dt, st
+
+    def allocation(lengths):
+        """uniform M'_i = 2M, then the planned rollout on the same inputs"""
+        ro, t_u, st_u = timed_rollout(lengths)
+        lens = ro.traj_scores()[0].cpu().numpy()
+        kept_u = ro.kept.clone()
+        ro.close()
+        # host planning, as an RL loop runs it between iterations
+        t0 = time.perf_counter()
+        sigma = B.darts_prompt_length_std(lens, None, P, m)
+        est, seen = np.zeros(P), np.zeros(P, np.uint8)
+        B.darts_ema_update(est, seen, sigma, 0.5)
+        m_total = int(round(1.5 * P * k))
+        plan = B.darts_allocate_redundancy(est, k, 2 * k, m_total, seen)
+        plan_us = (time.perf_counter() - t0) * 1e6
+        ro, t_p, st_p = timed_rollout(lengths, plan=plan)
+        ro.close()
+        return kept_u, t_u, {
+            "uniform": {"candidates": P * m, "time_to_kept_set_s": t_u, "tokens": st_u["tokens_decoded"],
+                        "steps": st_u["steps"]},
+            "planned": {"budget": m_total, "candidates": int(plan.sum()),
+                        "plan_histogram": {int(v): int((plan == v).sum()) for v in np.unique(plan)},
+                        "planning_us": plan_us, "time_to_kept_set_s": t_p,
+                        "tokens": st_p["tokens_decoded"], "steps": st_p["steps"],
+                        "time_vs_uniform": t_p / t_u,
+                        "tokens_vs_uniform": st_p["tokens_decoded"] / st_u["tokens_decoded"]}}
+
+    out = {"metric": "widened rows: adaptive redundancy, token-chunk streaming, group advantages",
+           "config": {"workload": workload_desc(model, run), "name": model.name}}
+    kept, t_u, out["allocation_same_spread"] = allocation(fl)
+    from workload.gen import heterogeneous_forced_lengths
+    fh = torch.from_numpy(heterogeneous_forced_lengths(run, run.workload_seed + 100)).cuda()
+    _, _, out["allocation_per_prompt_spread"] = allocation(fh)
+    # streaming
+    ro = B.Rollout(model, run, flags=B.FLAG_STREAM)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    n_disp = n_tok = 0
+    ro.darts_prefill(pr, fl)
+    ro.darts_select_and_prune()
+    while True:
+        done = ro.n_done >= P
+        got = ro.stream_chunks(threshold, flush=done)
+        if got is not None:
+            n_disp += 1
+            n_tok += len(got[1])
+        if done:
+            break
+        ro.darts_decode_step()
+        ro.darts_select_and_prune()
+    torch.cuda.synchronize()
+    t_s = time.perf_counter() - t0
+    print(f"[bench] next: streaming rollout {t_s:.1f} s", file=sys.stderr, flush=True)
+    st_s = ro.stats()
+    ro.close()
+    out["streaming"] = {"threshold_tokens": threshold, "dispatches": n_disp, "tokens_streamed": n_tok,
+                        "tokens_decoded": st_s["tokens_decoded"], "time_to_kept_set_s": t_s,
+                        "time_vs_uniform": t_s / t_u}
+    # advantages of the kept groups
+    rng = np.random.default_rng(0)
+    reward = torch.from_numpy((rng.random(P * m) < 0.5).astype(np.float32)).cuda()
+    adv = torch.empty((P, k), dtype=torch.float32, device="cuda")
+    for _ in range(3):
+        B.darts_group_advantages(kept, reward, adv)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(20):
+        B.darts_group_advantages(kept, reward, adv)
+    e1.record()
+    torch.cuda.synchronize()
+    out["advantages"] = {"groups": P, "k": k, "us": e0.elapsed_time(e1) / 20 * 1e3,
+                         "finite": bool(torch.isfinite(adv).all().item())}
+    return out
+
+
 ATTN_SOURCES = ("paper_2605_30859_amd/csrc/k_attn.hip", "paper_2605_30859_amd/csrc/common.h")
 
 
@@ -346,6 +459,10 @@ def main():
     ap.add_argument("--cost-model-check", action="store_true",
                     help="after the timed rollouts, run the no-abort counterfactual once and compare its "
                          "measured decode time with Eq. 4 on the PTL curve fitted to the early-stop run")
+    ap.add_argument("--next", action="store_true",
+                    help="the widened rows instead of the benchmark: adaptive redundancy (Alg. 1) against "
+                         "the uniform plan, token-chunk streaming, group advantages")
+    ap.add_argument("--stream-threshold", type=int, default=16384)
     ap.add_argument("--shared-prefix", action="store_true",
                     help="decode attention reads each prompt's shared pages once per group")
     ap.add_argument("--sweep", action="store_true",
@@ -391,6 +508,9 @@ def main():
         print(json.dumps(kernel_sweep(B, args.steps, args.warmup)), flush=True)
         return
     model, run = get_config(args.config)
+    if args.next:
+        print(json.dumps(next_rows(B, model, run, args.stream_threshold)), flush=True)
+        return
     prompts, forced = rollout_inputs(model, run)
     flags = (B.FLAG_TIMING | B.FLAG_STEP_TIMES | (B.FLAG_NO_ABORT if args.no_abort else 0) |
              (B.FLAG_SHARED_PREFIX if args.shared_prefix else 0))

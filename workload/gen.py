@@ -39,6 +39,26 @@ def rollout_inputs(model: ModelCfg, run: RunCfg):
     return prompts.astype(np.int32), d.astype(np.int32)
 
 
+def heterogeneous_forced_lengths(run: RunCfg, seed: int, sigmas=(0.3, 1.2)):
+    """Raw forced end-of-sequence draws [P*m] (int32, >= 1) whose spread
+    belongs to the prompt, as with prompts of unequal difficulty: prompt i
+    draws lognormal(ln median, sigmas[i % len(sigmas)]) lengths, and only the
+    prompts of the largest sigma have the Bernoulli(0.05) tail at U(5, 10) x
+    median (with ``len_tail``).  Used to exercise the adaptive allocation,
+    which needs a spread that persists per prompt."""
+    rng = np.random.default_rng(seed)
+    P, m = run.n_prompts, run.m
+    sig = np.repeat(np.array([sigmas[i % len(sigmas)] for i in range(P)], dtype=np.float64), m)
+    z = rng.standard_normal(P * m)
+    raw = run.len_median * np.exp(sig * z)
+    if run.len_tail:
+        tu = rng.random(P * m)
+        tf = rng.uniform(5.0, 10.0, P * m)
+        raw = np.where((tu < 0.05) & (sig == max(sigmas)), run.len_median * tf, raw)
+    d = np.maximum(1, np.rint(raw)).astype(np.int64)
+    return np.minimum(d, 1 << 30).astype(np.int32)
+
+
 def sweep_attention_inputs(rows=None, seed=None):
     """Context lengths [rows] (int32) and a page permutation seed for the attention sweep."""
     s = SWEEP
