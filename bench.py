@@ -396,7 +396,7 @@ def summarize_pmc(d):
     with --kernel-include-regex attn_bf16) and the rollout's bench line in
     d/bench_attn_fetch.json.  Each counter is scaled by what it reads for a
     plain 1 GiB device copy."""
-    out = {"kernel": "attn_bf16_kernel", "kernel_source_sha256": attn_source_hash()}
+    out = {"kernel": "attn_bf16_kernel + attn_bf16_db_kernel", "kernel_source_sha256": attn_source_hash()}
     cal = {}
     for c in ("FETCH_SIZE", "WRITE_SIZE"):
         rows = [v for n, v in _counter_rows(os.path.join(d, f"pmc_copy_{c}")) if "copyBuffer" in n]
@@ -619,7 +619,7 @@ def main():
         "sampling_steps": stats[-1]["steps"],
         "pages_hwm": stats[-1]["pages_hwm"],
         "kv_pool_pages": stats[-1]["n_pages"],
-        "roofline": {"bound": "hbm", "kernel": "attn_bf16_kernel (paged GQA decode attention)",
+        "roofline": {"bound": "hbm", "kernel": "attn_bf16_kernel + attn_bf16_db_kernel (paged GQA decode attention)",
                      "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": ach / HBM_PEAK_GBS, "traffic": measured_traffic(args.config),
                      "launches": attn_n, "avg_launch_us": 1e3 * attn_ms / max(attn_n, 1),
