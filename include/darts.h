@@ -372,7 +372,11 @@ size_t darts_attn_workspace_bytes(int32_t n_rows, int32_t n_q_heads, int32_t n_k
  *                 darts_fill_kv_pool); page ids are clamped into [0, n_pages)
  *   d_page_table  [n_rows][pt_stride] int32, pt_stride >= ceil(max_ctx/16)
  *   d_ctx_len     [n_rows] int32 in [1, max_ctx] (larger values are clamped,
- *                 rows with ctx <= 0 are left unwritten)
+ *                 rows with ctx <= 0 are left unwritten), or NULL: every row
+ *                 has max_ctx keys.  This equal-context form is the one a
+ *                 decode step takes (in bf16 the work is mapped without a
+ *                 device-built list, and from 64 rows each wavefront keeps
+ *                 two page pairs in flight).
  *   d_workspace   darts_attn_workspace_bytes(...) bytes, 256-byte aligned
  */
 int darts_attn_decode(const void* d_q, const void* d_k_pool, const void* d_v_pool,

@@ -161,8 +161,12 @@ def darts_attn_workspace_bytes(n_rows, n_q_heads, n_kv_heads, head_dim, max_ctx)
 
 
 def darts_attn_decode(q, k_pool, v_pool, n_pages, page_table, ctx_len, n_q_heads, n_kv_heads,
-                      head_dim, max_ctx, dtype, out, workspace, stream=None):
-    n_rows = ctx_len.numel()
+                      head_dim, max_ctx, dtype, out, workspace, stream=None, n_rows=None):
+    """ctx_len None: every one of n_rows rows has max_ctx keys."""
+    if ctx_len is not None:
+        n_rows = ctx_len.numel()
+    elif n_rows is None:
+        raise ValueError("n_rows is required when ctx_len is None")
     _check(load_library().darts_attn_decode(
         _ptr(q), _ptr(k_pool), _ptr(v_pool), n_pages, _ptr(page_table), page_table.shape[1],
         _ptr(ctx_len), n_rows, n_q_heads, n_kv_heads, head_dim, max_ctx, dtype, _ptr(out),

@@ -999,11 +999,14 @@ int darts_attn_decode(const void* d_q, const void* d_k_pool, const void* d_v_poo
   if (dtype != DARTS_F32 && dtype != DARTS_BF16) return DARTS_EINVAL;
   if (pt_stride < (max_ctx + kPage - 1) / kPage) return DARTS_EINVAL;
   if (n_rows == 0) return DARTS_OK;
-  if (!d_q || !d_k_pool || !d_v_pool || !d_page_table || !d_ctx_len || !d_out) return DARTS_EINVAL;
+  if (!d_q || !d_k_pool || !d_v_pool || !d_page_table || !d_out) return DARTS_EINVAL;
   if (workspace_bytes < attn_workspace_bytes(n_rows, n_q_heads, n_kv_heads, head_dim, max_ctx))
     return DARTS_EINVAL;
+  // no per-row contexts: every row attends to max_ctx keys (the equal-context
+  // form of a decode step)
   hipError_t e = launch_attention(d_q, d_k_pool, d_v_pool, n_pages, d_page_table, pt_stride, nullptr,
-                                  d_ctx_len, 0, 0, n_rows, n_q_heads, n_kv_heads, head_dim, max_ctx,
+                                  d_ctx_len, 0, d_ctx_len ? 0 : max_ctx, n_rows, n_q_heads, n_kv_heads,
+                                  head_dim, max_ctx,
                                   dtype == DARTS_BF16, d_out, d_workspace, workspace_bytes,
                                   (hipStream_t)stream);
   return e == hipSuccess ? DARTS_OK : DARTS_EHIP;

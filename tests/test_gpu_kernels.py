@@ -221,7 +221,7 @@ def test_sampler_full_sweep_size():
     assert (lp <= 1e-6).all()
 
 
-def _attn_case(rows, hq, hkv, hd, ctx, dtype, seed, spare=3):
+def _attn_case(rows, hq, hkv, hd, ctx, dtype, seed, spare=3, equal=False):
     B = _b()
     rng = np.random.default_rng(seed)
     pt, n_pages = sweep_page_table(ctx, 16, rng, spare=spare)
@@ -238,7 +238,8 @@ def _attn_case(rows, hq, hkv, hd, ctx, dtype, seed, spare=3):
     out = torch.zeros(rows * hq * hd, dtype=tdt, device=DEV)
     ws = torch.empty(B.darts_attn_workspace_bytes(rows, hq, hkv, hd, max_ctx), dtype=torch.uint8,
                      device=DEV)
-    B.darts_attn_decode(q, kp, vp, n_pages, ptd, ctxd, hq, hkv, hd, max_ctx, dt, out, ws)
+    B.darts_attn_decode(q, kp, vp, n_pages, ptd, None if equal else ctxd, hq, hkv, hd, max_ctx, dt,
+                        out, ws, n_rows=rows)
     torch.cuda.synchronize()
     return out.float().cpu().numpy().reshape(rows, hq, hd), pt
 
@@ -259,6 +260,34 @@ def test_attention_small_ragged(dtype, hq, hkv, hd):
         ref = OS.attention_row(r, int(ctx[r]), pt[r], seed, hq, hkv, hd)
         err = np.max(np.abs(got[r] - ref))
         assert err <= tol * max(1.0, np.max(np.abs(ref))), (r, ctx[r], err)
+
+
+@pytest.mark.parametrize("rows,hq,hkv,hd,ctx", [
+    (1, 32, 8, 128, 700),
+    (63, 32, 8, 128, 257),      # one row below the double-buffered form; odd page count
+    (64, 32, 8, 128, 257),      # the first double-buffered batch size
+    (64, 32, 8, 128, 17),       # one page pair, one key in its second page
+    (100, 32, 8, 128, 16),      # one page, no second page in the pair
+    (130, 32, 8, 128, 4111),    # rows split into chunks, combine
+    (512, 32, 8, 128, 1200),    # the rollout's first-step batch
+    (96, 16, 4, 64, 1500),
+    (80, 8, 8, 128, 33),        # G = 1
+    (72, 8, 2, 32, 600),
+])
+def test_attention_equal_contexts(rows, hq, hkv, hd, ctx):
+    """The equal-context form a decode step takes (no per-row contexts, work
+    mapped arithmetically; double-buffered page pairs from 64 rows) against
+    the oracle, on every row or a sample of them."""
+    say(f"attention equal contexts rows={rows} hq={hq} hkv={hkv} hd={hd} ctx={ctx}")
+    seed = 123
+    c = np.full(rows, ctx, dtype=np.int64)
+    got, pt = _attn_case(rows, hq, hkv, hd, c, "bf16", seed, equal=True)
+    sample = range(rows) if rows <= 64 else sorted({0, 1, rows // 2, rows - 1, *range(0, rows, 37)})
+    for r in sample:
+        ref = OS.attention_row(r, ctx, pt[r], seed, hq, hkv, hd)
+        err = np.max(np.abs(got[r] - ref))
+        assert err <= 2e-2 * max(1.0, np.max(np.abs(ref))), (r, err)
+    assert np.isfinite(got).all()
 
 
 def test_attention_full_sweep_sampled_rows():
