@@ -526,7 +526,9 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(
 // chunk were written directly by the attention kernel.  The chunk maxima and
 // denominators are reduced across lanes (lane = chunk), then each lane
 // accumulates its output dims over the chunks, taking each chunk's weight
-// exp(m_c - M) from the lane that computed it.
+// exp(m_c - M) from the lane that computed it.  The first batch of partial
+// outputs and the lane's own chunk statistics are loaded together, before
+// any reduction, so a row of up to kCB chunks costs one round trip to memory.
 template <typename OUT>
 __global__ void attn_combine_kernel(CtxSpec cs, int n_rows, int hq, int hd, int chunk_tokens,
                                     int uniform_nch, const int32_t* __restrict__ chunk_off,
@@ -541,35 +543,40 @@ __global__ void attn_combine_kernel(CtxSpec cs, int n_rows, int hq, int hd, int 
   // equal contexts (no work list): row r's chunks are partial sets r*nch ..
   const int c0 = uniform_nch > 0 ? row * uniform_nch : chunk_off[row];
   const float2* ml = ws_ml + (int64_t)c0 * hq + qh;          // chunk c at ml[c * hq]
-  float M = -INFINITY;
-  for (int c = lane; c < nch; c += 64) M = fmaxf(M, ml[(int64_t)c * hq].x);
-  M = wave_max(M);
-  float L = 0.f;
-  for (int c = lane; c < nch; c += 64) {
-    const float2 v = ml[(int64_t)c * hq];
-    L += v.y * __expf(v.x - M);
-  }
-  L = wave_sum(L);
-  const float invL = 1.0f / L;
   const int nd = (hd + 63) / 64;                             // output dims per lane: lane + 64 t
-  float acc[2] = {0.f, 0.f};
   const float* ob = ws_o + ((int64_t)c0 * hq + qh) * hd + lane;   // chunk c at ob[c * hq * hd]
   const int64_t cstride = (int64_t)hq * hd;
   // batches of up to kCB chunks: every partial of the batch is loaded before
   // any is accumulated, so a lane keeps 2 * kCB loads in flight
   constexpr int kCB = 16;
+  float o0[kCB], o1[kCB];
+  auto load_batch = [&](int c) {
+#pragma unroll
+    for (int j = 0; j < kCB; ++j) {
+      const float* o = ob + (int64_t)(c + j) * cstride;
+      const bool ok = c + j < nch;
+      o0[j] = (ok && lane < hd) ? o[0] : 0.f;
+      o1[j] = (ok && nd > 1) ? o[64] : 0.f;
+    }
+  };
+  load_batch(0);
+  const float2 v0 = lane < nch ? ml[(int64_t)lane * hq] : make_float2(-INFINITY, 0.f);
+  float M = v0.x;
+  for (int c = lane + 64; c < nch; c += 64) M = fmaxf(M, ml[(int64_t)c * hq].x);
+  M = wave_max(M);
+  float L = lane < nch ? v0.y * __expf(v0.x - M) : 0.f;
+  for (int c = lane + 64; c < nch; c += 64) {
+    const float2 v = ml[(int64_t)c * hq];
+    L += v.y * __expf(v.x - M);
+  }
+  L = wave_sum(L);
+  const float invL = 1.0f / L;
+  float acc[2] = {0.f, 0.f};
   for (int base = 0; base < nch; base += 64) {
     const int nb = min(64, nch - base);
-    const float w = lane < nb ? __expf(ml[(int64_t)(base + lane) * hq].x - M) : 0.f;
+    const float w = lane < nb ? __expf((base == 0 ? v0.x : ml[(int64_t)(base + lane) * hq].x) - M) : 0.f;
     for (int j0 = 0; j0 < nb; j0 += kCB) {
-      float o0[kCB], o1[kCB];
-#pragma unroll
-      for (int j = 0; j < kCB; ++j) {
-        const float* o = ob + (int64_t)(base + j0 + j) * cstride;
-        const bool ok = j0 + j < nb;
-        o0[j] = (ok && lane < hd) ? o[0] : 0.f;
-        o1[j] = (ok && nd > 1) ? o[64] : 0.f;
-      }
+      if (base + j0 > 0) load_batch(base + j0);
 #pragma unroll
       for (int j = 0; j < kCB; ++j) {
         const float wj = __shfl(w, (j0 + j) & 63, 64);
