@@ -274,19 +274,21 @@ def test_attention_small_ragged(dtype, hq, hkv, hd):
     (80, 8, 8, 128, 33),        # G = 1
     (72, 8, 2, 32, 600),
 ])
-def test_attention_equal_contexts(rows, hq, hkv, hd, ctx):
-    """The equal-context form a decode step takes (no per-row contexts, work
-    mapped arithmetically; double-buffered page pairs from 64 rows) against
-    the oracle, on every row or a sample of them."""
-    say(f"attention equal contexts rows={rows} hq={hq} hkv={hkv} hd={hd} ctx={ctx}")
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_attention_equal_contexts(rows, hq, hkv, hd, ctx, dtype):
+    """The equal-context form a decode step takes (no per-row contexts; in
+    bf16 the work is mapped arithmetically, with double-buffered page pairs
+    from 64 rows) against the oracle, on every row or a sample of them."""
+    say(f"attention equal contexts {dtype} rows={rows} hq={hq} hkv={hkv} hd={hd} ctx={ctx}")
     seed = 123
     c = np.full(rows, ctx, dtype=np.int64)
-    got, pt = _attn_case(rows, hq, hkv, hd, c, "bf16", seed, equal=True)
+    got, pt = _attn_case(rows, hq, hkv, hd, c, dtype, seed, equal=True)
+    tol = 2e-2 if dtype == "bf16" else 1e-5
     sample = range(rows) if rows <= 64 else sorted({0, 1, rows // 2, rows - 1, *range(0, rows, 37)})
     for r in sample:
         ref = OS.attention_row(r, ctx, pt[r], seed, hq, hkv, hd)
         err = np.max(np.abs(got[r] - ref))
-        assert err <= 2e-2 * max(1.0, np.max(np.abs(ref))), (r, err)
+        assert err <= tol * max(1.0, np.max(np.abs(ref))), (r, err)
     assert np.isfinite(got).all()
 
 

@@ -55,3 +55,14 @@ def test_bad_scalars_are_rejected(lib):
     assert lib.darts_select_groups(N, N, N, 0, 12, 8, 8, 16, 1, N, N, N) == EINVAL
     # streaming read: not whole 16-byte words
     assert lib.darts_stream_read(N, 24, N, N) == EINVAL
+
+
+def test_attention_equal_contexts_arguments(lib):
+    # NULL contexts (every row has max_ctx keys) pass the checks; with rows
+    # present a NULL q is still rejected before any device work
+    bf = B.DARTS_BF16
+    assert lib.darts_attn_decode(N, N, N, 1, N, 1, N, 0, 32, 8, 128, 16, bf, N, N, 0, N) == OK
+    assert lib.darts_attn_decode(N, N, N, 1, N, 1, N, 4, 32, 8, 128, 16, bf, N, N, 0, N) == EINVAL
+    # the binding needs the row count when no contexts are given
+    with pytest.raises(ValueError):
+        B.darts_attn_decode(None, None, None, 1, None, None, 32, 8, 128, 16, bf, None, None)
