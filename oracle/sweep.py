@@ -8,8 +8,12 @@ with logical layouts  Q: [rows][Hq][hd],  K and V pools: [page][Hkv][slot][hd].
 Decode attention for one row (definition, float64):
     out[h] = sum_j softmax_j(q_h . k_j / sqrt(hd)) v_j   over the row's ctx keys,
     key j lives in page table[j // page_size], slot j % page_size, kv head floor(h*Hkv/Hq).
-Pinned by: attention over one key returns that value; uniform keys give the
-mean of the values; GQA equals MHA with replicated kv heads (tests).
+Pinned (tests/test_oracle_sweep.py): sweep_values against the word mapping
+evaluated in float64 and rounded by PyTorch's bfloat16 conversion;
+attention_row against the paged pool gathered independently and passed to
+oracle.model.attention (itself pinned to PyTorch's grouped-query
+scaled dot-product attention), for 1, 4 and 8 query heads per kv head,
+ragged contexts and partly filled last pages; one key returns its value.
 """
 import math
 
