@@ -110,9 +110,13 @@ template <bool BF16, bool STATEFUL>
 __device__ __forceinline__ void finish_row(const SampleArgs& a, int r, const RowCtx& c, SoftState st,
                                            Best best) {
   const int g = c.g, step = c.step;
+  // A row with no finite perturbed score (every logit -inf or NaN) has no
+  // Gumbel-max winner: token 0 stands in (the lowest index, as for equal
+  // scores), and its log-prob and entropy are NaN.
+  const bool has_winner = best.i >= 0 && best.i < a.vocab;
   const float lse = st.m + logf(st.s);
-  const float ent = logf(st.s) - st.t / st.s;
-  const int sampled = best.i;
+  const float ent = has_winner ? logf(st.s) - st.t / st.s : NAN;
+  const int sampled = has_winner ? best.i : 0;
   int taken = sampled;
   uint8_t fin = 0;
   if (STATEFUL) {
@@ -126,9 +130,9 @@ __device__ __forceinline__ void finish_row(const SampleArgs& a, int r, const Row
   } else if (a.force && a.force[r] >= 0) {
     taken = a.force[r];
   }
-  if (taken < 0 || taken >= a.vocab) taken = sampled;
+  if (taken < 0 || taken >= a.vocab) taken = sampled;   // sampled is in [0, vocab)
   const float zt = logit_at<BF16>(c.row, taken, a.temperature != 1.0f, a.temperature);
-  const float lp = zt - lse;
+  const float lp = has_winner ? zt - lse : NAN;
   if (a.token_out) a.token_out[r] = taken;
   if (a.sampled_out) a.sampled_out[r] = sampled;
   if (a.logprob_out) a.logprob_out[r] = lp;

@@ -153,6 +153,40 @@ def test_sampler_edge_rows():
             assert stok in (5, 2049, 4095)
 
 
+def test_sampler_rows_without_finite_score():
+    """Rows whose every logit is -inf or NaN have no Gumbel-max winner: the
+    token is 0 (the lowest index, as the oracle's first-maximum argmax gives
+    for equal scores), a teacher-forced token is still taken, and log-prob
+    and entropy are NaN on both sides.  Ordinary rows in the same launch are
+    unaffected."""
+    B = _b()
+    V, seed = 4096, 77
+    rng = np.random.default_rng(21)
+    z = rng.normal(0, 1, (5, V)).astype(np.float32)
+    z[1] = -np.inf
+    z[2] = np.nan
+    z[3] = -np.inf
+    force = np.array([-1, -1, -1, 17, -1], dtype=np.int32)
+    traj = torch.arange(5, dtype=torch.int32, device=DEV) + 40
+    step = torch.full((5,), 3, dtype=torch.int32, device=DEV)
+    tok = torch.empty(5, dtype=torch.int32, device=DEV)
+    lp = torch.empty(5, dtype=torch.float32, device=DEV)
+    ent = torch.empty(5, dtype=torch.float32, device=DEV)
+    B.darts_sample(torch.from_numpy(z).to(DEV), B.DARTS_F32, seed, traj, step, 1.0,
+                   torch.from_numpy(force).to(DEV), tok, lp, ent)
+    torch.cuda.synchronize()
+    tok, lp, ent = tok.cpu().numpy(), lp.cpu().numpy(), ent.cpu().numpy()
+    for r in range(5):
+        stok, slp, sent = sample_row(z[r], 1.0, 40 + r, 3, seed, int(force[r]))
+        taken = stok if force[r] < 0 else int(force[r])
+        assert tok[r] == taken, (r, tok[r], taken)
+        if r in (1, 2, 3):
+            assert stok == 0 and np.isnan(slp) and np.isnan(sent)
+            assert np.isnan(lp[r]) and np.isnan(ent[r]), (r, lp[r], ent[r])
+        else:
+            assert abs(lp[r] - slp) < 1e-5 and abs(ent[r] - sent) < 1e-5, r
+
+
 def _bf16_tensor(bits):
     return torch.from_numpy(bits.view(np.int16)).to(DEV).view(torch.bfloat16)
 
