@@ -20,6 +20,7 @@ import os
 import sys
 import time
 
+T_PROCESS = time.perf_counter()
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -58,8 +59,15 @@ def cpu_baseline(model, run, budget_s=20.0):
 
     def layer():
         r = lambda *s: np.full(s, 1.0 / s[-1])
-        return OM.LayerW(wq=r(hq * hd, d), wk=r(hkv * hd, d), wv=r(hkv * hd, d), wo=r(d, hq * hd),
-                         wgate=r(F, d), wup=r(F, d), wdown=r(d, F))
+        lw = OM.LayerW(wq=r(hq * hd, d), wk=r(hkv * hd, d), wv=r(hkv * hd, d), wo=r(d, hq * hd))
+        if model.is_moe:
+            E, Fe = model.n_experts, model.expert_ffn
+            # distinct router rows, so routing picks top_k experts as it would
+            lw.router = rng.standard_normal((E, d)) / math.sqrt(d)
+            lw.egate, lw.eup, lw.edown = r(E, Fe, d), r(E, Fe, d), r(E, d, Fe)
+        else:
+            lw.wgate, lw.wup, lw.wdown = r(F, d), r(F, d), r(d, F)
+        return lw
 
     B = run.m
     ctx0 = run.prompt_len + 512
@@ -453,7 +461,15 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=1)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--config", default="qwen3-8b")
+    ap.add_argument("--config", default="qwen3-30b-a3b",
+                    help="workload (default: the Qwen3-30B-A3B-shaped MoE rollout, the largest that "
+                         "fits one GPU)")
+    ap.add_argument("--budget-s", type=float, default=420.0,
+                    help="wall-time budget of the whole run: a step is one full rollout, so warmup is "
+                         "clamped to 1 rollout and the timed rollouts to what fits (the line reports "
+                         "the counts run next to the counts requested)")
+    ap.add_argument("--timed-s", type=float, default=75.0,
+                    help="target length of the timed region (at least one rollout is timed)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-abort", action="store_true", help="counterfactual without early stop")
     ap.add_argument("--cost-model-check", action="store_true",
@@ -538,14 +554,27 @@ def main():
         torch.cuda.synchronize()
         return time.perf_counter() - t0, ro.stats()
 
-    for w in range(args.warmup):
+    # A step is a whole rollout (tens of seconds at the large configurations):
+    # one warmup rollout at most, then as many timed rollouts as fit both the
+    # timed-region target and what is left of the budget once the CPU
+    # baseline and the read-rate probe are reserved.
+    n_warm = min(max(args.warmup, 0), 1)
+    t_roll = None
+    for w in range(n_warm):
         dt, st = one_rollout()
+        t_roll = dt
         print(f"[bench] warmup {w}: {dt:.2f} s, {st['tokens_decoded']} tokens", file=sys.stderr,
               flush=True)
     torch.cuda.synchronize()
+    reserve = 0.0 if args.no_cpu_baseline else 45.0
+    left = args.budget_s - (time.perf_counter() - T_PROCESS) - reserve - 15.0
+    n_steps = max(1, args.steps)
+    if t_roll is not None:
+        n_steps = max(1, min(n_steps, int(min(args.timed_s, left) // t_roll)))
+    print(f"[bench] timing {n_steps} rollout(s) ({args.steps} requested)", file=sys.stderr, flush=True)
     walls, stats = [], []
     t0 = time.perf_counter()
-    for k in range(args.steps):
+    for k in range(n_steps):
         dt, st = one_rollout()
         walls.append(dt)
         stats.append(st)
@@ -553,6 +582,7 @@ def main():
               f"{st['steps']} sampling steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     total = time.perf_counter() - t0
+    n_timed = len(walls)
     tokens = sum(s["tokens_decoded"] for s in stats)
     attn_ms = sum(s["attn_ms"] for s in stats)
     attn_b = sum(s["attn_bytes"] for s in stats)
@@ -577,8 +607,31 @@ def main():
         ms = sum(s["gemm_cls_ms"][i] for s in stats)
         fl_ = sum(s["gemm_cls_flop"][i] for s in stats)
         cls[name] = {"ms": ms, "tflops": fl_ / (ms * 1e-3) / 1e12 if ms > 0 else 0.0}
+    moe_roof = None
+    if model.is_moe:
+        # the grouped expert GEMMs inside the MoE block: algorithmic bytes (the
+        # touched experts' weights once, routed rows in and out) over their own
+        # HIP-event time
+        moe_roof = {}
+        for i, name in enumerate(["expert_gate_up", "expert_down"]):
+            ms = sum(s["moe_expert_ms"][i] for s in stats)
+            by = sum(s["moe_expert_bytes"][i] for s in stats)
+            n_l = sum(s["moe_expert_launches"][i] for s in stats)
+            ach_m = by / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
+            moe_roof[name] = {"bound": "hbm", "achieved": ach_m, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                              "frac": ach_m / HBM_PEAK_GBS, "traffic": None,
+                              "kernel": "gemm_dma_grouped_kernel (" + ("gate/up + SwiGLU" if i == 0 else "down") + ")",
+                              "launches": n_l, "avg_launch_us": 1e3 * ms / max(n_l, 1),
+                              "algorithmic_bytes_per_launch": by / max(n_l, 1),
+                              "share_of_step_time": ms * 1e-3 / total}
+        cls["moe_block"]["routing_and_combine_ms"] = cls["moe_block"]["ms"] - sum(
+            sum(s["moe_expert_ms"][i] for s in stats) for i in range(2))
     ro.close()
-    read_gbs = hbm_read_rate(B)
+    try:
+        read_gbs = hbm_read_rate(B)
+    except Exception as e:  # reported next to the peak; never the metric itself
+        print(f"[bench] read-rate probe failed: {e!r}", file=sys.stderr, flush=True)
+        read_gbs = float("nan")
     roof = gemm_class_roofline(model, run, rows, HBM_PEAK_GBS, peak_mm)
     for name, rms in roof.items():
         if cls[name]["ms"] > 0:
@@ -602,9 +655,13 @@ def main():
         "value": tokens / total,
         "unit": "tokens/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": 1e3 * total / args.steps,
+        "steps": n_timed,
+        "warmup": n_warm,
+        "steps_requested": args.steps,
+        "warmup_requested": args.warmup,
+        "step_unit": "one whole rollout (prefill to the last kept set); warmup and timed rollouts are "
+                     "clamped to the run's wall budget",
+        "ms_per_step": 1e3 * total / n_timed,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -627,6 +684,7 @@ def main():
                      "algorithmic_bytes_per_launch": attn_b / max(attn_n, 1),
                      "measured_read_GBs": read_gbs, "frac_of_measured_read": ach / read_gbs,
                      "share_of_step_time": attn_ms * 1e-3 / total},
+        "roofline_moe_experts": moe_roof,
         "gemm": {"bound": "mfma", "achieved": gemm_tf, "peak": peak_mm, "unit": "TFLOP/s",
                  "frac": gemm_tf / peak_mm, "share_of_step_time": gemm_ms * 1e-3 / total,
                  "frac_of_roofline": (sum(v.get("roofline_ms", 0.0) for v in cls.values())
@@ -652,6 +710,7 @@ def main():
             out["cpu_baseline"] = cpu_baseline(model, run)
         except Exception as e:  # the baseline is context, never the product path
             out["cpu_baseline"] = {"error": repr(e)}
+    out["wall_s"] = time.perf_counter() - T_PROCESS
     print(json.dumps(out), flush=True)
 
 

@@ -155,6 +155,14 @@ typedef struct {
   double attn_traj_bytes;    /* the same launches' bytes if every row read its whole
                                 context itself (equal to attn_bytes unless
                                 DARTS_FLAG_SHARED_PREFIX) */
+  /* Mixture-of-experts models with DARTS_FLAG_TIMING: the grouped expert
+   * GEMMs inside the MoE block ([0] gate/up with the SwiGLU epilogue, [1]
+   * down), estimated for the whole run as above.  Bytes are algorithmic:
+   * the weights of every expert that received rows, once, plus the routed
+   * rows' inputs and outputs.                                              */
+  double moe_expert_ms[2];
+  double moe_expert_bytes[2];
+  int64_t moe_expert_launches[2];
 } darts_stats;
 
 typedef struct darts_ctx darts_ctx;
@@ -267,6 +275,24 @@ int darts_get_traj_scores(darts_ctx* ctx, int32_t* d_len, float* d_sum_lp, float
 /* Copy the last step's float32 logits [n_rows * vocab] (rows in the order of
  * the last darts_step_out) into d_dst.  For verification.                  */
 int darts_debug_logits(darts_ctx* ctx, float* d_dst, int32_t* h_n_rows);
+
+/* Verification of mixture-of-experts routing (MoE models only).  Until the
+ * next call, every prefill and decode step reads and writes, for each of its
+ * rows and each layer l, entries [key][l][0..top_k) of these device buffers
+ * (each [n_keys][n_layers][top_k], caller-owned, any may be NULL), where key
+ * is the prompt position i*prompt_len + t for prefill rows and the
+ * trajectory id for decode rows:
+ *   d_force_ids  int32 expert ids to combine instead of the router's own
+ *                top-k, weighted by their own softmax probabilities
+ *                renormalised over the k (the routing analogue of teacher
+ *                forcing); a row whose entry 0 is negative, or that holds an
+ *                id outside [0, n_experts), keeps its own routing
+ *   d_own_ids    int32 out: the router's own top-k ids, rank order
+ *   d_used_p     float out: softmax probability of each combined expert
+ * All NULL turns verification off.  Errors: DARTS_EINVAL for a dense model
+ * or n_keys < max(n_prompts*prompt_len, n_prompts*m).                      */
+int darts_debug_moe_routing(darts_ctx* ctx, const int32_t* d_force_ids, int32_t* d_own_ids,
+                            float* d_used_p, int64_t n_keys);
 
 int darts_destroy(darts_ctx* ctx);
 const char* darts_strerror(int status);
@@ -413,7 +439,10 @@ int darts_attn_decode_shared(const void* d_q, const void* d_k_pool, const void* 
 /* Fused sampler: for each row, Gumbel-max token with counter (traj, step),
  * log-prob of the taken token (d_force[r] if d_force != NULL and >= 0, else
  * the sample) and entropy of softmax(logits / T).
- *   d_logits [n_rows][vocab] (bf16 or f32), d_traj/d_step [n_rows] int32.   */
+ *   d_logits [n_rows][vocab] (bf16 or f32), d_traj/d_step [n_rows] int32.
+ * A row with no finite perturbed score (every logit -inf or NaN) samples
+ * token 0 and gets NaN log-prob and entropy; no memory outside the row is
+ * read.  (The rollout's sampler behaves the same way.)                      */
 int darts_sample(const void* d_logits, int32_t n_rows, int32_t vocab, int32_t dtype,
                  uint64_t seed, const int32_t* d_traj, const int32_t* d_step, float temperature,
                  const int32_t* d_force, int32_t* d_token, float* d_logprob, float* d_entropy,

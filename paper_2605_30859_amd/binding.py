@@ -50,7 +50,9 @@ class Stats(C.Structure):
                 ("n_done", C.c_int32), ("attn_ms", C.c_double), ("attn_bytes", C.c_double),
                 ("attn_launches", C.c_int64), ("gemm_ms", C.c_double), ("gemm_flop", C.c_double),
                 ("gemm_launches", C.c_int64), ("gemm_cls_ms", C.c_double * 6),
-                ("gemm_cls_flop", C.c_double * 6), ("attn_traj_bytes", C.c_double)]
+                ("gemm_cls_flop", C.c_double * 6), ("attn_traj_bytes", C.c_double),
+                ("moe_expert_ms", C.c_double * 2), ("moe_expert_bytes", C.c_double * 2),
+                ("moe_expert_launches", C.c_int64 * 2)]
 
 
 _P = C.c_void_p
@@ -63,6 +65,7 @@ _SIGS = {
     "darts_get_traj_scores": (C.c_int, [_P, _P, _P, _P, _P]),
     "darts_debug_logits": (C.c_int, [_P, _P, C.POINTER(C.c_int32)]),
     "darts_destroy": (C.c_int, [_P]),
+    "darts_debug_moe_routing": (C.c_int, [_P, _P, _P, _P, C.c_int64]),
     "darts_reset": (C.c_int, [_P]),
     "darts_set_plan": (C.c_int, [_P, _P]),
     "darts_prompt_length_std": (C.c_int, [_P, _P, C.c_int32, C.c_int32, _P]),
@@ -405,7 +408,7 @@ class Rollout:
         out = {}
         for f, _ in Stats._fields_:
             v = getattr(s, f)
-            out[f] = list(v) if f.startswith("gemm_cls") else v
+            out[f] = list(v) if (f.startswith("gemm_cls") or f.startswith("moe_expert")) else v
         return out
 
     def step_times(self):
@@ -451,6 +454,14 @@ class Rollout:
         st = t.zeros(self.n_traj, dtype=t.uint8, device=dev)
         _check(self.lib.darts_get_traj_scores(self.ctx, _ptr(ln), _ptr(slp), _ptr(mlp), _ptr(st)), self.ctx)
         return ln, slp, mlp, st
+
+    def debug_moe_routing(self, force_ids=None, own_ids=None, used_p=None):
+        """Routing verification buffers ([keys][n_layers][top_k] device tensors,
+        int32 / int32 / float32; None turns a buffer off)."""
+        ts = [t for t in (force_ids, own_ids, used_p) if t is not None]
+        n_keys = ts[0].shape[0] if ts else 0
+        _check(self.lib.darts_debug_moe_routing(self.ctx, _ptr(force_ids), _ptr(own_ids), _ptr(used_p),
+                                                n_keys), self.ctx)
 
     def debug_logits(self, rows):
         t = self.torch

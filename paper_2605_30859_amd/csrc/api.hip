@@ -37,6 +37,8 @@ struct TimedLaunch {
   double weight;   // launches of the whole run this one stands for
   double units_grp = 0.0;   // attention with a shared prefix: bytes per live prompt group
   double traj_units = 0.0;  // attention: bytes if every row read its whole context itself
+  int touched_slot = -1;    // grouped expert GEMMs: slot of the launch's touched-expert count
+  double rows = 0.0;        // grouped expert GEMMs: routed (row, expert) pairs
 };
 
 // With timing on, events are recorded in the prefill and in every
@@ -67,6 +69,12 @@ struct darts_ctx {
   float* m_y_perm = nullptr;
   float* m_logits = nullptr;      // router logits [rows][Epad]
   int32_t* m_mtiles = nullptr;    // n_mtiles | non-empty expert row tiles
+  int32_t* m_touched = nullptr;   // [n_layers] experts that received rows (timed launches)
+  int32_t* h_touched = nullptr;   // pinned host copy
+  // routing verification (darts_debug_moe_routing)
+  const int32_t* dbg_force_ids = nullptr;
+  int32_t* dbg_own_ids = nullptr;
+  float* dbg_used_p = nullptr;
   // device memory
   std::vector<void*> allocs;
   void* embed = nullptr;
@@ -149,6 +157,8 @@ struct darts_ctx {
   double gemm_ms = 0.0, gemm_flop = 0.0;
   int64_t gemm_launches = 0;
   double cls_ms[6] = {0, 0, 0, 0, 0, 0}, cls_flop[6] = {0, 0, 0, 0, 0, 0};
+  double moe_ms[2] = {0, 0}, moe_bytes[2] = {0, 0};
+  int64_t moe_launches[2] = {0, 0};
 };
 
 #define HIPCHK(ctx, expr)                                                      \
@@ -181,6 +191,8 @@ static void free_all(darts_ctx* c) {
   c->allocs.clear();
   if (c->h_info) (void)hipHostFree(c->h_info);
   c->h_info = nullptr;
+  if (c->h_touched) (void)hipHostFree(c->h_touched);
+  c->h_touched = nullptr;
   for (hipEvent_t e : c->events) (void)hipEventDestroy(e);
   c->events.clear();
   c->pending.clear();
@@ -459,6 +471,7 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
     A(&c->m_row_of, pairs * 4);
     A(&c->m_h_perm, pairs * c->Fe * 2);
     A(&c->m_y_perm, pairs * c->d * 4);
+    A(&c->m_touched, (size_t)c->nl * 4);
   }
   if (rc.flags & DARTS_FLAG_STREAM) {
     A(&c->hist_tok, (size_t)c->n_traj * c->cap * 4);
@@ -481,6 +494,8 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
                                                                                c->hd, c->Lp + c->cap, c->pp));
   A(&c->attn_ws, c->attn_ws_bytes);
   if (e == hipSuccess) e = hipHostMalloc((void**)&c->h_info, 64, hipHostMallocDefault);
+  if (e == hipSuccess && moe && (rc.flags & DARTS_FLAG_TIMING))
+    e = hipHostMalloc((void**)&c->h_touched, (size_t)c->nl * 4, hipHostMallocDefault);
   if (e == hipSuccess && (rc.flags & DARTS_FLAG_STEP_TIMES)) {
     e = hipEventCreate(&c->step_ev[0]);
     if (e == hipSuccess) e = hipEventCreate(&c->step_ev[1]);
@@ -563,6 +578,7 @@ int darts_reset(darts_ctx* c) {
   c->attn_ms = c->attn_bytes = c->attn_traj_bytes = 0.0; c->attn_launches = 0;
   c->gemm_ms = c->gemm_flop = 0.0; c->gemm_launches = 0;
   for (int i = 0; i < 6; ++i) c->cls_ms[i] = c->cls_flop[i] = 0.0;
+  for (int i = 0; i < 2; ++i) { c->moe_ms[i] = c->moe_bytes[i] = 0.0; c->moe_launches[i] = 0; }
   return DARTS_OK;
 }
 
@@ -625,6 +641,8 @@ static int run_attention(darts_ctx* c, int layer, int n_rows, const int32_t* row
 }
 
 enum { G_QKV = 0, G_O, G_GU, G_DOWN, G_LM, G_MOE };
+// TimedLaunch kinds of the grouped expert GEMMs (after the GEMM classes)
+enum { kMoeGu = 1 + G_MOE + 1, kMoeDown = kMoeGu + 1 };
 static hipError_t gemm_t(darts_ctx* c, int cls, const void* A, int lda, const void* W, int ldw,
                          void* C, int ldc, int M, int N, int K, int epi) {
   const int ti = tbegin(c, 1 + cls, 2.0 * M * N * K);
@@ -655,8 +673,8 @@ static hipError_t gemm_add_t(darts_ctx* c, int cls, const void* A, int lda, cons
 // Decoder layers over n rows whose residual stream is in c->x.  normed: c->xn
 // already holds RMSNorm(x) on entry; on return, whether it holds the final
 // residual's norm.
-static int run_layers(darts_ctx* c, int n, const int32_t* row_pt, int pos_mod, int pos_base,
-                      int ctx_mod, int ctx_base, int max_ctx, bool* normed) {
+static int run_layers(darts_ctx* c, int n, const int32_t* row_pt, const int32_t* row_key, int pos_mod,
+                      int pos_base, int ctx_mod, int ctx_base, int max_ctx, bool* normed) {
   const bool b = c->bf16;
   const int d = c->d, hqd = c->hq * c->hd;
   for (int l = 0; l < c->nl; ++l) {
@@ -685,7 +703,7 @@ static int run_layers(darts_ctx* c, int n, const int32_t* row_pt, int pos_mod, i
     HIPCHK(c, gemm_add_t(c, G_O, c->attn, hqd, w.wo, hqd, n, hqd, normed));
     if (!*normed) HIPCHK(c, launch_rmsnorm(c->x, n, d, c->mc.rms_eps, c->xn, b, c->st));
     if (c->moe) {
-      MoeArgs m;
+      MoeArgs m{};   // every optional pointer and event NULL unless set below
       m.xn = (bf16_t*)c->xn; m.x = c->x; m.n_rows = n; m.d = d; m.E = c->E; m.k = c->topk;
       m.eps = c->mc.rms_eps; m.row_of = c->m_row_of;
       m.Fe = c->Fe; m.w_router = (const bf16_t*)w.wrouter; m.w_gu = (const bf16_t*)w.wegu;
@@ -696,8 +714,26 @@ static int run_layers(darts_ctx* c, int n, const int32_t* row_pt, int pos_mod, i
       m.pos_of = c->m_pos_of; m.counts = c->m_cnt; m.offsets = c->m_cnt + c->E;
       m.cursors = c->m_cnt + 2 * c->E;
       m.h_perm = (bf16_t*)c->m_h_perm; m.y_perm = c->m_y_perm;
+      const int64_t dstride = (int64_t)c->nl * c->topk;
+      m.route_key = row_key; m.dbg_stride = dstride;
+      m.force_ids = c->dbg_force_ids ? c->dbg_force_ids + (int64_t)l * c->topk : nullptr;
+      m.own_ids_out = c->dbg_own_ids ? c->dbg_own_ids + (int64_t)l * c->topk : nullptr;
+      m.used_p_out = c->dbg_used_p ? c->dbg_used_p + (int64_t)l * c->topk : nullptr;
       const double flop = 2.0 * n * ((double)c->E * d + (double)c->topk * 3.0 * c->Fe * d);
       const int ti = tbegin(c, 1 + G_MOE, flop);
+      if (ti >= 0) {
+        // the two grouped expert GEMMs inside the block are timed on their
+        // own; their bytes follow from the touched-expert count read back
+        // after the step
+        const int tg = treserve(c, kMoeGu, 0.0), td = treserve(c, kMoeDown, 0.0);
+        if (tg >= 0 && td >= 0) {
+          m.ev_gu0 = c->events[2 * tg]; m.ev_gu1 = c->events[2 * tg + 1];
+          m.ev_down0 = c->events[2 * td]; m.ev_down1 = c->events[2 * td + 1];
+          m.touched_out = c->m_touched + l;
+          c->pending[tg].touched_slot = c->pending[td].touched_slot = l;
+          c->pending[tg].rows = c->pending[td].rows = (double)n * c->topk;
+        }
+      }
       HIPCHK(c, launch_moe_ffn(m, c->st, normed));
       tend(c, ti);
       continue;
@@ -735,7 +771,7 @@ int darts_prefill(darts_ctx* c, const int32_t* d_prompts, const int32_t* d_force
   if (b) HIPCHK(c, launch_embed_norm(c->embed, d_prompts, nullptr, rows, c->d, c->V, c->mc.rms_eps,
                                      c->x, c->xn, c->st));
   else HIPCHK(c, launch_embed_v(c->embed, b, d_prompts, nullptr, rows, c->d, c->V, c->x, c->st));
-  int r = run_layers(c, rows, c->prefill_pt, c->Lp, 0, c->Lp, 1, c->Lp, &normed);
+  int r = run_layers(c, rows, c->prefill_pt, nullptr, c->Lp, 0, c->Lp, 1, c->Lp, &normed);
   if (r != DARTS_OK) return r;
   HIPCHK(c, launch_gather_rows(c->x, c->last_rows, c->P, c->d, c->xlast, c->st));
   HIPCHK(c, launch_rmsnorm(c->xlast, c->P, c->d, c->mc.rms_eps, c->xn, b, c->st));
@@ -789,7 +825,7 @@ int darts_decode_step(darts_ctx* c, const int32_t* d_force_tokens, darts_step_ou
   if (b) HIPCHK(c, launch_embed_norm(c->embed, c->last_tok, live, n, c->d, c->V, c->mc.rms_eps, c->x,
                                      c->xn, c->st));
   else HIPCHK(c, launch_embed_v(c->embed, b, c->last_tok, live, n, c->d, c->V, c->x, c->st));
-  int r = run_layers(c, n, live, 0, pos, 0, pos + 1, pos + 1, &normed);
+  int r = run_layers(c, n, live, live, 0, pos, 0, pos + 1, pos + 1, &normed);
   if (r != DARTS_OK) return r;
   if (!normed) HIPCHK(c, launch_rmsnorm(c->x, n, c->d, c->mc.rms_eps, c->xn, b, c->st));
   HIPCHK(c, gemm_t(c, G_LM, c->xn, c->d, c->lm_head, c->d, c->logits, c->V, n, c->V, c->d, EPI_F32));
@@ -834,6 +870,10 @@ int darts_select_and_prune(darts_ctx* c, int32_t* d_kept, int32_t* d_done_step, 
   const int timed_rows = c->step_rows;
   if (timed_rows != 0) HIPCHK(c, hipEventRecord(c->step_ev[1], c->st));
   HIPCHK(c, hipMemcpyAsync(c->h_info, c->dcnt + 4, 32, hipMemcpyDeviceToHost, c->st));
+  bool touched = false;
+  for (const TimedLaunch& t : c->pending) touched = touched || t.touched_slot >= 0;
+  if (touched && c->h_touched)
+    HIPCHK(c, hipMemcpyAsync(c->h_touched, c->m_touched, (size_t)c->nl * 4, hipMemcpyDeviceToHost, c->st));
   HIPCHK(c, hipStreamSynchronize(c->st));
   if (timed_rows != 0) {
     float ms = 0.f;
@@ -857,8 +897,18 @@ int darts_select_and_prune(darts_ctx* c, int32_t* d_kept, int32_t* d_done_step, 
       const double units = t.units + (t.units_grp > 0.0 ? t.units_grp * c->h_info[4] : 0.0);
       c->attn_ms += w * ms; c->attn_bytes += w * units; c->attn_traj_bytes += w * t.traj_units;
       c->attn_launches += (int64_t)w;
-    }
-    else {
+    } else if (t.kind == kMoeGu || t.kind == kMoeDown) {
+      // algorithmic bytes: the touched experts' weights once, the routed
+      // rows' inputs and outputs (gate/up: bf16 rows in, bf16 SwiGLU rows out;
+      // down: bf16 rows in, fp32 rows out)
+      if (!c->h_touched || t.touched_slot < 0) continue;
+      const double ne = c->h_touched[t.touched_slot];
+      const double dd = c->d, fe = c->Fe;
+      const int i = t.kind == kMoeGu ? 0 : 1;
+      const double bytes = i == 0 ? ne * 2.0 * fe * dd * 2.0 + t.rows * (dd * 2.0 + fe * 2.0)
+                                  : ne * dd * fe * 2.0 + t.rows * (fe * 2.0 + dd * 4.0);
+      c->moe_ms[i] += w * ms; c->moe_bytes[i] += w * bytes; c->moe_launches[i] += (int64_t)w;
+    } else {
       c->gemm_ms += w * ms; c->gemm_flop += w * t.units; c->gemm_launches += (int64_t)w;
       c->cls_ms[t.kind - 1] += w * ms; c->cls_flop[t.kind - 1] += w * t.units;
     }
@@ -886,6 +936,11 @@ int darts_get_stats(const darts_ctx* c, darts_stats* s) {
   s->gemm_flop = c->gemm_flop;
   s->gemm_launches = c->gemm_launches;
   for (int i = 0; i < 6; ++i) { s->gemm_cls_ms[i] = c->cls_ms[i]; s->gemm_cls_flop[i] = c->cls_flop[i]; }
+  for (int i = 0; i < 2; ++i) {
+    s->moe_expert_ms[i] = c->moe_ms[i];
+    s->moe_expert_bytes[i] = c->moe_bytes[i];
+    s->moe_expert_launches[i] = c->moe_launches[i];
+  }
   return DARTS_OK;
 }
 
@@ -951,6 +1006,19 @@ int darts_debug_logits(darts_ctx* c, float* d_dst, int32_t* h_n_rows) {
   HIPCHK(c, hipMemcpyAsync(d_dst, c->logits, (size_t)rows * c->V * 4, hipMemcpyDeviceToDevice, c->st));
   HIPCHK(c, hipStreamSynchronize(c->st));
   if (h_n_rows) *h_n_rows = rows;
+  return DARTS_OK;
+}
+
+int darts_debug_moe_routing(darts_ctx* c, const int32_t* d_force_ids, int32_t* d_own_ids,
+                            float* d_used_p, int64_t n_keys) {
+  if (!c) return DARTS_EINVAL;
+  if (c->poisoned) return DARTS_EHIP;
+  if (!c->moe) return DARTS_EINVAL;
+  const bool any = d_force_ids || d_own_ids || d_used_p;
+  if (any && n_keys < std::max<int64_t>((int64_t)c->P * c->Lp, c->n_traj)) return DARTS_EINVAL;
+  c->dbg_force_ids = d_force_ids;
+  c->dbg_own_ids = d_own_ids;
+  c->dbg_used_p = d_used_p;
   return DARTS_OK;
 }
 

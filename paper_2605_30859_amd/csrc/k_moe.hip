@@ -29,12 +29,15 @@ namespace darts {
 // router GEMM needs no separate reduce.
 constexpr int kMoeMaxPerLane = 16;   // E <= 1024
 constexpr int kMoeMaxSplits = 8;     // router GEMM K splits the top-k kernel sums
-template <int NPL>
+// DBG (verification only): the router's own ids are exported, and a row whose
+// key has k forced ids in [0, E) combines those experts instead, with their
+// own softmax probabilities renormalised over the k.
+template <int NPL, bool DBG>
 __global__ void __launch_bounds__(256) moe_topk_kernel(const float* __restrict__ logits, int ld,
                                                        int n_split, int64_t split_stride,
                                                        int n_rows, int E, int k,
                                                        int32_t* __restrict__ topk_id,
-                                                       float* __restrict__ topk_w) {
+                                                       float* __restrict__ topk_w, MoeArgs dbg) {
   const int lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (r >= n_rows) return;
@@ -71,6 +74,11 @@ __global__ void __launch_bounds__(256) moe_topk_kernel(const float* __restrict__
   const float inv = 1.0f / sum;
 #pragma unroll
   for (int j = 0; j < NPL; ++j) p[j] = (lane + 64 * j < E) ? p[j] * inv : -2.0f;
+  float p0[DBG ? NPL : 1];
+  if (DBG) {
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) p0[j] = p[j];
+  }
   float wsum = 0.f;
   float my_w = 0.f;
   int my_id = 0;
@@ -93,6 +101,28 @@ __global__ void __launch_bounds__(256) moe_topk_kernel(const float* __restrict__
       if (lane + 64 * j == bi) p[j] = -2.0f;          // removed
     if (lane == t) { my_w = bv; my_id = bi; }         // lane t keeps round t's winner
     wsum += bv;
+  }
+  if (DBG) {
+    const int64_t key = dbg.route_key ? (int64_t)dbg.route_key[r] : (int64_t)r;
+    if (dbg.own_ids_out && lane < k) dbg.own_ids_out[key * dbg.dbg_stride + lane] = my_id;
+    if (dbg.force_ids) {
+      const int32_t* f = dbg.force_ids + key * dbg.dbg_stride;
+      const int fid = lane < k ? f[lane] : 0;
+      const bool forced = f[0] >= 0 && __all(fid >= 0 && fid < E);
+      if (forced) {
+        // probability of expert fid: lane fid % 64 holds it in slot fid / 64
+        float pf = 0.f;
+#pragma unroll
+        for (int j = 0; j < NPL; ++j) {
+          const float v = __shfl(p0[j], fid & 63, 64);
+          if ((fid >> 6) == j) pf = v;
+        }
+        my_id = fid;
+        my_w = pf;
+        wsum = wave_sum(lane < k ? pf : 0.f);
+      }
+    }
+    if (dbg.used_p_out && lane < k) dbg.used_p_out[key * dbg.dbg_stride + lane] = my_w;
   }
   if (lane < k) {
     topk_id[(int64_t)r * k + lane] = my_id;
@@ -128,7 +158,8 @@ __global__ void __launch_bounds__(1024) moe_offsets_kernel(const int32_t* __rest
                                                            int32_t* __restrict__ mtiles,
                                                            int32_t* __restrict__ n_mtiles,
                                                            int32_t* __restrict__ pos_of,
-                                                           int32_t* __restrict__ row_of) {
+                                                           int32_t* __restrict__ row_of,
+                                                           int32_t* __restrict__ touched_out) {
   __shared__ int32_t hist[1024];
   __shared__ int32_t sh[1024];
   const int tid = threadIdx.x;
@@ -152,6 +183,10 @@ __global__ void __launch_bounds__(1024) moe_offsets_kernel(const int32_t* __rest
     for (int j = 0; j < nt; ++j) mtiles[tex + j] = (tid << 16) | j;
   }
   if (tid == 0) *n_mtiles = ntiles;
+  if (touched_out) {
+    const int nz = __syncthreads_count(v > 0);
+    if (tid == 0) *touched_out = nz;
+  }
   // positions: pair i (row i / k) takes the next free slot of its expert's
   // segment; hist becomes the per-expert cursor
   hist[tid] = tid < E ? ex : 0;
@@ -234,26 +269,38 @@ hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st, bool* normed) {
   const float* lg = n_split > 1 ? (const float*)a.gemm_ws : a.logits;
   const int64_t zs = (int64_t)a.n_rows * a.E_pad;
   const dim3 gtk((a.n_rows + 3) / 4), btk(256);
-  if (a.E <= 128)
-    hipLaunchKernelGGL(moe_topk_kernel<2>, gtk, btk, 0, st, lg, a.E_pad, n_split, zs, a.n_rows, a.E, a.k,
-                       a.topk_id, a.topk_w);
-  else if (a.E <= 256)
-    hipLaunchKernelGGL(moe_topk_kernel<4>, gtk, btk, 0, st, lg, a.E_pad, n_split, zs, a.n_rows, a.E, a.k,
-                       a.topk_id, a.topk_w);
-  else
-    hipLaunchKernelGGL(moe_topk_kernel<kMoeMaxPerLane>, gtk, btk, 0, st, lg, a.E_pad, n_split, zs, a.n_rows,
-                       a.E, a.k, a.topk_id, a.topk_w);
+  const bool dbg = a.force_ids || a.own_ids_out || a.used_p_out;
+#define DARTS_TOPK(NPL)                                                                          \
+  if (dbg)                                                                                       \
+    hipLaunchKernelGGL((moe_topk_kernel<NPL, true>), gtk, btk, 0, st, lg, a.E_pad, n_split, zs,  \
+                       a.n_rows, a.E, a.k, a.topk_id, a.topk_w, a);                              \
+  else                                                                                           \
+    hipLaunchKernelGGL((moe_topk_kernel<NPL, false>), gtk, btk, 0, st, lg, a.E_pad, n_split, zs, \
+                       a.n_rows, a.E, a.k, a.topk_id, a.topk_w, a);
+  if (a.E <= 128) {
+    DARTS_TOPK(2)
+  } else if (a.E <= 256) {
+    DARTS_TOPK(4)
+  } else {
+    DARTS_TOPK(kMoeMaxPerLane)
+  }
+#undef DARTS_TOPK
   hipLaunchKernelGGL(moe_offsets_kernel, dim3(1), dim3(1024), 0, st, a.topk_id, a.n_rows * a.k, a.E, a.k,
-                     a.counts, a.offsets, a.cursors, a.mtiles, a.n_mtiles, a.pos_of, a.row_of);
+                     a.counts, a.offsets, a.cursors, a.mtiles, a.n_mtiles, a.pos_of, a.row_of,
+                     a.touched_out);
   const int Fe = a.Fe, d = a.d;
   // gate/up: N = 2*Fe, K = d (SwiGLU into h_perm), A rows gathered from xn;
   // down: N = d, K = Fe
+  if (a.ev_gu0 && (e = hipEventRecord(a.ev_gu0, st)) != hipSuccess) return e;
   e = launch_gemm_grouped(a.xn, d, a.w_gu, (int64_t)2 * Fe * d, d, a.h_perm, Fe, 2 * Fe, d,
                           EPI_SWIGLU, a.offsets, a.counts, a.mtiles, a.n_mtiles, a.row_of, st);
   if (e != hipSuccess) return e;
+  if (a.ev_gu1 && (e = hipEventRecord(a.ev_gu1, st)) != hipSuccess) return e;
+  if (a.ev_down0 && (e = hipEventRecord(a.ev_down0, st)) != hipSuccess) return e;
   e = launch_gemm_grouped(a.h_perm, Fe, a.w_down, (int64_t)d * Fe, Fe, a.y_perm, d, d, Fe, EPI_F32,
                           a.offsets, a.counts, a.mtiles, a.n_mtiles, nullptr, st);
   if (e != hipSuccess) return e;
+  if (a.ev_down1 && (e = hipEventRecord(a.ev_down1, st)) != hipSuccess) return e;
   const bool fuse = d <= 1024 * kCombVec;
   hipLaunchKernelGGL(moe_combine_kernel, dim3(a.n_rows), dim3(256), 0, st, a.y_perm, d, a.k,
                      a.pos_of, a.topk_w, a.x, a.eps, fuse ? a.xn : nullptr);

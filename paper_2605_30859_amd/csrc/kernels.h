@@ -190,6 +190,19 @@ struct MoeArgs {
   int32_t* mtiles;          // [n_rows*k / kGroupedTileRows + E] non-empty expert row tiles
   int32_t* n_mtiles;        // [1]
   bf16_t* h_perm; float* y_perm;                               // [n_rows*k][Fe | d]
+  // Verification of the routing (all NULL in normal use).  Row r has key
+  // route_key[r] (NULL: r); each pointer addresses this layer's k entries of
+  // key 0, keys dbg_stride elements apart.
+  const int32_t* route_key;
+  const int32_t* force_ids;  // k expert ids to combine instead of the router's own
+                             // choice (entry 0 < 0, or any id outside [0, E): own choice)
+  int32_t* own_ids_out;      // the router's own top-k ids, rank order
+  float* used_p_out;         // softmax probability of each combined expert
+  int64_t dbg_stride;
+  // Timing (NULL in normal use): events recorded around the grouped gate/up
+  // and down GEMMs, and the number of experts that received rows.
+  hipEvent_t ev_gu0, ev_gu1, ev_down0, ev_down1;
+  int32_t* touched_out;
 };
 // *normed: the combine also wrote xn = bf16(RMSNorm(x)) (d <= 4096)
 hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st, bool* normed);
