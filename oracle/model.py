@@ -53,21 +53,42 @@ def round_bf16(x32: np.ndarray) -> np.ndarray:
     return r.astype(np.uint32).view(np.float32)
 
 
-def init_tensor(seed, tensor_id, layer, n_out, n_in, fan_in, dtype, chunk=1 << 24):
-    """Generate one weight tensor [n_out, n_in] as float64 (values exact in the model dtype)."""
+def _weight_values(args):
+    """Elements [start, start + n) of one weight tensor, float32 (exact)."""
+    start, n, tensor_id, layer, seed, fan_in, dtype = args
     a = np.float32(math.sqrt(3.0 / fan_in))
+    w = philox_range(start, n, tensor_id, layer, TAG_WEIGHT, seed)
+    k = ((w >> np.uint32(8)) | np.uint32(1)).astype(np.float32)
+    v = (k * np.float32(2.0 ** -23) - np.float32(1.0)).astype(np.float32)
+    x = (v * a).astype(np.float32)
+    if dtype == "bf16":
+        x = round_bf16(x)
+    return x
+
+
+def init_tensor(seed, tensor_id, layer, n_out, n_in, fan_in, dtype, chunk=1 << 24, pool=None):
+    """Generate one weight tensor [n_out, n_in] as float64 (values exact in the model dtype).
+    ``pool``: an optional multiprocessing pool that generates the chunks in parallel
+    (the same elements; only the wall time changes)."""
     total = n_out * n_in
     out = np.empty(total, dtype=np.float64)
-    for s in range(0, total, chunk):
-        n = min(total, s + chunk) - s
-        w = philox_range(s, n, tensor_id, layer, TAG_WEIGHT, seed)
-        k = ((w >> np.uint32(8)) | np.uint32(1)).astype(np.float32)
-        v = (k * np.float32(2.0 ** -23) - np.float32(1.0)).astype(np.float32)
-        x = (v * a).astype(np.float32)
-        if dtype == "bf16":
-            x = round_bf16(x)
+    jobs = [(s, min(total, s + chunk) - s, tensor_id, layer, seed, fan_in, dtype)
+            for s in range(0, total, chunk)]
+    parts = pool.imap(_weight_values, jobs) if pool is not None else map(_weight_values, jobs)
+    for (s, n, *_), x in zip(jobs, parts):
         out[s:s + n] = x
     return out.reshape(n_out, n_in)
+
+
+def init_rows(seed, tensor_id, layer, rows, n_in, fan_in, dtype):
+    """Rows ``rows`` of the tensor init_tensor would generate, [len(rows), n_in]
+    float64 (element (r, i) is element r * n_in + i of the tensor); n_in % 4 == 0."""
+    assert n_in % 4 == 0
+    rows = np.asarray(rows, dtype=np.int64).reshape(-1)
+    out = np.empty((len(rows), n_in), dtype=np.float64)
+    for j, r in enumerate(rows):
+        out[j] = _weight_values((int(r) * n_in, n_in, tensor_id, layer, seed, fan_in, dtype))
+    return out
 
 
 @dataclass
@@ -85,26 +106,27 @@ class LayerW:
     edown: np.ndarray = None     # [E, d, Fe]
 
 
-def init_layer(cfg, layer):
+def init_layer(cfg, layer, pool=None):
     s, d, dt = cfg.weight_seed, cfg.d_model, cfg.dtype
     hq, hkv, hd = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    it = lambda *a: init_tensor(*a, pool=pool)
     lw = LayerW(
-        wq=init_tensor(s, T_WQ, layer, hq * hd, d, d, dt),
-        wk=init_tensor(s, T_WK, layer, hkv * hd, d, d, dt),
-        wv=init_tensor(s, T_WV, layer, hkv * hd, d, d, dt),
-        wo=init_tensor(s, T_WO, layer, d, hq * hd, hq * hd, dt),
+        wq=it(s, T_WQ, layer, hq * hd, d, d, dt),
+        wk=it(s, T_WK, layer, hkv * hd, d, d, dt),
+        wv=it(s, T_WV, layer, hkv * hd, d, d, dt),
+        wo=it(s, T_WO, layer, d, hq * hd, hq * hd, dt),
     )
     if cfg.n_experts:
         E, Fe = cfg.n_experts, cfg.expert_ffn
-        lw.router = init_tensor(s, T_ROUTER, layer, E, d, d, dt)
-        lw.egate = init_tensor(s, T_EGATE, layer, E * Fe, d, d, dt).reshape(E, Fe, d)
-        lw.eup = init_tensor(s, T_EUP, layer, E * Fe, d, d, dt).reshape(E, Fe, d)
-        lw.edown = init_tensor(s, T_EDOWN, layer, E * d, Fe, Fe, dt).reshape(E, d, Fe)
+        lw.router = it(s, T_ROUTER, layer, E, d, d, dt)
+        lw.egate = it(s, T_EGATE, layer, E * Fe, d, d, dt).reshape(E, Fe, d)
+        lw.eup = it(s, T_EUP, layer, E * Fe, d, d, dt).reshape(E, Fe, d)
+        lw.edown = it(s, T_EDOWN, layer, E * d, Fe, Fe, dt).reshape(E, d, Fe)
     else:
         F = cfg.ffn_dim
-        lw.wgate = init_tensor(s, T_WGATE, layer, F, d, d, dt)
-        lw.wup = init_tensor(s, T_WUP, layer, F, d, d, dt)
-        lw.wdown = init_tensor(s, T_WDOWN, layer, d, F, F, dt)
+        lw.wgate = it(s, T_WGATE, layer, F, d, d, dt)
+        lw.wup = it(s, T_WUP, layer, F, d, d, dt)
+        lw.wdown = it(s, T_WDOWN, layer, d, F, F, dt)
     return lw
 
 
@@ -176,6 +198,26 @@ def ffn(cfg, lw, h, margins=None):
             a = silu(lw.egate[e] @ h[r]) * (lw.eup[e] @ h[r])
             out[r] += w[r, j] * (lw.edown[e] @ a)
     return out
+
+
+def moe_ffn_by_expert(cfg, lw, h):
+    """The MoE FFN of ``ffn`` for many rows at once: routing as in moe_route,
+    y[r, j] = expert_{ids[r, j]}(h[r]) evaluated for all rows routed to an
+    expert together (one matrix product per expert), then
+    out[r] = sum_j w[r, j] y[r, j] in slot order j.
+    Returns (out, ids [n, k], p at ids [n, k] (softmax probabilities before
+    renormalisation), route_margin [n])."""
+    ids, w, p = moe_route(cfg, lw.router, h)
+    n, k = ids.shape
+    y = np.empty((n, k, h.shape[1]))
+    for e in np.unique(ids):
+        rr, jj = np.nonzero(ids == e)
+        a = silu(h[rr] @ lw.egate[e].T) * (h[rr] @ lw.eup[e].T)
+        y[rr, jj] = a @ lw.edown[e].T
+    out = np.zeros_like(h)
+    for j in range(k):
+        out += w[:, j:j + 1] * y[:, j]
+    return out, ids, np.take_along_axis(p, ids, axis=-1), route_margin(cfg, p)
 
 
 def attention(q, K, V, n_kv):

@@ -142,3 +142,12 @@ def synthetic_rewards(n, seed, p_correct=0.5):
     """Verifiable-reward stand-in: float32 {0, 1} per trajectory, Bernoulli(p_correct)."""
     rng = np.random.default_rng([seed, 7])
     return (rng.random(n) < p_correct).astype(np.float32)
+
+
+def teacher_forcing_tokens(model: ModelCfg, run: RunCfg, n_steps: int) -> np.ndarray:
+    """Token table [P*m, n_steps] (int32) for teacher-forced parity runs: row g
+    holds the tokens trajectory g takes at generated indices 0 .. n_steps-1,
+    uniform over [0, vocab-1) (the end-of-sequence id vocab-1 only comes from
+    the forced lengths).  Drawn independently of both sides' samplers."""
+    rng = np.random.default_rng([run.workload_seed, 5])
+    return rng.integers(0, model.vocab - 1, size=(run.n_prompts * run.m, n_steps)).astype(np.int32)
