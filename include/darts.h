@@ -411,6 +411,27 @@ int darts_attn_decode(const void* d_q, const void* d_k_pool, const void* d_v_poo
                       int32_t n_kv_heads, int32_t head_dim, int32_t max_ctx, int32_t dtype,
                       void* d_out, void* d_workspace, size_t workspace_bytes, void* stream);
 
+/* Allocation-free decode attention, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same computation, kernels and results as
+ * darts_attn_decode (bit for bit), with the workspace taken from an array of
+ * DARTS_ATTN_NOALLOC_SCRATCH_BYTES that the library's code object holds on
+ * each GPU for the life of the process.  The call allocates nothing, neither
+ * device nor host memory.  Arguments as for darts_attn_decode without the
+ * workspace.  Errors: DARTS_EINVAL as there, and also when
+ * darts_attn_workspace_bytes(n_rows, n_q_heads, n_kv_heads, head_dim,
+ * max_ctx) exceeds DARTS_ATTN_NOALLOC_SCRATCH_BYTES (nothing is launched);
+ * DARTS_EHIP if the array's device address cannot be looked up.  Every call
+ * on one GPU uses that GPU's one array: calls that overlap in time on the
+ * same GPU (other streams, other threads) race and must be serialised by
+ * the caller.                                                              */
+#define DARTS_ATTN_NOALLOC_SCRATCH_BYTES (64u << 20)
+int darts_attn_decode_noalloc(const void* d_q, const void* d_k_pool, const void* d_v_pool,
+                              int64_t n_pages, const int32_t* d_page_table, int32_t pt_stride,
+                              const int32_t* d_ctx_len, int32_t n_rows, int32_t n_q_heads,
+                              int32_t n_kv_heads, int32_t head_dim, int32_t max_ctx, int32_t dtype,
+                              void* d_out, void* stream);
+
 /* Bytes of workspace darts_attn_decode_shared needs for these sizes.       */
 size_t darts_attn_shared_workspace_bytes(int32_t n_rows, int32_t n_q_heads, int32_t n_kv_heads,
                                          int32_t head_dim, int32_t ctx_len, int32_t prefix_pages);

@@ -87,6 +87,8 @@ _SIGS = {
     "darts_attn_workspace_bytes": (C.c_size_t, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32]),
     "darts_attn_decode": (C.c_int, [_P, _P, _P, C.c_int64, _P, C.c_int32, _P, C.c_int32, C.c_int32,
                                     C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P, _P, C.c_size_t, _P]),
+    "darts_attn_decode_noalloc": (C.c_int, [_P, _P, _P, C.c_int64, _P, C.c_int32, _P, C.c_int32,
+                                            C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P, _P]),
     "darts_attn_shared_workspace_bytes": (C.c_size_t, [C.c_int32] * 6),
     "darts_attn_decode_shared": (C.c_int, [_P, _P, _P, C.c_int64, _P, C.c_int32, C.c_int32, _P,
                                            C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
@@ -174,6 +176,22 @@ def darts_attn_decode(q, k_pool, v_pool, n_pages, page_table, ctx_len, n_q_heads
         _ptr(q), _ptr(k_pool), _ptr(v_pool), n_pages, _ptr(page_table), page_table.shape[1],
         _ptr(ctx_len), n_rows, n_q_heads, n_kv_heads, head_dim, max_ctx, dtype, _ptr(out),
         _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+ATTN_NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def darts_attn_decode_noalloc(q, k_pool, v_pool, n_pages, page_table, ctx_len, n_q_heads, n_kv_heads,
+                              head_dim, max_ctx, dtype, out, stream=None, n_rows=None):
+    """darts_attn_decode with the library's own workspace array (no allocation)."""
+    if ctx_len is not None:
+        n_rows = ctx_len.numel()
+    elif n_rows is None:
+        raise ValueError("n_rows is required when ctx_len is None")
+    _check(load_library().darts_attn_decode_noalloc(
+        _ptr(q), _ptr(k_pool), _ptr(v_pool), n_pages, _ptr(page_table), page_table.shape[1],
+        _ptr(ctx_len), n_rows, n_q_heads, n_kv_heads, head_dim, max_ctx, dtype, _ptr(out),
+        _stream(stream)))
 
 
 def darts_attn_shared_workspace_bytes(n_rows, n_q_heads, n_kv_heads, head_dim, ctx_len, prefix_pages):

@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -1077,6 +1078,63 @@ int darts_attn_decode(const void* d_q, const void* d_k_pool, const void* d_v_poo
                                   head_dim, max_ctx,
                                   dtype == DARTS_BF16, d_out, d_workspace, workspace_bytes,
                                   (hipStream_t)stream);
+  return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
+}
+
+}  // extern "C"
+
+// Workspace of darts_attn_decode_noalloc: a fixed array in this library's code
+// object, one copy per GPU (the runtime places it when the code object is
+// loaded on that device).  Host code never uses the array's name as an
+// address: the device address is looked up once per device with
+// hipGetSymbolAddress and kept in g_scratch_ptr.  No call reads what an
+// earlier call left in it (the attention kernels write every workspace entry
+// they read within the same call), so nothing needs clearing between calls.
+static __device__ __align__(256) unsigned char scratch[DARTS_ATTN_NOALLOC_SCRATCH_BYTES];
+constexpr int kMaxScratchDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+static hipError_t scratch_on_current_device(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+extern "C" {
+
+int darts_attn_decode_noalloc(const void* d_q, const void* d_k_pool, const void* d_v_pool,
+                              int64_t n_pages, const int32_t* d_page_table, int32_t pt_stride,
+                              const int32_t* d_ctx_len, int32_t n_rows, int32_t n_q_heads,
+                              int32_t n_kv_heads, int32_t head_dim, int32_t max_ctx, int32_t dtype,
+                              void* d_out, void* stream) {
+  if (n_rows < 0 || n_q_heads < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads ||
+      n_q_heads / n_kv_heads > 16 || max_ctx < 1 || n_pages < 1)
+    return DARTS_EINVAL;
+  if (!(head_dim == 32 || head_dim == 64 || head_dim == 128)) return DARTS_EINVAL;
+  if (dtype != DARTS_F32 && dtype != DARTS_BF16) return DARTS_EINVAL;
+  if (pt_stride < (max_ctx + kPage - 1) / kPage) return DARTS_EINVAL;
+  if (n_rows == 0) return DARTS_OK;
+  if (!d_q || !d_k_pool || !d_v_pool || !d_page_table || !d_out) return DARTS_EINVAL;
+  if (attn_workspace_bytes(n_rows, n_q_heads, n_kv_heads, head_dim, max_ctx) >
+      (size_t)DARTS_ATTN_NOALLOC_SCRATCH_BYTES)
+    return DARTS_EINVAL;
+  void* ws = nullptr;
+  if (scratch_on_current_device(&ws) != hipSuccess) return DARTS_EHIP;
+  hipError_t e = launch_attention(d_q, d_k_pool, d_v_pool, n_pages, d_page_table, pt_stride, nullptr,
+                                  d_ctx_len, 0, d_ctx_len ? 0 : max_ctx, n_rows, n_q_heads, n_kv_heads,
+                                  head_dim, max_ctx, dtype == DARTS_BF16, d_out, ws,
+                                  (size_t)DARTS_ATTN_NOALLOC_SCRATCH_BYTES, (hipStream_t)stream);
   return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
 }
 
