@@ -38,15 +38,23 @@ def workload_desc(model, run):
             f"cap {run.cap}, forced lengths lognormal(median {run.len_median:g}, sigma {run.len_sigma:g}){tail}")
 
 
+SUBSET_PROMPTS, SUBSET_STEPS = 2, 64
+
+
 def cpu_baseline(model, run, budget_s=20.0):
-    """The oracle's decode step (float64 numpy forward + Gumbel-max sampler) on
-    one prompt group (m rows) at context prompt_len + 512, timed per layer and
-    for the fixed part (embedding, final norm, LM head, sampler), scaled to the
-    model's layer count.  Weights are constant-filled matrices of the real
-    shapes: dense float64 products cost the same for any values, and
-    generating the Philox weights would only add setup time."""
+    """The oracle on a bounded sample of the teacher-forced parity subset: two
+    prompts and their 2*m trajectories, the whole prompt prefill and the first
+    64 generated tokens of each (2*m*64 tokens), as oracle/forced.py computes
+    it layer by layer.  Timed: one decoder layer over all the subset's rows
+    (scaled by the layer count), the LM head on a sample of rows and the
+    Gumbel-max sampler on a sample of rows (scaled to all of them).  Weight
+    generation is setup, not timed; the weights are random matrices of the
+    real shapes (float64 products cost the same for any values; the router
+    is random so that tokens spread over the experts as they would)."""
     import numpy as np
+    from dataclasses import replace
     from oracle import model as OM
+    from oracle.forced import forced_forward
     from oracle.sampler import sample_row
     try:
         from threadpoolctl import threadpool_info
@@ -56,57 +64,83 @@ def cpu_baseline(model, run, budget_s=20.0):
     rng = np.random.default_rng(0)
     d, hq, hkv, hd, F, V = (model.d_model, model.n_q_heads, model.n_kv_heads, model.head_dim,
                             model.ffn_dim, model.vocab)
-
-    def layer():
-        r = lambda *s: np.full(s, 1.0 / s[-1])
-        lw = OM.LayerW(wq=r(hq * hd, d), wk=r(hkv * hd, d), wv=r(hkv * hd, d), wo=r(d, hq * hd))
-        if model.is_moe:
-            E, Fe = model.n_experts, model.expert_ffn
-            # distinct router rows, so routing picks top_k experts as it would
-            lw.router = rng.standard_normal((E, d)) / math.sqrt(d)
-            lw.egate, lw.eup, lw.edown = r(E, Fe, d), r(E, Fe, d), r(E, d, Fe)
-        else:
-            lw.wgate, lw.wup, lw.wdown = r(F, d), r(F, d), r(d, F)
-        return lw
-
-    B = run.m
-    ctx0 = run.prompt_len + 512
+    r = lambda *sh: np.full(sh, 1.0 / sh[-1])
+    lw = OM.LayerW(wq=r(hq * hd, d), wk=r(hkv * hd, d), wv=r(hkv * hd, d), wo=r(d, hq * hd))
+    if model.is_moe:
+        E, Fe = model.n_experts, model.expert_ffn
+        lw.router = rng.standard_normal((E, d)) / math.sqrt(d)
+        lw.egate, lw.eup, lw.edown = r(E, Fe, d), r(E, Fe, d), r(E, d, Fe)
+    else:
+        lw.wgate, lw.wup, lw.wdown = r(F, d), r(F, d), r(d, F)
+    Ps, m, S, Lp = SUBSET_PROMPTS, run.m, SUBSET_STEPS, run.prompt_len
+    T = Ps * m
+    prompts = rng.integers(0, V - 1, (Ps, Lp))
+    consumed = rng.integers(0, V - 1, (T, S - 1))
     emb = np.full((V, d), 0.5)
-    head = np.full((V, d), 1.0 / d)
-    l1, l2 = layer(), layer()
-    caches = [(rng.standard_normal((B, ctx0, hkv, hd)), rng.standard_normal((B, ctx0, hkv, hd)))
-              for _ in range(2)]
-    toks = rng.integers(0, V, B)
-    W1 = OM.Weights(embed=emb, layers=[l1], lm_head=head)
-    W2 = OM.Weights(embed=emb, layers=[l1, l2], lm_head=head)
-    t_one, t_two, t_samp = [], [], []
+    one = replace(model, n_layers=1)
     t_start = time.perf_counter()
-    reps = 0
-    while True:
+    t_layer = []
+    while not t_layer or (time.perf_counter() - t_start < 0.5 * budget_s and len(t_layer) < 3):
         t0 = time.perf_counter()
-        lg, _ = OM.decode_batch(model, W1, toks, caches[:1])
-        t1 = time.perf_counter()
-        OM.decode_batch(model, W2, toks, caches)
-        t2 = time.perf_counter()
-        for b in range(B):
-            sample_row(lg[b], 1.0, b, 0, 1)
-        t3 = time.perf_counter()
-        t_one.append(t1 - t0)
-        t_two.append(t2 - t1)
-        t_samp.append(t3 - t2)
-        reps += 1
-        if time.perf_counter() - t_start > budget_s or reps >= 20:
-            break
-    one, two, samp = (float(np.median(t_one)), float(np.median(t_two)), float(np.median(t_samp)))
-    per_layer = max(two - one, 1e-9)
-    fixed = max(one - per_layer, 0.0) + samp
-    step_s = fixed + model.n_layers * per_layer
-    return {"value": B / step_s, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": (f"oracle float64 decode step of one prompt group ({B} rows) at context {ctx0}: "
-                       f"1- and 2-layer forwards (per layer {per_layer:.3f} s, fixed part incl. "
-                       f"LM head and {B} Gumbel-max samples {fixed:.3f} s) scaled to "
-                       f"{model.n_layers} layers; {reps} repetitions, "
-                       f"{time.perf_counter() - t_start:.1f} s of CPU work")}
+        h_last, h_dec = forced_forward(one, prompts, np.repeat(np.arange(Ps), m), consumed, lambda l: lw,
+                                       lambda tk: emb[np.asarray(tk)])
+        t_layer.append(time.perf_counter() - t0)
+    n_head = min(T * S, 256)
+    head = np.full((V, d), 1.0 / d)
+    t0 = time.perf_counter()
+    lg = h_dec.reshape(-1, d)[:n_head] @ head.T
+    t_head = (time.perf_counter() - t0) * (T * S) / n_head
+    del head
+    n_samp = 0
+    t0 = time.perf_counter()
+    while n_samp < 4 or (n_samp < n_head and time.perf_counter() - t0 < 0.2 * budget_s):
+        sample_row(lg[n_samp], 1.0, n_samp, 0, 1)
+        n_samp += 1
+    t_samp = (time.perf_counter() - t0) * (T * S) / n_samp
+    layer = float(np.median(t_layer))
+    total = model.n_layers * layer + t_head + t_samp
+    return {"value": T * S / total, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": (f"oracle float64 teacher-forced subset ({Ps} prompts x {Lp} tokens prefilled, "
+                       f"{T} trajectories x {S} generated tokens = {T * S} tokens): one decoder layer over "
+                       f"all {Ps * Lp + T * (S - 1)} rows {layer:.2f} s (median of {len(t_layer)}) x "
+                       f"{model.n_layers} layers, LM head {t_head:.2f} s (timed on {n_head} rows), "
+                       f"sampler {t_samp:.2f} s (timed on {n_samp} rows); estimated subset time "
+                       f"{total:.1f} s from {time.perf_counter() - t_start:.1f} s of CPU work"),
+            "subset_tokens": T * S, "subset_s_estimated": total}
+
+
+def gpu_subset_rate(B, model, run, reps=2):
+    """The GPU on the same subset as cpu_baseline, as a separate small run: a
+    batch of the subset's two prompts (their trajectories' lengths capped at
+    64 generated tokens, so every one generates exactly 64), prefill plus
+    decode steps through the C ABI.  Best of ``reps`` timed runs after one
+    untimed run."""
+    import numpy as np
+    import torch
+    from dataclasses import replace
+    from workload import rollout_inputs
+    sub = replace(run, n_prompts=SUBSET_PROMPTS, cap=SUBSET_STEPS, kv_pool_gb=0.0)
+    prompts, _ = rollout_inputs(model, run)
+    pr = torch.from_numpy(np.ascontiguousarray(prompts[:SUBSET_PROMPTS].reshape(-1))).cuda()
+    fl = torch.full((SUBSET_PROMPTS * run.m,), SUBSET_STEPS + 1, dtype=torch.int32, device="cuda")
+    ro = B.Rollout(model, sub, flags=B.FLAG_NO_ABORT)
+    best, tokens = float("inf"), 0
+    for i in range(reps + 1):
+        ro.darts_reset()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ro.darts_prefill(pr, fl)
+        ro.darts_select_and_prune()
+        while ro.n_done < SUBSET_PROMPTS:
+            ro.darts_decode_step()
+            ro.darts_select_and_prune()
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        tokens = ro.stats()["tokens_decoded"]
+        if i > 0:
+            best = min(best, dt)
+    ro.close()
+    return {"value": tokens / best, "unit": "tokens/s", "tokens": int(tokens), "seconds": best}
 
 
 def rollout_bound(model, run, rows, hbm_gbs, mfma_tflops):
@@ -253,6 +287,20 @@ def kernel_sweep(B, steps, warmup):
     comp = torch.empty(len(ln) // m, dtype=torch.uint8, device="cuda")
     us = timed(lambda: B.darts_select_groups(std, lnd, mld, m, k, 1, 2 * k, 1, kept, comp), n)
     out["selection"] = {"trajectories": len(ln), "groups": len(ln) // m, "us": us}
+    # with page reclaim of the completed groups: the final step, every group
+    # completes and frees all of its members' pages
+    from workload.gen import sweep_selection_pages
+    off, pages = sweep_selection_pages(ln)
+    off_d, pages_d = torch.from_numpy(off).cuda(), torch.from_numpy(pages).cuda()
+    free = torch.empty_like(pages_d)
+    nfree = torch.zeros(1, dtype=torch.int32, device="cuda")
+    work = torch.empty(len(ln) // m + 1, dtype=torch.int32, device="cuda")
+    us = timed(lambda: B.darts_select_groups(std, lnd, mld, m, k, 1, 2 * k, 1, kept, comp, off_d, pages_d,
+                                             free, nfree, work), n)
+    torch.cuda.synchronize()
+    out["selection_reclaim"] = {"trajectories": len(ln), "page_ids": len(pages),
+                                "reclaimed": int(nfree.item()), "us": us,
+                                "page_id_GBs": 2 * 4 * len(pages) / (us * 1e-6) / 1e9}
     return out
 
 
@@ -708,6 +756,12 @@ def main():
     if not args.no_cpu_baseline:
         try:
             out["cpu_baseline"] = cpu_baseline(model, run)
+            try:
+                gs = gpu_subset_rate(B, model, run)
+                out["cpu_baseline"]["gpu_same_subset"] = gs
+                out["cpu_baseline"]["gpu_over_oracle"] = gs["value"] / out["cpu_baseline"]["value"]
+            except Exception as e:
+                out["cpu_baseline"]["gpu_same_subset"] = {"error": repr(e)}
         except Exception as e:  # the baseline is context, never the product path
             out["cpu_baseline"] = {"error": repr(e)}
     out["wall_s"] = time.perf_counter() - T_PROCESS

@@ -112,6 +112,13 @@ typedef struct {
   uint32_t flags;        /* DARTS_FLAG_* */
   uint64_t page_perm_seed; /* used with DARTS_FLAG_PERMUTE_PAGES */
   void* stream;          /* hipStream_t */
+  int32_t traj_base;     /* global id of this batch's trajectory 0, >= 0: the sampler's
+                            counters use traj_base + g.  A data-parallel rank that runs
+                            prompts [a, b) of a batch sets a*m, so its trajectories draw
+                            the random numbers they would draw in a one-GPU run of the
+                            whole batch (Sec. 4.2.1: the batch's cost is the maximum
+                            over the data-parallel groups).  Every id the library reports
+                            stays local (0 .. n_prompts*m-1). */
 } darts_run_cfg;
 
 /* Per-step outputs, one row per trajectory decoded in the step (live-list
@@ -469,17 +476,31 @@ int darts_sample(const void* d_logits, int32_t n_rows, int32_t vocab, int32_t dt
                  const int32_t* d_force, int32_t* d_token, float* d_logprob, float* d_entropy,
                  void* stream);
 
-/* Stateless selection over groups of m consecutive trajectories (Alg. 2).
+/* Stateless selection over groups of m consecutive trajectories (Alg. 2),
+ * with the page reclaim of the aborted and finished candidates (Alg. 2's
+ * abort; Sec. 4.3.1, proactive early stopping frees the pruned candidates).
  *   d_status   [n_traj] uint8 in/out: 0 live, 1 eos, 2 truncated, 3 aborted
- *              (aborted is written for pruned live members)
+ *              (aborted is written for pruned live members: the abort mask)
  *   d_len      [n_traj] int32 generated lengths (< 2^20)
  *   d_mean_lp  [n_traj] float32 mean log-probs (tie-break only)
  *   d_kept     [n_groups * k] int32 out (rows of incomplete groups untouched)
  *   d_complete [n_groups] uint8 out: 1 if the group completed now
- *   m_up: shortest-only when m >= m_up; early_stop: 0 or 1.                 */
+ *   m_up: shortest-only when m >= m_up; early_stop: 0 or 1.
+ * Page reclaim (d_page_off NULL: none, and the next four pointers are
+ * ignored): trajectory g owns the KV page ids d_pages[d_page_off[g] ..
+ * d_page_off[g+1]) (d_page_off: [n_traj + 1] int32, non-decreasing, from 0).
+ * Every group that completes in this call frees the pages of all its
+ * members, which are all done once it completes: they are written to
+ * d_free_out (capacity d_page_off[n_traj] ids) in group order, member order
+ * and list order, and their number to the device int32 *d_n_free.  d_work:
+ * n_traj / m + 1 int32 of scratch.  The call keeps no state: a caller passes
+ * each group's pages until the call that completes the group, then drops
+ * them (or gives that group an empty list).                                */
 int darts_select_groups(uint8_t* d_status, const int32_t* d_len, const float* d_mean_lp,
                         int32_t n_traj, int32_t m, int32_t k, int32_t L, int32_t m_up,
-                        int32_t early_stop, int32_t* d_kept, uint8_t* d_complete, void* stream);
+                        int32_t early_stop, int32_t* d_kept, uint8_t* d_complete,
+                        const int32_t* d_page_off, const int32_t* d_pages, int32_t* d_free_out,
+                        int32_t* d_n_free, int32_t* d_work, void* stream);
 
 /* Group-normalised advantages of the kept training groups (Sec. 3.1, Eq. 2):
  * for group i with kept ids d_kept[i*k + j] (as written by

@@ -85,3 +85,16 @@ def group_decision(members, k, L, m_up, early_stop=True):
     if live:
         return False, [], []
     return True, select_dual(done, k, L), []
+
+
+def reclaimed_pages(page_lists, completed, m):
+    """KV page ids a selection frees: for every group that completed (ascending
+    group index), the page lists of its members j = 0 .. m-1 in member order
+    (at completion every member is done: finished, or aborted by the early
+    stop, and all their pages return to the pool; Alg. 2's abort, Sec. 4.3.1).
+    page_lists[g]: the pages trajectory g = i*m + j holds."""
+    out = []
+    for i in sorted(completed):
+        for j in range(m):
+            out.extend(int(p) for p in page_lists[i * m + j])
+    return out

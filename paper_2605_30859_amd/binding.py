@@ -35,7 +35,7 @@ class RunCfg(C.Structure):
                 ("L", C.c_int32), ("m_up", C.c_int32), ("page_size", C.c_int32),
                 ("kv_pool_bytes", C.c_uint64), ("sample_seed", C.c_uint64),
                 ("temperature", C.c_float), ("flags", C.c_uint32),
-                ("page_perm_seed", C.c_uint64), ("stream", C.c_void_p)]
+                ("page_perm_seed", C.c_uint64), ("stream", C.c_void_p), ("traj_base", C.c_int32)]
 
 
 class StepOut(C.Structure):
@@ -103,7 +103,7 @@ _SIGS = {
     "darts_gemm": (C.c_int, [_P, _P, _P, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                              _P, C.c_size_t, _P]),
     "darts_select_groups": (C.c_int, [_P, _P, _P, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
-                                      C.c_int32, C.c_int32, _P, _P, _P]),
+                                      C.c_int32, C.c_int32, _P, _P, _P, _P, _P, _P, _P, _P]),
 }
 
 _lib = None
@@ -219,10 +219,13 @@ def darts_sample(logits, dtype, seed, traj, step, temperature, force, token, log
 
 
 def darts_select_groups(status, length, mean_lp, m, k, L, m_up, early_stop, kept, complete,
-                        stream=None):
+                        page_off=None, pages=None, free_out=None, n_free=None, work=None, stream=None):
+    """Stateless Alg. 2 over groups of m; with page lists (CSR page_off / pages)
+    the completed groups' pages go to free_out and their count to n_free."""
     _check(load_library().darts_select_groups(_ptr(status), _ptr(length), _ptr(mean_lp),
-                                              status.numel(), m, k, L, m_up, int(early_stop),
-                                              _ptr(kept), _ptr(complete), _stream(stream)))
+                                              status.numel(), m, k, L, m_up, early_stop, _ptr(kept),
+                                              _ptr(complete), _ptr(page_off), _ptr(pages), _ptr(free_out),
+                                              _ptr(n_free), _ptr(work), _stream(stream)))
 
 
 def darts_group_advantages(kept, reward, adv, eps=1e-6, stream=None):
@@ -335,10 +338,10 @@ def model_cfg_struct(model):
                     DARTS_BF16 if model.dtype == "bf16" else DARTS_F32, model.weight_seed)
 
 
-def run_cfg_struct(run, stream, flags=0, page_perm_seed=0, kv_pool_bytes=None):
+def run_cfg_struct(run, stream, flags=0, page_perm_seed=0, kv_pool_bytes=None, traj_base=0):
     pool = int(run.kv_pool_gb * (1 << 30)) if kv_pool_bytes is None else int(kv_pool_bytes)
     return RunCfg(run.n_prompts, run.prompt_len, run.cap, run.L, run.m_up or 0, 16, pool,
-                  run.sample_seed, run.temperature, flags, page_perm_seed, stream)
+                  run.sample_seed, run.temperature, flags, page_perm_seed, stream, traj_base)
 
 
 class Rollout:
@@ -346,7 +349,7 @@ class Rollout:
     darts_decode_step / darts_select_and_prune).  Output buffers are torch
     tensors on the current device; PyTorch only allocates them."""
 
-    def __init__(self, model, run, flags=0, page_perm_seed=0, kv_pool_bytes=None, stream=None):
+    def __init__(self, model, run, flags=0, page_perm_seed=0, kv_pool_bytes=None, stream=None, traj_base=0):
         import torch
         self.torch = torch
         self.lib = load_library()
@@ -355,7 +358,7 @@ class Rollout:
         self.n_traj = run.n_prompts * run.m
         self.stream = stream or torch.cuda.current_stream()
         self._mc = model_cfg_struct(model)
-        self._rc = run_cfg_struct(run, self.stream.cuda_stream, flags, page_perm_seed, kv_pool_bytes)
+        self._rc = run_cfg_struct(run, self.stream.cuda_stream, flags, page_perm_seed, kv_pool_bytes, traj_base)
         ctx = C.c_void_p()
         _check(self.lib.darts_init(C.byref(self._mc), run.m, run.k, C.byref(self._rc), C.byref(ctx)))
         self.ctx = ctx

@@ -349,6 +349,8 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
   if (rc.page_size != 16 || rc.prompt_len < 16 || rc.prompt_len % 16 != 0) return DARTS_EINVAL;
   if (rc.n_prompts < 1 || rc.cap < 1 || rc.cap >= (1 << 20) || !(rc.temperature > 0.f))
     return DARTS_EINVAL;
+  if (rc.traj_base < 0 || (int64_t)rc.traj_base + (int64_t)rc.n_prompts * m > ((int64_t)1 << 31))
+    return DARTS_EINVAL;
   if (mc.n_layers < 1 || mc.d_model < 1 || mc.n_q_heads < 1 || mc.n_kv_heads < 1 ||
       mc.n_q_heads % mc.n_kv_heads != 0 || mc.n_q_heads / mc.n_kv_heads > 16)
     return DARTS_EINVAL;
@@ -780,7 +782,7 @@ int darts_prefill(darts_ctx* c, const int32_t* d_prompts, const int32_t* d_force
                         EPI_F32, c->gemm_ws, c->gemm_ws_bytes, c->st));
   SampleArgs a{};
   a.logits = c->logits; a.n_rows = c->n_start; a.vocab = c->V; a.bf16 = false;
-  a.seed = c->rc.sample_seed; a.temperature = c->rc.temperature;
+  a.seed = c->rc.sample_seed; a.temperature = c->rc.temperature; a.traj_base = c->rc.traj_base;
   a.row_logit = nullptr; a.logit_div = c->m;
   a.traj = c->live[c->cur]; a.step = nullptr; a.force = d_force_tokens;
   a.token_out = out->token; a.sampled_out = out->sampled; a.logprob_out = out->logprob;
@@ -832,7 +834,7 @@ int darts_decode_step(darts_ctx* c, const int32_t* d_force_tokens, darts_step_ou
   HIPCHK(c, gemm_t(c, G_LM, c->xn, c->d, c->lm_head, c->d, c->logits, c->V, n, c->V, c->d, EPI_F32));
   SampleArgs a{};
   a.logits = c->logits; a.n_rows = n; a.vocab = c->V; a.bf16 = false;
-  a.seed = c->rc.sample_seed; a.temperature = c->rc.temperature;
+  a.seed = c->rc.sample_seed; a.temperature = c->rc.temperature; a.traj_base = c->rc.traj_base;
   a.row_logit = nullptr; a.logit_div = 0;
   a.traj = live; a.step = nullptr; a.force = d_force_tokens;
   a.token_out = out->token; a.sampled_out = out->sampled; a.logprob_out = out->logprob;
@@ -1231,15 +1233,20 @@ int darts_group_advantages(const int32_t* d_kept, int32_t n_groups, int32_t k, c
 
 int darts_select_groups(uint8_t* d_status, const int32_t* d_len, const float* d_mean_lp,
                         int32_t n_traj, int32_t m, int32_t k, int32_t L, int32_t m_up,
-                        int32_t early_stop, int32_t* d_kept, uint8_t* d_complete, void* stream) {
+                        int32_t early_stop, int32_t* d_kept, uint8_t* d_complete,
+                        const int32_t* d_page_off, const int32_t* d_pages, int32_t* d_free_out,
+                        int32_t* d_n_free, int32_t* d_work, void* stream) {
   if (m < 1 || m > 64 || k < 1 || k > m || n_traj < 0 || n_traj % m) return DARTS_EINVAL;
   if (m < m_up && (L < 1 || L >= k)) return DARTS_EINVAL;
   if (n_traj == 0) return DARTS_OK;
   if (!d_status || !d_len || !d_mean_lp || !d_kept || !d_complete) return DARTS_EINVAL;
+  if (d_page_off && (!d_pages || !d_free_out || !d_n_free || !d_work)) return DARTS_EINVAL;
   GroupArgs a{};
   a.status = d_status; a.len = d_len; a.mean_lp = d_mean_lp; a.n_groups = n_traj / m;
   a.m = m; a.k = k; a.L = L; a.m_up = m_up; a.early_stop = early_stop ? 1 : 0;
   a.kept = d_kept; a.complete = d_complete;
+  a.page_off = d_page_off; a.pages = d_pages; a.free_out = d_free_out; a.n_free = d_n_free;
+  a.work = d_work;
   hipError_t e = launch_select(a, (hipStream_t)stream);
   return e == hipSuccess ? DARTS_OK : DARTS_EHIP;
 }

@@ -164,6 +164,7 @@ __global__ void __launch_bounds__(256) sample_kernel(SampleArgs a) {
   const int tid = threadIdx.x;
   const RowCtx c = row_ctx<BF16, STATEFUL>(a, r);
   const int g = c.g, step = c.step;
+  const uint32_t gc = (uint32_t)g + (uint32_t)a.traj_base;   // the counter's (global) trajectory id
   const void* row = c.row;
   const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
   const bool tscale = a.temperature != 1.0f;
@@ -180,7 +181,7 @@ __global__ void __launch_bounds__(256) sample_kernel(SampleArgs a) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) z[e] = __fdiv_rn(z[e], a.temperature);
     }
-    const Philox4 p = philox4x32_10((uint32_t)j, (uint32_t)g, (uint32_t)step, kTagSample, k0, k1);
+    const Philox4 p = philox4x32_10((uint32_t)j, gc, (uint32_t)step, kTagSample, k0, k1);
     float lm = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
     if (lm > st.m) {
       if (st.s > 0.f) {   // rescale the running sums to the new maximum
@@ -211,14 +212,14 @@ __global__ void __launch_bounds__(256) sample_kernel(SampleArgs a) {
       2.0f * (kGumbelFastBound + 2.384185791015625e-07f * fmaxf(fabsf(b1), fabsf(b2)));   // 2^-22 |s|
   if (b1 - b2 > margin) {
     const int j = i1 >> 2, e = i1 & 3;
-    const Philox4 p = philox4x32_10((uint32_t)j, (uint32_t)g, (uint32_t)step, kTagSample, k0, k1);
+    const Philox4 p = philox4x32_10((uint32_t)j, gc, (uint32_t)step, kTagSample, k0, k1);
     best.v = logit_at<BF16>(row, i1, tscale, a.temperature) + gumbel_of(open_unit(p.x[e]));
     best.i = i1;
   } else {
     for (int j = jb + tid; j < je; j += 256) {
       float z[4];
       load4<BF16>(row, j, z);
-      const Philox4 p = philox4x32_10((uint32_t)j, (uint32_t)g, (uint32_t)step, kTagSample, k0, k1);
+      const Philox4 p = philox4x32_10((uint32_t)j, gc, (uint32_t)step, kTagSample, k0, k1);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const float zz = tscale ? __fdiv_rn(z[e], a.temperature) : z[e];

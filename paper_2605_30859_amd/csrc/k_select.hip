@@ -106,11 +106,68 @@ __global__ void select_groups_kernel(uint8_t* status, const int32_t* len, const 
   if (lane == 0) complete[grp] = c ? 1 : 0;
 }
 
+// Page reclaim after a stateless selection, step 1 (single block): each
+// group's freed count (all its members' pages if it completed, else 0), their
+// exclusive scan into work[0 .. n_groups) and the total into work[n_groups]
+// and *n_free.
+__global__ void __launch_bounds__(1024) reclaim_scan_kernel(const uint8_t* __restrict__ complete,
+                                                            const int32_t* __restrict__ page_off,
+                                                            int n_groups, int m,
+                                                            int32_t* __restrict__ work,
+                                                            int32_t* __restrict__ n_free) {
+  __shared__ int32_t sums[1024];
+  __shared__ int32_t running;
+  const int tid = threadIdx.x;
+  if (tid == 0) running = 0;
+  __syncthreads();
+  for (int base = 0; base < n_groups; base += 1024) {
+    const int grp = base + tid;
+    const int c = (grp < n_groups && complete[grp])
+                      ? page_off[(int64_t)(grp + 1) * m] - page_off[(int64_t)grp * m] : 0;
+    sums[tid] = c;
+    __syncthreads();
+    for (int o = 1; o < 1024; o <<= 1) {     // inclusive Hillis-Steele scan
+      const int v = tid >= o ? sums[tid - o] : 0;
+      __syncthreads();
+      sums[tid] += v;
+      __syncthreads();
+    }
+    if (grp < n_groups) work[grp] = running + sums[tid] - c;
+    __syncthreads();
+    if (tid == 1023) running += sums[1023];
+    __syncthreads();
+  }
+  if (tid == 0) {
+    work[n_groups] = running;
+    *n_free = running;
+  }
+}
+
+// Step 2: one block per group copies a completed group's page ids (its
+// members' lists are contiguous in the page array) to its slot of free_out.
+__global__ void __launch_bounds__(256) reclaim_copy_kernel(const uint8_t* __restrict__ complete,
+                                                           const int32_t* __restrict__ page_off,
+                                                           const int32_t* __restrict__ pages, int m,
+                                                           const int32_t* __restrict__ work,
+                                                           int32_t* __restrict__ free_out) {
+  const int grp = blockIdx.x;
+  if (!complete[grp]) return;
+  const int64_t b = page_off[(int64_t)grp * m], e = page_off[(int64_t)(grp + 1) * m];
+  int32_t* dst = free_out + work[grp] - b;
+  for (int64_t i = b + threadIdx.x; i < e; i += 256) dst[i] = pages[i];
+}
+
 hipError_t launch_select(const GroupArgs& a, hipStream_t st) {
   if (a.n_groups <= 0) return hipSuccess;
   hipLaunchKernelGGL(select_groups_kernel, dim3((a.n_groups + 3) / 4), dim3(256), 0, st, a.status,
                      a.len, a.mean_lp, a.n_groups, a.m, a.k, a.L, a.m_up, a.early_stop, a.kept,
                      a.complete);
+  if (a.page_off) {
+    hipLaunchKernelGGL(reclaim_scan_kernel, dim3(1), dim3(1024), 0, st, a.complete, a.page_off, a.n_groups,
+                       a.m, a.work, a.n_free);
+    hipLaunchKernelGGL(reclaim_copy_kernel, dim3(a.n_groups), dim3(256), 0, st, a.complete, a.page_off,
+                       a.pages, a.m, a.work, a.free_out);
+  }
   return hipGetLastError();
 }
 

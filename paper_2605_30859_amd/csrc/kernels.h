@@ -105,7 +105,8 @@ struct SampleArgs {
   const void* logits; int n_rows; int vocab; bool bf16; uint64_t seed; float temperature;
   const int32_t* row_logit;   // row r reads logits row row_logit[r], else traj[r] / logit_div, else r
   int logit_div;
-  const int32_t* traj;        // [n_rows] trajectory id (counter word 1)
+  const int32_t* traj;        // [n_rows] trajectory id (counter word 1 is traj + traj_base)
+  int traj_base;
   const int32_t* step;        // NULL: use per-trajectory gen count (stateful)
   const int32_t* force;       // NULL or indexed by row (stateless) / by traj (stateful)
   int32_t* token_out; int32_t* sampled_out; float* logprob_out; float* entropy_out;
@@ -138,6 +139,11 @@ struct GroupArgs {
   uint8_t* status; const int32_t* len; const float* sum_lp; const float* mean_lp;
   int n_groups; int m; int k; int L; int m_up; int early_stop; int step;
   int32_t* kept; uint8_t* complete;
+  // page reclaim (page_off NULL: none): trajectory g owns pages[page_off[g] ..
+  // page_off[g+1]); the pages of every member of each group that completes
+  // are written to free_out in group, member and list order, their number to
+  // *n_free; work holds n_groups + 1 ints of scratch (per-group offsets)
+  const int32_t* page_off; const int32_t* pages; int32_t* free_out; int32_t* n_free; int32_t* work;
 };
 hipError_t launch_select(const GroupArgs& a, hipStream_t st);
 struct PruneArgs {

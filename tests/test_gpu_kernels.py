@@ -12,10 +12,11 @@ torch = pytest.importorskip("torch")
 
 from oracle.fp32math import gumbel_f32
 from oracle.sampler import sample_row
-from oracle.selection import group_decision, LIVE, EOS, TRUNC, ABORTED
+from oracle.selection import group_decision, reclaimed_pages, LIVE, EOS, TRUNC, ABORTED
 from oracle import sweep as OS
 from workload import sweep_attention_inputs, sweep_sampler_logits, sweep_selection_inputs
-from workload.gen import sweep_page_table, shared_prefix_page_table, f32_from_bf16_bits
+from workload.gen import (sweep_page_table, shared_prefix_page_table, f32_from_bf16_bits,
+                          sweep_selection_pages)
 from workload.configs import SWEEP
 
 pytestmark = pytest.mark.gpu
@@ -430,7 +431,9 @@ def _oracle_select(status, length, mlp, m, k, L, m_up, early_stop):
 @pytest.mark.parametrize("mode", ["short_final", "short_mid", "dual_final", "dual_mid", "no_abort_mid"])
 def test_selection_sweep(mode):
     """65536 trajectories in groups of m=16, k=8 (L=1), lengths lognormal,
-    mean log-probs on a 2^-10 grid (exact ties): kept sets bit-exact."""
+    mean log-probs on a 2^-10 grid (exact ties): kept sets and statuses
+    bit-exact, and the page ids the completed groups free (ceil(len/16) per
+    trajectory from a shuffled pool) bit-exact in order and count."""
     B = _b()
     say(f"selection sweep {mode}")
     raw, mlp = sweep_selection_inputs()
@@ -456,7 +459,14 @@ def test_selection_sweep(mode):
     mlp_d = torch.from_numpy(mlp).to(DEV)
     kept_d = torch.full((n // m, k), -1, dtype=torch.int32, device=DEV)
     comp_d = torch.zeros(n // m, dtype=torch.uint8, device=DEV)
-    B.darts_select_groups(st_d, len_d, mlp_d, m, k, L, m_up, early, kept_d, comp_d)
+    # page lists: ceil(len / 16) ids per trajectory (its length at this step)
+    off, pages = sweep_selection_pages(cur_len)
+    off_d, pages_d = torch.from_numpy(off).to(DEV), torch.from_numpy(pages).to(DEV)
+    free_d = torch.full((len(pages),), -1, dtype=torch.int32, device=DEV)
+    nfree_d = torch.full((1,), -1, dtype=torch.int32, device=DEV)
+    work_d = torch.empty(n // m + 1, dtype=torch.int32, device=DEV)
+    B.darts_select_groups(st_d, len_d, mlp_d, m, k, L, m_up, early, kept_d, comp_d, off_d, pages_d,
+                          free_d, nfree_d, work_d)
     torch.cuda.synchronize()
     kept, comp, st = kept_d.cpu().numpy(), comp_d.cpu().numpy(), st_d.cpu().numpy()
     assert np.array_equal(st, st_ref)
@@ -467,6 +477,13 @@ def test_selection_sweep(mode):
         else:
             assert comp[grp] == 0 and (kept[grp] == -1).all()
     assert len(kept_ref) > 0
+    # reclaimed pages: bit-exact list and count (the oracle's group / member / list order)
+    lists = [pages[off[g]:off[g + 1]] for g in range(n)]
+    want = np.array(reclaimed_pages(lists, set(kept_ref), m), dtype=np.int32)
+    nf = int(nfree_d.item())
+    free = free_d.cpu().numpy()
+    say(f"selection sweep {mode}: {len(kept_ref)} groups complete, {nf} of {len(pages)} page ids reclaimed")
+    assert nf == len(want) and np.array_equal(free[:nf], want) and (free[nf:] == -1).all()
 
 
 def test_stream_read_reads_every_word():

@@ -23,7 +23,7 @@ def test_zero_size_calls_are_noops(lib):
                                         B.DARTS_BF16, N, N, 0, N) == OK
     assert lib.darts_sample(N, 0, 151936, B.DARTS_BF16, 1, N, N, 1.0, N, N, N, N, N) == OK
     assert lib.darts_gemm(N, N, N, 0, 4096, 4096, B.DARTS_BF16, 0, N, 0, N) == OK
-    assert lib.darts_select_groups(N, N, N, 0, 16, 8, 1, 16, 1, N, N, N) == OK
+    assert lib.darts_select_groups(N, N, N, 0, 16, 8, 1, 16, 1, N, N, N, N, N, N, N, N) == OK
     assert lib.darts_group_advantages(N, 0, 8, N, 0, C.c_float(1e-6), N, N) == OK
     assert lib.darts_stream_read(N, 0, N, N) == OK
     assert lib.darts_debug_gumbel(N, N, 0, N) == OK
@@ -49,10 +49,14 @@ def test_bad_scalars_are_rejected(lib):
     assert lib.darts_gemm(N, N, N, 0, 48, 64, B.DARTS_F32, 3, N, 0, N) == EINVAL
     assert lib.darts_gemm(N, N, N, 1, 4096, 4096, bf, 0, N, 0, N) == EINVAL
     # selection: k > m, m > 64, trajectories not whole groups, dual-end with L >= k
-    assert lib.darts_select_groups(N, N, N, 0, 8, 9, 1, 16, 1, N, N, N) == EINVAL
-    assert lib.darts_select_groups(N, N, N, 0, 65, 8, 1, 16, 1, N, N, N) == EINVAL
-    assert lib.darts_select_groups(N, N, N, 17, 16, 8, 1, 16, 1, N, N, N) == EINVAL
-    assert lib.darts_select_groups(N, N, N, 0, 12, 8, 8, 16, 1, N, N, N) == EINVAL
+    assert lib.darts_select_groups(N, N, N, 0, 8, 9, 1, 16, 1, N, N, N, N, N, N, N, N) == EINVAL
+    assert lib.darts_select_groups(N, N, N, 0, 65, 8, 1, 16, 1, N, N, N, N, N, N, N, N) == EINVAL
+    assert lib.darts_select_groups(N, N, N, 17, 16, 8, 1, 16, 1, N, N, N, N, N, N, N, N) == EINVAL
+    assert lib.darts_select_groups(N, N, N, 0, 12, 8, 8, 16, 1, N, N, N, N, N, N, N, N) == EINVAL
+    # selection with page reclaim: page lists without the output, count or scratch buffers
+    D = C.c_void_p(256)          # never dereferenced: the call fails its argument check first
+    assert lib.darts_select_groups(D, D, D, 16, 16, 8, 1, 16, 1, D, D, D, D, N, D, D, N) == EINVAL
+    assert lib.darts_select_groups(D, D, D, 16, 16, 8, 1, 16, 1, D, D, D, D, D, D, N, N) == EINVAL
     # streaming read: not whole 16-byte words
     assert lib.darts_stream_read(N, 24, N, N) == EINVAL
 

@@ -171,3 +171,22 @@ def test_group_decision_waits_when_not_enough_valid():
     assert c and kept == [0, 1] and ab == [2]
     # dual mode waits for every member
     assert group_decision(mem, 2, 1, 5)[0] is False
+
+
+def test_reclaimed_pages_hand_example_and_conservation():
+    from oracle.selection import reclaimed_pages
+    # 3 groups of m = 2; groups 0 and 2 complete
+    lists = [[5, 6], [], [1], [2], [9, 7, 8], [3]]
+    assert reclaimed_pages(lists, {2, 0}, 2) == [5, 6, 9, 7, 8, 3]
+    assert reclaimed_pages(lists, set(), 2) == []
+    import numpy as np
+    rng = np.random.default_rng(1)
+    m, n_groups = 4, 50
+    sizes = rng.integers(0, 6, n_groups * m)
+    perm = rng.permutation(int(sizes.sum()))
+    off = np.concatenate([[0], np.cumsum(sizes)])
+    lists = [list(perm[off[g]:off[g + 1]]) for g in range(n_groups * m)]
+    done = set(int(i) for i in rng.choice(n_groups, 20, replace=False))
+    got = reclaimed_pages(lists, done, m)
+    want = sorted(p for i in done for j in range(m) for p in lists[i * m + j])
+    assert sorted(got) == want and len(set(got)) == len(got)

@@ -151,3 +151,15 @@ def teacher_forcing_tokens(model: ModelCfg, run: RunCfg, n_steps: int) -> np.nda
     the forced lengths).  Drawn independently of both sides' samplers."""
     rng = np.random.default_rng([run.workload_seed, 5])
     return rng.integers(0, model.vocab - 1, size=(run.n_prompts * run.m, n_steps)).astype(np.int32)
+
+
+def sweep_selection_pages(length, page=16, seed=None):
+    """KV page lists of the selection sweep's trajectories, CSR: trajectory g
+    holds ceil(length[g] / page) ids, pages[off[g] : off[g+1]], drawn from a
+    shuffled pool.  Returns (off [n+1] int32, pages [total] int32)."""
+    s = SWEEP
+    seed = s["seed"] if seed is None else seed
+    rng = np.random.default_rng([seed, 3])
+    npg = (np.asarray(length, dtype=np.int64) + page - 1) // page
+    off = np.concatenate([[0], np.cumsum(npg)]).astype(np.int32)
+    return off, rng.permutation(int(npg.sum())).astype(np.int32)
