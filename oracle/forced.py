@@ -71,14 +71,17 @@ def forced_forward(cfg, prompts, traj_prompt, consumed, get_layer, embed_rows, r
     def attend(q, K, V, mask):
         """q [n, hq, hd], K/V [c, hkv, hd], mask [n, c] -> [n, hq, hd]."""
         out = np.empty_like(q)
+        # per-head operands as contiguous arrays, so the products go to BLAS
+        Kt = [np.ascontiguousarray(K[:, j, :].T) for j in range(hkv)]
+        Vh = [np.ascontiguousarray(V[:, j, :]) for j in range(hkv)]
         for h in range(hq):
             kh = (h * hkv) // hq
-            s = (q[:, h, :] @ K[:, kh, :].T) * scale
+            s = (np.ascontiguousarray(q[:, h, :]) @ Kt[kh]) * scale
             s = np.where(mask, s, -np.inf)
             s = s - s.max(axis=1, keepdims=True)
             p = np.exp(s)
             p /= p.sum(axis=1, keepdims=True)
-            out[:, h, :] = p @ V[:, kh, :]
+            out[:, h, :] = p @ Vh[kh]
         return out
 
     for l in range(cfg.n_layers):
@@ -133,3 +136,77 @@ def taken_tokens(forced_len, tokens, cap, eos):
             taken[t, d - 1] = eos
         n_gen[t] = min(S, d, cap)
     return taken, n_gen
+
+
+def reference_values(cfg, run, prompts, forced, tokens, prompt_ids, n_steps, pool=None, n_idx=256,
+                     idx_seed=2605, log=None):
+    """The oracle's teacher-forced values for prompts ``prompt_ids`` of a batch
+    and their m trajectories each (global ids g = i*m + j), for generated
+    indices 0 .. n_steps-1, as a dict of arrays:
+
+      traj [T], prompts [Ps], steps, tokens / taken [T, S] (forcing table and
+      the tokens actually taken, the forced end-of-sequence included), n_gen [T]
+      idx [n_idx] fixed vocabulary ids, logits_at_idx [T, S, n_idx]
+      zmax, zabs, argmax, lse [T, S]: largest logit, largest |logit|, its id,
+      log-sum-exp of the logits / T
+      sampled, logprob, entropy, margin [T, S]: the Gumbel-max sample of
+      (g, s), log-prob of the taken token, entropy, top-2 perturbed margin
+      MoE: route_ids / route_p [R, L, k], route_margin [R, L] (forced_forward)
+
+    Weights are generated layer by layer from the model's seed (``pool``: an
+    optional multiprocessing pool for the generator and the sampler rows)."""
+    from .sampler import sample_row, top2_margin
+    say = log or (lambda *a: None)
+    m, eos = run.m, cfg.vocab - 1
+    prompt_ids = list(prompt_ids)
+    traj = np.array([p * m + j for p in prompt_ids for j in range(m)])
+    traj_prompt = np.repeat(np.arange(len(prompt_ids)), m)
+    tokens = np.asarray(tokens)[traj][:, :n_steps]
+    taken, n_gen = taken_tokens(np.asarray(forced)[traj], tokens, run.cap, eos)
+    seed, d, dt = cfg.weight_seed, cfg.d_model, cfg.dtype
+    routing = {}
+
+    def get_layer(l):
+        lw = M.init_layer(cfg, l, pool=pool)
+        say(f"layer {l} ready")
+        return lw
+
+    emb = lambda tk: M.init_rows(seed, M.T_EMBED, 0, tk, d, 1, dt)
+    last, dec = forced_forward(cfg, np.asarray(prompts)[prompt_ids], traj_prompt, taken[:, :n_steps - 1],
+                               get_layer, emb, routing=routing)
+    head = M.init_tensor(seed, M.T_LM, 0, cfg.vocab, d, d, dt, pool=pool)
+    T = len(traj)
+    hid = np.concatenate([last[traj_prompt][:, None, :], dec], axis=1)
+    logits = (hid.reshape(T * n_steps, d) @ head.T).reshape(T, n_steps, cfg.vocab)
+    del head
+    say("logits ready")
+    jobs = [(logits[t, s], run.temperature, int(traj[t]), s, run.sample_seed, int(taken[t, s]))
+            for t in range(T) for s in range(n_steps)]
+    res = pool.map(_score_row, jobs, chunksize=8) if pool is not None else list(map(_score_row, jobs))
+    res = np.array(res, dtype=np.float64).reshape(T, n_steps, 5)
+    if n_idx >= cfg.vocab:
+        idx = np.arange(cfg.vocab)
+    else:
+        idx = np.sort(np.random.default_rng(idx_seed).choice(cfg.vocab, n_idx, replace=False))
+    z = logits / float(run.temperature)
+    out = dict(
+        prompts=np.array(prompt_ids), traj=traj.astype(np.int32), steps=np.int32(n_steps),
+        tokens=tokens.astype(np.int32), taken=taken.astype(np.int32), n_gen=n_gen.astype(np.int32),
+        idx=idx.astype(np.int32), logits_at_idx=logits[:, :, idx].astype(np.float32),
+        zmax=logits.max(axis=-1), zabs=np.abs(logits).max(axis=-1),
+        argmax=logits.argmax(axis=-1).astype(np.int32),
+        lse=z.max(axis=-1) + np.log(np.exp(z - z.max(axis=-1, keepdims=True)).sum(axis=-1)),
+        sampled=res[..., 0].astype(np.int32), logprob=res[..., 1], entropy=res[..., 2], margin=res[..., 3])
+    if cfg.n_experts:
+        out["route_ids"] = routing["ids"].astype(np.uint8 if cfg.n_experts <= 256 else np.int32)
+        out["route_p"] = routing["p"].astype(np.float32)
+        out["route_margin"] = routing["margin"].astype(np.float32)
+    return out
+
+
+def _score_row(args):
+    """Sampler outputs of one row: (sample, log-prob, entropy, top-2 margin, 0)."""
+    from .sampler import sample_row, top2_margin
+    logits, temperature, g, s, seed, force = args
+    tok, lp, ent = sample_row(logits, temperature, g, s, seed, force)
+    return tok, lp, ent, top2_margin(np.asarray(logits).astype(np.float32), temperature, g, s, seed), 0.0

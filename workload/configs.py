@@ -81,8 +81,19 @@ SWEEP = dict(
 )
 
 
+# Reduced shapes used only by parity tests: the Qwen3-30B-A3B-shaped MoE layer
+# at full width (d 2048, 32/4 heads x 128, 128 experts top-8, expert FFN 768)
+# with 2 layers and a 4096-token vocabulary, 2 prompts x 32 tokens, m 16,
+# k 8, cap 20 (early stop fires inside a 20-token window).
+PARITY = {
+    "moe-full-width": (replace(QWEN3_30B_A3B[0], name="moe-full-width", n_layers=2, vocab=4096),
+                       replace(QWEN3_30B_A3B[1], n_prompts=2, prompt_len=32, cap=20, len_median=10.0,
+                               len_tail=False, kv_pool_gb=0.0)),
+}
+
+
 def get_config(name: str, **run_overrides):
-    model, run = CONFIGS[name]
+    model, run = CONFIGS[name] if name in CONFIGS else PARITY[name]
     if run_overrides:
         run = replace(run, **run_overrides)
     return model, run
