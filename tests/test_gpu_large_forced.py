@@ -53,3 +53,7 @@ def _check(config):
 
 def test_qwen3_8b_full_depth_teacher_forced():
     _check("qwen3-8b")
+
+
+def test_qwen3_30b_a3b_full_depth_teacher_forced():
+    _check("qwen3-30b-a3b")
