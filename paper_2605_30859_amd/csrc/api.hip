@@ -470,7 +470,7 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
     A(&c->m_pos_of, pairs * 4);
     A(&c->m_cnt, (size_t)3 * c->E * 4);
     A(&c->m_logits, (size_t)rows_max * c->Epad * 4);
-    A(&c->m_mtiles, (pairs / kGroupedTileRows + c->E + 1) * 4);
+    A(&c->m_mtiles, (pairs / kGroupedTileRowsMin + c->E + 1) * 4);
     A(&c->m_row_of, pairs * 4);
     A(&c->m_h_perm, pairs * c->Fe * 2);
     A(&c->m_y_perm, pairs * c->d * 4);

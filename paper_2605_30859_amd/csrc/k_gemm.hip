@@ -658,15 +658,20 @@ static void dma_go(const Plan& p, const void* A, int lda, const void* W, int ldw
   }
 }
 
-template <int EPI>
+int grouped_tile_rows(int64_t n_pairs, int E) {
+  return n_pairs <= (int64_t)96 * E ? kGroupedTileRowsMin : kGroupedTileRows;
+}
+
+// One block per CU, persistent over (row tile, n tile) items.  128-row tiles:
+// 128x128 with a 4-stage ring.  64-row tiles: 64x128 with a 6-stage ring
+// (the same 16 KB of weights per stage, half the input rows), so more
+// weight bytes are in flight per CU while the weights are streamed.
+template <int BM_, int ST, int EPI>
 static hipError_t grouped_launch(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
                                  void* C, int ldc, int N, int K, const int32_t* g_off,
                                  const int32_t* g_cnt, const int32_t* mtiles,
                                  const int32_t* n_mtiles, const int32_t* arow, hipStream_t st) {
-  // 128x128 tiles, 4-stage ring (one block per CU): expert weights are
-  // streamed once per row tile
-  constexpr int BM_ = 128, BN_ = 128, KB = 64, ST = 4;
-  static_assert(BM_ == kGroupedTileRows, "row tile of the m-tile list");
+  constexpr int BN_ = 128, KB = 64;
   const int nt = N / BN_;
   const size_t lds = (size_t)ST * (BM_ + BN_) * KB * sizeof(bf16_t);
   auto kern = gemm_dma_grouped_kernel<BM_, BN_, KB, 2, 2, ST, EPI>;
@@ -680,16 +685,30 @@ static hipError_t grouped_launch(const void* A, int lda, const void* W, int64_t 
   return hipGetLastError();
 }
 
+template <int EPI>
+static hipError_t grouped_by_rows(int tile_rows, const void* A, int lda, const void* W, int64_t w_stride,
+                                  int ldw, void* C, int ldc, int N, int K, const int32_t* g_off,
+                                  const int32_t* g_cnt, const int32_t* mtiles, const int32_t* n_mtiles,
+                                  const int32_t* arow, hipStream_t st) {
+  if (tile_rows == kGroupedTileRowsMin)
+    return grouped_launch<kGroupedTileRowsMin, 6, EPI>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt,
+                                                       mtiles, n_mtiles, arow, st);
+  if (tile_rows == kGroupedTileRows)
+    return grouped_launch<kGroupedTileRows, 4, EPI>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt,
+                                                    mtiles, n_mtiles, arow, st);
+  return hipErrorInvalidValue;
+}
+
 hipError_t launch_gemm_grouped(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
                                void* C, int ldc, int N, int K, int epi, const int32_t* g_off,
                                const int32_t* g_cnt, const int32_t* mtiles, const int32_t* n_mtiles,
-                               const int32_t* arow, hipStream_t st) {
+                               const int32_t* arow, int tile_rows, hipStream_t st) {
   if (N % 128 != 0 || K % 64 != 0 || K < 64) return hipErrorInvalidValue;
   switch (epi) {
-    case EPI_F32: return grouped_launch<EPI_F32>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
-    case EPI_BF16: return grouped_launch<EPI_BF16>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
-    case EPI_ADD_F32: return grouped_launch<EPI_ADD_F32>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
-    case EPI_SWIGLU: return grouped_launch<EPI_SWIGLU>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
+    case EPI_F32: return grouped_by_rows<EPI_F32>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
+    case EPI_BF16: return grouped_by_rows<EPI_BF16>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
+    case EPI_ADD_F32: return grouped_by_rows<EPI_ADD_F32>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
+    case EPI_SWIGLU: return grouped_by_rows<EPI_SWIGLU>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
     default: return hipErrorInvalidValue;
   }
 }

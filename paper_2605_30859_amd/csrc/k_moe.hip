@@ -159,7 +159,8 @@ __global__ void __launch_bounds__(1024) moe_offsets_kernel(const int32_t* __rest
                                                            int32_t* __restrict__ n_mtiles,
                                                            int32_t* __restrict__ pos_of,
                                                            int32_t* __restrict__ row_of,
-                                                           int32_t* __restrict__ touched_out) {
+                                                           int32_t* __restrict__ touched_out,
+                                                           int tile_rows) {
   __shared__ int32_t hist[1024];
   __shared__ int32_t sh[1024];
   const int tid = threadIdx.x;
@@ -173,7 +174,7 @@ __global__ void __launch_bounds__(1024) moe_offsets_kernel(const int32_t* __rest
   const int v = tid < E ? hist[tid] : 0;
   int total;
   const int ex = block_excl_scan1024(v, sh, &total);
-  const int nt = (v + kGroupedTileRows - 1) / kGroupedTileRows;
+  const int nt = (v + tile_rows - 1) / tile_rows;
   int ntiles;
   const int tex = block_excl_scan1024(nt, sh, &ntiles);
   if (tid < E) {
@@ -258,7 +259,7 @@ hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st, bool* normed) {
   *normed = false;
   if (a.n_rows <= 0) return hipSuccess;
   if (a.E > 64 * kMoeMaxPerLane || a.E > 1024 || a.k > 64 || a.k > a.E || a.d % 4 ||
-      a.n_rows > 65536 * kGroupedTileRows)
+      a.n_rows > 65536 * kGroupedTileRowsMin)
     return hipErrorInvalidValue;
   // router logits, or their split-K partial planes (summed by the top-k kernel)
   int n_split = 1;
@@ -269,6 +270,7 @@ hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st, bool* normed) {
   const float* lg = n_split > 1 ? (const float*)a.gemm_ws : a.logits;
   const int64_t zs = (int64_t)a.n_rows * a.E_pad;
   const dim3 gtk((a.n_rows + 3) / 4), btk(256);
+  const int tile_rows = grouped_tile_rows((int64_t)a.n_rows * a.k, a.E);
   const bool dbg = a.force_ids || a.own_ids_out || a.used_p_out;
 #define DARTS_TOPK(NPL)                                                                          \
   if (dbg)                                                                                       \
@@ -287,18 +289,18 @@ hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st, bool* normed) {
 #undef DARTS_TOPK
   hipLaunchKernelGGL(moe_offsets_kernel, dim3(1), dim3(1024), 0, st, a.topk_id, a.n_rows * a.k, a.E, a.k,
                      a.counts, a.offsets, a.cursors, a.mtiles, a.n_mtiles, a.pos_of, a.row_of,
-                     a.touched_out);
+                     a.touched_out, tile_rows);
   const int Fe = a.Fe, d = a.d;
   // gate/up: N = 2*Fe, K = d (SwiGLU into h_perm), A rows gathered from xn;
   // down: N = d, K = Fe
   if (a.ev_gu0 && (e = hipEventRecord(a.ev_gu0, st)) != hipSuccess) return e;
   e = launch_gemm_grouped(a.xn, d, a.w_gu, (int64_t)2 * Fe * d, d, a.h_perm, Fe, 2 * Fe, d,
-                          EPI_SWIGLU, a.offsets, a.counts, a.mtiles, a.n_mtiles, a.row_of, st);
+                          EPI_SWIGLU, a.offsets, a.counts, a.mtiles, a.n_mtiles, a.row_of, tile_rows, st);
   if (e != hipSuccess) return e;
   if (a.ev_gu1 && (e = hipEventRecord(a.ev_gu1, st)) != hipSuccess) return e;
   if (a.ev_down0 && (e = hipEventRecord(a.ev_down0, st)) != hipSuccess) return e;
   e = launch_gemm_grouped(a.h_perm, Fe, a.w_down, (int64_t)d * Fe, Fe, a.y_perm, d, d, Fe, EPI_F32,
-                          a.offsets, a.counts, a.mtiles, a.n_mtiles, nullptr, st);
+                          a.offsets, a.counts, a.mtiles, a.n_mtiles, nullptr, tile_rows, st);
   if (e != hipSuccess) return e;
   if (a.ev_down1 && (e = hipEventRecord(a.ev_down1, st)) != hipSuccess) return e;
   const bool fuse = d <= 1024 * kCombVec;

@@ -66,14 +66,20 @@ hipError_t launch_gather_rows(const float* src, const int32_t* rows, int n, int 
 
 // Grouped bf16 GEMM (mixture of experts): group e owns rows [g_off[e],
 // g_off[e] + g_cnt[e]) of A and C and the weights W + e * w_stride ([N][K],
-// row stride ldw).  mtiles lists the non-empty row tiles of
-// kGroupedTileRows rows, e << 16 | tile, *n_mtiles of them (device values).
+// row stride ldw).  mtiles lists the non-empty row tiles of tile_rows rows
+// (grouped_tile_rows), e << 16 | tile, *n_mtiles of them (device values).
 // N % 128 == 0, K % 64 == 0.
-constexpr int kGroupedTileRows = 128;
+constexpr int kGroupedTileRows = 128;      // largest row tile
+constexpr int kGroupedTileRowsMin = 64;    // smallest row tile (sizes the tile list)
+// Row tile for n_pairs routed (row, expert) pairs over E experts: 64-row
+// tiles while an expert gets few rows (decode batches: the weights are
+// streamed and half-empty 128-row tiles would double the operand traffic),
+// 128-row tiles for large batches (the prefill: more reuse of each weight tile).
+int grouped_tile_rows(int64_t n_pairs, int E);
 hipError_t launch_gemm_grouped(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
                                void* C, int ldc, int N, int K, int epi, const int32_t* g_off,
                                const int32_t* g_cnt, const int32_t* mtiles, const int32_t* n_mtiles,
-                               const int32_t* arow, hipStream_t st);
+                               const int32_t* arow, int tile_rows, hipStream_t st);
 
 // ---- attention (k_attn.hip)
 size_t attn_workspace_bytes(int n_rows, int hq, int hkv, int hd, int max_ctx);
@@ -193,7 +199,7 @@ struct MoeArgs {
   int32_t* topk_id; float* topk_w; int32_t* pos_of;            // [n_rows*k]
   int32_t* row_of;          // [n_rows*k]: input row of each expert-sorted position
   int32_t* counts; int32_t* offsets; int32_t* cursors;         // [E]
-  int32_t* mtiles;          // [n_rows*k / kGroupedTileRows + E] non-empty expert row tiles
+  int32_t* mtiles;          // [n_rows*k / kGroupedTileRowsMin + E] non-empty expert row tiles
   int32_t* n_mtiles;        // [1]
   bf16_t* h_perm; float* y_perm;                               // [n_rows*k][Fe | d]
   // Verification of the routing (all NULL in normal use).  Row r has key
