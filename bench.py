@@ -418,15 +418,21 @@ def next_rows(B, model, run, threshold):
 
 
 ATTN_SOURCES = ("paper_2605_30859_amd/csrc/k_attn.hip", "paper_2605_30859_amd/csrc/common.h")
+EXPERT_SOURCES = ("paper_2605_30859_amd/csrc/k_gemm.hip", "paper_2605_30859_amd/csrc/k_moe.hip",
+                  "paper_2605_30859_amd/csrc/common.h")
 
 
-def attn_source_hash():
+def source_hash(rels=ATTN_SOURCES):
     import hashlib
     h = hashlib.sha256()
-    for rel in ATTN_SOURCES:
+    for rel in rels:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
+
+
+def attn_source_hash():
+    return source_hash(ATTN_SOURCES)
 
 
 def _counter_rows(d):
@@ -445,13 +451,25 @@ def _counter_rows(d):
     return list(per.values())
 
 
-def summarize_pmc(d):
-    """HBM traffic of the decode-attention kernel from four rocprofv3 --pmc
-    runs under d (pmc_copy_FETCH_SIZE, pmc_copy_WRITE_SIZE: bench.py
-    --copy-calibration; pmc_attn_FETCH_SIZE, pmc_attn_WRITE_SIZE: the rollout
-    with --kernel-include-regex attn_bf16) and the rollout's bench line in
-    d/bench_attn_fetch.json.  Each counter is scaled by what it reads for a
-    plain 1 GiB device copy."""
+def _pmc_class(name):
+    """Kernel class of a profiled dispatch: decode attention or one of the
+    two grouped expert GEMMs (SwiGLU epilogue = gate/up, fp32 store = down)."""
+    import re
+    if "attn_bf16" in name:
+        return "attention"
+    mt = re.search(r"gemm_dma_grouped_kernel<[^>]*?(\d+)>", name)
+    if mt:
+        return "expert_gate_up" if mt.group(1) == "3" else "expert_down"
+    return None
+
+
+def summarize_pmc(d, name="attn"):
+    """HBM traffic per launch of the decode-attention kernel (and, in MoE runs,
+    of the grouped expert GEMMs) from rocprofv3 --pmc runs under d:
+    pmc_copy_FETCH_SIZE / pmc_copy_WRITE_SIZE (bench.py --copy-calibration)
+    and pmc_<name>_FETCH_SIZE / pmc_<name>_WRITE_SIZE (the rollout with a
+    kernel-name filter), plus the rollout's bench line in d/bench_<name>.json.
+    Each counter is scaled by what it reads for a plain 1 GiB device copy."""
     out = {"kernel": "attn_bf16_kernel + attn_bf16_db_kernel", "kernel_source_sha256": attn_source_hash()}
     cal = {}
     for c in ("FETCH_SIZE", "WRITE_SIZE"):
@@ -459,17 +477,73 @@ def summarize_pmc(d):
         kib = sum(rows) / len(rows)
         cal[c] = {"KiB_per_1GiB_copy": kib, "scale": (1 << 30) / (kib * 1024.0), "copies": len(rows)}
     out["copy_calibration"] = cal
-    with open(os.path.join(d, "bench_attn_fetch.json")) as f:
+    with open(os.path.join(d, f"bench_{name}.json")) as f:
         line = [l for l in f.read().splitlines() if l.startswith("{")][-1]
     b = json.loads(line)
     out["workload"] = b["config"]["workload"]
-    out["algorithmic_bytes_per_launch"] = b["roofline"]["algorithmic_bytes_per_launch"]
+    alg = {"attention": b["roofline"]["algorithmic_bytes_per_launch"]}
+    for k, v in (b.get("roofline_moe_experts") or {}).items():
+        alg[k] = v["algorithmic_bytes_per_launch"]
+    per = {}
     for c, key in (("FETCH_SIZE", "fetch_bytes_per_launch"), ("WRITE_SIZE", "write_bytes_per_launch")):
-        rows = [v for n, v in _counter_rows(os.path.join(d, f"pmc_attn_{c}")) if "attn_bf16" in n]
-        out[key] = sum(rows) / len(rows) * 1024.0 * cal[c]["scale"]
-        out[f"launches_{c}"] = len(rows)
-    out["traffic_bytes_per_launch"] = out["fetch_bytes_per_launch"] + out["write_bytes_per_launch"]
-    out["measured_over_algorithmic"] = out["traffic_bytes_per_launch"] / out["algorithmic_bytes_per_launch"]
+        groups = {}
+        for n, v in _counter_rows(os.path.join(d, f"pmc_{name}_{c}")):
+            k = _pmc_class(n)
+            if k:
+                groups.setdefault(k, []).append(v)
+        for k, vals in groups.items():
+            e = per.setdefault(k, {})
+            e[key] = sum(vals) / len(vals) * 1024.0 * cal[c]["scale"]
+            e[f"launches_{c}"] = len(vals)
+    for k, e in per.items():
+        e["algorithmic_bytes_per_launch"] = alg.get(k)
+        e["traffic_bytes_per_launch"] = e.get("fetch_bytes_per_launch", 0.0) + e.get("write_bytes_per_launch", 0.0)
+        if alg.get(k):
+            e["measured_over_algorithmic"] = e["traffic_bytes_per_launch"] / alg[k]
+        if k != "attention":
+            e["kernel_source_sha256"] = source_hash(EXPERT_SOURCES)
+    out.update(per.get("attention", {}))
+    out["kernels"] = per
+    return out
+
+
+def summarize_mfma(d):
+    """MFMA utilisation of the GEMM kernels from one rocprofv3 --pmc pass
+    under d collecting MfmaUtil (the busy cycles of the matrix cores over
+    active cycles x SIMDs, per dispatch), MfmaFlopsBF16 and GRBM_GUI_ACTIVE,
+    per kernel (template configuration) and over all of them, each dispatch
+    weighted by its active cycles."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if len(files) != 1:
+        raise SystemExit(f"expected one counter_collection.csv under {d}, found {len(files)}")
+    per = {}
+    with open(files[0]) as f:
+        for r in csv.DictReader(f):
+            key = int(r["Dispatch_Id"])
+            e = per.setdefault(key, {"name": r["Kernel_Name"]})
+            e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    by = {}
+    for e in per.values():
+        name = e["name"].split("(")[0].replace("void ", "").replace("darts::", "")
+        k = by.setdefault(name, {"dispatches": 0, "gui": 0.0, "busy_weighted": 0.0, "bf16_flop": 0.0})
+        g = e.get("GRBM_GUI_ACTIVE", 0.0)
+        k["dispatches"] += 1
+        k["gui"] += g
+        k["busy_weighted"] += g * e.get("MfmaUtil", 0.0) / 100.0
+        k["bf16_flop"] += e.get("MfmaFlopsBF16", 0.0)
+    tot = {"dispatches": 0, "gui": 0.0, "busy_weighted": 0.0, "bf16_flop": 0.0}
+    out = {"kernels": {}}
+    for name, k in sorted(by.items(), key=lambda kv: -kv[1]["gui"]):
+        for f in tot:
+            tot[f] += k[f]
+        out["kernels"][name] = {"dispatches": k["dispatches"], "active_cycles": k["gui"],
+                                "mfma_util": k["busy_weighted"] / max(k["gui"], 1.0),
+                                "bf16_flop": k["bf16_flop"]}
+    out["all_gemm_kernels"] = {"dispatches": tot["dispatches"], "active_cycles": tot["gui"],
+                               "mfma_util": tot["busy_weighted"] / max(tot["gui"], 1.0),
+                               "bf16_flop": tot["bf16_flop"]}
     return out
 
 
@@ -490,18 +564,23 @@ def summarize_stats(path, top=16):
     return "\n".join(lines)
 
 
-def measured_traffic(config):
-    """Per-launch HBM bytes of the attention kernel from the committed counter
-    summary, or None when there is none for this workload or the kernel's
-    source changed since the counters were taken."""
+def measured_traffic(config, kernel="attention"):
+    """Per-launch HBM bytes of a kernel from the committed counter summary, or
+    None when there is none for this workload or the kernel's sources changed
+    since the counters were taken."""
     p = os.path.join(ROOT, "profiles", f"attn_traffic_{config}_rollout.json")
     if not os.path.exists(p):
         return None
     with open(p) as f:
         t = json.load(f)
-    if t.get("kernel_source_sha256") != attn_source_hash():
+    if kernel == "attention":
+        if t.get("kernel_source_sha256") != attn_source_hash():
+            return None
+        return t["traffic_bytes_per_launch"]
+    e = t.get("kernels", {}).get(kernel)
+    if not e or e.get("kernel_source_sha256") != source_hash(EXPERT_SOURCES):
         return None
-    return t["traffic_bytes_per_launch"]
+    return e["traffic_bytes_per_launch"]
 
 
 def main():
@@ -535,12 +614,18 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="three 1 GiB device copies (reference for HBM byte counters), then exit")
     ap.add_argument("--summarize-pmc", metavar="DIR",
-                    help="print the attention traffic summary (JSON) of the rocprofv3 counter runs in DIR")
+                    help="print the traffic summary (JSON) of the rocprofv3 counter runs in DIR")
+    ap.add_argument("--pmc-name", default="attn", help="run name of the counter directories in DIR")
+    ap.add_argument("--summarize-mfma", metavar="DIR",
+                    help="print the GEMM MFMA utilisation (JSON) of a rocprofv3 --pmc run in DIR")
     ap.add_argument("--summarize-stats", metavar="CSV",
                     help="print a markdown table of a rocprofv3 kernel_stats.csv")
     args = ap.parse_args()
     if args.summarize_pmc:
-        print(json.dumps(summarize_pmc(args.summarize_pmc), indent=1))
+        print(json.dumps(summarize_pmc(args.summarize_pmc, args.pmc_name), indent=1))
+        return
+    if args.summarize_mfma:
+        print(json.dumps(summarize_mfma(args.summarize_mfma), indent=1))
         return
     if args.summarize_stats:
         print(summarize_stats(args.summarize_stats))
@@ -667,7 +752,7 @@ def main():
             n_l = sum(s["moe_expert_launches"][i] for s in stats)
             ach_m = by / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
             moe_roof[name] = {"bound": "hbm", "achieved": ach_m, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                              "frac": ach_m / HBM_PEAK_GBS, "traffic": None,
+                              "frac": ach_m / HBM_PEAK_GBS, "traffic": measured_traffic(args.config, name),
                               "kernel": "gemm_dma_grouped_kernel (" + ("gate/up + SwiGLU" if i == 0 else "down") + ")",
                               "launches": n_l, "avg_launch_us": 1e3 * ms / max(n_l, 1),
                               "algorithmic_bytes_per_launch": by / max(n_l, 1),
