@@ -662,16 +662,22 @@ int grouped_tile_rows(int64_t n_pairs, int E) {
   return n_pairs <= (int64_t)96 * E ? kGroupedTileRowsMin : kGroupedTileRows;
 }
 
-// One block per CU, persistent over (row tile, n tile) items.  128-row tiles:
-// 128x128 with a 4-stage ring.  64-row tiles: 64x128 with a 6-stage ring
-// (the same 16 KB of weights per stage, half the input rows), so more
-// weight bytes are in flight per CU while the weights are streamed.
-template <int BM_, int ST, int EPI>
+// Persistent blocks over (row tile, n tile) items.  128-row tiles (the
+// prefill): 128x128 with a 4-stage ring, one block per CU.  64-row tiles
+// (decode batches, where the expert weights are streamed): two blocks per
+// CU, so one block's loads stream while the other waits at its barrier or
+// refills its ring at an item boundary; 64x64 tiles with a 4-stage ring for
+// the gate/up projection (K = d), 64x128 tiles with a 3-stage ring for the
+// down projection (K = expert FFN).  Measured on the Qwen3-30B-A3B expert
+// shapes from 1 to 1024 rows against one block per CU with 64x128 tiles and
+// a 6-stage ring: 6-18% faster for gate/up, 10-18% for down.
+template <int BM_, int ST, int EPI, int BN_ = 128, int BPC = 1>
 static hipError_t grouped_launch(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
                                  void* C, int ldc, int N, int K, const int32_t* g_off,
                                  const int32_t* g_cnt, const int32_t* mtiles,
                                  const int32_t* n_mtiles, const int32_t* arow, hipStream_t st) {
-  constexpr int BN_ = 128, KB = 64;
+  constexpr int KB = 64;
+  if (N % BN_ != 0) return hipErrorInvalidValue;
   const int nt = N / BN_;
   const size_t lds = (size_t)ST * (BM_ + BN_) * KB * sizeof(bf16_t);
   auto kern = gemm_dma_grouped_kernel<BM_, BN_, KB, 2, 2, ST, EPI>;
@@ -680,7 +686,7 @@ static hipError_t grouped_launch(const void* A, int lda, const void* W, int64_t 
     (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     attr_done = true;
   }
-  hipLaunchKernelGGL(kern, dim3(kCus), dim3(256), lds, st, (const bf16_t*)A, lda, (const bf16_t*)W,
+  hipLaunchKernelGGL(kern, dim3(kCus * BPC), dim3(256), lds, st, (const bf16_t*)A, lda, (const bf16_t*)W,
                      w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, nt, arow);
   return hipGetLastError();
 }
@@ -690,9 +696,14 @@ static hipError_t grouped_by_rows(int tile_rows, const void* A, int lda, const v
                                   int ldw, void* C, int ldc, int N, int K, const int32_t* g_off,
                                   const int32_t* g_cnt, const int32_t* mtiles, const int32_t* n_mtiles,
                                   const int32_t* arow, hipStream_t st) {
-  if (tile_rows == kGroupedTileRowsMin)
-    return grouped_launch<kGroupedTileRowsMin, 6, EPI>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt,
-                                                       mtiles, n_mtiles, arow, st);
+  if (tile_rows == kGroupedTileRowsMin) {
+    if constexpr (EPI == EPI_SWIGLU)
+      return grouped_launch<kGroupedTileRowsMin, 4, EPI, 64, 2>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off,
+                                                                g_cnt, mtiles, n_mtiles, arow, st);
+    else
+      return grouped_launch<kGroupedTileRowsMin, 3, EPI, 128, 2>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off,
+                                                                 g_cnt, mtiles, n_mtiles, arow, st);
+  }
   if (tile_rows == kGroupedTileRows)
     return grouped_launch<kGroupedTileRows, 4, EPI>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt,
                                                     mtiles, n_mtiles, arow, st);
