@@ -130,20 +130,33 @@ __global__ void __launch_bounds__(256) moe_topk_kernel(const float* __restrict__
   }
 }
 
+// Exclusive scan of one int per thread over a 1024-thread block: inclusive
+// scans inside each wavefront (shuffles), the 16 wavefront totals scanned by
+// the first wavefront through LDS, then added back.  sh holds >= 16 ints.
 __device__ __forceinline__ int block_excl_scan1024(int v, int32_t* sh, int* total) {
-  const int tid = threadIdx.x;
-  sh[tid] = v;
-  __syncthreads();
-  for (int o = 1; o < 1024; o <<= 1) {
-    const int x = tid >= o ? sh[tid - o] : 0;
-    __syncthreads();
-    sh[tid] += x;
-    __syncthreads();
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  int incl = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int x = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += x;
   }
-  const int incl = sh[tid];
-  *total = sh[1023];
+  if (lane == 63) sh[w] = incl;
   __syncthreads();
-  return incl - v;
+  if (w == 0) {
+    int t = lane < 16 ? sh[lane] : 0;
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) {
+      const int x = __shfl_up(t, o, 64);
+      if (lane >= o) t += x;
+    }
+    if (lane < 16) sh[16 + lane] = t;    // inclusive totals of wavefronts 0..lane
+  }
+  __syncthreads();
+  const int before = w > 0 ? sh[16 + w - 1] : 0;
+  *total = sh[16 + 15];
+  __syncthreads();                      // sh may be reused by the next scan
+  return before + incl - v;
 }
 
 // Single block: per-expert counts of the n_pairs routed (row, slot) pairs
