@@ -212,6 +212,68 @@ def hbm_read_rate(B, gib=8, reps=10):
     return rate
 
 
+def gemm_compare(B, reps=12):
+    """The library's bf16 GEMM (its own plan, fp32 output, split-K reduce
+    included) against torch.nn.functional.linear (hipBLASLt, bf16 output) on
+    the decode projections of the Qwen3-8B and Qwen3-30B-A3B shapes, at batch
+    heights 1..512, weights cold: each timed launch reads a different copy of
+    the weight, with at least 1.2 GB of copies, so that no launch finds its
+    weight in the L2 or the Infinity Cache.  Returns a markdown table."""
+    import numpy as np
+    import torch
+    shapes = [("8B qkv", 6144, 4096), ("8B o", 4096, 4096), ("8B gate/up", 24576, 4096),
+              ("8B down", 4096, 12288), ("8B lm head", 151936, 4096),
+              ("30B-A3B qkv", 5120, 2048), ("30B-A3B o", 2048, 4096), ("30B-A3B lm head", 151936, 2048)]
+    Ms = [1, 16, 64, 128, 256, 384, 512]
+    lines = ["| projection (N x K) | rows | library us | hipBLASLt us | library / hipBLASLt time | "
+             "library TFLOP/s | library weight GB/s |", "|---|---:|---:|---:|---:|---:|---:|"]
+    tot_l = tot_t = 0.0
+    for name, N, K in shapes:
+        wb = N * K * 2
+        ncopy = max(2, int(np.ceil(1.2e9 / wb)))
+        W = []
+        for i in range(ncopy):
+            w = torch.empty(N * K, dtype=torch.bfloat16, device="cuda")
+            B.darts_fill_uniform(w, 40 + i, 5, B.DARTS_BF16)
+            W.append(w)
+        A = torch.empty(512 * K, dtype=torch.bfloat16, device="cuda")
+        B.darts_fill_uniform(A, 39, 5, B.DARTS_BF16)
+        C = torch.empty(512 * N, dtype=torch.float32, device="cuda")
+        for M in Ms:
+            ws = torch.empty(max(B.darts_gemm_workspace_bytes(M, N, K), 256), dtype=torch.uint8, device="cuda")
+            a2 = A[:M * K].view(M, K)
+            it = max(ncopy, reps)
+
+            def ours(j):
+                B.darts_gemm(A, W[j % ncopy], C, M, N, K, B.DARTS_BF16, 0, ws)
+
+            def theirs(j):
+                torch.nn.functional.linear(a2, W[j % ncopy].view(N, K))
+
+            res = []
+            for fn in (ours, theirs):
+                for j in range(ncopy):
+                    fn(j)
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for j in range(it):
+                    fn(j)
+                e1.record()
+                torch.cuda.synchronize()
+                res.append(e0.elapsed_time(e1) * 1e3 / it)
+            us, ref = res
+            tot_l += us
+            tot_t += ref
+            lines.append(f"| {name} ({N} x {K}) | {M} | {us:.1f} | {ref:.1f} | {us / ref:.2f} | "
+                         f"{2.0 * M * N * K / us / 1e6:.0f} | {wb / us / 1e3:.0f} |")
+            print(f"[bench] gemm {name} M={M}: {us:.1f} us, hipBLASLt {ref:.1f} us", file=sys.stderr, flush=True)
+        del W, A, C
+        torch.cuda.empty_cache()
+    lines.append(f"| all cases (sum of times) | | {tot_l:.0f} | {tot_t:.0f} | {tot_l / tot_t:.2f} | | |")
+    return "\n".join(lines)
+
+
 def kernel_sweep(B, steps, warmup):
     """Stateless kernels on the sweep's inputs (bf16, data seed 1): decode
     attention over 1024 trajectories with lognormal(1500, 1.0) contexts clipped
@@ -564,6 +626,50 @@ def summarize_stats(path, top=16):
     return "\n".join(lines)
 
 
+def summarize_gaps(path):
+    """GPU idle time of the last rollout in a rocprofv3 kernel_trace.csv: the
+    window runs from its first prefill_pages_kernel to its last prune_kernel.
+    Gaps from a prune_kernel up to the next step's first kernel (an embedding
+    or page-allocation kernel) are step boundaries: the copies that follow
+    the selection, the host's read of the live count and the queueing of the
+    next step.  Every other gap lies between two kernels of one step."""
+    import csv
+    with open(path) as f:
+        rows = [(int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"])
+                for r in csv.DictReader(f)]
+    rows.sort()
+    starts = [i for i, r in enumerate(rows) if "prefill_pages_kernel" in r[2]]
+    if not starts:
+        raise SystemExit("no prefill_pages_kernel in the trace")
+    lo = starts[-1]
+    hi = max(i for i, r in enumerate(rows) if "prune_kernel" in r[2] and i >= lo)
+    win = rows[lo:hi + 1]
+    busy = step_gap = intra_gap = 0
+    n_steps = big = 0
+    end = win[0][0]
+    after_prune = False
+    for s, e, name in win:
+        if s > end:
+            g = s - end
+            if after_prune:
+                step_gap += g
+            else:
+                intra_gap += g
+            big += g > 50_000
+        busy += max(0, e - max(s, end))
+        end = max(end, e)
+        if "prune_kernel" in name:
+            after_prune = True
+            n_steps += 1
+        elif "embed" in name or "alloc_pages" in name:
+            after_prune = False
+    span = win[-1][1] - win[0][0]
+    return {"kernels": len(win), "prune_launches": n_steps, "span_s": span / 1e9, "busy_s": busy / 1e9,
+            "idle_s": (span - busy) / 1e9, "step_boundary_idle_s": step_gap / 1e9,
+            "step_boundary_idle_us_per_step": step_gap / 1e3 / max(1, n_steps),
+            "intra_step_idle_s": intra_gap / 1e9, "gaps_over_50us": big}
+
+
 def measured_traffic(config, kernel="attention"):
     """Per-launch HBM bytes of a kernel from the committed counter summary, or
     None when there is none for this workload or the kernel's sources changed
@@ -620,7 +726,15 @@ def main():
                     help="print the GEMM MFMA utilisation (JSON) of a rocprofv3 --pmc run in DIR")
     ap.add_argument("--summarize-stats", metavar="CSV",
                     help="print a markdown table of a rocprofv3 kernel_stats.csv")
+    ap.add_argument("--gemm-compare", action="store_true",
+                    help="time the library's GEMM against torch linear (hipBLASLt) on the decode "
+                         "projections, weights cold; print a markdown table")
+    ap.add_argument("--summarize-gaps", metavar="CSV",
+                    help="print the GPU idle time (JSON) of the last rollout in a rocprofv3 kernel_trace.csv")
     args = ap.parse_args()
+    if args.summarize_gaps:
+        print(json.dumps(summarize_gaps(args.summarize_gaps), indent=1))
+        return
     if args.summarize_pmc:
         print(json.dumps(summarize_pmc(args.summarize_pmc, args.pmc_name), indent=1))
         return
@@ -655,6 +769,9 @@ def main():
     B.load_library()
     if args.sweep:
         print(json.dumps(kernel_sweep(B, args.steps, args.warmup)), flush=True)
+        return
+    if args.gemm_compare:
+        print(gemm_compare(B), flush=True)
         return
     model, run = get_config(args.config)
     if args.next:

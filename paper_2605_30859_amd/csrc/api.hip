@@ -67,7 +67,7 @@ struct darts_ctx {
   int32_t* m_cnt = nullptr;       // counts | offsets | cursors, E each
   int32_t* m_row_of = nullptr;    // [pairs] input row of each expert-sorted position
   void* m_h_perm = nullptr;
-  float* m_y_perm = nullptr;
+  void* m_y_perm = nullptr;
   float* m_logits = nullptr;      // router logits [rows][Epad]
   int32_t* m_mtiles = nullptr;    // n_mtiles | non-empty expert row tiles
   int32_t* m_touched = nullptr;   // [n_layers] experts that received rows (timed launches)
@@ -473,7 +473,7 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
     A(&c->m_mtiles, (pairs / kGroupedTileRowsMin + c->E + 1) * 4);
     A(&c->m_row_of, pairs * 4);
     A(&c->m_h_perm, pairs * c->Fe * 2);
-    A(&c->m_y_perm, pairs * c->d * 4);
+    A(&c->m_y_perm, pairs * c->d * 2);
     A(&c->m_touched, (size_t)c->nl * 4);
   }
   if (rc.flags & DARTS_FLAG_STREAM) {
@@ -716,7 +716,7 @@ static int run_layers(darts_ctx* c, int n, const int32_t* row_pt, const int32_t*
       m.w_down = (const bf16_t*)w.wedown; m.topk_id = c->m_topk_id; m.topk_w = c->m_topk_w;
       m.pos_of = c->m_pos_of; m.counts = c->m_cnt; m.offsets = c->m_cnt + c->E;
       m.cursors = c->m_cnt + 2 * c->E;
-      m.h_perm = (bf16_t*)c->m_h_perm; m.y_perm = c->m_y_perm;
+      m.h_perm = (bf16_t*)c->m_h_perm; m.y_perm = (bf16_t*)c->m_y_perm;
       const int64_t dstride = (int64_t)c->nl * c->topk;
       m.route_key = row_key; m.dbg_stride = dstride;
       m.force_ids = c->dbg_force_ids ? c->dbg_force_ids + (int64_t)l * c->topk : nullptr;
@@ -903,13 +903,13 @@ int darts_select_and_prune(darts_ctx* c, int32_t* d_kept, int32_t* d_done_step, 
     } else if (t.kind == kMoeGu || t.kind == kMoeDown) {
       // algorithmic bytes: the touched experts' weights once, the routed
       // rows' inputs and outputs (gate/up: bf16 rows in, bf16 SwiGLU rows out;
-      // down: bf16 rows in, fp32 rows out)
+      // down: bf16 rows in, bf16 rows out)
       if (!c->h_touched || t.touched_slot < 0) continue;
       const double ne = c->h_touched[t.touched_slot];
       const double dd = c->d, fe = c->Fe;
       const int i = t.kind == kMoeGu ? 0 : 1;
       const double bytes = i == 0 ? ne * 2.0 * fe * dd * 2.0 + t.rows * (dd * 2.0 + fe * 2.0)
-                                  : ne * dd * fe * 2.0 + t.rows * (fe * 2.0 + dd * 4.0);
+                                  : ne * dd * fe * 2.0 + t.rows * (fe * 2.0 + dd * 2.0);
       c->moe_ms[i] += w * ms; c->moe_bytes[i] += w * bytes; c->moe_launches[i] += (int64_t)w;
     } else {
       c->gemm_ms += w * ms; c->gemm_flop += w * t.units; c->gemm_launches += (int64_t)w;

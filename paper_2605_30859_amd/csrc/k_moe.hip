@@ -214,10 +214,26 @@ __global__ void __launch_bounds__(1024) moe_offsets_kernel(const int32_t* __rest
   }
 }
 
-// x[r] += sum_j w[r][j] * y[pos(r, j)]   (slot order), 4 columns per thread;
+// x[r] += sum_j w[r][j] * y[pos(r, j)]   (slot order, y in bf16, the sum in
+// fp32), 8 columns per thread: the k expert rows of a column chunk are
+// loaded (16 bytes each) before any is summed, so their latencies overlap;
 // with xn (d <= 4096) also xn[r] = bf16(x[r] / sqrt(mean(x[r]^2) + eps)).
-constexpr int kCombVec = 4;
-__global__ void __launch_bounds__(256) moe_combine_kernel(const float* __restrict__ y, int d, int k,
+constexpr int kCombCols = 8;
+constexpr int kCombIters = 2;
+constexpr int kCombBatch = 8;   // expert rows loaded before summing
+
+__device__ __forceinline__ void comb_fma8(float* s, float w, const uint4& v) {
+  s[0] = fmaf(w, bf16_to_f32((bf16_t)(v.x & 0xffffu)), s[0]);
+  s[1] = fmaf(w, bf16_to_f32((bf16_t)(v.x >> 16)), s[1]);
+  s[2] = fmaf(w, bf16_to_f32((bf16_t)(v.y & 0xffffu)), s[2]);
+  s[3] = fmaf(w, bf16_to_f32((bf16_t)(v.y >> 16)), s[3]);
+  s[4] = fmaf(w, bf16_to_f32((bf16_t)(v.z & 0xffffu)), s[4]);
+  s[5] = fmaf(w, bf16_to_f32((bf16_t)(v.z >> 16)), s[5]);
+  s[6] = fmaf(w, bf16_to_f32((bf16_t)(v.w & 0xffffu)), s[6]);
+  s[7] = fmaf(w, bf16_to_f32((bf16_t)(v.w >> 16)), s[7]);
+}
+
+__global__ void __launch_bounds__(256) moe_combine_kernel(const bf16_t* __restrict__ y, int d, int k,
                                                           const int32_t* __restrict__ pos_of,
                                                           const float* __restrict__ topk_w,
                                                           float* __restrict__ x, float eps,
@@ -231,47 +247,67 @@ __global__ void __launch_bounds__(256) moe_combine_kernel(const float* __restric
     sw[tid] = topk_w[(int64_t)r * k + tid];
   }
   __syncthreads();
-  float4 keep[kCombVec];
-  float ss = 0.f;
-  int t = 0;
-  for (int c = tid * 4; c < d; c += 1024, ++t) {
-    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int j = 0; j < k; ++j) {
-      const float4 v = *(const float4*)(y + (int64_t)sp[j] * d + c);
-      const float w = sw[j];
-      s.x = fmaf(w, v.x, s.x);
-      s.y = fmaf(w, v.y, s.y);
-      s.z = fmaf(w, v.z, s.z);
-      s.w = fmaf(w, v.w, s.w);
+  // one chunk: sum the k expert rows, add into x, return the new x values
+  auto chunk = [&](int c, float* xv) {
+    float s[kCombCols];
+#pragma unroll
+    for (int u = 0; u < kCombCols; ++u) s[u] = 0.f;
+    for (int j0 = 0; j0 < k; j0 += kCombBatch) {
+      uint4 v[kCombBatch];
+#pragma unroll
+      for (int u = 0; u < kCombBatch; ++u)
+        if (j0 + u < k) v[u] = *(const uint4*)(y + (int64_t)sp[j0 + u] * d + c);
+#pragma unroll
+      for (int u = 0; u < kCombBatch; ++u)
+        if (j0 + u < k) comb_fma8(s, sw[j0 + u], v[u]);
     }
     float4* xp = (float4*)(x + (int64_t)r * d + c);
-    float4 xv = *xp;
-    xv.x += s.x; xv.y += s.y; xv.z += s.z; xv.w += s.w;
-    *xp = xv;
-    if (t < kCombVec) keep[t] = xv;
-    ss = fmaf(xv.x, xv.x, ss);
-    ss = fmaf(xv.y, xv.y, ss);
-    ss = fmaf(xv.z, xv.z, ss);
-    ss = fmaf(xv.w, xv.w, ss);
+    float4 x0 = xp[0], x1 = xp[1];
+    x0.x += s[0]; x0.y += s[1]; x0.z += s[2]; x0.w += s[3];
+    x1.x += s[4]; x1.y += s[5]; x1.z += s[6]; x1.w += s[7];
+    xp[0] = x0;
+    xp[1] = x1;
+    xv[0] = x0.x; xv[1] = x0.y; xv[2] = x0.z; xv[3] = x0.w;
+    xv[4] = x1.x; xv[5] = x1.y; xv[6] = x1.z; xv[7] = x1.w;
+  };
+  if (xn == nullptr) {
+    float xv[kCombCols];
+    for (int c = tid * kCombCols; c < d; c += 256 * kCombCols) chunk(c, xv);
+    return;
   }
-  if (xn == nullptr) return;
+  // fused RMSNorm (d <= 256 * kCombCols * kCombIters): x stays in registers
+  float keep[kCombIters][kCombCols];
+  float ss = 0.f;
+#pragma unroll
+  for (int t = 0; t < kCombIters; ++t) {
+    const int c = (tid + 256 * t) * kCombCols;
+    if (c < d) {
+      chunk(c, keep[t]);
+#pragma unroll
+      for (int u = 0; u < kCombCols; ++u) ss = fmaf(keep[t][u], keep[t][u], ss);
+    }
+  }
   ss = wave_sum(ss);
   if ((tid & 63) == 0) red[tid >> 6] = ss;
   __syncthreads();
   const float inv = 1.0f / sqrtf((red[0] + red[1] + red[2] + red[3]) / (float)d + eps);
-  t = 0;
-  for (int c = tid * 4; c < d && t < kCombVec; c += 1024, ++t) {
-    uint2 q;
-    q.x = (uint32_t)f32_to_bf16(keep[t].x * inv) | ((uint32_t)f32_to_bf16(keep[t].y * inv) << 16);
-    q.y = (uint32_t)f32_to_bf16(keep[t].z * inv) | ((uint32_t)f32_to_bf16(keep[t].w * inv) << 16);
-    *(uint2*)(xn + (int64_t)r * d + c) = q;
+#pragma unroll
+  for (int t = 0; t < kCombIters; ++t) {
+    const int c = (tid + 256 * t) * kCombCols;
+    if (c >= d) continue;
+    uint4 q;
+    q.x = (uint32_t)f32_to_bf16(keep[t][0] * inv) | ((uint32_t)f32_to_bf16(keep[t][1] * inv) << 16);
+    q.y = (uint32_t)f32_to_bf16(keep[t][2] * inv) | ((uint32_t)f32_to_bf16(keep[t][3] * inv) << 16);
+    q.z = (uint32_t)f32_to_bf16(keep[t][4] * inv) | ((uint32_t)f32_to_bf16(keep[t][5] * inv) << 16);
+    q.w = (uint32_t)f32_to_bf16(keep[t][6] * inv) | ((uint32_t)f32_to_bf16(keep[t][7] * inv) << 16);
+    *(uint4*)(xn + (int64_t)r * d + c) = q;
   }
 }
 
 hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st, bool* normed) {
   *normed = false;
   if (a.n_rows <= 0) return hipSuccess;
-  if (a.E > 64 * kMoeMaxPerLane || a.E > 1024 || a.k > 64 || a.k > a.E || a.d % 4 ||
+  if (a.E > 64 * kMoeMaxPerLane || a.E > 1024 || a.k > 64 || a.k > a.E || a.d % kCombCols ||
       a.n_rows > 65536 * kGroupedTileRowsMin)
     return hipErrorInvalidValue;
   // router logits, or their split-K partial planes (summed by the top-k kernel)
@@ -312,11 +348,11 @@ hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st, bool* normed) {
   if (e != hipSuccess) return e;
   if (a.ev_gu1 && (e = hipEventRecord(a.ev_gu1, st)) != hipSuccess) return e;
   if (a.ev_down0 && (e = hipEventRecord(a.ev_down0, st)) != hipSuccess) return e;
-  e = launch_gemm_grouped(a.h_perm, Fe, a.w_down, (int64_t)d * Fe, Fe, a.y_perm, d, d, Fe, EPI_F32,
+  e = launch_gemm_grouped(a.h_perm, Fe, a.w_down, (int64_t)d * Fe, Fe, a.y_perm, d, d, Fe, EPI_BF16,
                           a.offsets, a.counts, a.mtiles, a.n_mtiles, nullptr, tile_rows, st);
   if (e != hipSuccess) return e;
   if (a.ev_down1 && (e = hipEventRecord(a.ev_down1, st)) != hipSuccess) return e;
-  const bool fuse = d <= 1024 * kCombVec;
+  const bool fuse = d <= 256 * kCombCols * kCombIters;
   hipLaunchKernelGGL(moe_combine_kernel, dim3(a.n_rows), dim3(256), 0, st, a.y_perm, d, a.k,
                      a.pos_of, a.topk_w, a.x, a.eps, fuse ? a.xn : nullptr);
   e = hipGetLastError();

@@ -201,7 +201,7 @@ struct MoeArgs {
   int32_t* counts; int32_t* offsets; int32_t* cursors;         // [E]
   int32_t* mtiles;          // [n_rows*k / kGroupedTileRowsMin + E] non-empty expert row tiles
   int32_t* n_mtiles;        // [1]
-  bf16_t* h_perm; float* y_perm;                               // [n_rows*k][Fe | d]
+  bf16_t* h_perm; bf16_t* y_perm;                              // [n_rows*k][Fe | d]
   // Verification of the routing (all NULL in normal use).  Row r has key
   // route_key[r] (NULL: r); each pointer addresses this layer's k entries of
   // key 0, keys dbg_stride elements apart.

@@ -21,3 +21,28 @@ def test_cpu_baseline_runs_on_shrunk_configs(name):
     assert out["kind"] == "oracle" and out["unit"] == "tokens/s"
     assert out["value"] > 0 and out["cores"] >= 1
     assert isinstance(out["sample"], str) and out["sample"]
+
+
+def test_gap_summary_splits_step_boundaries(tmp_path):
+    """Idle time of the last rollout of a kernel trace: a gap after a
+    prune_kernel is a step boundary, every other gap is inside a step;
+    overlapping kernels count once toward busy time."""
+    import csv
+    rows = [("init_weights_kernel", 0, 10),
+            ("prefill_pages_kernel", 100, 110), ("embed_kernel", 115, 120), ("prune_kernel", 120, 130),
+            ("embed_norm_kernel", 180, 200), ("gemm_a", 205, 300), ("gemm_b", 250, 280),
+            ("prune_kernel", 300, 310), ("copyBuffer", 320, 325), ("embed_norm_kernel", 400, 410),
+            ("prune_kernel", 410, 420)]
+    p = tmp_path / "kernel_trace.csv"
+    with open(p, "w", newline="") as f:
+        w = csv.writer(f)
+        w.writerow(["Kernel_Name", "Start_Timestamp", "End_Timestamp"])
+        for n, s, e in rows:
+            w.writerow([n, s, e])
+    out = bench.summarize_gaps(str(p))
+    # boundaries: 130..180 and 310..320..325..400 (a copy after the selection)
+    assert out["kernels"] == 10 and out["prune_launches"] == 3
+    assert out["step_boundary_idle_s"] == pytest.approx(135e-9)
+    assert out["intra_step_idle_s"] == pytest.approx(10e-9)
+    assert out["span_s"] == pytest.approx(320e-9) and out["busy_s"] == pytest.approx(175e-9)
+    assert out["idle_s"] == pytest.approx(145e-9)
