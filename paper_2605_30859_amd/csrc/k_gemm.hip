@@ -255,7 +255,19 @@ __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_grouped_kernel(
     const int32_t* __restrict__ n_mtiles, int nt, const int32_t* __restrict__ arow) {
   const int total = n_mtiles[0] * nt;
   constexpr int esz = (EPI == EPI_F32 || EPI == EPI_ADD_F32) ? 4 : 2;
-  for (int it = blockIdx.x; it < total; it += gridDim.x) {
+  // Items are (row tile, column tile) in row-tile order.  With gathered A
+  // rows, each XCD takes one contiguous eighth of the items (blocks are dealt
+  // to the 8 XCDs round robin, block b on XCD b % 8), so the column tiles of
+  // one expert row tile run on one XCD and find its gathered input rows in
+  // that XCD's L2; the grid is a multiple of 8 blocks and the eighths
+  // partition [0, total).  Otherwise items go to blocks round robin (the
+  // down projection measured no gain from the XCD split).
+  const bool by_xcd = arow != nullptr;
+  const int chunk = (total + 7) >> 3;
+  const int lo = by_xcd ? (int)(blockIdx.x & 7) * chunk : 0;
+  const int hi = by_xcd ? min(total, lo + chunk) : total;
+  const int step = by_xcd ? (int)(gridDim.x >> 3) : (int)gridDim.x;
+  for (int it = by_xcd ? lo + (int)(blockIdx.x >> 3) : (int)blockIdx.x; it < hi; it += step) {
     const int mt = mtiles[it / nt], ni = it % nt;
     const int e = mt >> 16, mi = mt & 0xffff;
     const int cnt = g_cnt[e];
@@ -686,6 +698,7 @@ static hipError_t grouped_launch(const void* A, int lda, const void* W, int64_t 
     (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     attr_done = true;
   }
+  static_assert((kCus * BPC) % 8 == 0, "the grouped kernel deals items to 8 XCDs");
   hipLaunchKernelGGL(kern, dim3(kCus * BPC), dim3(256), lds, st, (const bf16_t*)A, lda, (const bf16_t*)W,
                      w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, nt, arow);
   return hipGetLastError();
