@@ -726,6 +726,9 @@ def main():
                     help="print the GEMM MFMA utilisation (JSON) of a rocprofv3 --pmc run in DIR")
     ap.add_argument("--summarize-stats", metavar="CSV",
                     help="print a markdown table of a rocprofv3 kernel_stats.csv")
+    ap.add_argument("--step-log", metavar="JSONL",
+                    help="write the last timed rollout's per-step metrics (live rows, device ms) "
+                         "to this file, one JSON object a line")
     ap.add_argument("--gemm-compare", action="store_true",
                     help="time the library's GEMM against torch linear (hipBLASLt) on the decode "
                          "projections, weights cold; print a markdown table")
@@ -845,6 +848,13 @@ def main():
     # rollout cost model (Eq. 4) on this engine: PTL fitted to the last timed
     # rollout's per-step (live rows, device ms) samples
     rows, sms, pf_ms = ro.step_times()
+    if args.step_log:
+        # per-step metrics of the last timed rollout, one JSON object a line
+        with open(args.step_log, "w") as f:
+            f.write(json.dumps({"phase": "prefill", "device_ms": float(pf_ms)}) + "\n")
+            for i, (nr, ms) in enumerate(zip(rows.tolist(), sms.tolist())):
+                f.write(json.dumps({"phase": "decode", "step": i + 1, "live_rows": int(nr),
+                                    "device_ms": float(ms)}) + "\n")
     lens = ro.traj_scores()[0].cpu().numpy()
     ptl = B.darts_fit_ptl(rows, sms.astype(np.float64))
     eq4 = B.darts_rollout_cost(np.maximum(lens[lens > 0] - 1, 0), ptl)
