@@ -95,7 +95,24 @@ typedef struct {
   int32_t dtype;         /* darts_dtype: F32 (all fp32) or BF16 (bf16 operands,
                             fp32 accumulation and residual stream) */
   uint64_t weight_seed;
+  const void* const* weights;  /* NULL: every tensor is generated from weight_seed.
+     Otherwise darts_weight_count() device pointers, caller-owned, one per tensor
+     in this order, each a row-major [rows][cols] array in the model's dtype (fp32,
+     or bf16 bits for DARTS_BF16):
+       embed [V][d], lm_head [V][d], then for every layer
+         wq [hq*hd][d], wk [hkv*hd][d], wv [hkv*hd][d], wo [d][hq*hd], and
+         dense:  w_gate [F][d], w_up [F][d], w_down [d][F]
+         MoE:    router [E][d], expert_gate [E][Fe][d], expert_up [E][Fe][d],
+                 expert_down [E][d][Fe]
+     (the same tensors and layout the generated weights follow; ffn out = w_down
+     (silu(w_gate x) * (w_up x))).  darts_init copies them into the context's own
+     layout (fused QKV rows, gate/up rows interleaved for the SwiGLU epilogue) and
+     keeps no reference: the caller may free them once darts_init returns. */
 } darts_model_cfg;
+
+/* Number of tensors in darts_model_cfg.weights for this model: 2 + n_layers *
+ * (7 dense, 8 MoE).  0 for a null model.                                    */
+int32_t darts_weight_count(const darts_model_cfg* model);
 
 /* One rollout batch.  m and k are passed to darts_init separately.          */
 typedef struct {
@@ -176,14 +193,15 @@ typedef struct darts_ctx darts_ctx;
 
 /* ---------------------------------------------------------------- stateful */
 
-/* Allocate a context: generated weights, paged KV pool (page = 16 tokens,
+/* Allocate a context: weights generated from the seed or copied from the
+ * caller's (model->weights), paged KV pool (page = 16 tokens,
  * one pool per layer, prompt pages shared by the prompt's m trajectories),
  * page tables, per-trajectory state and scratch, all owned by the context.
  * m = M'_i (uniform), k = M (paper Tab. 1).  Errors: DARTS_EINVAL if k < 1,
  * k > m, m > 64, L < 1 or L >= k, prompt_len % 16 != 0, cap out of range,
  * unsupported head_dim, or GEMM dimensions that are not multiples of 64/128
- * for BF16; DARTS_ENOMEM if device memory is short.  *out is written only
- * on success.                                                              */
+ * for BF16, a null entry in model->weights; DARTS_ENOMEM if device memory
+ * is short.  *out is written only on success.                              */
 int darts_init(const darts_model_cfg* model, int32_t m, int32_t k,
                const darts_run_cfg* run, darts_ctx** out);
 

@@ -27,7 +27,7 @@ class ModelCfg(C.Structure):
                 ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("ffn_dim", C.c_int32),
                 ("vocab", C.c_int32), ("n_experts", C.c_int32), ("top_k", C.c_int32),
                 ("expert_ffn", C.c_int32), ("rope_theta", C.c_float), ("rms_eps", C.c_float),
-                ("dtype", C.c_int32), ("weight_seed", C.c_uint64)]
+                ("dtype", C.c_int32), ("weight_seed", C.c_uint64), ("weights", C.c_void_p)]
 
 
 class RunCfg(C.Structure):
@@ -65,6 +65,7 @@ _SIGS = {
     "darts_get_traj_scores": (C.c_int, [_P, _P, _P, _P, _P]),
     "darts_debug_logits": (C.c_int, [_P, _P, C.POINTER(C.c_int32)]),
     "darts_destroy": (C.c_int, [_P]),
+    "darts_weight_count": (C.c_int32, [C.POINTER(ModelCfg)]),
     "darts_debug_moe_routing": (C.c_int, [_P, _P, _P, _P, C.c_int64]),
     "darts_reset": (C.c_int, [_P]),
     "darts_set_plan": (C.c_int, [_P, _P]),
@@ -331,11 +332,27 @@ def darts_fit_ptl(bsz, lat):
 
 
 # ---------------------------------------------------------------- stateful
-def model_cfg_struct(model):
+def model_cfg_struct(model, weights=None):
+    """weights: None, or a ctypes array of device pointers (weight_pointer_array)."""
     return ModelCfg(model.n_layers, model.d_model, model.n_q_heads, model.n_kv_heads,
                     model.head_dim, model.ffn_dim, model.vocab, model.n_experts, model.top_k,
                     model.expert_ffn, model.rope_theta, model.rms_eps,
-                    DARTS_BF16 if model.dtype == "bf16" else DARTS_F32, model.weight_seed)
+                    DARTS_BF16 if model.dtype == "bf16" else DARTS_F32, model.weight_seed,
+                    C.cast(weights, C.c_void_p) if weights is not None else None)
+
+
+def weight_pointer_array(tensors):
+    """ctypes array of the data pointers of caller weight tensors (device
+    tensors in the order darts_model_cfg.weights documents)."""
+    arr = (C.c_void_p * len(tensors))()
+    for i, t in enumerate(tensors):
+        arr[i] = t.data_ptr()
+    return arr
+
+
+def darts_weight_count(model):
+    mc = model_cfg_struct(model)
+    return int(load_library().darts_weight_count(C.byref(mc)))
 
 
 def run_cfg_struct(run, stream, flags=0, page_perm_seed=0, kv_pool_bytes=None, traj_base=0):
@@ -349,7 +366,11 @@ class Rollout:
     darts_decode_step / darts_select_and_prune).  Output buffers are torch
     tensors on the current device; PyTorch only allocates them."""
 
-    def __init__(self, model, run, flags=0, page_perm_seed=0, kv_pool_bytes=None, stream=None, traj_base=0):
+    def __init__(self, model, run, flags=0, page_perm_seed=0, kv_pool_bytes=None, stream=None, traj_base=0,
+                 weights=None):
+        """weights: None (generated from model.weight_seed) or the caller's
+        device tensors in the order of darts_model_cfg.weights; the library
+        copies them during darts_init."""
         import torch
         self.torch = torch
         self.lib = load_library()
@@ -357,10 +378,12 @@ class Rollout:
         self.m, self.k = run.m, run.k
         self.n_traj = run.n_prompts * run.m
         self.stream = stream or torch.cuda.current_stream()
-        self._mc = model_cfg_struct(model)
+        w_arr = weight_pointer_array(weights) if weights is not None else None
+        self._mc = model_cfg_struct(model, w_arr)
         self._rc = run_cfg_struct(run, self.stream.cuda_stream, flags, page_perm_seed, kv_pool_bytes, traj_base)
         ctx = C.c_void_p()
         _check(self.lib.darts_init(C.byref(self._mc), run.m, run.k, C.byref(self._rc), C.byref(ctx)))
+        self._mc.weights = None   # the library copied the tensors and keeps no reference
         self.ctx = ctx
         dev = torch.device("cuda", torch.cuda.current_device())
         n = self.n_traj

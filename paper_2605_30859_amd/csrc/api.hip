@@ -280,6 +280,46 @@ static int init_weights(darts_ctx* c) {
   return DARTS_OK;
 }
 
+// The caller's tensors (model->weights, in the order darts_weight_count
+// documents) copied into the same physical layout init_weights generates.
+static int copy_weights(darts_ctx* c) {
+  const int d = c->d, hq = c->hq, hkv = c->hkv, hd = c->hd, F = c->F, V = c->V;
+  const bool b = c->bf16;
+  const void* const* src = c->mc.weights;
+  int t = 0;
+  HIPCHK(c, launch_copy_rows(c->embed, src[t++], b, V, d, rowmap_plain(V, 0), c->st));
+  HIPCHK(c, launch_copy_rows(c->lm_head, src[t++], b, V, d, rowmap_plain(V, 0), c->st));
+  for (int l = 0; l < c->nl; ++l) {
+    LayerW& w = c->layers[l];
+    HIPCHK(c, launch_copy_rows(w.wqkv, src[t++], b, (int64_t)hq * hd, d, rowmap_plain(hq * hd, 0), c->st));
+    HIPCHK(c, launch_copy_rows(w.wqkv, src[t++], b, (int64_t)hkv * hd, d, rowmap_plain(hkv * hd, hq * hd),
+                               c->st));
+    HIPCHK(c, launch_copy_rows(w.wqkv, src[t++], b, (int64_t)hkv * hd, d,
+                               rowmap_plain(hkv * hd, (hq + hkv) * hd), c->st));
+    HIPCHK(c, launch_copy_rows(w.wo, src[t++], b, d, (int64_t)hq * hd, rowmap_plain(d, 0), c->st));
+    if (c->moe) {
+      const int E = c->E, Fe = c->Fe;
+      HIPCHK(c, launch_copy_rows(w.wrouter, src[t++], b, E, d, rowmap_plain(E, 0), c->st));
+      if (c->Epad > E)   // padding rows of the router: zero logits, never selected
+        HIPCHK(c, hipMemsetAsync((char*)w.wrouter + (size_t)E * d * c->esz, 0,
+                                 (size_t)(c->Epad - E) * d * c->esz, c->st));
+      RowMap eg{Fe, 2 * (int64_t)Fe, 16, 32, 0}, eu{Fe, 2 * (int64_t)Fe, 16, 32, 16};
+      HIPCHK(c, launch_copy_rows(w.wegu, src[t++], b, (int64_t)E * Fe, d, eg, c->st));
+      HIPCHK(c, launch_copy_rows(w.wegu, src[t++], b, (int64_t)E * Fe, d, eu, c->st));
+      HIPCHK(c, launch_copy_rows(w.wedown, src[t++], b, (int64_t)E * d, Fe, rowmap_plain((int64_t)E * d, 0),
+                                 c->st));
+      continue;
+    }
+    RowMap gate{F, 0, 16, 32, 0}, up{F, 0, 16, 32, 16};
+    HIPCHK(c, launch_copy_rows(w.wgu, src[t++], b, F, d, gate, c->st));
+    HIPCHK(c, launch_copy_rows(w.wgu, src[t++], b, F, d, up, c->st));
+    HIPCHK(c, launch_copy_rows(w.wdown, src[t++], b, d, F, rowmap_plain(d, 0), c->st));
+  }
+  // the copies are complete before darts_init returns (it synchronises the
+  // stream), after which the context keeps no reference to the caller's array
+  return DARTS_OK;
+}
+
 static size_t gemm_ws_need(const darts_ctx* c) {
   // every row count a launch can see: decode batches 1..n_traj, the prefill
   // (P*Lp rows) and the prefill's LM head (P rows)
@@ -338,6 +378,11 @@ static hipError_t upload_plan(darts_ctx* c) {
   return e;
 }
 
+int32_t darts_weight_count(const darts_model_cfg* model) {
+  if (!model || model->n_layers < 1) return 0;
+  return 2 + model->n_layers * (model->n_experts > 0 ? 8 : 7);
+}
+
 int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_run_cfg* run,
                darts_ctx** out) {
   if (!model || !run || !out) return DARTS_EINVAL;
@@ -376,6 +421,11 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
   }
   const int64_t n_traj64 = (int64_t)rc.n_prompts * m;
   if (n_traj64 > 65536 || (int64_t)rc.n_prompts * rc.prompt_len > (1 << 22)) return DARTS_EINVAL;
+  if (mc.weights) {
+    const int32_t nw = darts_weight_count(&mc);
+    for (int32_t i = 0; i < nw; ++i)
+      if (!mc.weights[i]) return DARTS_EINVAL;
+  }
 
   darts_ctx* c = new (std::nothrow) darts_ctx();
   if (!c) return DARTS_ENOMEM;
@@ -520,7 +570,7 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
   }
   int rcode = DARTS_OK;
   if (e != hipSuccess) rcode = fail_hip(c, e, "upload index tables");
-  if (rcode == DARTS_OK) rcode = init_weights(c);
+  if (rcode == DARTS_OK) rcode = c->mc.weights ? copy_weights(c) : init_weights(c);
   if (rcode == DARTS_OK) {
     e = launch_rope_table(c->rope, max_pos, c->hd, (double)mc.rope_theta, c->st);
     if (e == hipSuccess)
@@ -548,6 +598,7 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
     return rcode;
   }
   c->free_top = (int)n_pages;
+  c->mc.weights = nullptr;   // the caller's array is not referenced after init
   *out = c;
   return DARTS_OK;
 }

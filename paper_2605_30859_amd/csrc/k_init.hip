@@ -62,6 +62,34 @@ hipError_t launch_init_weights(void* dst, bool bf16, int64_t n_out, int64_t n_in
   return hipGetLastError();
 }
 
+// One thread per element of the logical [n_out][n_in] tensor (grid stride);
+// the copy is made once, when a context takes the caller's weights.
+template <typename T>
+__global__ void copy_rows_kernel(T* __restrict__ dst, const T* __restrict__ src, int64_t n_out,
+                                 int64_t n_in, RowMap map) {
+  const int64_t total = n_out * n_in;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = idx / n_in, c = idx % n_in;
+    dst[map_row(map, r) * n_in + c] = src[idx];
+  }
+}
+
+hipError_t launch_copy_rows(void* dst, const void* src, bool bf16, int64_t n_out, int64_t n_in, RowMap map,
+                            hipStream_t st) {
+  const int64_t total = n_out * n_in;
+  if (total <= 0) return hipSuccess;
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  if (bf16)
+    hipLaunchKernelGGL(copy_rows_kernel<bf16_t>, dim3((unsigned)blocks), dim3(256), 0, st, (bf16_t*)dst,
+                       (const bf16_t*)src, n_out, n_in, map);
+  else
+    hipLaunchKernelGGL(copy_rows_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st, (float*)dst,
+                       (const float*)src, n_out, n_in, map);
+  return hipGetLastError();
+}
+
 // table[p][i] = (cos(p * theta^(-2i/hd)), sin(...)) evaluated in float64.
 __global__ void rope_table_kernel(float2* table, int max_pos, int half, int hd, double theta) {
   const int64_t n = (int64_t)max_pos * half;

@@ -17,6 +17,10 @@ RowMap rowmap_plain(int64_t n_out, int64_t row_off);
 hipError_t launch_init_weights(void* dst, bool bf16, int64_t n_out, int64_t n_in, int64_t fan_in,
                                uint32_t tensor_id, uint32_t layer, uint64_t seed, RowMap map,
                                hipStream_t st);
+// Copy a caller's row-major logical [n_out][n_in] tensor (fp32 or bf16) into
+// its physical rows under map.
+hipError_t launch_copy_rows(void* dst, const void* src, bool bf16, int64_t n_out, int64_t n_in, RowMap map,
+                            hipStream_t st);
 hipError_t launch_rope_table(float2* table, int max_pos, int hd, double theta, hipStream_t st);
 // streaming read (HBM read-rate reference): kStreamReadBlocks x 256 threads,
 // one float per wavefront written to sink

@@ -64,3 +64,27 @@ def test_invalid_config_rejected_before_any_device_call(lib_path):
     rc.prompt_len = 17
     assert lib.darts_init(ctypes.byref(mc), 8, 4, ctypes.byref(rc), ctypes.byref(ctx)) == binding.DARTS_EINVAL
     assert not ctx.value
+
+
+def test_caller_weights_count_and_null_entry_rejected(lib_path):
+    """darts_weight_count: 2 + n_layers * (7 dense, 8 MoE); a caller weight
+    array with a null entry is rejected by host validation, before any device
+    call, and *out stays untouched."""
+    from paper_2605_30859_amd import binding
+    from workload import get_config
+    lib = binding.load_library()
+    for name, per_layer in (("tiny", 7), ("dense-small", 7), ("qwen3-30b-a3b", 8)):
+        model, _ = get_config(name)
+        assert binding.darts_weight_count(model) == 2 + model.n_layers * per_layer
+    assert lib.darts_weight_count(None) == 0
+    model, run = get_config("tiny")
+    n = binding.darts_weight_count(model)
+    arr = (ctypes.c_void_p * n)()
+    for i in range(n):
+        arr[i] = 0x1000 * (i + 1)        # never dereferenced: entry 3 is null
+    arr[3] = None
+    mc = binding.model_cfg_struct(model, arr)
+    rc = binding.run_cfg_struct(run, None)
+    ctx = ctypes.c_void_p()
+    assert lib.darts_init(ctypes.byref(mc), run.m, run.k, ctypes.byref(rc), ctypes.byref(ctx)) == binding.DARTS_EINVAL
+    assert not ctx.value
