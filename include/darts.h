@@ -200,7 +200,8 @@ typedef struct darts_ctx darts_ctx;
  * m = M'_i (uniform), k = M (paper Tab. 1).  Errors: DARTS_EINVAL if k < 1,
  * k > m, m > 64, L < 1 or L >= k, prompt_len % 16 != 0, cap out of range,
  * unsupported head_dim, or GEMM dimensions that are not multiples of 64/128
- * for BF16, a null entry in model->weights; DARTS_ENOMEM if device memory
+ * for BF16, a null entry in model->weights or one that does not point into
+ * a device allocation of at least its size; DARTS_ENOMEM if device memory
  * is short.  *out is written only on success.                              */
 int darts_init(const darts_model_cfg* model, int32_t m, int32_t k,
                const darts_run_cfg* run, darts_ctx** out);

@@ -378,6 +378,23 @@ static hipError_t upload_plan(darts_ctx* c) {
   return e;
 }
 
+// Bytes of caller weight tensor i (the order of darts_model_cfg.weights).
+static int64_t caller_weight_bytes(const darts_model_cfg& mc, int32_t i) {
+  const int64_t d = mc.d_model, V = mc.vocab, qd = (int64_t)mc.n_q_heads * mc.head_dim,
+                kvd = (int64_t)mc.n_kv_heads * mc.head_dim, F = mc.ffn_dim, E = mc.n_experts,
+                Fe = mc.expert_ffn;
+  const int64_t esz = mc.dtype == DARTS_BF16 ? 2 : 4;
+  if (i < 2) return V * d * esz;                        // embed, lm_head
+  const int per = mc.n_experts > 0 ? 8 : 7, j = (i - 2) % per;
+  int64_t n;
+  if (j == 0) n = qd * d;                               // wq
+  else if (j <= 2) n = kvd * d;                         // wk, wv
+  else if (j == 3) n = d * qd;                          // wo
+  else if (mc.n_experts > 0) n = j == 4 ? E * d : E * Fe * d;   // router; expert gate, up, down
+  else n = F * d;                                       // w_gate, w_up, w_down
+  return n * esz;
+}
+
 int32_t darts_weight_count(const darts_model_cfg* model) {
   if (!model || model->n_layers < 1) return 0;
   return 2 + model->n_layers * (model->n_experts > 0 ? 8 : 7);
@@ -452,6 +469,21 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
 
   size_t free_b = 0, total_b = 0;
   if (hipMemGetInfo(&free_b, &total_b) != hipSuccess) { delete c; return DARTS_EHIP; }
+  if (mc.weights) {
+    // every caller tensor must lie inside one device allocation of at least
+    // its size, so the copy never reads past the caller's memory
+    const int32_t nw = darts_weight_count(&mc);
+    for (int32_t i = 0; i < nw; ++i) {
+      void* base = nullptr;
+      size_t size = 0;
+      if (hipMemGetAddressRange(&base, &size, const_cast<void*>(mc.weights[i])) != hipSuccess ||
+          (const char*)mc.weights[i] + caller_weight_bytes(mc, i) > (const char*)base + size) {
+        (void)hipGetLastError();
+        delete c;
+        return DARTS_EINVAL;
+      }
+    }
+  }
   const int rows_pf = c->P * c->Lp;
   const int rows_max = std::max(rows_pf, c->n_traj);
   const size_t ffn_elems = moe ? (size_t)c->E * c->d + (size_t)3 * c->E * c->Fe * c->d

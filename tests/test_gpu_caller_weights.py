@@ -96,3 +96,27 @@ def test_caller_weights_moe_bf16():
     run = replace(run, n_prompts=2, prompt_len=32, m=8, k=4, cap=24, len_median=10.0, len_tail=False,
                   kv_pool_gb=0.0)
     _check(model, run, "moe-small")
+
+
+def test_caller_weight_outside_device_memory_rejected():
+    """An entry that is not inside a device allocation (here a host buffer)
+    is rejected with DARTS_EINVAL before anything is copied."""
+    import ctypes
+    from paper_2605_30859_amd import binding as B
+    lib = B.load_library()
+    model, run = get_config("tiny")
+    W = OM.init_weights(model)
+    ts = _weights_on_device(model, W)
+    host = np.zeros(ts[5].numel(), dtype=np.float32)
+    arr = B.weight_pointer_array(ts)
+    arr[5] = host.ctypes.data
+    mc = B.model_cfg_struct(model, arr)
+    rc = B.run_cfg_struct(run, torch.cuda.current_stream().cuda_stream)
+    ctx = ctypes.c_void_p()
+    st = lib.darts_init(ctypes.byref(mc), run.m, run.k, ctypes.byref(rc), ctypes.byref(ctx))
+    assert st == B.DARTS_EINVAL and not ctx.value
+    # the same tensors with the device entry back in place are accepted
+    arr[5] = ts[5].data_ptr()
+    mc = B.model_cfg_struct(model, arr)
+    assert lib.darts_init(ctypes.byref(mc), run.m, run.k, ctypes.byref(rc), ctypes.byref(ctx)) == B.DARTS_OK
+    assert lib.darts_destroy(ctx) == B.DARTS_OK
