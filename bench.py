@@ -274,6 +274,62 @@ def gemm_compare(B, reps=12):
     return "\n".join(lines)
 
 
+def launch_gap(B, n=1000, reps=3):
+    """GPU time per kernel of a chain of n dependent one-block launches (the
+    library's fill kernel over 1024 floats), launched one by one on a stream
+    and replayed from a captured HIP graph.  Four 8 GiB streaming reads are
+    queued first each time, so the host has queued the whole chain before the
+    GPU reaches it and the figure is the device-side cost of a launch, not the
+    host's launch rate.  Every graph replay's output is checked against the
+    same fill done eagerly."""
+    import torch
+    s = torch.cuda.Stream()
+    big = torch.zeros(8 << 30, dtype=torch.uint8, device="cuda")
+    sink = torch.empty(8192, dtype=torch.float32, device="cuda")
+    tiny = torch.zeros(1024, dtype=torch.float32, device="cuda")
+    ref = torch.empty_like(tiny)
+    out = {"chain": n}
+    with torch.cuda.stream(s):
+        B.darts_fill_uniform(ref, 7, 11, B.DARTS_F32)
+
+        def fill_chain():
+            for i in range(n):
+                B.darts_fill_uniform(tiny, 7, 11, B.DARTS_F32)
+
+        def timed(run):
+            best = []
+            for _ in range(reps):
+                for _ in range(4):
+                    B.darts_stream_read(big, sink)
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(s)
+                run()
+                e1.record(s)
+                s.synchronize()
+                best.append(e0.elapsed_time(e1) * 1e3 / n)
+            return min(best)
+
+        out["stream_us_per_launch"] = timed(fill_chain)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            fill_chain()
+        ok = True
+
+        def replay():
+            g.replay()
+
+        out["graph_us_per_launch"] = timed(replay)
+        for _ in range(3):
+            tiny.zero_()
+            g.replay()
+            s.synchronize()
+            ok = ok and bool(torch.equal(tiny, ref))
+        out["graph_replays_match_eager"] = ok
+    del big
+    torch.cuda.empty_cache()
+    return out
+
+
 def kernel_sweep(B, steps, warmup):
     """Stateless kernels on the sweep's inputs (bf16, data seed 1): decode
     attention over 1024 trajectories with lognormal(1500, 1.0) contexts clipped
@@ -729,6 +785,9 @@ def main():
     ap.add_argument("--step-log", metavar="JSONL",
                     help="write the last timed rollout's per-step metrics (live rows, device ms) "
                          "to this file, one JSON object a line")
+    ap.add_argument("--launch-gap", action="store_true",
+                    help="device-side cost per launch of a chain of dependent one-block kernels, "
+                         "stream launches against a replayed HIP graph (JSON)")
     ap.add_argument("--gemm-compare", action="store_true",
                     help="time the library's GEMM against torch linear (hipBLASLt) on the decode "
                          "projections, weights cold; print a markdown table")
@@ -775,6 +834,9 @@ def main():
         return
     if args.gemm_compare:
         print(gemm_compare(B), flush=True)
+        return
+    if args.launch_gap:
+        print(json.dumps(launch_gap(B)), flush=True)
         return
     model, run = get_config(args.config)
     if args.next:
