@@ -434,12 +434,22 @@ def test_selection_sweep(mode):
     mean log-probs on a 2^-10 grid (exact ties): kept sets and statuses
     bit-exact, and the page ids the completed groups free (ceil(len/16) per
     trajectory from a shuffled pool) bit-exact in order and count."""
+    _selection_case(mode, SWEEP["sel_m"], SWEEP["sel_k"], 1, None)
+
+
+@pytest.mark.parametrize("mode", ["short_mid", "dual_mid", "dual_final"])
+def test_selection_full_wavefront_groups(mode):
+    """Groups of the largest size, m = 64 (one full wavefront per group),
+    k = 32, L = 3; 16384 trajectories: the same bit-exact checks."""
+    _selection_case(mode, 64, 32, 3, 16384)
+
+
+def _selection_case(mode, m, k, L, n_traj):
     B = _b()
-    say(f"selection sweep {mode}")
-    raw, mlp = sweep_selection_inputs()
+    say(f"selection {mode}, m {m}, k {k}, L {L}")
+    raw, mlp = sweep_selection_inputs(n=n_traj)
     cap = SWEEP["sel_cap"]
-    m, k, L = SWEEP["sel_m"], SWEEP["sel_k"], 1
-    m_up = 16 if mode.startswith("short") or mode.startswith("no_abort") else 17
+    m_up = m if mode.startswith("short") or mode.startswith("no_abort") else m + 1
     early = 0 if mode.startswith("no_abort") else 1
     length = np.minimum(raw, cap).astype(np.int32)
     trunc = raw > cap
@@ -448,8 +458,12 @@ def test_selection_sweep(mode):
     elif m_up <= m and early:
         s = int(np.median(length))
     else:
-        # modes that wait for every member: a step at which about half the groups are done
-        s = int(np.median(length.reshape(-1, m).max(axis=1)))
+        # modes that wait for every member: a step at which about half the
+        # groups are done (a quarter when half of the groups reach the cap)
+        gmax = length.reshape(-1, m).max(axis=1)
+        s = int(np.median(gmax))
+        if s >= cap:
+            s = int(np.percentile(gmax, 25))
     status = np.where(length <= s, np.where(trunc, TRUNC, EOS), LIVE).astype(np.uint8)
     cur_len = np.minimum(length, s).astype(np.int32)
     kept_ref, st_ref = _oracle_select(status, cur_len, mlp, m, k, L, m_up, early)
@@ -482,7 +496,7 @@ def test_selection_sweep(mode):
     want = np.array(reclaimed_pages(lists, set(kept_ref), m), dtype=np.int32)
     nf = int(nfree_d.item())
     free = free_d.cpu().numpy()
-    say(f"selection sweep {mode}: {len(kept_ref)} groups complete, {nf} of {len(pages)} page ids reclaimed")
+    say(f"selection {mode} m {m}: {len(kept_ref)} groups complete, {nf} of {len(pages)} page ids reclaimed")
     assert nf == len(want) and np.array_equal(free[:nf], want) and (free[nf:] == -1).all()
 
 

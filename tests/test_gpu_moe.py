@@ -96,6 +96,51 @@ def test_moe_small_teacher_forced():
     assert got["stats"]["steps"] == ref.steps and got["stats"]["pages_used"] == 0
 
 
+@pytest.mark.parametrize("E,top_k", [(8, 1), (8, 8)])
+def test_moe_routing_extremes_teacher_forced(E, top_k):
+    """The two ends of the routing: top-1 (one expert per token, weight 1
+    after renormalisation) and top-k = E (every expert takes every row, the
+    weights are the whole softmax; 8 of the router's 128 padded rows are
+    real).  bf16 MoE against the oracle under teacher forcing, as in the
+    reduced test: logits within 2e-2 of the row max wherever the routing is
+    at least 1e-3 from a top-k tie (with k = E there is no decision to tie,
+    so every row is compared)."""
+    model = ModelCfg(f"moe-e{E}-k{top_k}", 2, 256, 4, 2, 64, 0, 512, "bf16", 23, rope_theta=1e6,
+                     n_experts=E, top_k=top_k, expert_ffn=256)
+    _, run = get_config("qwen3-30b-a3b")
+    run = replace(run, n_prompts=2, prompt_len=32, m=8, k=4, cap=20, len_median=10.0, len_tail=False,
+                  kv_pool_gb=0.0)
+    prompts, forced = rollout_inputs(model, run)
+    say(f"moe E={E} top-{top_k}: oracle")
+    W = OM.init_weights(model)
+    ref = rollout(model, W, prompts, forced, run.m, run.k, run.cap, run.sample_seed, keep_logits=True)
+    say(f"moe E={E} top-{top_k}: GPU")
+    got = _run_gpu(model, run, prompts, forced, force_tokens=ref.tokens, keep_logits=True)
+    checked = excused = 0
+    worst = 0.0
+    for s, rec in enumerate(got["steps"]):
+        for r, g in enumerate(rec["traj"]):
+            g = int(g)
+            if ref.route_margins[g][s] < 1e-3:
+                excused += 1
+                continue
+            row = r if s > 0 else g // run.m
+            lg, lr = rec["logits"][row], ref.logits[g][s]
+            dz = np.max(np.abs(lg - lr))
+            scale = np.max(np.abs(lr))
+            worst = max(worst, dz / scale)
+            assert dz <= 2e-2 * scale, (s, g, dz / scale)
+            checked += 1
+    say(f"moe E={E} top-{top_k}: {checked} rows checked, {excused} near-tie routing rows excused, "
+        f"worst {worst:.2e}")
+    if top_k == E:
+        assert excused == 0
+    assert checked > 0.5 * (checked + excused)
+    for i in range(run.n_prompts):
+        assert got["done"][i] == ref.done_step[i]
+    assert got["stats"]["steps"] == ref.steps and got["stats"]["pages_used"] == 0
+
+
 def test_moe_full_size_schedule():
     """Qwen3-30B-A3B shape (48 layers, d 2048, 32/4 heads, 128 experts top-8,
     expert FFN 768, vocab 151936; 64 prompts x 512, m 16, k 8, cap 16384):
