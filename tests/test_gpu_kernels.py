@@ -308,6 +308,8 @@ def test_attention_small_ragged(dtype, hq, hkv, hd):
     (96, 16, 4, 64, 1500),
     (80, 8, 8, 128, 33),        # G = 1
     (72, 8, 2, 32, 600),
+    (256, 32, 4, 128, 1500),    # the MoE shape's heads (G = 8), double-buffered
+    (20, 32, 4, 128, 3001),     # G = 8, few rows: context chunks and combine
 ])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_attention_equal_contexts(rows, hq, hkv, hd, ctx, dtype):
