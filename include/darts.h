@@ -302,6 +302,14 @@ int darts_get_traj_scores(darts_ctx* ctx, int32_t* d_len, float* d_sum_lp, float
  * the last darts_step_out) into d_dst.  For verification.                  */
 int darts_debug_logits(darts_ctx* ctx, float* d_dst, int32_t* h_n_rows);
 
+/* Set every byte of the context's key and value pools to `byte` (0..255;
+ * 0xff makes every element a NaN), as memory left by earlier work might
+ * hold.  For verification that no result depends on pool contents the
+ * rollout has not written itself.  Synchronises the stream.  Errors:
+ * DARTS_ESTATE unless called after darts_init or darts_reset and before
+ * darts_prefill; DARTS_EINVAL for a byte outside 0..255.                   */
+int darts_debug_fill_kv(darts_ctx* ctx, int32_t byte);
+
 /* Verification of mixture-of-experts routing (MoE models only).  Until the
  * next call, every prefill and decode step reads and writes, for each of its
  * rows and each layer l, entries [key][l][0..top_k) of these device buffers
@@ -430,6 +438,9 @@ size_t darts_attn_workspace_bytes(int32_t n_rows, int32_t n_q_heads, int32_t n_k
  *                 device-built list, and from 64 rows each wavefront keeps
  *                 two page pairs in flight).
  *   d_workspace   darts_attn_workspace_bytes(...) bytes, 256-byte aligned
+ * In bf16 the value slots of a row's last page at or past ctx_len[r] take
+ * part in the P.V product with weight 0, so they must hold finite values
+ * (the context's own decode appends clear them when they open a page).
  */
 int darts_attn_decode(const void* d_q, const void* d_k_pool, const void* d_v_pool,
                       int64_t n_pages, const int32_t* d_page_table, int32_t pt_stride,

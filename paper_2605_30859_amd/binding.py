@@ -67,6 +67,7 @@ _SIGS = {
     "darts_destroy": (C.c_int, [_P]),
     "darts_weight_count": (C.c_int32, [C.POINTER(ModelCfg)]),
     "darts_debug_moe_routing": (C.c_int, [_P, _P, _P, _P, C.c_int64]),
+    "darts_debug_fill_kv": (C.c_int, [_P, C.c_int32]),
     "darts_reset": (C.c_int, [_P]),
     "darts_set_plan": (C.c_int, [_P, _P]),
     "darts_prompt_length_std": (C.c_int, [_P, _P, C.c_int32, C.c_int32, _P]),
@@ -506,6 +507,10 @@ class Rollout:
         n_keys = ts[0].shape[0] if ts else 0
         _check(self.lib.darts_debug_moe_routing(self.ctx, _ptr(force_ids), _ptr(own_ids), _ptr(used_p),
                                                 n_keys), self.ctx)
+
+    def debug_fill_kv(self, byte):
+        """Set every byte of the KV pools (before prefill; 0xff = NaN everywhere)."""
+        _check(self.lib.darts_debug_fill_kv(self.ctx, int(byte)), self.ctx)
 
     def debug_logits(self, rows):
         t = self.torch

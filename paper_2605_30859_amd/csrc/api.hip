@@ -1095,6 +1095,17 @@ int darts_debug_logits(darts_ctx* c, float* d_dst, int32_t* h_n_rows) {
   return DARTS_OK;
 }
 
+int darts_debug_fill_kv(darts_ctx* c, int32_t byte) {
+  if (!c || byte < 0 || byte > 255) return DARTS_EINVAL;
+  if (c->poisoned) return DARTS_EHIP;
+  if (c->phase != 0) return DARTS_ESTATE;
+  const size_t bytes = (size_t)c->nl * c->pool_layer_elems * c->esz;
+  HIPCHK(c, hipMemsetAsync(c->kpool, byte, bytes, c->st));
+  HIPCHK(c, hipMemsetAsync(c->vpool, byte, bytes, c->st));
+  HIPCHK(c, hipStreamSynchronize(c->st));
+  return DARTS_OK;
+}
+
 int darts_debug_moe_routing(darts_ctx* c, const int32_t* d_force_ids, int32_t* d_own_ids,
                             float* d_used_p, int64_t n_keys) {
   if (!c) return DARTS_EINVAL;

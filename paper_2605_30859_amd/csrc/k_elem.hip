@@ -264,6 +264,19 @@ __global__ void rope_append_kernel(const float* __restrict__ qkv, int n_split, i
     const int64_t o = v_off(page, h, slot, dd, hkv, hd);
     if (BF16) ((bf16_t*)v_pool)[o] = f32_to_bf16(v);
     else ((float*)v_pool)[o] = v;
+    // A decode append that opens a page (slot 0; the row owns the page) also
+    // clears the page's later value slots.  Attention weighs keys at or past
+    // the row's context by 0 but still multiplies their values in the P.V
+    // product, so those slots must hold finite values, whatever the memory
+    // held before (0 x NaN is NaN).  Key slots need nothing: their scores
+    // are replaced, not multiplied.  A prefill writes whole pages itself.
+    if (pos_mod == 0 && slot == 0) {
+      for (int s2 = 1; s2 < kPage; ++s2) {
+        const int64_t o2 = v_off(page, h, s2, dd, hkv, hd);
+        if (BF16) ((bf16_t*)v_pool)[o2] = 0;
+        else ((float*)v_pool)[o2] = 0.f;
+      }
+    }
   }
 }
 

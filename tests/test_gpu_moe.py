@@ -23,10 +23,12 @@ def say(*a):
     print(*a, flush=True)
 
 
-def _run_gpu(model, run, prompts, forced, force_tokens=None, keep_logits=False):
+def _run_gpu(model, run, prompts, forced, force_tokens=None, keep_logits=False, kv_fill=None):
     from paper_2605_30859_amd import binding as B
     B.load_library()
     ro = B.Rollout(model, run)
+    if kv_fill is not None:
+        ro.debug_fill_kv(kv_fill)
     pr = torch.from_numpy(np.ascontiguousarray(prompts.reshape(-1))).to(DEV)
     fl = torch.from_numpy(forced.astype(np.int32)).to(DEV)
     steps = []
@@ -96,15 +98,19 @@ def test_moe_small_teacher_forced():
     assert got["stats"]["steps"] == ref.steps and got["stats"]["pages_used"] == 0
 
 
-@pytest.mark.parametrize("E,top_k", [(8, 1), (8, 8)])
-def test_moe_routing_extremes_teacher_forced(E, top_k):
+@pytest.mark.parametrize("E,top_k,kv_fill", [(8, 1, None), (8, 8, None), (8, 1, 0xFF)])
+def test_moe_routing_extremes_teacher_forced(E, top_k, kv_fill):
     """The two ends of the routing: top-1 (one expert per token, weight 1
     after renormalisation) and top-k = E (every expert takes every row, the
     weights are the whole softmax; 8 of the router's 128 padded rows are
     real).  bf16 MoE against the oracle under teacher forcing, as in the
     reduced test: logits within 2e-2 of the row max wherever the routing is
     at least 1e-3 from a top-k tie (with k = E there is no decision to tie,
-    so every row is compared)."""
+    so every row is compared).  With kv_fill the KV pools start as NaN in
+    every byte: the value slots of a freshly opened decode page past the
+    context take part in the bf16 P.V product with weight 0, so the append
+    that opens a page must clear them (a NaN there once reached the logits
+    of every row on that page)."""
     model = ModelCfg(f"moe-e{E}-k{top_k}", 2, 256, 4, 2, 64, 0, 512, "bf16", 23, rope_theta=1e6,
                      n_experts=E, top_k=top_k, expert_ffn=256)
     _, run = get_config("qwen3-30b-a3b")
@@ -115,17 +121,19 @@ def test_moe_routing_extremes_teacher_forced(E, top_k):
     W = OM.init_weights(model)
     ref = rollout(model, W, prompts, forced, run.m, run.k, run.cap, run.sample_seed, keep_logits=True)
     say(f"moe E={E} top-{top_k}: GPU")
-    got = _run_gpu(model, run, prompts, forced, force_tokens=ref.tokens, keep_logits=True)
+    got = _run_gpu(model, run, prompts, forced, force_tokens=ref.tokens, keep_logits=True,
+                   kv_fill=kv_fill)
     checked = excused = 0
     worst = 0.0
     for s, rec in enumerate(got["steps"]):
         for r, g in enumerate(rec["traj"]):
             g = int(g)
+            row = r if s > 0 else g // run.m
+            lg, lr = rec["logits"][row], ref.logits[g][s]
+            assert np.all(np.isfinite(lg)), (s, g)
             if ref.route_margins[g][s] < 1e-3:
                 excused += 1
                 continue
-            row = r if s > 0 else g // run.m
-            lg, lr = rec["logits"][row], ref.logits[g][s]
             dz = np.max(np.abs(lg - lr))
             scale = np.max(np.abs(lr))
             worst = max(worst, dz / scale)

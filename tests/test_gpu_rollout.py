@@ -34,9 +34,11 @@ def _b():
 
 
 def run_gpu(model, run, prompts, forced, force_tokens=None, flags=0, perm_seed=0, keep_logits=False,
-            kv_pool_bytes=None):
+            kv_pool_bytes=None, kv_fill=None):
     B = _b()
     ro = B.Rollout(model, run, flags=flags, page_perm_seed=perm_seed, kv_pool_bytes=kv_pool_bytes)
+    if kv_fill is not None:
+        ro.debug_fill_kv(kv_fill)
     pr = torch.from_numpy(np.ascontiguousarray(prompts.reshape(-1))).to(DEV)
     fl = torch.from_numpy(forced.astype(np.int32)).to(DEV)
     steps = []
@@ -155,6 +157,27 @@ def test_determinism_and_page_permutation(tiny):
         for key in ("logprob", "entropy"):
             assert np.array_equal(x[key].view(np.uint32), y[key].view(np.uint32))
     assert np.array_equal(a["kept"], b["kept"])
+
+
+def _same_steps(a, b, keys=("traj", "token", "sampled", "finished")):
+    assert len(a["steps"]) == len(b["steps"])
+    for s, (x, y) in enumerate(zip(a["steps"], b["steps"])):
+        for key in keys:
+            assert np.array_equal(x[key], y[key]), (s, key)
+        for key in ("logprob", "entropy"):
+            assert np.array_equal(x[key].view(np.uint32), y[key].view(np.uint32)), (s, key)
+        if "logits" in x:
+            assert np.array_equal(x["logits"].view(np.uint32), y["logits"].view(np.uint32)), s
+    assert np.array_equal(a["kept"], b["kept"])
+
+
+def test_tiny_pool_contents_do_not_matter(tiny):
+    """KV pools holding NaN in every byte before the prefill (as memory left
+    by earlier work may) change no output: every value the decode reads is
+    one the rollout wrote."""
+    model, run, prompts, forced, ref, got = tiny
+    p = run_gpu(model, run, prompts, forced, force_tokens=ref.tokens, keep_logits=True, kv_fill=0xFF)
+    _same_steps(got, p)
 
 
 def test_no_abort_counterfactual(tiny):
@@ -307,6 +330,17 @@ def _check_bf16(name, run, ref, got):
 def test_dense_small_bf16_parity(dense_small_reduced):
     model, run, ref, got = dense_small_reduced
     _check_bf16("dense-small", run, ref, got)
+
+
+def test_dense_small_bf16_pool_contents_do_not_matter(dense_small_reduced):
+    """bf16: the value slots of a decode page past the context enter the
+    P.V product with weight 0; with the pools NaN in every byte before the
+    prefill, the append that opens a page clears them, and every output is
+    bit for bit that of the run on fresh pools."""
+    model, run, ref, got = dense_small_reduced
+    prompts, forced = rollout_inputs(model, run)
+    p = run_gpu(model, run, prompts, forced, force_tokens=ref.tokens, keep_logits=True, kv_fill=0xFF)
+    _same_steps(got, p)
 
 
 @pytest.fixture(scope="module")

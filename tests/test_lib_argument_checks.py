@@ -70,3 +70,8 @@ def test_attention_equal_contexts_arguments(lib):
     # the binding needs the row count when no contexts are given
     with pytest.raises(ValueError):
         B.darts_attn_decode(None, None, None, 1, None, None, 32, 8, 128, 16, bf, None, None)
+
+
+def test_context_calls_reject_a_null_context(lib):
+    assert lib.darts_debug_fill_kv(N, 0xFF) == EINVAL
+    assert lib.darts_debug_logits(N, N, N) == EINVAL
