@@ -87,7 +87,8 @@ typedef struct {
   int32_t head_dim;      /* 32, 64 or 128 */
   int32_t ffn_dim;       /* dense FFN hidden size (ignored for MoE) */
   int32_t vocab;         /* multiple of 4; the end-of-sequence id is vocab-1 */
-  int32_t n_experts;     /* 0 for dense; MoE needs BF16, d_model % 256 == 0 */
+  int32_t n_experts;     /* 0 for dense; MoE needs BF16, d_model % 256 == 0,
+                            d_model <= 5120 */
   int32_t top_k;         /* experts per token (renormalised softmax weights) */
   int32_t expert_ffn;    /* expert SwiGLU hidden size, multiple of 256 */
   float rope_theta;

@@ -69,7 +69,8 @@ struct darts_ctx {
   void* m_h_perm = nullptr;
   void* m_y_perm = nullptr;
   float* m_logits = nullptr;      // router logits [rows][Epad]
-  int32_t* m_mtiles = nullptr;    // n_mtiles | non-empty expert row tiles
+  int32_t* m_mtiles = nullptr;    // n_mtiles | non-empty expert row tiles (gate/up)
+  int32_t* m_mtiles_dn = nullptr; // the same for the down projection
   int32_t* m_touched = nullptr;   // [n_layers] experts that received rows (timed launches)
   int32_t* h_touched = nullptr;   // pinned host copy
   // routing verification (darts_debug_moe_routing)
@@ -320,6 +321,14 @@ static int copy_weights(darts_ctx* c) {
   return DARTS_OK;
 }
 
+// The experts' gate/up matrices ([E][2Fe][d], generated or copied row-major)
+// are reordered in place into the strip layout their grouped GEMM reads.
+static int pack_expert_weights(darts_ctx* c) {
+  for (int l = 0; l < c->nl; ++l)
+    HIPCHK(c, launch_pack_strips(c->layers[l].wegu, (int64_t)c->E * 2 * c->Fe, c->d, c->st));
+  return DARTS_OK;
+}
+
 static size_t gemm_ws_need(const darts_ctx* c) {
   // every row count a launch can see: decode batches 1..n_traj, the prefill
   // (P*Lp rows) and the prefill's LM head (P rows)
@@ -424,7 +433,7 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
     // grouped expert GEMMs: K/8 a multiple of 32 for both d and expert_ffn; bf16 only
     if (mc.dtype != DARTS_BF16 || mc.n_experts > 1024 || mc.top_k < 1 || mc.top_k > 64 ||
         mc.top_k > mc.n_experts || mc.expert_ffn < 256 || mc.expert_ffn % 256 != 0 ||
-        mc.d_model % 256 != 0)
+        mc.d_model % 256 != 0 || mc.d_model > 5120)   // 5120: a packed weight strip fits LDS
       return DARTS_EINVAL;
   } else if (mc.ffn_dim < 16 || mc.ffn_dim % 16 != 0) {
     return DARTS_EINVAL;
@@ -553,6 +562,7 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
     A(&c->m_cnt, (size_t)3 * c->E * 4);
     A(&c->m_logits, (size_t)rows_max * c->Epad * 4);
     A(&c->m_mtiles, (pairs / kGroupedTileRowsMin + c->E + 1) * 4);
+    A(&c->m_mtiles_dn, (pairs / kGroupedTileRowsMin + c->E + 1) * 4);
     A(&c->m_row_of, pairs * 4);
     A(&c->m_h_perm, pairs * c->Fe * 2);
     A(&c->m_y_perm, pairs * c->d * 2);
@@ -603,6 +613,7 @@ int darts_init(const darts_model_cfg* model, int32_t m, int32_t k, const darts_r
   int rcode = DARTS_OK;
   if (e != hipSuccess) rcode = fail_hip(c, e, "upload index tables");
   if (rcode == DARTS_OK) rcode = c->mc.weights ? copy_weights(c) : init_weights(c);
+  if (rcode == DARTS_OK && c->moe) rcode = pack_expert_weights(c);
   if (rcode == DARTS_OK) {
     e = launch_rope_table(c->rope, max_pos, c->hd, (double)mc.rope_theta, c->st);
     if (e == hipSuccess)
@@ -795,6 +806,7 @@ static int run_layers(darts_ctx* c, int n, const int32_t* row_pt, const int32_t*
       m.Fe = c->Fe; m.w_router = (const bf16_t*)w.wrouter; m.w_gu = (const bf16_t*)w.wegu;
       m.E_pad = c->Epad; m.logits = c->m_logits; m.gemm_ws = c->gemm_ws;
       m.n_mtiles = c->m_mtiles; m.mtiles = c->m_mtiles + 1;
+      m.n_mtiles_dn = c->m_mtiles_dn; m.mtiles_dn = c->m_mtiles_dn + 1;
       m.gemm_ws_bytes = c->gemm_ws_bytes;
       m.w_down = (const bf16_t*)w.wedown; m.topk_id = c->m_topk_id; m.topk_w = c->m_topk_w;
       m.pos_of = c->m_pos_of; m.counts = c->m_cnt; m.offsets = c->m_cnt + c->E;

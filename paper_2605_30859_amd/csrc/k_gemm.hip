@@ -69,6 +69,32 @@ __device__ __forceinline__ void store_partial(float* P, int M, int N, int r0, in
   }
 }
 
+// ------------------------------------------------------------ strip layout
+// Strip-packed weights: a [N][K] matrix (N % 16 == 0, K % 32 == 0) is stored
+// as N/16 strips of 16 consecutive rows; strip g holds K/32 blocks of 64 x 8
+// bf16, and lane l of block s holds W[16g + l%16][32s + 8(l/16), +8), the B
+// operand of v_mfma_f32_16x16x32_bf16 for that strip and K step.  A strip
+// occupies the same 16*K elements as in the row-major layout, only reordered.
+// Element offset of the 8-element chunk W[n][k, k+8), k % 8 == 0:
+__device__ __forceinline__ int64_t strip_off(int n, int k, int K) {
+  return (((int64_t)(n >> 4) * (K >> 5) + (k >> 5)) * 64 + (n & 15) + 16 * ((k >> 3) & 3)) * 8;
+}
+
+// In-place repack of a row-major [16 * gridDim.x][K] bf16 matrix into the
+// strip layout: one block per strip, staged through 16*K*2 bytes of LDS.
+__global__ void __launch_bounds__(256) pack_strips_kernel(bf16_t* __restrict__ W, int K) {
+  extern __shared__ __attribute__((aligned(16))) bf16_t strip[];
+  bf16_t* base = W + (int64_t)blockIdx.x * 16 * K;
+  const int nch = 2 * K;                     // 16-byte chunks per strip
+  for (int c = threadIdx.x; c < nch; c += blockDim.x)
+    *(u32x4_t*)(strip + c * 8) = *(const u32x4_t*)(base + (int64_t)c * 8);
+  __syncthreads();
+  for (int c = threadIdx.x; c < nch; c += blockDim.x) {
+    const int s = c >> 6, l = c & 63;        // block s, lane l: row l%16, K 32s + 8(l/16)
+    *(u32x4_t*)(base + (int64_t)c * 8) = *(const u32x4_t*)(strip + (l & 15) * K + 32 * s + 8 * (l >> 4));
+  }
+}
+
 // ------------------------------------------------------------------ tiled
 // Operand tiles travel global -> LDS with direct 16-byte LDS loads (no
 // staging registers) through a STAGES-deep ring of LDS buffers.  A KB-wide K
@@ -98,7 +124,10 @@ __device__ __forceinline__ int dma_swz(int r) {
 
 // One BM x BN output tile (rows m0.., cols n0.., K range [z*k_chunk, +k_chunk)).
 // arow != NULL: row r of the tile's A operand is row arow[r] of A (a gather).
-template <int BM, int BN, int KB, int WGM, int WGN, int STAGES, int EPI, bool SPLIT>
+// PW: W is strip-packed (pack_strips_kernel; ldw = K): the same LDS tile is
+// filled from the packed addresses, so results are bitwise those of the
+// row-major layout.
+template <int BM, int BN, int KB, int WGM, int WGN, int STAGES, int EPI, bool SPLIT, bool PW = false>
 __device__ __forceinline__ void dma_gemm_tile(const bf16_t* __restrict__ A, int lda,
                                               const bf16_t* __restrict__ W, int ldw,
                                               void* __restrict__ C, int ldc, int M, int N,
@@ -135,8 +164,14 @@ __device__ __forceinline__ void dma_gemm_tile(const bf16_t* __restrict__ A, int 
     asrc[j] = A + (int64_t)r * lda + kbeg + gchunk * 8;
   }
 #pragma unroll
-  for (int j = 0; j < WI; ++j)
-    wsrc[j] = W + (int64_t)(n0 + wave * (BN / NW) + RPI * j + lrow) * ldw + kbeg + gchunk * 8;
+  for (int j = 0; j < WI; ++j) {
+    const int n = n0 + wave * (BN / NW) + RPI * j + lrow;
+    if constexpr (PW) wsrc[j] = W + strip_off(n, kbeg + gchunk * 8, ldw);
+    else wsrc[j] = W + (int64_t)n * ldw + kbeg + gchunk * 8;
+  }
+  // one KB-wide K step moves a row-major source KB elements on, a packed one
+  // KB/32 blocks of 512 elements
+  constexpr int WSTEP = PW ? KB * 16 : KB;
 
   auto issue = [&](int kt, int buf) {
     bf16_t* sa = smem + buf * STAGE_ELEMS;
@@ -147,7 +182,7 @@ __device__ __forceinline__ void dma_gemm_tile(const bf16_t* __restrict__ A, int 
                                        (lds_void_t*)(sa + (wave * (BM / NW) + RPI * j) * KB), 16, 0, 0);
 #pragma unroll
     for (int j = 0; j < WI; ++j)
-      __builtin_amdgcn_global_load_lds((const void*)(wsrc[j] + kt * KB),
+      __builtin_amdgcn_global_load_lds((const void*)(wsrc[j] + kt * WSTEP),
                                        (lds_void_t*)(sw + (wave * (BN / NW) + RPI * j) * KB), 16, 0, 0);
   };
 
@@ -246,8 +281,8 @@ __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_kernel(const bf16_t* 
 // matrix W + e * w_stride ([N][K]).  The
 // non-empty row tiles are listed on the device (mtiles[i] = e << 16 | m tile,
 // *n_mtiles of them); persistent blocks take items (row tile, n tile), n tile
-// fastest, in a grid-stride loop.
-template <int BM, int BN, int KB, int WGM, int WGN, int STAGES, int EPI>
+// fastest, in a grid-stride loop.  PW: W strip-packed.
+template <int BM, int BN, int KB, int WGM, int WGN, int STAGES, int EPI, bool PW>
 __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_grouped_kernel(
     const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ W, int64_t w_stride, int ldw,
     void* __restrict__ C, int ldc, int N, int K, const int32_t* __restrict__ g_off,
@@ -278,7 +313,7 @@ __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_grouped_kernel(
     __builtin_amdgcn_s_barrier();
     void* Ce = (char*)C + off * ldc * esz;
     // with arow, A rows are gathered: segment row r is A row arow[off + r]
-    dma_gemm_tile<BM, BN, KB, WGM, WGN, STAGES, EPI, false>(arow ? A : A + off * lda, lda,
+    dma_gemm_tile<BM, BN, KB, WGM, WGN, STAGES, EPI, false, PW>(arow ? A : A + off * lda, lda,
                                                             W + (int64_t)e * w_stride, ldw, Ce, ldc,
                                                             cnt, N, K, mi, ni, 0, nullptr,
                                                             arow ? arow + off : nullptr);
@@ -670,8 +705,24 @@ static void dma_go(const Plan& p, const void* A, int lda, const void* W, int ldw
   }
 }
 
-int grouped_tile_rows(int64_t n_pairs, int E) {
-  return n_pairs <= (int64_t)96 * E ? kGroupedTileRowsMin : kGroupedTileRows;
+int grouped_tile_rows(int64_t n_pairs, int E, bool gate_up) {
+  if (n_pairs > (int64_t)96 * E) return kGroupedTileRows;
+  return gate_up && n_pairs > (int64_t)48 * E ? kGroupedTileRowsGU : kGroupedTileRowsMin;
+}
+
+hipError_t launch_pack_strips(void* W, int64_t rows, int K, hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  if (rows % 16 || K % 32 || K < 32 || (size_t)16 * K * 2 > 160 * 1024 || rows / 16 > INT32_MAX)
+    return hipErrorInvalidValue;
+  const size_t lds = (size_t)16 * K * sizeof(bf16_t);
+  static bool attr_done = false;
+  if (!attr_done) {
+    (void)hipFuncSetAttribute((const void*)pack_strips_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              160 * 1024);
+    attr_done = true;
+  }
+  hipLaunchKernelGGL(pack_strips_kernel, dim3((unsigned)(rows / 16)), dim3(256), lds, st, (bf16_t*)W, K);
+  return hipGetLastError();
 }
 
 // Persistent blocks over (row tile, n tile) items.  128-row tiles (the
@@ -682,17 +733,24 @@ int grouped_tile_rows(int64_t n_pairs, int E) {
 // the gate/up projection (K = d), 64x128 tiles with a 3-stage ring for the
 // down projection (K = expert FFN).  Measured on the Qwen3-30B-A3B expert
 // shapes from 1 to 1024 rows against one block per CU with 64x128 tiles and
-// a 6-stage ring: 6-18% faster for gate/up, 10-18% for down.
-template <int BM_, int ST, int EPI, int BN_ = 128, int BPC = 1>
+// a 6-stage ring: 6-18% faster for gate/up, 10-18% for down.  96-row tiles
+// (gate/up from 48 rows per expert on average): 96x128 with a 3-stage ring,
+// one block per CU.  At 64 rows per expert about half the experts exceed 64
+// rows, and a 64-row tile list streams their weights twice; the 96-row tile
+// streams them once (171-180 us per launch at 1024 rows against 222 us).
+// The down projection gains nothing from it (its second pass mostly hits
+// in cache) and keeps 64-row tiles up to 96 rows per expert.
+template <int BM_, int ST, int EPI, int BN_, int BPC, bool PW>
 static hipError_t grouped_launch(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
                                  void* C, int ldc, int N, int K, const int32_t* g_off,
                                  const int32_t* g_cnt, const int32_t* mtiles,
                                  const int32_t* n_mtiles, const int32_t* arow, hipStream_t st) {
   constexpr int KB = 64;
   if (N % BN_ != 0) return hipErrorInvalidValue;
+  if (PW && (ldw != K || K % 32 != 0)) return hipErrorInvalidValue;
   const int nt = N / BN_;
   const size_t lds = (size_t)ST * (BM_ + BN_) * KB * sizeof(bf16_t);
-  auto kern = gemm_dma_grouped_kernel<BM_, BN_, KB, 2, 2, ST, EPI>;
+  auto kern = gemm_dma_grouped_kernel<BM_, BN_, KB, 2, 2, ST, EPI, PW>;
   static bool attr_done = false;
   if (!attr_done) {
     (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -704,35 +762,44 @@ static hipError_t grouped_launch(const void* A, int lda, const void* W, int64_t 
   return hipGetLastError();
 }
 
-template <int EPI>
+template <int EPI, bool PW>
 static hipError_t grouped_by_rows(int tile_rows, const void* A, int lda, const void* W, int64_t w_stride,
                                   int ldw, void* C, int ldc, int N, int K, const int32_t* g_off,
                                   const int32_t* g_cnt, const int32_t* mtiles, const int32_t* n_mtiles,
                                   const int32_t* arow, hipStream_t st) {
   if (tile_rows == kGroupedTileRowsMin) {
     if constexpr (EPI == EPI_SWIGLU)
-      return grouped_launch<kGroupedTileRowsMin, 4, EPI, 64, 2>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off,
-                                                                g_cnt, mtiles, n_mtiles, arow, st);
+      return grouped_launch<kGroupedTileRowsMin, 4, EPI, 64, 2, PW>(A, lda, W, w_stride, ldw, C, ldc, N, K,
+                                                                    g_off, g_cnt, mtiles, n_mtiles, arow, st);
     else
-      return grouped_launch<kGroupedTileRowsMin, 3, EPI, 128, 2>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off,
-                                                                 g_cnt, mtiles, n_mtiles, arow, st);
+      return grouped_launch<kGroupedTileRowsMin, 3, EPI, 128, 2, PW>(A, lda, W, w_stride, ldw, C, ldc, N, K,
+                                                                     g_off, g_cnt, mtiles, n_mtiles, arow, st);
   }
+  if (tile_rows == kGroupedTileRowsGU)
+    return grouped_launch<kGroupedTileRowsGU, 3, EPI, 128, 1, PW>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off,
+                                                                  g_cnt, mtiles, n_mtiles, arow, st);
   if (tile_rows == kGroupedTileRows)
-    return grouped_launch<kGroupedTileRows, 4, EPI>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt,
-                                                    mtiles, n_mtiles, arow, st);
+    return grouped_launch<kGroupedTileRows, 4, EPI, 128, 1, PW>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off,
+                                                                g_cnt, mtiles, n_mtiles, arow, st);
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_gemm_grouped(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
                                void* C, int ldc, int N, int K, int epi, const int32_t* g_off,
                                const int32_t* g_cnt, const int32_t* mtiles, const int32_t* n_mtiles,
-                               const int32_t* arow, int tile_rows, hipStream_t st) {
+                               const int32_t* arow, int tile_rows, bool packed_w, hipStream_t st) {
   if (N % 128 != 0 || K % 64 != 0 || K < 64) return hipErrorInvalidValue;
+  if (packed_w) {
+    // strip-packed weights: the gate/up projection
+    if (epi != EPI_SWIGLU) return hipErrorInvalidValue;
+    return grouped_by_rows<EPI_SWIGLU, true>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt,
+                                             mtiles, n_mtiles, arow, st);
+  }
   switch (epi) {
-    case EPI_F32: return grouped_by_rows<EPI_F32>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
-    case EPI_BF16: return grouped_by_rows<EPI_BF16>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
-    case EPI_ADD_F32: return grouped_by_rows<EPI_ADD_F32>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
-    case EPI_SWIGLU: return grouped_by_rows<EPI_SWIGLU>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
+    case EPI_F32: return grouped_by_rows<EPI_F32, false>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
+    case EPI_BF16: return grouped_by_rows<EPI_BF16, false>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
+    case EPI_ADD_F32: return grouped_by_rows<EPI_ADD_F32, false>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
+    case EPI_SWIGLU: return grouped_by_rows<EPI_SWIGLU, false>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
     default: return hipErrorInvalidValue;
   }
 }

@@ -170,10 +170,12 @@ __global__ void __launch_bounds__(1024) moe_offsets_kernel(const int32_t* __rest
                                                            int32_t* __restrict__ cursors,
                                                            int32_t* __restrict__ mtiles,
                                                            int32_t* __restrict__ n_mtiles,
+                                                           int32_t* __restrict__ mtiles2,
+                                                           int32_t* __restrict__ n_mtiles2,
                                                            int32_t* __restrict__ pos_of,
                                                            int32_t* __restrict__ row_of,
                                                            int32_t* __restrict__ touched_out,
-                                                           int tile_rows) {
+                                                           int tile_rows, int tile_rows2) {
   __shared__ int32_t hist[1024];
   __shared__ int32_t sh[1024];
   const int tid = threadIdx.x;
@@ -197,6 +199,13 @@ __global__ void __launch_bounds__(1024) moe_offsets_kernel(const int32_t* __rest
     for (int j = 0; j < nt; ++j) mtiles[tex + j] = (tid << 16) | j;
   }
   if (tid == 0) *n_mtiles = ntiles;
+  // the second list (another row tile for the other projection)
+  const int nt2 = (v + tile_rows2 - 1) / tile_rows2;
+  int ntiles2;
+  const int tex2 = block_excl_scan1024(nt2, sh, &ntiles2);
+  if (tid < E)
+    for (int j = 0; j < nt2; ++j) mtiles2[tex2 + j] = (tid << 16) | j;
+  if (tid == 0) *n_mtiles2 = ntiles2;
   if (touched_out) {
     const int nz = __syncthreads_count(v > 0);
     if (tid == 0) *touched_out = nz;
@@ -319,7 +328,8 @@ hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st, bool* normed) {
   const float* lg = n_split > 1 ? (const float*)a.gemm_ws : a.logits;
   const int64_t zs = (int64_t)a.n_rows * a.E_pad;
   const dim3 gtk((a.n_rows + 3) / 4), btk(256);
-  const int tile_rows = grouped_tile_rows((int64_t)a.n_rows * a.k, a.E);
+  const int tile_gu = grouped_tile_rows((int64_t)a.n_rows * a.k, a.E, true);
+  const int tile_dn = grouped_tile_rows((int64_t)a.n_rows * a.k, a.E, false);
   const bool dbg = a.force_ids || a.own_ids_out || a.used_p_out;
 #define DARTS_TOPK(NPL)                                                                          \
   if (dbg)                                                                                       \
@@ -337,19 +347,20 @@ hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st, bool* normed) {
   }
 #undef DARTS_TOPK
   hipLaunchKernelGGL(moe_offsets_kernel, dim3(1), dim3(1024), 0, st, a.topk_id, a.n_rows * a.k, a.E, a.k,
-                     a.counts, a.offsets, a.cursors, a.mtiles, a.n_mtiles, a.pos_of, a.row_of,
-                     a.touched_out, tile_rows);
+                     a.counts, a.offsets, a.cursors, a.mtiles, a.n_mtiles, a.mtiles_dn, a.n_mtiles_dn,
+                     a.pos_of, a.row_of, a.touched_out, tile_gu, tile_dn);
   const int Fe = a.Fe, d = a.d;
   // gate/up: N = 2*Fe, K = d (SwiGLU into h_perm), A rows gathered from xn;
   // down: N = d, K = Fe
   if (a.ev_gu0 && (e = hipEventRecord(a.ev_gu0, st)) != hipSuccess) return e;
   e = launch_gemm_grouped(a.xn, d, a.w_gu, (int64_t)2 * Fe * d, d, a.h_perm, Fe, 2 * Fe, d,
-                          EPI_SWIGLU, a.offsets, a.counts, a.mtiles, a.n_mtiles, a.row_of, tile_rows, st);
+                          EPI_SWIGLU, a.offsets, a.counts, a.mtiles, a.n_mtiles, a.row_of, tile_gu,
+                          true, st);
   if (e != hipSuccess) return e;
   if (a.ev_gu1 && (e = hipEventRecord(a.ev_gu1, st)) != hipSuccess) return e;
   if (a.ev_down0 && (e = hipEventRecord(a.ev_down0, st)) != hipSuccess) return e;
   e = launch_gemm_grouped(a.h_perm, Fe, a.w_down, (int64_t)d * Fe, Fe, a.y_perm, d, d, Fe, EPI_BF16,
-                          a.offsets, a.counts, a.mtiles, a.n_mtiles, nullptr, tile_rows, st);
+                          a.offsets, a.counts, a.mtiles_dn, a.n_mtiles_dn, nullptr, tile_dn, false, st);
   if (e != hipSuccess) return e;
   if (a.ev_down1 && (e = hipEventRecord(a.ev_down1, st)) != hipSuccess) return e;
   const bool fuse = d <= 256 * kCombCols * kCombIters;

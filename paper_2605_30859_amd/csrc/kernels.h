@@ -72,18 +72,27 @@ hipError_t launch_gather_rows(const float* src, const int32_t* rows, int n, int 
 // g_off[e] + g_cnt[e]) of A and C and the weights W + e * w_stride ([N][K],
 // row stride ldw).  mtiles lists the non-empty row tiles of tile_rows rows
 // (grouped_tile_rows), e << 16 | tile, *n_mtiles of them (device values).
-// N % 128 == 0, K % 64 == 0.
+// N % 128 == 0, K % 64 == 0.  packed_w: W is in the strip layout of
+// launch_pack_strips (ldw = K; SwiGLU epilogue only).
 constexpr int kGroupedTileRows = 128;      // largest row tile
-constexpr int kGroupedTileRowsMin = 64;    // smallest row tile (sizes the tile list)
+constexpr int kGroupedTileRowsGU = 96;     // gate/up row tile of large decode batches
+constexpr int kGroupedTileRowsMin = 64;    // smallest row tile (sizes the tile lists)
 // Row tile for n_pairs routed (row, expert) pairs over E experts: 64-row
 // tiles while an expert gets few rows (decode batches: the weights are
 // streamed and half-empty 128-row tiles would double the operand traffic),
-// 128-row tiles for large batches (the prefill: more reuse of each weight tile).
-int grouped_tile_rows(int64_t n_pairs, int E);
+// 96-row tiles for the gate/up projection from 48 rows per expert (so an
+// expert's weights are not streamed twice), 128-row tiles for large batches
+// (the prefill: more reuse of each weight tile).
+int grouped_tile_rows(int64_t n_pairs, int E, bool gate_up);
 hipError_t launch_gemm_grouped(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
                                void* C, int ldc, int N, int K, int epi, const int32_t* g_off,
                                const int32_t* g_cnt, const int32_t* mtiles, const int32_t* n_mtiles,
-                               const int32_t* arow, int tile_rows, hipStream_t st);
+                               const int32_t* arow, int tile_rows, bool packed_w, hipStream_t st);
+// Reorder a row-major bf16 [rows][K] matrix in place into the strip layout
+// (rows % 16 == 0, K % 32 == 0, 16*K*2 bytes <= 160 KiB): N/16 strips of 16
+// rows; strip g holds K/32 blocks of 64 lanes x 8 bf16, lane l of block s
+// holding row 16g + l%16, columns 32s + 8(l/16) .. +8 (the MFMA B operand).
+hipError_t launch_pack_strips(void* W, int64_t rows, int K, hipStream_t st);
 
 // ---- attention (k_attn.hip)
 size_t attn_workspace_bytes(int n_rows, int hq, int hkv, int hd, int max_ctx);
@@ -198,13 +207,15 @@ struct MoeArgs {
   const bf16_t* w_router;   // [E_pad][d]
   float* logits;            // [n_rows][E_pad] router logits
   void* gemm_ws; size_t gemm_ws_bytes;   // workspace of the router GEMM
-  const bf16_t* w_gu;       // [E][2Fe][d], gate/up rows interleaved in groups of 16
+  const bf16_t* w_gu;       // [E][2Fe][d], gate/up rows interleaved in groups of 16, strip-packed
   const bf16_t* w_down;     // [E][d][Fe]
   int32_t* topk_id; float* topk_w; int32_t* pos_of;            // [n_rows*k]
   int32_t* row_of;          // [n_rows*k]: input row of each expert-sorted position
   int32_t* counts; int32_t* offsets; int32_t* cursors;         // [E]
   int32_t* mtiles;          // [n_rows*k / kGroupedTileRowsMin + E] non-empty expert row tiles
   int32_t* n_mtiles;        // [1]
+  int32_t* mtiles_dn;       // the same for the down projection's row tiles
+  int32_t* n_mtiles_dn;     // [1]
   bf16_t* h_perm; bf16_t* y_perm;                              // [n_rows*k][Fe | d]
   // Verification of the routing (all NULL in normal use).  Row r has key
   // route_key[r] (NULL: r); each pointer addresses this layer's k entries of
