@@ -571,13 +571,15 @@ def _counter_rows(d):
 
 def _pmc_class(name):
     """Kernel class of a profiled dispatch: decode attention or one of the
-    two grouped expert GEMMs (SwiGLU epilogue = gate/up, fp32 store = down)."""
+    two grouped expert GEMMs (template argument 7, the epilogue: 3 = SwiGLU =
+    gate/up, otherwise down)."""
     import re
     if "attn_bf16" in name:
         return "attention"
-    mt = re.search(r"gemm_dma_grouped_kernel<[^>]*?(\d+)>", name)
+    mt = re.search(r"gemm_dma_grouped_kernel<([^>]*)>", name)
     if mt:
-        return "expert_gate_up" if mt.group(1) == "3" else "expert_down"
+        args = [a.strip() for a in mt.group(1).split(",")]
+        return "expert_gate_up" if len(args) > 6 and args[6] == "3" else "expert_down"
     return None
 
 

@@ -46,3 +46,13 @@ def test_gap_summary_splits_step_boundaries(tmp_path):
     assert out["intra_step_idle_s"] == pytest.approx(10e-9)
     assert out["span_s"] == pytest.approx(320e-9) and out["busy_s"] == pytest.approx(175e-9)
     assert out["idle_s"] == pytest.approx(145e-9)
+
+
+def test_pmc_class_reads_the_epilogue_argument():
+    import bench
+    assert bench._pmc_class("void darts::attn_bf16_db_kernel<128>(darts::AttnBf16Args)") == "attention"
+    gu = "void darts::gemm_dma_grouped_kernel<96, 128, 64, 2, 2, 3, 3, true>(unsigned short const*, int)"
+    dn = "void darts::gemm_dma_grouped_kernel<64, 128, 64, 2, 2, 3, 1, false>(unsigned short const*, int)"
+    assert bench._pmc_class(gu) == "expert_gate_up"
+    assert bench._pmc_class(dn) == "expert_down"
+    assert bench._pmc_class("void darts::gemm_dma_kernel<128, 128, 64, 2, 2, 4, 3, false>(int)") is None
