@@ -96,7 +96,8 @@ def run_forced(model, run, prompts, forced, g, label, strict_all=False):
         rec["sampled"][act, s] = h["sampled"][r_of]
         if strict_all or s in STRICT_STEPS:
             for j, t in enumerate(act):
-                strict.append((t, s, int(h["sampled"][r_of[j]]), lg[j].copy()))
+                strict.append((t, s, int(h["sampled"][r_of[j]]), lg[j].copy(),
+                               float(h["logprob"][r_of[j]]), float(h["entropy"][r_of[j]])))
         if moe:
             if s == 0:
                 for i, p in enumerate(sub_p):
@@ -140,10 +141,20 @@ def check_forced(model, run, g, rec, strict, route, label):
     # log-prob = z_taken - LSE and entropy = LSE - E_p[z]: each moves by at most
     # twice the largest logit deviation
     assert (dlp <= 2 * tol[valid]).all() and (dent <= 2 * tol[valid]).all()
-    # the GPU's sample is the oracle sampler's choice on the GPU's own logits
-    for t, s, tok, lrow in strict:
-        want, _, _ = sample_row(lrow, run.temperature, int(g["traj"][t]), s, run.sample_seed)
+    # the GPU's sample is the oracle sampler's choice on the GPU's own logits,
+    # and its log-prob (of the token taken) and entropy are the oracle's values
+    # on those logits within the 1e-3 of the specification
+    dlp_own, dent_own = [], []
+    for t, s, tok, lrow, lp_g, ent_g in strict:
+        want, lp_o, ent_o = sample_row(lrow, run.temperature, int(g["traj"][t]), s, run.sample_seed,
+                                       force=int(g["taken"][t, s]))
         assert tok == want, (config, t, s, tok, want)
+        dlp_own.append(abs(lp_g - lp_o))
+        dent_own.append(abs(ent_g - ent_o))
+    if strict:
+        say(f"{config}: on the GPU's own logits ({len(strict)} rows): |d logprob| worst "
+            f"{max(dlp_own):.3e}, |d entropy| worst {max(dent_own):.3e}")
+        assert max(dlp_own) <= 1e-3 and max(dent_own) <= 1e-3
     # and the oracle's own sample wherever the margin exceeds twice the tolerance
     clear = valid & (g["margin"] > 2 * tol)
     mism = clear & (rec["sampled"] != g["sampled"])

@@ -15,6 +15,7 @@ torch = pytest.importorskip("torch")
 
 from oracle import model as OM
 from oracle.rollout import rollout, schedule_only
+from oracle.sampler import sample_row
 from oracle.selection import LIVE, EOS, TRUNC, ABORTED
 from workload import get_config, rollout_inputs
 
@@ -321,6 +322,23 @@ def _check_bf16(name, run, ref, got):
     say(f"{name}: {checked} rows, worst logit dev {worst:.3e}, {excused} excused")
     assert mism == 0
     assert excused <= checked // 5
+    # given the same logits (the GPU's own), the sample is the oracle
+    # sampler's and the log-prob and entropy are its values within 1e-3
+    dlp_own = dent_own = 0.0
+    n_own = 0
+    for s, rec in enumerate(got["steps"]):
+        for r in range(min(4, len(rec["traj"]))):
+            g = int(rec["traj"][r])
+            row = r if s > 0 else g // run.m
+            tok, lp_o, ent_o = sample_row(rec["logits"][row], run.temperature, g, s, run.sample_seed,
+                                          force=int(rec["token"][r]))
+            assert tok == rec["sampled"][r], (s, g)
+            dlp_own = max(dlp_own, abs(float(rec["logprob"][r]) - lp_o))
+            dent_own = max(dent_own, abs(float(rec["entropy"][r]) - ent_o))
+            n_own += 1
+    say(f"{name}: on the GPU's own logits ({n_own} rows): |d logprob| worst {dlp_own:.3e}, "
+        f"|d entropy| worst {dent_own:.3e}")
+    assert dlp_own <= 1e-3 and dent_own <= 1e-3
     for i in range(run.n_prompts):
         assert got["done"][i] == ref.done_step[i]
     assert got["stats"]["steps"] == ref.steps
