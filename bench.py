@@ -571,15 +571,17 @@ def _counter_rows(d):
 
 def _pmc_class(name):
     """Kernel class of a profiled dispatch: decode attention or one of the
-    two grouped expert GEMMs (template argument 7, the epilogue: 3 = SwiGLU =
-    gate/up, otherwise down)."""
+    two grouped expert GEMMs, told apart by the epilogue template argument
+    (3 = SwiGLU = gate/up, otherwise down): argument 7 of the LDS-tiled
+    gemm_dma_grouped_kernel, argument 4 of gemm_wd_grouped_kernel."""
     import re
     if "attn_bf16" in name:
         return "attention"
-    mt = re.search(r"gemm_dma_grouped_kernel<([^>]*)>", name)
-    if mt:
-        args = [a.strip() for a in mt.group(1).split(",")]
-        return "expert_gate_up" if len(args) > 6 and args[6] == "3" else "expert_down"
+    for kern, pos in (("gemm_dma_grouped_kernel", 6), ("gemm_wd_grouped_kernel", 3)):
+        mt = re.search(kern + r"<([^>]*)>", name)
+        if mt:
+            args = [a.strip() for a in mt.group(1).split(",")]
+            return "expert_gate_up" if len(args) > pos and args[pos] == "3" else "expert_down"
     return None
 
 
@@ -944,7 +946,9 @@ def main():
             ach_m = by / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
             moe_roof[name] = {"bound": "hbm", "achieved": ach_m, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                               "frac": ach_m / HBM_PEAK_GBS, "traffic": measured_traffic(args.config, name),
-                              "kernel": "gemm_dma_grouped_kernel (" + ("gate/up + SwiGLU" if i == 0 else "down") + ")",
+                              "kernel": ("gemm_wd_grouped_kernel (gate/up + SwiGLU; gemm_dma_grouped_kernel "
+                                         "below 2 and above 96 rows per expert)") if i == 0 else
+                                        "gemm_dma_grouped_kernel (down)",
                               "launches": n_l, "avg_launch_us": 1e3 * ms / max(n_l, 1),
                               "algorithmic_bytes_per_launch": by / max(n_l, 1),
                               "share_of_step_time": ms * 1e-3 / total}

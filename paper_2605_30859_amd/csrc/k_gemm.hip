@@ -320,6 +320,135 @@ __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_grouped_kernel(
   }
 }
 
+// ------------------------------------------- grouped, weights into registers
+// Grouped GEMM for decode batches with strip-packed W (the MoE gate/up
+// projection).  Block = 4 wavefronts over an item (expert row tile of BM
+// rows, slab of 4 x CPW columns); wavefront w owns CPW columns and loads
+// their W blocks (one 1 KB block per 16-column strip and 32-wide K step)
+// straight from memory into MFMA B-operand registers, P K steps of 64
+// ahead, so W never passes through LDS.  The BM x 64 A tiles of the
+// expert's rows (gathered through arow when given; rows past the expert's
+// count repeat its last row) go through a P-stage LDS ring shared by the
+// four wavefronts, filled by direct 16-byte LDS loads in the swizzled layout
+// of the tiled kernel.  Per output tile the MFMAs run over K in order, as in
+// the tiled kernel, so results are bitwise those of the tiled kernel.
+// Items are dealt XCD by XCD as in the tiled grouped kernel.
+template <int BM, int CPW, int P, int EPI>
+__global__ void __launch_bounds__(256, 2) gemm_wd_grouped_kernel(
+    const bf16_t* __restrict__ A, int lda, const bf16_t* Wp, int64_t w_stride,
+    void* __restrict__ C, int ldc, int N, int K, const int32_t* __restrict__ g_off,
+    const int32_t* __restrict__ g_cnt, const int32_t* __restrict__ mtiles,
+    const int32_t* __restrict__ n_mtiles, const int32_t* __restrict__ arow) {
+  constexpr int NW = 4, KB = 64, CH = KB / 8, RPI = 64 / CH;
+  constexpr int AI = BM / (RPI * NW);                 // A load instructions per wave per stage
+  static_assert(AI * RPI * NW == BM, "A tile rows must split over the waves");
+  static_assert(CPW % 32 == 0 || EPI != EPI_SWIGLU, "SwiGLU pairs gate and up strips");
+  constexpr int TM = BM / 16, TN = CPW / 16;
+  constexpr int WL = 2 * TN;                          // W loads per wave per 64-wide K step
+  constexpr int STAGE = BM * KB;
+  constexpr int SLAB = NW * CPW;
+  constexpr int esz = (EPI == EPI_F32 || EPI == EPI_ADD_F32) ? 4 : 2;
+  __shared__ __attribute__((aligned(16))) bf16_t sA[P * STAGE];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nt = N / SLAB;
+  const int total = n_mtiles[0] * nt;
+  const int nk = K / KB;                              // a multiple of P
+  const int k32 = K >> 5;
+  const int chunk = (total + 7) >> 3;
+  const int lo = (int)(blockIdx.x & 7) * chunk;
+  const int hi = min(total, lo + chunk);
+  const int step = (int)(gridDim.x >> 3);
+  const int lrow = lane / CH;
+  const int gchunk = (lane % CH) ^ dma_swz<KB>(lrow);
+  const int fr = lane & 15, fq = lane >> 4;
+  for (int it = lo + (int)(blockIdx.x >> 3); it < hi; it += step) {
+    const int mt = mtiles[it / nt], ni = it % nt;
+    const int e = mt >> 16, mi = mt & 0xffff;
+    const int cnt = g_cnt[e];
+    const int64_t off = g_off[e];
+    // the previous item's last LDS stage may still be read by other waves
+    __builtin_amdgcn_s_barrier();
+    const bf16_t* asrc[AI];
+#pragma unroll
+    for (int j = 0; j < AI; ++j) {
+      int r = mi * BM + wave * (BM / NW) + RPI * j + lrow;
+      r = r < cnt ? r : cnt - 1;
+      const int64_t row = arow ? (int64_t)arow[off + r] : off + r;
+      asrc[j] = A + row * lda + gchunk * 8;
+    }
+    // this wave's first strip; block (strip g0 + j, K step q) at (j*k32 + q)*512
+    const int g0 = (ni * SLAB + wave * CPW) >> 4;
+    const bf16_t* wsrc = Wp + (int64_t)e * w_stride + (int64_t)g0 * k32 * 512 + lane * 8;
+    f32x4_t acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+    bf16x8_t wr[P][2][TN];   // register ring: slot u holds K step k0 + u
+#define DARTS_WD_ISSUE(KT, SLOT)                                                                  \
+    {                                                                                            \
+      bf16_t* sa_ = sA + (SLOT) * STAGE;                                                         \
+      _Pragma("unroll") for (int j = 0; j < AI; ++j)                                             \
+        __builtin_amdgcn_global_load_lds((const void*)(asrc[j] + (KT) * KB),                    \
+                                         (lds_void_t*)(sa_ + (wave * (BM / NW) + RPI * j) * KB), \
+                                         16, 0, 0);                                              \
+      _Pragma("unroll") for (int h = 0; h < 2; ++h)                                              \
+        _Pragma("unroll") for (int j = 0; j < TN; ++j)                                           \
+          wr[SLOT][h][j] = *(const bf16x8_t*)(wsrc + ((int64_t)j * k32 + 2 * (KT) + h) * 512);  \
+    }
+#pragma unroll
+    for (int u = 0; u < P - 1; ++u)
+      if (u < nk) DARTS_WD_ISSUE(u, u)
+    for (int k0 = 0; k0 < nk; k0 += P) {
+#pragma unroll
+      for (int u = 0; u < P; ++u) {
+        const int kt = k0 + u;
+        // K step kt's A and W loads are done once at most the loads of the
+        // (P - 2) later steps are outstanding (whatever the order of the A
+        // and W loads inside a step); the raw barrier then publishes every
+        // wave's A stage kt, and the scheduling barrier keeps the next
+        // step's loads from moving above it
+        if (kt + P - 2 < nk) vm_wait<(P - 2) * (AI + WL)>();
+        else vm_wait<0>();
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        const int kn = kt + P - 1;
+        if (kn < nk) DARTS_WD_ISSUE(kn, (u + P - 1) % P)
+        const bf16_t* sa = sA + u * STAGE;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          bf16x8_t a[TM];
+#pragma unroll
+          for (int i = 0; i < TM; ++i) {
+            const int r = 16 * i + fr;
+            a[i] = *(const bf16x8_t*)(sa + r * KB + (((h * 4 + fq) ^ dma_swz<KB>(r)) * 8));
+          }
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], wr[u][h][j], acc[i][j], 0, 0, 0);
+        }
+      }
+    }
+#undef DARTS_WD_ISSUE
+    void* Ce = (char*)C + off * ldc * esz;
+    const int r0 = mi * BM, c0 = ni * SLAB + wave * CPW;
+    if constexpr (EPI == EPI_SWIGLU) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; j += 2)
+          store_swiglu((bf16_t*)Ce, ldc, cnt, r0 + 16 * i, c0 + 16 * j, lane, acc[i][j], acc[i][j + 1]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) store_tile<EPI>(Ce, ldc, cnt, r0 + 16 * i, c0 + 16 * j, lane, acc[i][j]);
+    }
+  }
+}
+
 // ----------------------------------------------------------------- skinny
 // Block: 8 wavefronts, NS*16 output columns, all M <= 16*MT rows.  Wavefront
 // w handles K range [kbeg + w*kw, kbeg + (w+1)*kw).
@@ -705,9 +834,11 @@ static void dma_go(const Plan& p, const void* A, int lda, const void* W, int ldw
   }
 }
 
-int grouped_tile_rows(int64_t n_pairs, int E, bool gate_up) {
-  if (n_pairs > (int64_t)96 * E) return kGroupedTileRows;
-  return gate_up && n_pairs > (int64_t)48 * E ? kGroupedTileRowsGU : kGroupedTileRowsMin;
+GroupedPlan grouped_plan(int64_t n_pairs, int E, bool gate_up) {
+  if (n_pairs > (int64_t)96 * E) return {kGroupedTileRows, false};
+  if (!gate_up) return {kGroupedTileRowsMin, false};
+  if (n_pairs > (int64_t)48 * E) return {kGroupedTileRowsGU, true};
+  return {kGroupedTileRowsMin, n_pairs >= (int64_t)2 * E};
 }
 
 hipError_t launch_pack_strips(void* W, int64_t rows, int K, hipStream_t st) {
@@ -784,17 +915,49 @@ static hipError_t grouped_by_rows(int tile_rows, const void* A, int lda, const v
   return hipErrorInvalidValue;
 }
 
+// Weights into registers: 32 columns per wavefront (a 128-column slab per
+// block), a 2-step register ring and 2-stage A ring, two blocks per CU.
+// Measured against the tiled kernel on the Qwen3-30B-A3B gate/up shape
+// (random routings, weights cache-cold, outputs bitwise equal), per launch:
+// 96-row tiles 154 against 178 us at 1024 rows and 147 against 170 us at
+// 768; 64-row tiles 139 against 150 us at 512, 132 against 138 at 256,
+// 128 against 132 at 64 and 86 against 88 at 16; below 2 rows per expert
+// (8 live rows) the tiled kernel is faster (67 against 73 us).
+template <int BM>
+static hipError_t wd_launch(const void* A, int lda, const void* W, int64_t w_stride, int ldw, void* C, int ldc,
+                            int N, int K, const int32_t* g_off, const int32_t* g_cnt, const int32_t* mtiles,
+                            const int32_t* n_mtiles, const int32_t* arow, hipStream_t st) {
+  constexpr int CPW = 32, P = 2, BPC = 2;
+  if (N % (4 * CPW) != 0 || ldw != K || (K / 64) % P != 0) return hipErrorInvalidValue;
+  static_assert((kCus * BPC) % 8 == 0, "the grouped kernel deals items to 8 XCDs");
+  hipLaunchKernelGGL((gemm_wd_grouped_kernel<BM, CPW, P, EPI_SWIGLU>), dim3(kCus * BPC), dim3(256), 0, st,
+                     (const bf16_t*)A, lda, (const bf16_t*)W, w_stride, C, ldc, N, K, g_off, g_cnt, mtiles,
+                     n_mtiles, arow);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm_grouped(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
                                void* C, int ldc, int N, int K, int epi, const int32_t* g_off,
                                const int32_t* g_cnt, const int32_t* mtiles, const int32_t* n_mtiles,
-                               const int32_t* arow, int tile_rows, bool packed_w, hipStream_t st) {
+                               const int32_t* arow, GroupedPlan plan, bool packed_w, hipStream_t st) {
   if (N % 128 != 0 || K % 64 != 0 || K < 64) return hipErrorInvalidValue;
+  const int tile_rows = plan.tile_rows;
   if (packed_w) {
     // strip-packed weights: the gate/up projection
     if (epi != EPI_SWIGLU) return hipErrorInvalidValue;
+    if (plan.wdirect) {
+      if (tile_rows == kGroupedTileRowsMin)
+        return wd_launch<kGroupedTileRowsMin>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles,
+                                              n_mtiles, arow, st);
+      if (tile_rows == kGroupedTileRowsGU)
+        return wd_launch<kGroupedTileRowsGU>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles,
+                                             n_mtiles, arow, st);
+      return hipErrorInvalidValue;
+    }
     return grouped_by_rows<EPI_SWIGLU, true>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt,
                                              mtiles, n_mtiles, arow, st);
   }
+  if (plan.wdirect) return hipErrorInvalidValue;
   switch (epi) {
     case EPI_F32: return grouped_by_rows<EPI_F32, false>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
     case EPI_BF16: return grouped_by_rows<EPI_BF16, false>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);

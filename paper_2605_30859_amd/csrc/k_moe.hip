@@ -328,8 +328,8 @@ hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st, bool* normed) {
   const float* lg = n_split > 1 ? (const float*)a.gemm_ws : a.logits;
   const int64_t zs = (int64_t)a.n_rows * a.E_pad;
   const dim3 gtk((a.n_rows + 3) / 4), btk(256);
-  const int tile_gu = grouped_tile_rows((int64_t)a.n_rows * a.k, a.E, true);
-  const int tile_dn = grouped_tile_rows((int64_t)a.n_rows * a.k, a.E, false);
+  const GroupedPlan plan_gu = grouped_plan((int64_t)a.n_rows * a.k, a.E, true);
+  const GroupedPlan plan_dn = grouped_plan((int64_t)a.n_rows * a.k, a.E, false);
   const bool dbg = a.force_ids || a.own_ids_out || a.used_p_out;
 #define DARTS_TOPK(NPL)                                                                          \
   if (dbg)                                                                                       \
@@ -348,19 +348,19 @@ hipError_t launch_moe_ffn(const MoeArgs& a, hipStream_t st, bool* normed) {
 #undef DARTS_TOPK
   hipLaunchKernelGGL(moe_offsets_kernel, dim3(1), dim3(1024), 0, st, a.topk_id, a.n_rows * a.k, a.E, a.k,
                      a.counts, a.offsets, a.cursors, a.mtiles, a.n_mtiles, a.mtiles_dn, a.n_mtiles_dn,
-                     a.pos_of, a.row_of, a.touched_out, tile_gu, tile_dn);
+                     a.pos_of, a.row_of, a.touched_out, plan_gu.tile_rows, plan_dn.tile_rows);
   const int Fe = a.Fe, d = a.d;
   // gate/up: N = 2*Fe, K = d (SwiGLU into h_perm), A rows gathered from xn;
   // down: N = d, K = Fe
   if (a.ev_gu0 && (e = hipEventRecord(a.ev_gu0, st)) != hipSuccess) return e;
   e = launch_gemm_grouped(a.xn, d, a.w_gu, (int64_t)2 * Fe * d, d, a.h_perm, Fe, 2 * Fe, d,
-                          EPI_SWIGLU, a.offsets, a.counts, a.mtiles, a.n_mtiles, a.row_of, tile_gu,
+                          EPI_SWIGLU, a.offsets, a.counts, a.mtiles, a.n_mtiles, a.row_of, plan_gu,
                           true, st);
   if (e != hipSuccess) return e;
   if (a.ev_gu1 && (e = hipEventRecord(a.ev_gu1, st)) != hipSuccess) return e;
   if (a.ev_down0 && (e = hipEventRecord(a.ev_down0, st)) != hipSuccess) return e;
   e = launch_gemm_grouped(a.h_perm, Fe, a.w_down, (int64_t)d * Fe, Fe, a.y_perm, d, d, Fe, EPI_BF16,
-                          a.offsets, a.counts, a.mtiles_dn, a.n_mtiles_dn, nullptr, tile_dn, false, st);
+                          a.offsets, a.counts, a.mtiles_dn, a.n_mtiles_dn, nullptr, plan_dn, false, st);
   if (e != hipSuccess) return e;
   if (a.ev_down1 && (e = hipEventRecord(a.ev_down1, st)) != hipSuccess) return e;
   const bool fuse = d <= 256 * kCombCols * kCombIters;

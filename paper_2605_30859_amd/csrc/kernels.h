@@ -71,23 +71,30 @@ hipError_t launch_gather_rows(const float* src, const int32_t* rows, int n, int 
 // Grouped bf16 GEMM (mixture of experts): group e owns rows [g_off[e],
 // g_off[e] + g_cnt[e]) of A and C and the weights W + e * w_stride ([N][K],
 // row stride ldw).  mtiles lists the non-empty row tiles of tile_rows rows
-// (grouped_tile_rows), e << 16 | tile, *n_mtiles of them (device values).
+// (grouped_plan), e << 16 | tile, *n_mtiles of them (device values).
 // N % 128 == 0, K % 64 == 0.  packed_w: W is in the strip layout of
 // launch_pack_strips (ldw = K; SwiGLU epilogue only).
 constexpr int kGroupedTileRows = 128;      // largest row tile
 constexpr int kGroupedTileRowsGU = 96;     // gate/up row tile of large decode batches
 constexpr int kGroupedTileRowsMin = 64;    // smallest row tile (sizes the tile lists)
-// Row tile for n_pairs routed (row, expert) pairs over E experts: 64-row
-// tiles while an expert gets few rows (decode batches: the weights are
-// streamed and half-empty 128-row tiles would double the operand traffic),
-// 96-row tiles for the gate/up projection from 48 rows per expert (so an
-// expert's weights are not streamed twice), 128-row tiles for large batches
-// (the prefill: more reuse of each weight tile).
-int grouped_tile_rows(int64_t n_pairs, int E, bool gate_up);
+// Plan for n_pairs routed (row, expert) pairs over E experts: the row tile
+// of the tile list and the kernel family.  64-row tiles while an expert gets
+// few rows (decode batches: the weights are streamed and half-empty 128-row
+// tiles would double the operand traffic), 96-row tiles for the gate/up
+// projection from 48 rows per expert (so an expert's weights are not
+// streamed twice), 128-row tiles for large batches (the prefill: more reuse
+// of each weight tile).  wdirect: the gate/up weights go straight into MFMA
+// registers (from 2 rows per expert up to the prefill), otherwise through
+// the LDS tile ring.
+struct GroupedPlan {
+  int tile_rows;
+  bool wdirect;
+};
+GroupedPlan grouped_plan(int64_t n_pairs, int E, bool gate_up);
 hipError_t launch_gemm_grouped(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
                                void* C, int ldc, int N, int K, int epi, const int32_t* g_off,
                                const int32_t* g_cnt, const int32_t* mtiles, const int32_t* n_mtiles,
-                               const int32_t* arow, int tile_rows, bool packed_w, hipStream_t st);
+                               const int32_t* arow, GroupedPlan plan, bool packed_w, hipStream_t st);
 // Reorder a row-major bf16 [rows][K] matrix in place into the strip layout
 // (rows % 16 == 0, K % 32 == 0, 16*K*2 bytes <= 160 KiB): N/16 strips of 16
 // rows; strip g holds K/32 blocks of 64 lanes x 8 bf16, lane l of block s

@@ -56,3 +56,5 @@ def test_pmc_class_reads_the_epilogue_argument():
     assert bench._pmc_class(gu) == "expert_gate_up"
     assert bench._pmc_class(dn) == "expert_down"
     assert bench._pmc_class("void darts::gemm_dma_kernel<128, 128, 64, 2, 2, 4, 3, false>(int)") is None
+    assert bench._pmc_class("void darts::gemm_wd_grouped_kernel<96, 32, 2, 3>(unsigned short const*)") == \
+        "expert_gate_up"
