@@ -262,20 +262,32 @@ __global__ void rope_append_kernel(const float* __restrict__ qkv, int n_split, i
     float v = src[(hq + hkv) * hd + t];
     for (int z = 1; z < n_split; ++z) v += src[z * split_stride + (hq + hkv) * hd + t];
     const int64_t o = v_off(page, h, slot, dd, hkv, hd);
-    if (BF16) ((bf16_t*)v_pool)[o] = f32_to_bf16(v);
-    else ((float*)v_pool)[o] = v;
-    // A decode append that opens a page (slot 0; the row owns the page) also
-    // clears the page's later value slots.  Attention weighs keys at or past
-    // the row's context by 0 but still multiplies their values in the P.V
-    // product, so those slots must hold finite values, whatever the memory
-    // held before (0 x NaN is NaN).  Key slots need nothing: their scores
-    // are replaced, not multiplied.  A prefill writes whole pages itself.
     if (pos_mod == 0 && slot == 0) {
-      for (int s2 = 1; s2 < kPage; ++s2) {
-        const int64_t o2 = v_off(page, h, s2, dd, hkv, hd);
-        if (BF16) ((bf16_t*)v_pool)[o2] = 0;
-        else ((float*)v_pool)[o2] = 0.f;
+      // A decode append that opens a page (slot 0; the row owns the page) also
+      // clears the page's later value slots.  Attention weighs keys at or past
+      // the row's context by 0 but still multiplies their values in the P.V
+      // product, so those slots must hold finite values, whatever the memory
+      // held before (0 x NaN is NaN).  Key slots need nothing: their scores
+      // are replaced, not multiplied.  A prefill writes whole pages itself.
+      // Slots 0-7 and 8-15 of one dim are 8 consecutive elements each: two
+      // aligned vector stores write this slot's value and the zeros.
+      static_assert(kPage == 16, "two groups of 8 value slots per page");
+      const int64_t o8 = v_off(page, h, 8, dd, hkv, hd);
+      if (BF16) {
+        *(uint4*)((bf16_t*)v_pool + o) = make_uint4((uint32_t)f32_to_bf16(v), 0u, 0u, 0u);
+        *(uint4*)((bf16_t*)v_pool + o8) = make_uint4(0u, 0u, 0u, 0u);
+      } else {
+        float4* p0 = (float4*)((float*)v_pool + o);
+        float4* p8 = (float4*)((float*)v_pool + o8);
+        p0[0] = make_float4(v, 0.f, 0.f, 0.f);
+        p0[1] = make_float4(0.f, 0.f, 0.f, 0.f);
+        p8[0] = make_float4(0.f, 0.f, 0.f, 0.f);
+        p8[1] = make_float4(0.f, 0.f, 0.f, 0.f);
       }
+    } else if (BF16) {
+      ((bf16_t*)v_pool)[o] = f32_to_bf16(v);
+    } else {
+      ((float*)v_pool)[o] = v;
     }
   }
 }
