@@ -21,9 +21,14 @@
 
 namespace darts {
 
-// One wavefront per row: softmax over the E router logits (fp32), then k
-// rounds of wavefront argmax (value descending, expert id ascending), each
-// winner removed; weights renormalised over the k.  NPL logits per lane
+// One wavefront per row: softmax over the E router logits (fp32); the k
+// largest probabilities (value descending, expert id ascending) are found by
+// rank: the row's sort keys go to LDS, every lane counts for each of its
+// experts how many experts come before it in that order, and the experts of
+// rank < k are written to their rank's slot.  This gives the order k rounds
+// of wavefront argmax would (a probability that is NaN ranks after every
+// number), without their chain of dependent cross-lane steps.  The weights
+// are renormalised over the k, summed in rank order.  NPL logits per lane
 // (E <= 64 * NPL).  The logits are the sum of n_split split-K partial planes
 // split_stride apart, added in plane order (the dense reduce's order), so the
 // router GEMM needs no separate reduce.
@@ -38,8 +43,13 @@ __global__ void __launch_bounds__(256) moe_topk_kernel(const float* __restrict__
                                                        int n_rows, int E, int k,
                                                        int32_t* __restrict__ topk_id,
                                                        float* __restrict__ topk_w, MoeArgs dbg) {
-  const int lane = threadIdx.x & 63;
-  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  // each wavefront's row of sort keys: (order-preserving probability bits,
+  // 0xffff - expert id); a larger key ranks first, and keys are distinct
+  __shared__ __attribute__((aligned(16))) uint64_t sk[4][64 * NPL];
+  __shared__ float sv[4][64];            // selected probabilities by rank
+  __shared__ int32_t si[4][64];          // selected expert ids by rank
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int r = blockIdx.x * 4 + w;
   if (r >= n_rows) return;
   const float* lg = logits + (int64_t)r * ld;
   float p[NPL];
@@ -72,41 +82,56 @@ __global__ void __launch_bounds__(256) moe_topk_kernel(const float* __restrict__
   }
   sum = wave_sum(sum);
   const float inv = 1.0f / sum;
+  // probabilities (>= 0, so their bits order as unsigned integers); a NaN
+  // ranks after every number, the padding past E after everything
+  uint64_t key[NPL];
 #pragma unroll
-  for (int j = 0; j < NPL; ++j) p[j] = (lane + 64 * j < E) ? p[j] * inv : -2.0f;
+  for (int j = 0; j < NPL; ++j) {
+    const int e = lane + 64 * j;
+    p[j] *= inv;
+    const uint32_t ok = e < E ? (p[j] == p[j] ? __float_as_uint(p[j]) + 2u : 1u) : 0u;
+    key[j] = ((uint64_t)ok << 32) | (uint32_t)(0xffff - e);
+    sk[w][e] = key[j];
+  }
+  __builtin_amdgcn_s_waitcnt(0xc07f);    // lgkmcnt(0): this wavefront's LDS writes are done
+  __builtin_amdgcn_wave_barrier();
+  int rank[NPL];
+#pragma unroll
+  for (int j = 0; j < NPL; ++j) rank[j] = 0;
+  const int E2 = (E + 1) & ~1;
+  // unrolled so that several LDS reads are in flight
+#pragma unroll 8
+  for (int y = 0; y < E2; y += 2) {
+    const uint4 q = *(const uint4*)&sk[w][y];             // the same address in every lane
+    const uint64_t q0 = ((uint64_t)q.y << 32) | q.x, q1 = ((uint64_t)q.w << 32) | q.z;
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) rank[j] += (q0 > key[j]) + (q1 > key[j]);
+  }
   float p0[DBG ? NPL : 1];
   if (DBG) {
 #pragma unroll
     for (int j = 0; j < NPL; ++j) p0[j] = p[j];
   }
-  float wsum = 0.f;
-  float my_w = 0.f;
-  int my_id = 0;
-  for (int t = 0; t < k; ++t) {
-    float bv = -3.0f;
-    int bi = 0x7fffffff;
 #pragma unroll
-    for (int j = 0; j < NPL; ++j) {
-      const int e = lane + 64 * j;
-      if (p[j] > bv || (p[j] == bv && e < bi)) { bv = p[j]; bi = e; }
+  for (int j = 0; j < NPL; ++j) {
+    const int e = lane + 64 * j;
+    if (e < E && rank[j] < k) {
+      sv[w][rank[j]] = p[j];
+      si[w][rank[j]] = e;
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, 64);
-      const int oi = __shfl_xor(bi, o, 64);
-      if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
-    }
-#pragma unroll
-    for (int j = 0; j < NPL; ++j)
-      if (lane + 64 * j == bi) p[j] = -2.0f;          // removed
-    if (lane == t) { my_w = bv; my_id = bi; }         // lane t keeps round t's winner
-    wsum += bv;
   }
+  __builtin_amdgcn_s_waitcnt(0xc07f);
+  __builtin_amdgcn_wave_barrier();
+  float wsum = 0.f;
+#pragma unroll 8
+  for (int t = 0; t < k; ++t) wsum += sv[w][t];        // rank order
+  float my_w = lane < k ? sv[w][lane] : 0.f;
+  int my_id = lane < k ? si[w][lane] : 0;
   if (DBG) {
-    const int64_t key = dbg.route_key ? (int64_t)dbg.route_key[r] : (int64_t)r;
-    if (dbg.own_ids_out && lane < k) dbg.own_ids_out[key * dbg.dbg_stride + lane] = my_id;
+    const int64_t rk = dbg.route_key ? (int64_t)dbg.route_key[r] : (int64_t)r;
+    if (dbg.own_ids_out && lane < k) dbg.own_ids_out[rk * dbg.dbg_stride + lane] = my_id;
     if (dbg.force_ids) {
-      const int32_t* f = dbg.force_ids + key * dbg.dbg_stride;
+      const int32_t* f = dbg.force_ids + rk * dbg.dbg_stride;
       const int fid = lane < k ? f[lane] : 0;
       const bool forced = f[0] >= 0 && __all(fid >= 0 && fid < E);
       if (forced) {
@@ -122,7 +147,7 @@ __global__ void __launch_bounds__(256) moe_topk_kernel(const float* __restrict__
         wsum = wave_sum(lane < k ? pf : 0.f);
       }
     }
-    if (dbg.used_p_out && lane < k) dbg.used_p_out[key * dbg.dbg_stride + lane] = my_w;
+    if (dbg.used_p_out && lane < k) dbg.used_p_out[rk * dbg.dbg_stride + lane] = my_w;
   }
   if (lane < k) {
     topk_id[(int64_t)r * k + lane] = my_id;
