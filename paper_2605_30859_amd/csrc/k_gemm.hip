@@ -23,6 +23,12 @@
 // workspace and a reduce kernel adds them in a fixed order (bitwise
 // deterministic).  The plan is a pure function of (M, N, K), so results do
 // not depend on the device or on earlier calls.
+//
+// Grouped GEMMs (mixture of experts) run the tiled kernel over a device-built
+// list of expert row tiles, or, for the gate/up projection in decode batches,
+// a kernel that streams strip-packed weights straight into MFMA registers
+// (see the strip layout below); a plan per launch (grouped_plan) picks the
+// row tile and the kernel from the routed pairs per expert.
 #include <algorithm>
 #include <cmath>
 
@@ -864,13 +870,15 @@ hipError_t launch_pack_strips(void* W, int64_t rows, int K, hipStream_t st) {
 // the gate/up projection (K = d), 64x128 tiles with a 3-stage ring for the
 // down projection (K = expert FFN).  Measured on the Qwen3-30B-A3B expert
 // shapes from 1 to 1024 rows against one block per CU with 64x128 tiles and
-// a 6-stage ring: 6-18% faster for gate/up, 10-18% for down.  96-row tiles
-// (gate/up from 48 rows per expert on average): 96x128 with a 3-stage ring,
-// one block per CU.  At 64 rows per expert about half the experts exceed 64
-// rows, and a 64-row tile list streams their weights twice; the 96-row tile
-// streams them once (171-180 us per launch at 1024 rows against 222 us).
-// The down projection gains nothing from it (its second pass mostly hits
-// in cache) and keeps 64-row tiles up to 96 rows per expert.
+// a 6-stage ring: 6-18% faster for gate/up, 10-18% for down.  96-row tiles:
+// 96x128 with a 3-stage ring, one block per CU.  At 64 rows per expert about
+// half the experts exceed 64 rows, and a 64-row tile list streams their
+// weights twice; the 96-row tile streams them once (171-180 us per launch at
+// 1024 rows against 222 us).  The gate/up plan now runs its 96-row (and most
+// of its 64-row) tiles on the weights-into-registers kernel below, which is
+// faster still; the down projection gains nothing from 96-row tiles (its
+// second pass mostly hits in cache) and keeps 64-row tiles up to 96 rows per
+// expert.
 template <int BM_, int ST, int EPI, int BN_, int BPC, bool PW>
 static hipError_t grouped_launch(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
                                  void* C, int ldc, int N, int K, const int32_t* g_off,

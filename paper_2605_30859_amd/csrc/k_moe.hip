@@ -4,11 +4,13 @@
 //             zero-padded to a multiple of 128); per row r = softmax over the E
 //             logits, the k largest (ties to the lower expert id), weights
 //             renormalised over the k
-//   offsets:  per-expert counts (block histogram), their exclusive scan, and
-//             a position in its expert's segment for every (row, slot) pair
-//   experts:  grouped tiled GEMMs over the expert segments: gate/up (+ SwiGLU
+//   offsets:  per-expert counts (block histogram), their exclusive scan, one
+//             list of expert row tiles per projection, and a position in its
+//             expert's segment for every (row, slot) pair
+//   experts:  grouped GEMMs over the expert segments: gate/up (+ SwiGLU
 //             epilogue; its A rows are gathered from the normalised input
-//             through the position -> row list), then down
+//             through the position -> row list; strip-packed weights, in
+//             decode batches streamed straight into MFMA registers), then down
 //   combine:  x[row] += sum_j w[row][j] * y[pos(row, j)]   (slot order),
 //             then the next RMSNorm of the updated row
 // Positions inside a segment come from atomics, so their order varies from
