@@ -149,6 +149,49 @@ def test_moe_routing_extremes_teacher_forced(E, top_k, kv_fill):
     assert got["stats"]["steps"] == ref.steps and got["stats"]["pages_used"] == 0
 
 
+def test_moe_expert_kernel_paths_teacher_forced():
+    """One rollout through every kernel path of the grouped expert GEMMs:
+    16 experts top-4, 32 prompts x 8 trajectories, so the prefill has 256
+    routed rows per expert (128-row tiled tiles), the first decode steps
+    51-64 (96-row gate/up tiles, weights straight into registers), the
+    middle 4-46 (64-row, weights into registers) and the last steps 1.25
+    (64-row tiled tiles, strip-packed weights); down runs 128- and 64-row
+    tiled tiles.  The whole batch decodes on the GPU; prompt 0 and prompt 23
+    (the last to complete) are teacher-forced with the oracle's tokens and
+    experts (oracle.forced, computed here), and every row of theirs is
+    compared as in the full-width test: logits at 256 ids, row max and
+    log-sum-exp within 2e-2 of max|z|, log-prob and entropy, the sampled
+    token bit-exact on the GPU's own logits, the router's probabilities and
+    own top-k."""
+    from forced_parity import check_forced, run_forced
+    from oracle.forced import reference_values
+    from workload.gen import teacher_forcing_tokens
+    model = ModelCfg("moe-paths", 2, 256, 4, 2, 64, 0, 512, "bf16", 29, rope_theta=1e6,
+                     n_experts=16, top_k=4, expert_ffn=256)
+    _, run = get_config("qwen3-30b-a3b")
+    run = replace(run, n_prompts=32, prompt_len=32, m=8, k=4, cap=40, len_median=10.0, len_tail=False,
+                  kv_pool_gb=0.0, workload_seed=8)
+    prompts, forced = rollout_inputs(model, run)
+    sched = schedule_only(forced, run.n_prompts, run.m, run.k, run.cap, run.prompt_len)
+    length = np.asarray(sched["length"])
+    E, k = model.n_experts, model.top_k
+    per_expert = [int((length > s).sum()) * k / E for s in range(1, sched["steps"])]
+    say(f"moe kernel paths: decode rows per expert {per_expert}")
+    assert run.n_prompts * run.prompt_len * k / E > 96          # the prefill's 128-row tiles
+    assert any(48 < x <= 96 for x in per_expert) and any(2 <= x <= 48 for x in per_expert)
+    assert any(x < 2 for x in per_expert)
+    last = int(np.argmax(sched["done_step"]))
+    steps = int(sched["done_step"][last]) + 1
+    say("moe kernel paths: oracle")
+    tokens = teacher_forcing_tokens(model, run, steps)
+    g = reference_values(model, run, prompts, forced, tokens, [0, last], steps)
+    rec, strict, route = run_forced(model, run, prompts, forced, g, "moe kernel paths", strict_all=True)
+    n = check_forced(model, run, g, rec, strict, route, "moe kernel paths")
+    decoded = int(rec["seen"].sum())
+    say(f"moe kernel paths: {n} of {decoded} decoded subset rows compared")
+    assert decoded > 0 and n == decoded
+
+
 def test_moe_full_size_schedule():
     """Qwen3-30B-A3B shape (48 layers, d 2048, 32/4 heads, 128 experts top-8,
     expert FFN 768, vocab 151936; 64 prompts x 512, m 16, k 8, cap 16384):
