@@ -119,6 +119,13 @@ __device__ __forceinline__ void vm_wait() {
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
+// Cache-policy operand of the direct LDS loads that marks them non-temporal
+// (the nt bit of gfx950's global loads).  A streaming read of 8 GiB measured
+// 7.0 TB/s with non-temporal 16-byte loads against 6.3 TB/s with plain ones;
+// the weight streams of the MoE expert GEMMs gain 4-13% from it wherever each
+// weight tile is read once per launch.
+constexpr int kNtLoad = 2;
+
 // LDS chunk swizzle for a tile row of KB bf16 (KB/8 chunks of 16 bytes): the
 // chunk order of row r is permuted so that the 8 rows a 16-byte fragment read
 // touches in one LDS pass land in distinct banks.
@@ -132,8 +139,10 @@ __device__ __forceinline__ int dma_swz(int r) {
 // arow != NULL: row r of the tile's A operand is row arow[r] of A (a gather).
 // PW: W is strip-packed (pack_strips_kernel; ldw = K): the same LDS tile is
 // filled from the packed addresses, so results are bitwise those of the
-// row-major layout.
-template <int BM, int BN, int KB, int WGM, int WGN, int STAGES, int EPI, bool SPLIT, bool PW = false>
+// row-major layout.  WAUX: cache policy of the W loads (kNtLoad: non-temporal,
+// for weights a launch reads once).
+template <int BM, int BN, int KB, int WGM, int WGN, int STAGES, int EPI, bool SPLIT, bool PW = false,
+          int WAUX = 0>
 __device__ __forceinline__ void dma_gemm_tile(const bf16_t* __restrict__ A, int lda,
                                               const bf16_t* __restrict__ W, int ldw,
                                               void* __restrict__ C, int ldc, int M, int N,
@@ -189,7 +198,7 @@ __device__ __forceinline__ void dma_gemm_tile(const bf16_t* __restrict__ A, int 
 #pragma unroll
     for (int j = 0; j < WI; ++j)
       __builtin_amdgcn_global_load_lds((const void*)(wsrc[j] + kt * WSTEP),
-                                       (lds_void_t*)(sw + (wave * (BN / NW) + RPI * j) * KB), 16, 0, 0);
+                                       (lds_void_t*)(sw + (wave * (BN / NW) + RPI * j) * KB), 16, 0, WAUX);
   };
 
   f32x4_t acc[TM][TN];
@@ -287,8 +296,8 @@ __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_kernel(const bf16_t* 
 // matrix W + e * w_stride ([N][K]).  The
 // non-empty row tiles are listed on the device (mtiles[i] = e << 16 | m tile,
 // *n_mtiles of them); persistent blocks take items (row tile, n tile), n tile
-// fastest, in a grid-stride loop.  PW: W strip-packed.
-template <int BM, int BN, int KB, int WGM, int WGN, int STAGES, int EPI, bool PW>
+// fastest, in a grid-stride loop.  PW: W strip-packed; WAUX: W cache policy.
+template <int BM, int BN, int KB, int WGM, int WGN, int STAGES, int EPI, bool PW, int WAUX>
 __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_grouped_kernel(
     const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ W, int64_t w_stride, int ldw,
     void* __restrict__ C, int ldc, int N, int K, const int32_t* __restrict__ g_off,
@@ -319,7 +328,7 @@ __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_grouped_kernel(
     __builtin_amdgcn_s_barrier();
     void* Ce = (char*)C + off * ldc * esz;
     // with arow, A rows are gathered: segment row r is A row arow[off + r]
-    dma_gemm_tile<BM, BN, KB, WGM, WGN, STAGES, EPI, false, PW>(arow ? A : A + off * lda, lda,
+    dma_gemm_tile<BM, BN, KB, WGM, WGN, STAGES, EPI, false, PW, WAUX>(arow ? A : A + off * lda, lda,
                                                             W + (int64_t)e * w_stride, ldw, Ce, ldc,
                                                             cnt, N, K, mi, ni, 0, nullptr,
                                                             arow ? arow + off : nullptr);
@@ -332,7 +341,8 @@ __global__ void __launch_bounds__(64 * WGM * WGN) gemm_dma_grouped_kernel(
 // rows, slab of 4 x CPW columns); wavefront w owns CPW columns and loads
 // their W blocks (one 1 KB block per 16-column strip and 32-wide K step)
 // straight from memory into MFMA B-operand registers, P K steps of 64
-// ahead, so W never passes through LDS.  The BM x 64 A tiles of the
+// ahead (non-temporal loads: each block is read once), so W never passes
+// through LDS.  The BM x 64 A tiles of the
 // expert's rows (gathered through arow when given; rows past the expert's
 // count repeat its last row) go through a P-stage LDS ring shared by the
 // four wavefronts, filled by direct 16-byte LDS loads in the swizzled layout
@@ -400,7 +410,9 @@ __global__ void __launch_bounds__(256, 2) gemm_wd_grouped_kernel(
                                          16, 0, 0);                                              \
       _Pragma("unroll") for (int h = 0; h < 2; ++h)                                              \
         _Pragma("unroll") for (int j = 0; j < TN; ++j)                                           \
-          wr[SLOT][h][j] = *(const bf16x8_t*)(wsrc + ((int64_t)j * k32 + 2 * (KT) + h) * 512);  \
+          wr[SLOT][h][j] = __builtin_bit_cast(                                                  \
+              bf16x8_t, __builtin_nontemporal_load(                                              \
+                            (const u32x4_t*)(wsrc + ((int64_t)j * k32 + 2 * (KT) + h) * 512)));  \
     }
 #pragma unroll
     for (int u = 0; u < P - 1; ++u)
@@ -841,10 +853,10 @@ static void dma_go(const Plan& p, const void* A, int lda, const void* W, int ldw
 }
 
 GroupedPlan grouped_plan(int64_t n_pairs, int E, bool gate_up) {
-  if (n_pairs > (int64_t)96 * E) return {kGroupedTileRows, false};
-  if (!gate_up) return {kGroupedTileRowsMin, false};
-  if (n_pairs > (int64_t)48 * E) return {kGroupedTileRowsGU, true};
-  return {kGroupedTileRowsMin, n_pairs >= (int64_t)2 * E};
+  if (n_pairs > (int64_t)96 * E) return {kGroupedTileRows, false, false};
+  if (!gate_up) return {kGroupedTileRowsMin, false, n_pairs <= (int64_t)48 * E};
+  if (n_pairs > (int64_t)48 * E) return {kGroupedTileRowsGU, true, true};
+  return {kGroupedTileRowsMin, n_pairs >= (int64_t)2 * E, true};
 }
 
 hipError_t launch_pack_strips(void* W, int64_t rows, int K, hipStream_t st) {
@@ -879,7 +891,7 @@ hipError_t launch_pack_strips(void* W, int64_t rows, int K, hipStream_t st) {
 // faster still; the down projection gains nothing from 96-row tiles (its
 // second pass mostly hits in cache) and keeps 64-row tiles up to 96 rows per
 // expert.
-template <int BM_, int ST, int EPI, int BN_, int BPC, bool PW>
+template <int BM_, int ST, int EPI, int BN_, int BPC, bool PW, int WAUX>
 static hipError_t grouped_launch(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
                                  void* C, int ldc, int N, int K, const int32_t* g_off,
                                  const int32_t* g_cnt, const int32_t* mtiles,
@@ -889,7 +901,7 @@ static hipError_t grouped_launch(const void* A, int lda, const void* W, int64_t 
   if (PW && (ldw != K || K % 32 != 0)) return hipErrorInvalidValue;
   const int nt = N / BN_;
   const size_t lds = (size_t)ST * (BM_ + BN_) * KB * sizeof(bf16_t);
-  auto kern = gemm_dma_grouped_kernel<BM_, BN_, KB, 2, 2, ST, EPI, PW>;
+  auto kern = gemm_dma_grouped_kernel<BM_, BN_, KB, 2, 2, ST, EPI, PW, WAUX>;
   static bool attr_done = false;
   if (!attr_done) {
     (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -901,26 +913,37 @@ static hipError_t grouped_launch(const void* A, int lda, const void* W, int64_t 
   return hipGetLastError();
 }
 
-template <int EPI, bool PW>
-static hipError_t grouped_by_rows(int tile_rows, const void* A, int lda, const void* W, int64_t w_stride,
-                                  int ldw, void* C, int ldc, int N, int K, const int32_t* g_off,
-                                  const int32_t* g_cnt, const int32_t* mtiles, const int32_t* n_mtiles,
-                                  const int32_t* arow, hipStream_t st) {
+template <int EPI, bool PW, int WAUX>
+static hipError_t grouped_by_rows_aux(int tile_rows, const void* A, int lda, const void* W, int64_t w_stride,
+                                      int ldw, void* C, int ldc, int N, int K, const int32_t* g_off,
+                                      const int32_t* g_cnt, const int32_t* mtiles, const int32_t* n_mtiles,
+                                      const int32_t* arow, hipStream_t st) {
   if (tile_rows == kGroupedTileRowsMin) {
     if constexpr (EPI == EPI_SWIGLU)
-      return grouped_launch<kGroupedTileRowsMin, 4, EPI, 64, 2, PW>(A, lda, W, w_stride, ldw, C, ldc, N, K,
-                                                                    g_off, g_cnt, mtiles, n_mtiles, arow, st);
+      return grouped_launch<kGroupedTileRowsMin, 4, EPI, 64, 2, PW, WAUX>(A, lda, W, w_stride, ldw, C, ldc, N, K,
+                                                                          g_off, g_cnt, mtiles, n_mtiles, arow, st);
     else
-      return grouped_launch<kGroupedTileRowsMin, 3, EPI, 128, 2, PW>(A, lda, W, w_stride, ldw, C, ldc, N, K,
-                                                                     g_off, g_cnt, mtiles, n_mtiles, arow, st);
+      return grouped_launch<kGroupedTileRowsMin, 3, EPI, 128, 2, PW, WAUX>(A, lda, W, w_stride, ldw, C, ldc, N, K,
+                                                                           g_off, g_cnt, mtiles, n_mtiles, arow, st);
   }
   if (tile_rows == kGroupedTileRowsGU)
-    return grouped_launch<kGroupedTileRowsGU, 3, EPI, 128, 1, PW>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off,
-                                                                  g_cnt, mtiles, n_mtiles, arow, st);
+    return grouped_launch<kGroupedTileRowsGU, 3, EPI, 128, 1, PW, WAUX>(A, lda, W, w_stride, ldw, C, ldc, N, K,
+                                                                        g_off, g_cnt, mtiles, n_mtiles, arow, st);
   if (tile_rows == kGroupedTileRows)
-    return grouped_launch<kGroupedTileRows, 4, EPI, 128, 1, PW>(A, lda, W, w_stride, ldw, C, ldc, N, K, g_off,
-                                                                g_cnt, mtiles, n_mtiles, arow, st);
+    return grouped_launch<kGroupedTileRows, 4, EPI, 128, 1, PW, WAUX>(A, lda, W, w_stride, ldw, C, ldc, N, K,
+                                                                      g_off, g_cnt, mtiles, n_mtiles, arow, st);
   return hipErrorInvalidValue;
+}
+
+template <int EPI, bool PW>
+static hipError_t grouped_by_rows(int tile_rows, bool nt_w, const void* A, int lda, const void* W,
+                                  int64_t w_stride, int ldw, void* C, int ldc, int N, int K,
+                                  const int32_t* g_off, const int32_t* g_cnt, const int32_t* mtiles,
+                                  const int32_t* n_mtiles, const int32_t* arow, hipStream_t st) {
+  return nt_w ? grouped_by_rows_aux<EPI, PW, kNtLoad>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off,
+                                                      g_cnt, mtiles, n_mtiles, arow, st)
+              : grouped_by_rows_aux<EPI, PW, 0>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt,
+                                                mtiles, n_mtiles, arow, st);
 }
 
 // Weights into registers: 32 columns per wavefront (a 128-column slab per
@@ -962,15 +985,15 @@ hipError_t launch_gemm_grouped(const void* A, int lda, const void* W, int64_t w_
                                              n_mtiles, arow, st);
       return hipErrorInvalidValue;
     }
-    return grouped_by_rows<EPI_SWIGLU, true>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt,
-                                             mtiles, n_mtiles, arow, st);
+    return grouped_by_rows<EPI_SWIGLU, true>(tile_rows, plan.nt_w, A, lda, W, w_stride, ldw, C, ldc, N, K,
+                                             g_off, g_cnt, mtiles, n_mtiles, arow, st);
   }
   if (plan.wdirect) return hipErrorInvalidValue;
   switch (epi) {
-    case EPI_F32: return grouped_by_rows<EPI_F32, false>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
-    case EPI_BF16: return grouped_by_rows<EPI_BF16, false>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
-    case EPI_ADD_F32: return grouped_by_rows<EPI_ADD_F32, false>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
-    case EPI_SWIGLU: return grouped_by_rows<EPI_SWIGLU, false>(tile_rows, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
+    case EPI_F32: return grouped_by_rows<EPI_F32, false>(tile_rows, plan.nt_w, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
+    case EPI_BF16: return grouped_by_rows<EPI_BF16, false>(tile_rows, plan.nt_w, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
+    case EPI_ADD_F32: return grouped_by_rows<EPI_ADD_F32, false>(tile_rows, plan.nt_w, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
+    case EPI_SWIGLU: return grouped_by_rows<EPI_SWIGLU, false>(tile_rows, plan.nt_w, A, lda, W, w_stride, ldw, C, ldc, N, K, g_off, g_cnt, mtiles, n_mtiles, arow, st);
     default: return hipErrorInvalidValue;
   }
 }

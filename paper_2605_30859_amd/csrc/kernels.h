@@ -85,10 +85,13 @@ constexpr int kGroupedTileRowsMin = 64;    // smallest row tile (sizes the tile 
 // streamed twice), 128-row tiles for large batches (the prefill: more reuse
 // of each weight tile).  wdirect: the gate/up weights go straight into MFMA
 // registers (from 2 rows per expert up to the prefill), otherwise through
-// the LDS tile ring.
+// the LDS tile ring.  nt_w: the weights are loaded non-temporal (gate/up in
+// every decode batch; down while no expert needs a second row tile, whose
+// second pass over the same weights would then miss the cache).
 struct GroupedPlan {
   int tile_rows;
   bool wdirect;
+  bool nt_w;
 };
 GroupedPlan grouped_plan(int64_t n_pairs, int E, bool gate_up);
 hipError_t launch_gemm_grouped(const void* A, int lda, const void* W, int64_t w_stride, int ldw,
