@@ -415,7 +415,8 @@ int darts_stream_read(const void* d_src, int64_t bytes, float* d_sink, void* str
 /* Fill the paged K and V pools of the attention sweep with the values above
  * (tensor 1 for K, 2 for V) at logical index ((page*Hkv + h)*16 + slot)*hd + d,
  * written in the library's physical pool layouts (n_pages pages, dtype as
- * for darts_fill_uniform).  Each pool holds n_pages*Hkv*16*hd elements.    */
+ * for darts_fill_uniform).  Each pool holds n_pages*Hkv*16*hd elements;
+ * head_dim must be a positive multiple of 32 (else DARTS_EINVAL).          */
 int darts_fill_kv_pool(void* d_k_pool, void* d_v_pool, int64_t n_pages, int32_t n_kv_heads,
                        int32_t head_dim, uint64_t seed, int32_t dtype, void* stream);
 

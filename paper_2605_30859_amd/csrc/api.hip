@@ -1151,7 +1151,8 @@ int darts_stream_read(const void* d_src, int64_t bytes, float* d_sink, void* str
 
 int darts_fill_kv_pool(void* d_k_pool, void* d_v_pool, int64_t n_pages, int32_t n_kv_heads,
                        int32_t head_dim, uint64_t seed, int32_t dtype, void* stream) {
-  if (!d_k_pool || !d_v_pool || n_pages < 1 || n_kv_heads < 1 || head_dim % 8) return DARTS_EINVAL;
+  if (!d_k_pool || !d_v_pool || n_pages < 1 || n_kv_heads < 1 || head_dim < 32 || head_dim % 32)
+    return DARTS_EINVAL;
   if (dtype != DARTS_F32 && dtype != DARTS_BF16) return DARTS_EINVAL;
   hipError_t e = launch_fill_kv_pool(d_k_pool, d_v_pool, n_pages, n_kv_heads, head_dim, seed,
                                      dtype == DARTS_BF16, (hipStream_t)stream);

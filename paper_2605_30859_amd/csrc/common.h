@@ -103,13 +103,16 @@ __device__ __forceinline__ float wave_sum(float v) {
 }  // namespace darts
 
 namespace darts {
-// Paged KV pool layout (one pool per layer, page = 16 token slots):
-//   K page of kv head h: [slot][hd]  (token-major; MFMA B operand of q.k^T)
+// Paged KV pool layout (one pool per layer, page = 16 token slots, hd a
+// multiple of 32):
+//   K page of kv head h: [hd/32][slot][32]  (token-major within each 32-dim
+//   block: the MFMA B operand of q.k^T for one 32-wide K step is 1 KB
+//   contiguous, 16 B per lane)
 //   V page of kv head h: [slot/8][hd][slot%8]  (8 consecutive tokens of one
 //   dim contiguous; MFMA B operand of p.V with the contraction over tokens)
 __host__ __device__ __forceinline__ int64_t k_off(int64_t page, int h, int slot, int d, int hkv,
                                                   int hd) {
-  return ((page * hkv + h) * kPage + slot) * (int64_t)hd + d;
+  return (page * hkv + h) * (int64_t)kPage * hd + ((int64_t)(d >> 5) * kPage + slot) * 32 + (d & 31);
 }
 __host__ __device__ __forceinline__ int64_t v_off(int64_t page, int h, int slot, int d, int hkv,
                                                   int hd) {

@@ -164,7 +164,8 @@ constexpr int kPst = 40;   // P row stride in LDS (bf16): 80 bytes
 //   S[16 x 32]  = Q[16 x hd] . K^T      MFMA 16x16x32 bf16 per pair of pages
 //   online softmax per query row (16-lane shuffles)
 //   O[16 x hd] += P[16 x 32] . V[32 x hd]   MFMA 16x16x32 bf16, P via LDS
-// K is read token-major straight into the MFMA B operand (16 B per lane);
+// K is read token-major straight into the MFMA B operand (16 B per lane, one
+// contiguous 1 KB block of the page per 32-wide K step);
 // V pages store 8 consecutive tokens of one dim contiguously, so the P.V
 // B operand is also one 16 B load per lane.  Page ids of the next pair are
 // fetched one iteration ahead so that the page-id -> key/value load chain is
@@ -189,8 +190,8 @@ __device__ __forceinline__ void attn_page_loop(const bf16x8_t (&qa)[HD / 32], co
     const bf16_t* kpb = kpool + k_off(pb, kvh, col, quad * 8, hkv, HD);
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) {
-      F.ka[kk] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(kpa + 32 * kk));
-      F.kb[kk] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(kpb + 32 * kk));
+      F.ka[kk] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(kpa + kk * kPage * 32));
+      F.kb[kk] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(kpb + kk * kPage * 32));
     }
     const int vpage = quad < 2 ? pa : pb;
     const bf16_t* vb = vpool + v_off(vpage, kvh, (quad & 1) * 8, col, hkv, HD);
@@ -496,7 +497,7 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(
       const float* kp = kpool + k_off(page, kvh, slot, 0, hkv, HD);
       float s = 0.f;
 #pragma unroll
-      for (int d = 0; d < HD; ++d) s = fmaf(qreg[d], kp[d], s);
+      for (int d = 0; d < HD; ++d) s = fmaf(qreg[d], kp[(d >> 5) * kPage * 32 + (d & 31)], s);
       s *= scale;
       const float mn = fmaxf(m, s);
       const float a = __expf(m - mn), pj = __expf(s - mn);
