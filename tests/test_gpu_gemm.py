@@ -82,7 +82,12 @@ def test_gemm_qkv_shape_all_batch_sizes(M):
                                        (64, 4096, 4096, 2), (100, 4096, 4096, 2), (16, 4096, 12288, 2),
                                        (64, 4096, 12288, 2), (50, 24576, 4096, 3), (128, 24576, 4096, 3),
                                        (60, 6144, 4096, 1), (97, 6144, 4096, 1), (40, 8192, 1024, 3),
-                                       (33, 2048, 4096, 2)])
+                                       (33, 2048, 4096, 2),
+                                       # the Qwen3-30B-A3B attention projections (QKV, O with the
+                                       # residual add) at 100-513 rows, with and without a K split
+                                       (128, 5120, 2048, 0), (200, 5120, 2048, 0), (354, 5120, 2048, 0),
+                                       (513, 5120, 2048, 0), (100, 2048, 4096, 2), (200, 2048, 4096, 2),
+                                       (256, 2048, 4096, 2), (354, 2048, 4096, 2), (512, 2048, 4096, 2)])
 def test_gemm_decoder_shapes(M, N, K, epi):
     print(f"gemm M={M} N={N} K={K} epi={epi}", flush=True)
     _run(M, N, K, epi)
