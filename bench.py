@@ -193,7 +193,7 @@ def gemm_class_roofline(model, run, rows, hbm_gbs, mfma_tflops):
 
 def hbm_read_rate(B, gib=8, reps=10):
     """HBM read rate this device sustains (GB/s): the library's streaming-read
-    kernel (16-byte loads, 2048 blocks, grid-stride) over a `gib` GiB buffer."""
+    kernel (16-byte non-temporal loads, 2048 blocks, grid-stride) over a `gib` GiB buffer."""
     import torch
     src = torch.zeros(gib << 30, dtype=torch.uint8, device="cuda")
     sink = torch.empty(8192, dtype=torch.float32, device="cuda")

@@ -405,10 +405,11 @@ int darts_fit_ptl(const int32_t* h_bsz, const double* h_lat, int32_t n, double* 
 int darts_fill_uniform(void* d_dst, uint64_t n, int32_t tensor, uint64_t seed, int32_t dtype,
                        void* stream);
 
-/* Read d_src[0..bytes) once with 16-byte loads (2048 blocks x 256 threads,
- * grid-stride) and write 8192 wavefront sums to d_sink (caller-owned, 8192
- * floats).  A streaming-read reference: the HBM read rate this device
- * sustains, against which the bandwidth-bound kernels are also reported.
+/* Read d_src[0..bytes) once with 16-byte non-temporal loads (2048 blocks x
+ * 256 threads, grid-stride) and write 8192 wavefront sums to d_sink
+ * (caller-owned, 8192 floats).  A streaming-read reference: the HBM read
+ * rate this device sustains (non-temporal loads stream faster than plain
+ * ones), against which the bandwidth-bound kernels are also reported.
  * bytes must be a multiple of 16 and d_src 16-byte aligned.                */
 int darts_stream_read(const void* d_src, int64_t bytes, float* d_sink, void* stream);
 
